@@ -1,0 +1,143 @@
+/*
+ * stagefrontier.h -- C ABI of libstagefrontier.
+ *
+ * StageFrontier frontier accounting over per-rank ordered stage durations
+ * (Sec. 3 "Frontier Accounting", Eq. (1) and Eq. (2); window reduction and
+ * top-2 routing of Sec. 4), computed on an AMD Instinct MI355X (gfx950).
+ *
+ * Notation (Sec. 3): d[t][s][r] >= 0 is the duration of ordered stage s on
+ * rank r in training step t.  With 0-based stage indices
+ *     P[t][r][s] = sum_{j <= s} d[t][j][r]          rank-local prefix
+ *     F[t][s]    = max_r P[t][r][s]                 frontier
+ *     a[t][s]    = F[t][s] - F[t][s-1],  F[t][-1] = 0   frontier advance
+ * and the leader of boundary (t, s) is the lowest rank index r with
+ * P[t][r][s] == F[t][s].
+ *
+ * Conventions shared by every entry point:
+ *  - All array pointers are DEVICE pointers (hipMalloc'd memory or memory
+ *    the device can address).  Arrays are dense, row-major, with no padding.
+ *  - Every call that takes a stream is asynchronous on that stream: it
+ *    validates its arguments on the host, enqueues kernels and returns.
+ *    Outputs are valid once the stream has reached that point.  A NULL
+ *    stream means the legacy default stream.
+ *  - The caller allocates and frees every buffer.  The library allocates no
+ *    memory, never synchronises a stream and keeps no mutable global state,
+ *    so calls are reentrant and may be issued from several host threads.
+ *  - Inputs are read only.  Output arrays must not overlap each other or
+ *    any input (checked: SF_EINVAL).
+ *  - Errors found on the host are returned before anything is enqueued.
+ *    SF_EHIP reports a failed kernel launch; nothing is left enqueued by
+ *    the failing call after its first failed launch.
+ */
+#ifndef STAGEFRONTIER_H
+#define STAGEFRONTIER_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* hipStream_t, passed as an opaque pointer so that the header needs no HIP
+ * include.  NULL selects the default stream. */
+typedef void* sf_stream_t;
+
+/* Status codes returned by every int-returning entry point. */
+enum {
+    SF_OK = 0,
+    SF_EINVAL = 1, /* bad argument: NULL pointer, size out of range,
+                      misaligned pointer, overlapping outputs, overflow   */
+    SF_ERANGE = 2, /* reserved for data-range errors                     */
+    SF_EHIP = 3    /* the HIP runtime rejected a kernel launch            */
+};
+
+/* Largest rank count: the leader is carried in 16 bits of a packed
+ * (prefix, rank) key. */
+#define SF_MAX_R 65536
+/* Largest stage count per call. */
+#define SF_MAX_S 1024
+/* Every rank-local prefix P[t][r][s] must be below this many ns (about
+ * 39 hours) so that the packed key fits in 64 bits. */
+#define SF_MAX_PREFIX_NS ((int64_t)1 << 47)
+
+/*
+ * sf_frontier -- per-step frontier advances and leaders (Sec. 3, Eq. (1);
+ * the single streaming pass over steps, stages and ranks of Sec. 3).
+ *
+ *   durations      [T][S][R] int64, ns; rank index fastest.  Read once.
+ *   T              number of steps, 0 <= T.  T == 0 is a no-op (pointers
+ *                  may then be NULL).
+ *   R              number of ranks, 1 <= R <= SF_MAX_R.
+ *   S              number of ordered stages, 1 <= S <= SF_MAX_S.
+ *   out_increment  [T][S] int64, ns: a[t][s].  Written.
+ *   out_leader     [T][S] int32: lowest rank attaining F[t][s].  Written.
+ *   stream         HIP stream the work is enqueued on.
+ *
+ * Data preconditions (not checked): every d >= 0 (Sec. 3 requires
+ * nonnegative durations) and every prefix P < SF_MAX_PREFIX_NS.  Outputs
+ * are unspecified when they are violated.  Pointers must be aligned to
+ * their element size (checked).
+ *
+ * Steps are independent, so a long step axis may be processed in chunks:
+ * pass durations + t0*S*R, out_increment + t0*S, out_leader + t0*S with
+ * T = chunk length.  The result equals one call over the whole range.
+ *
+ * Returns SF_OK, SF_EINVAL or SF_EHIP.
+ */
+int sf_frontier(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                int64_t* out_increment, int32_t* out_leader,
+                sf_stream_t stream);
+
+/*
+ * sf_num_windows -- number of windows W = ceil(T / window) that
+ * sf_window_summary produces; the last window holds the remaining
+ * T - (W-1)*window steps.  Returns -1 when T < 0 or window < 1.
+ * Host only; no device work.
+ */
+int64_t sf_num_windows(int64_t T, int64_t window);
+
+/*
+ * sf_window_summary -- window reduction of the per-step results (Eq. (2) of
+ * Sec. 3: numerators of the stage shares; leader counts; the top-2 stage
+ * routing of Sec. 4).
+ *
+ *   increment          [T][S] int64 from sf_frontier.
+ *   leader             [T][S] int32 from sf_frontier.  Entries outside
+ *                      [0, R) are not counted anywhere.
+ *   T, R, S            as for sf_frontier (T == 0 is a no-op).
+ *   window             steps per window, >= 1.  Window w covers steps
+ *                      [w*window, min((w+1)*window, T)).
+ *   out_stage_exposed  [W][S] int64: sum over the window of a[t][s].  The
+ *                      share A_s of Eq. (2) is this value divided by the
+ *                      sum over s of the same row (Theorem 1).
+ *   out_lead_counts    [W][S][R] int32: number of steps of the window whose
+ *                      leader at stage s is rank r (zeros included).
+ *   out_top2           [W][2][2] int32: {{s1, r1}, {s2, r2}}.  s1, s2 are
+ *                      the two stages with the largest exposed totals
+ *                      (ties go to the lower stage index); rk is the rank
+ *                      with the largest lead count at stage sk (ties go to
+ *                      the lower rank; -1 if that count is 0).  When S == 1
+ *                      the second pair is {-1, -1}.
+ *   stream             HIP stream.
+ *
+ * The sums are exact in int64 as long as they do not overflow (they cannot
+ * under the sf_frontier preconditions and W*window*SF_MAX_PREFIX_NS < 2^63).
+ *
+ * Returns SF_OK, SF_EINVAL or SF_EHIP.
+ */
+int sf_window_summary(const int64_t* increment, const int32_t* leader,
+                      int64_t T, int32_t R, int32_t S, int64_t window,
+                      int64_t* out_stage_exposed, int32_t* out_lead_counts,
+                      int32_t* out_top2, sf_stream_t stream);
+
+/* sf_strerror -- static, NUL-terminated description of a status code. */
+const char* sf_strerror(int status);
+
+/* sf_version -- static, NUL-terminated library version string. */
+const char* sf_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STAGEFRONTIER_H */

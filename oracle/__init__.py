@@ -1,0 +1,119 @@
+"""CPU oracle for StageFrontier frontier accounting -- TEST INFRASTRUCTURE.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product library never calls it;
+the GPU path and the oracle share no code.
+
+Two independent statements of the same definitions (Sec. 3, Eq. (1) and
+Eq. (2); top-2 routing of Sec. 4):
+
+* ``frontier`` / ``window_summary`` -- plain C nested loops in
+  ``sf_oracle.c`` (fast enough for the full workloads on sampled steps),
+  called through ctypes on numpy arrays;
+* ``pyref`` -- the same definitions as pure-Python loops for tiny inputs.
+
+Both follow the readings documented in ``sf_oracle.c``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "sf_oracle.c")
+_LIB = os.path.join(_HERE, "libsforacle.so")
+
+
+def build(force: bool = True, src: str = _SRC, out: str = _LIB) -> str:
+    """Compile the C oracle with gcc (plain -O2, single thread)."""
+    if force or not os.path.exists(out):
+        tmp = out + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-std=c99", "-Wall", "-Wextra", "-fPIC", "-shared",
+             src, "-o", tmp])
+        os.replace(tmp, out)
+    return out
+
+
+class COracle:
+    """ctypes view of one compiled copy of ``sf_oracle.c``."""
+
+    def __init__(self, path: str):
+        lib = ctypes.CDLL(path)
+        i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+        lib.sfo_frontier.argtypes = [vp, i64, i32, i32, vp, vp]
+        lib.sfo_frontier.restype = ctypes.c_int
+        lib.sfo_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp]
+        lib.sfo_window_summary.restype = None
+        self.lib = lib
+        self.path = path
+
+    def frontier(self, d: np.ndarray):
+        """Eq. (1) for every step.
+
+        ``d``: int64 array of shape [T, S, R] (ns).  Returns ``(inc, lead)``
+        with shapes [T, S] (int64 ns and int32 rank).
+        """
+        d = np.ascontiguousarray(d, dtype=np.int64)
+        if d.ndim != 3:
+            raise ValueError("durations must be [T, S, R]")
+        T, S, R = d.shape
+        inc = np.empty((T, S), dtype=np.int64)
+        lead = np.empty((T, S), dtype=np.int32)
+        if T and S and R:
+            rc = self.lib.sfo_frontier(d.ctypes.data, T, R, S,
+                                       inc.ctypes.data, lead.ctypes.data)
+            if rc != 0:
+                raise MemoryError("oracle prefix scratch allocation failed")
+        return inc, lead
+
+    def window_summary(self, inc: np.ndarray, lead: np.ndarray, R: int, window: int):
+        """Window reduction of per-step results.
+
+        Returns ``(exposed [W,S] int64, counts [W,S,R] int32,
+        top2 [W,2,2] int32)``.
+        """
+        inc = np.ascontiguousarray(inc, dtype=np.int64)
+        lead = np.ascontiguousarray(lead, dtype=np.int32)
+        T, S = inc.shape
+        W = num_windows(T, window)
+        exposed = np.empty((W, S), dtype=np.int64)
+        counts = np.empty((W, S, R), dtype=np.int32)
+        top2 = np.empty((W, 2, 2), dtype=np.int32)
+        if W:
+            self.lib.sfo_window_summary(
+                inc.ctypes.data, lead.ctypes.data, T, R, S, window,
+                exposed.ctypes.data, counts.ctypes.data, top2.ctypes.data)
+        return exposed, counts, top2
+
+
+def num_windows(T: int, window: int) -> int:
+    return (T + window - 1) // window
+
+
+_default = None
+
+
+def _get() -> COracle:
+    global _default
+    if _default is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        _default = COracle(_LIB)
+    return _default
+
+
+def frontier(d: np.ndarray):
+    return _get().frontier(d)
+
+
+def window_summary(inc: np.ndarray, lead: np.ndarray, R: int, window: int):
+    return _get().window_summary(inc, lead, R, window)
+
+
+from . import pyref  # noqa: E402  (pure-Python twin, no compiled code)
+
+__all__ = ["build", "COracle", "frontier", "window_summary", "num_windows", "pyref"]

@@ -1,0 +1,56 @@
+"""Pure-Python statement of frontier accounting, for tiny inputs.
+
+TEST INFRASTRUCTURE ONLY (same rules as the rest of ``oracle``).  It restates
+the definitions of Sec. 3 (Eq. (1), Eq. (2)) and the top-2 routing of Sec. 4
+as literal Python loops over lists, with the same readings as
+``sf_oracle.c``, so that the C oracle can be cross-checked on small inputs by
+a second, independently written statement.
+"""
+from __future__ import annotations
+
+
+def frontier(d):
+    """``d[t][s][r]`` nested lists of ints -> ``(inc[t][s], lead[t][s])``."""
+    inc, lead = [], []
+    for step in d:
+        S = len(step)
+        R = len(step[0])
+        P = [0] * R
+        F_prev = 0
+        inc_t, lead_t = [], []
+        for s in range(S):
+            for r in range(R):
+                P[r] = P[r] + step[s][r]
+            F = max(P)
+            inc_t.append(F - F_prev)
+            lead_t.append(P.index(F))  # first (lowest) rank attaining F
+            F_prev = F
+        inc.append(inc_t)
+        lead.append(lead_t)
+    return inc, lead
+
+
+def window_summary(inc, lead, R, window):
+    """Returns ``(exposed[w][s], counts[w][s][r], top2[w][k][2])``."""
+    T = len(inc)
+    S = len(inc[0]) if T else 0
+    W = (T + window - 1) // window
+    exposed, counts, top2 = [], [], []
+    for w in range(W):
+        steps = range(w * window, min((w + 1) * window, T))
+        ex_w = [sum(inc[t][s] for t in steps) for s in range(S)]
+        c_w = [[sum(1 for t in steps if lead[t][s] == r) for r in range(R)]
+               for s in range(S)]
+        order = sorted(range(S), key=lambda s: (-ex_w[s], s))
+        picks = order[:2] + [-1] * (2 - len(order[:2]))
+        t2 = []
+        for sk in picks:
+            if sk < 0:
+                t2.append([-1, -1])
+                continue
+            m = max(c_w[sk])
+            t2.append([sk, c_w[sk].index(m) if m > 0 else -1])
+        exposed.append(ex_w)
+        counts.append(c_w)
+        top2.append(t2)
+    return exposed, counts, top2

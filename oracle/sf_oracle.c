@@ -1,0 +1,126 @@
+/*
+ * sf_oracle.c -- reference CPU statement of StageFrontier frontier
+ * accounting.  TEST INFRASTRUCTURE ONLY: nothing in the product library
+ * calls, links or includes this file.  It exists so that the tests, the
+ * smoke check and the CPU baseline of the benchmark have an obviously
+ * correct answer to compare the GPU path against.
+ *
+ * The method is exact (no approximation, heuristic or iteration), so this
+ * file is its definition written out as nested loops, in signed int64
+ * nanoseconds, in the paper's order of operations:
+ *
+ *   Sec. 3, Eq. (1):  P[t,r,s] = sum_{j<=s} d[t,r,j]
+ *                     F[t,s]   = max_r P[t,r,s]
+ *                     a[t,s]   = F[t,s] - F[t,s-1],  F[t,0] = 0 (1-based s)
+ *   Sec. 3, the accounting core: one pass over steps; for each step the
+ *   running prefix of every rank is advanced stage by stage and the
+ *   frontier is re-taken at every boundary.
+ *   Sec. 3, Eq. (2):  the window share numerator sum_{t in window} a[t,s].
+ *   Sec. 4: top-2 routing = the two stages with the highest shares.
+ *
+ * Readings where the paper leaves a choice open (each is listed with its
+ * reason in the design notes of the repository):
+ *   - leader = lowest rank index attaining F (the paper reports a tie set);
+ *   - the leader is emitted and counted at every boundary, also where a = 0;
+ *   - top-2 orders stages by the exposed window total (equivalently by the
+ *     share, whose denominator is common), lower stage index on ties, and
+ *     pairs each with its most frequent leader, lower rank on ties, -1 when
+ *     that stage has no counted leader;
+ *   - W = ceil(T / window); the last window may be shorter;
+ *   - leaders outside [0, R) are not counted.
+ *
+ * Layout: d is [T][S][R] (rank fastest), increments and leaders [T][S],
+ * exposed [W][S], counts [W][S][R], top2 [W][2][2].
+ *
+ * Parity status: every function here is pinned by the CPU test suite
+ * (printed worked examples, closed forms, brute force); see tests/.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+
+/* Frontier advances and leaders, Eq. (1).  Returns 0, or -1 if the prefix
+ * scratch cannot be allocated. */
+int sfo_frontier(const int64_t* d, int64_t T, int32_t R, int32_t S,
+                 int64_t* inc, int32_t* lead)
+{
+    int64_t* P = (int64_t*)malloc(sizeof(int64_t) * (size_t)(R > 0 ? R : 1));
+    if (!P) return -1;
+    for (int64_t t = 0; t < T; ++t) {
+        /* rank-local prefixes start at zero for every step */
+        for (int32_t r = 0; r < R; ++r) P[r] = 0;
+        int64_t F_prev = 0; /* F[t,0] = 0 */
+        for (int32_t s = 0; s < S; ++s) {
+            const int64_t* row = d + (t * S + s) * (int64_t)R;
+            for (int32_t r = 0; r < R; ++r) P[r] += row[r];
+            /* F[t,s] = max over ranks; strict '>' keeps the lowest rank */
+            int64_t F = P[0];
+            int32_t L = 0;
+            for (int32_t r = 1; r < R; ++r) {
+                if (P[r] > F) {
+                    F = P[r];
+                    L = r;
+                }
+            }
+            inc[t * S + s] = F - F_prev;
+            lead[t * S + s] = L;
+            F_prev = F;
+        }
+    }
+    free(P);
+    return 0;
+}
+
+/* Window reduction of per-step results: Eq. (2) numerators, leader counts
+ * and top-2 routing. */
+void sfo_window_summary(const int64_t* inc, const int32_t* lead,
+                        int64_t T, int32_t R, int32_t S, int64_t window,
+                        int64_t* exposed, int32_t* counts, int32_t* top2)
+{
+    int64_t W = (T + window - 1) / window;
+    for (int64_t w = 0; w < W; ++w) {
+        int64_t t0 = w * window;
+        int64_t t1 = t0 + window < T ? t0 + window : T;
+
+        for (int32_t s = 0; s < S; ++s) {
+            int64_t sum = 0;
+            for (int64_t t = t0; t < t1; ++t) sum += inc[t * S + s];
+            exposed[w * S + s] = sum;
+
+            int32_t* c = counts + (w * S + s) * (int64_t)R;
+            for (int32_t r = 0; r < R; ++r) c[r] = 0;
+            for (int64_t t = t0; t < t1; ++t) {
+                int32_t r = lead[t * S + s];
+                if (r >= 0 && r < R) c[r] += 1;
+            }
+        }
+
+        /* first stage: largest exposed, lower index on ties */
+        int32_t s1 = 0;
+        for (int32_t s = 1; s < S; ++s)
+            if (exposed[w * S + s] > exposed[w * S + s1]) s1 = s;
+        /* second stage: same rule among the remaining stages */
+        int32_t s2 = -1;
+        for (int32_t s = 0; s < S; ++s) {
+            if (s == s1) continue;
+            if (s2 < 0 || exposed[w * S + s] > exposed[w * S + s2]) s2 = s;
+        }
+
+        int32_t pick[2] = {s1, s2};
+        for (int k = 0; k < 2; ++k) {
+            int32_t sk = pick[k];
+            int32_t rk = -1;
+            if (sk >= 0) {
+                const int32_t* c = counts + (w * S + sk) * (int64_t)R;
+                int32_t best = 0;
+                for (int32_t r = 0; r < R; ++r) {
+                    if (c[r] > best) {
+                        best = c[r];
+                        rk = r;
+                    }
+                }
+            }
+            top2[w * 4 + 2 * k + 0] = sk;
+            top2[w * 4 + 2 * k + 1] = rk;
+        }
+    }
+}

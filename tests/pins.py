@@ -1,0 +1,417 @@
+"""Pins of the frontier-accounting oracle to facts outside the oracle itself.
+
+Each ``pin_*`` takes a frontier function ``f(d[T,S,R]) -> (inc, lead)`` and
+(where needed) a summary function ``g(inc, lead, R, window) -> (exposed,
+counts, top2)`` and raises ``AssertionError`` on a violation.  The suite in
+``test_oracle_pins.py`` applies them to the oracle; ``test_oracle_mutants.py``
+applies them to copies of the oracle with planted mistakes and requires that
+every mistake is caught by at least one pin.
+
+What pins what:
+  * printed worked examples (Sec. 2, Fig. fig:frontier-accounting, Sec. 4);
+  * Theorem 1 (telescoping: advances sum to the largest rank total) and the
+    nonnegativity of advances stated after Eq. (1);
+  * the slack identity, Eq. (3), an independent formula for each advance;
+  * Propositions 1 and 2 (max overcount / average undercount bounds, with the
+    tight constructions of Appendix D);
+  * the measurement-error stability proposition of Appendix D;
+  * the R = 1 edge case (Sec. 3: the frontier is the rank's own vector);
+  * brute force over every small integer matrix;
+  * structural invariants: rank relabelling, stage refinement (the
+    accumulation-expansion remark of Sec. 3), zero stages, step chunking;
+  * the hand-built single-rank data stall of the Sec. 2 pattern.
+"""
+from __future__ import annotations
+
+import itertools
+import os
+
+import numpy as np
+
+MS = 1_000_000
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+# ----------------------------------------------------------------------------
+# helpers that do not restate the frontier recursion
+
+
+def load_golden(name: str) -> dict:
+    """Parse one fixture of tests/golden (see the files for the format)."""
+    rows, out = {}, {}
+    with open(os.path.join(GOLDEN, name)) as fh:
+        for line in fh:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            key, *vals = line.split()
+            if key == "d":
+                rows[int(vals[0])] = [int(v) for v in vals[1:]]
+            elif key == "stages":
+                out["stages"] = vals
+            else:
+                out[key] = [int(v) for v in vals]
+    R = len(rows)
+    # fixture rows are per rank; the oracle layout is [T][S][R]
+    out["d"] = np.array([[rows[r] for r in range(R)]], dtype=np.int64).transpose(0, 2, 1).copy()
+    return out
+
+
+GOLDEN_FILES = ["motivating_example.txt", "frontier_figure.txt", "non_identifiable_pair.txt"]
+
+
+def rank_totals(d):
+    """[T, R] total duration of every rank (sum over all stages)."""
+    return d.sum(axis=1)
+
+
+def random_cases(seed=0):
+    """A mix of tie-free and tie-heavy random inputs of several shapes."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    cases = []
+    for (T, S, R) in [(50, 6, 8), (40, 3, 1), (30, 1, 5), (25, 12, 33), (20, 7, 64), (10, 5, 130)]:
+        cases.append(rng.integers(0, 10**9, size=(T, S, R), dtype=np.int64))
+        cases.append(rng.integers(0, 4, size=(T, S, R), dtype=np.int64))  # many ties
+    return cases
+
+
+def stall_case():
+    """Hand-built single-rank data stall (Sec. 2 pattern) with four ranks.
+
+    All ranks share the base stage durations (20, 60, 120, 2, 15, 3) ms of
+    (data, fwd, bwd, callback, optim, other).  Rank 2's data stage is 30 ms
+    late; ranks 0, 1 and 3 observe the same delay as 30 ms of backward wait.
+    """
+    base = np.array([20, 60, 120, 2, 15, 3], dtype=np.int64) * MS
+    d = np.repeat(base[:, None], 4, axis=1)
+    d[0, 2] += 30 * MS
+    for r in (0, 1, 3):
+        d[2, r] += 30 * MS
+    return d[None].copy()
+
+
+# ----------------------------------------------------------------------------
+# frontier pins
+
+
+def pin_golden(f):
+    for name in GOLDEN_FILES:
+        g = load_golden(name)
+        inc, lead = f(g["d"])
+        assert inc[0].tolist() == g["inc"], (name, inc[0].tolist())
+        assert lead[0].tolist() == g["lead"], (name, lead[0].tolist())
+        assert int(inc[0].sum()) == g["makespan"][0], name
+        if "stage_max_total" in g:
+            # the per-stage max baseline printed beside the frontier
+            assert int(g["d"][0].max(axis=1).sum()) == g["stage_max_total"][0]
+
+
+def pin_stall(f):
+    """Sec. 2 pattern: the delay is charged once, to data, on the stalled
+    rank; backward is not inflated by the wait of the other ranks."""
+    d = stall_case()
+    inc, lead = f(d)
+    assert inc[0].tolist() == [50 * MS, 60 * MS, 120 * MS, 2 * MS, 15 * MS, 3 * MS], inc
+    # data led by the stalled rank; from bwd on all four ranks tie at the
+    # same prefix and the lowest index leads
+    assert lead[0].tolist() == [2, 2, 0, 0, 0, 0], lead
+    assert int(inc[0].sum()) == 250 * MS == int(rank_totals(d).max())
+    # the naive per-stage max double counts the wait
+    assert int(d[0].max(axis=1).sum()) == 280 * MS
+
+
+def pin_telescoping(f):
+    """Theorem 1 and a >= 0 (Sec. 3)."""
+    for d in random_cases(1):
+        inc, lead = f(d)
+        assert inc.shape == d.shape[:2] and lead.shape == d.shape[:2]
+        assert (inc >= 0).all()
+        assert np.array_equal(inc.sum(axis=1), rank_totals(d).max(axis=1))
+
+
+def pin_slack_identity(f):
+    """Eq. (3): a[t,s] = max_r (d[t,r,s] - lambda[t,r,s]) with
+    lambda[t,r,s] = F[t,s-1] - P[t,r,s-1]; every lambda >= 0."""
+    for d in random_cases(2):
+        inc, _ = f(d)
+        T, S, R = d.shape
+        F = np.cumsum(inc, axis=1)  # frontier from the function under test
+        for t in range(T):
+            P_prev = np.zeros(R, dtype=np.int64)
+            F_prev = 0
+            for s in range(S):
+                lam = F_prev - P_prev
+                assert (lam >= 0).all()
+                assert inc[t, s] == (d[t, s] - lam).max()
+                P_prev = P_prev + d[t, s]
+                F_prev = F[t, s]
+
+
+def pin_single_rank(f):
+    """Sec. 3 edge case: with R = 1 the frontier is the rank's own vector."""
+    rng = np.random.Generator(np.random.PCG64(3))
+    d = rng.integers(0, 10**9, size=(17, 9, 1), dtype=np.int64)
+    inc, lead = f(d)
+    assert np.array_equal(inc, d[:, :, 0])
+    assert (lead == 0).all()
+
+
+def pin_props(f):
+    """Propositions 1 and 2 (integer form) and their tight constructions
+    (Appendix D)."""
+    for d in random_cases(4):
+        inc, _ = f(d)
+        T, S, R = d.shape
+        F = inc.sum(axis=1)
+        M = d.max(axis=2).sum(axis=1)          # sum_s max_r d
+        tot = d.sum(axis=(1, 2))               # R * mean-based summary
+        assert (F <= M).all() and (M <= min(R, S) * F).all()
+        assert (F <= tot).all() and (tot <= R * F).all()
+    # Prop. 1 tight: D on min(R,S) distinct (rank, stage) pairs, one per rank
+    for R, S in [(3, 5), (6, 4), (5, 5)]:
+        D = 7 * MS
+        d = np.zeros((1, S, R), dtype=np.int64)
+        for k in range(min(R, S)):
+            d[0, k, k] = D
+        inc, _ = f(d)
+        assert int(inc.sum()) == D
+        assert int(d[0].max(axis=1).sum()) == min(R, S) * int(inc.sum())
+    # Prop. 2 tight: one rank carries total D, the others zero
+    R, S = 5, 4
+    d = np.zeros((1, S, R), dtype=np.int64)
+    d[0, :, 3] = [1 * MS, 2 * MS, 3 * MS, 4 * MS]
+    inc, lead = f(d)
+    assert int(inc.sum()) == 10 * MS == int(d.sum())
+    assert lead[0].tolist() == [3, 3, 3, 3]
+
+
+def pin_stability(f):
+    """Appendix D: every duration moved by at most eps moves the frontier
+    at 1-based boundary s by at most s*eps and the advance by at most
+    (2s-1)*eps."""
+    rng = np.random.Generator(np.random.PCG64(5))
+    for (T, S, R) in [(40, 6, 8), (20, 12, 50)]:
+        d = rng.integers(10**6, 10**8, size=(T, S, R), dtype=np.int64)
+        for eps in (1, 1000, 10**6):
+            e = rng.integers(-eps, eps + 1, size=d.shape, dtype=np.int64)
+            inc0, _ = f(d)
+            inc1, _ = f(d + e)
+            F0, F1 = np.cumsum(inc0, axis=1), np.cumsum(inc1, axis=1)
+            s1 = np.arange(1, S + 1)
+            assert (np.abs(F1 - F0) <= s1 * eps).all()
+            assert (np.abs(inc1 - inc0) <= (2 * s1 - 1) * eps).all()
+            # the bound is reached: one rank's first stages all move by +eps
+    d = np.zeros((1, 4, 2), dtype=np.int64) + 5 * MS
+    e = np.zeros_like(d)
+    e[0, :, 0] = 1000
+    inc0, _ = f(d)
+    inc1, _ = f(d + e)
+    assert (np.cumsum(inc1 - inc0, axis=1) == 1000 * np.arange(1, 5)).all()
+
+
+def _brute_prefix_max(case, R, S):
+    """Largest total of the first s+1 stages over ranks, and the lowest rank
+    reaching it, by summing each rank's stages from scratch."""
+    inc, lead = [], []
+    prev = 0
+    for s in range(S):
+        sums = [sum(case[j][r] for j in range(s + 1)) for r in range(R)]
+        best = max(sums)
+        inc.append(best - prev)
+        lead.append(min(r for r in range(R) if sums[r] == best))
+        prev = best
+    return inc, lead
+
+
+def pin_bruteforce(f):
+    """Every d in {0,1,2}^(S x R) for four small shapes."""
+    for (R, S) in [(2, 2), (2, 3), (3, 2), (3, 3)]:
+        cases = list(itertools.product(range(3), repeat=R * S))
+        d = np.array(cases, dtype=np.int64).reshape(len(cases), S, R)
+        inc, lead = f(d)
+        for i, flat in enumerate(cases):
+            case = [list(flat[s * R:(s + 1) * R]) for s in range(S)]
+            ei, el = _brute_prefix_max(case, R, S)
+            assert inc[i].tolist() == ei, (R, S, case)
+            assert lead[i].tolist() == el, (R, S, case)
+
+
+def pin_permutation(f):
+    """Relabelling ranks permutes leaders where the leader is unique; at a
+    tie the leader is the lowest relabelled index of the tie set."""
+    rng = np.random.Generator(np.random.PCG64(6))
+    for d in random_cases(7):
+        T, S, R = d.shape
+        perm = rng.permutation(R)            # new rank k holds old rank perm[k]
+        inv = np.argsort(perm)               # old rank r becomes inv[r]
+        inc0, lead0 = f(d)
+        inc1, lead1 = f(d[:, :, perm])
+        assert np.array_equal(inc0, inc1)
+        P = np.cumsum(d, axis=1)
+        for t in range(T):
+            for s in range(S):
+                ties = np.flatnonzero(P[t, s] == P[t, s].max())
+                assert lead0[t, s] == ties.min()
+                assert lead1[t, s] == inv[ties].min()
+
+
+def pin_structure(f):
+    """Stage refinement, zero stages, constant shifts, scaling, step order
+    and step chunking (steps are independent, Sec. 3)."""
+    rng = np.random.Generator(np.random.PCG64(8))
+    d = rng.integers(0, 10**7, size=(30, 6, 11), dtype=np.int64)
+    inc, lead = f(d)
+    # refinement: split stage 2 into two consecutive sub-stages on every rank
+    frac = rng.integers(0, 10**7, size=(30, 11), dtype=np.int64)
+    part = np.minimum(frac, d[:, 2])
+    dr = np.concatenate([d[:, :2], part[:, None], (d[:, 2] - part)[:, None], d[:, 3:]], axis=1)
+    ir, lr = f(dr)
+    assert np.array_equal(ir[:, 2] + ir[:, 3], inc[:, 2])
+    assert np.array_equal(np.delete(ir, [2, 3], axis=1), np.delete(inc, 2, axis=1))
+    assert np.array_equal(lr[:, 3], lead[:, 2])
+    # appending a zero stage: zero advance, leader of the last boundary kept
+    dz = np.concatenate([d, np.zeros((30, 1, 11), dtype=np.int64)], axis=1)
+    iz, lz = f(dz)
+    assert (iz[:, -1] == 0).all() and np.array_equal(lz[:, -1], lead[:, -1])
+    # adding c to stage 4 on every rank adds c to that advance only
+    dc = d.copy()
+    dc[:, 4] += 12345
+    ic, lc = f(dc)
+    expect = inc.copy()
+    expect[:, 4] += 12345
+    assert np.array_equal(ic, expect) and np.array_equal(lc, lead)
+    # scaling every duration scales every advance
+    i3, l3 = f(3 * d)
+    assert np.array_equal(i3, 3 * inc) and np.array_equal(l3, lead)
+    # steps are independent: reversing steps reverses results
+    ib, lb = f(d[::-1].copy())
+    assert np.array_equal(ib, inc[::-1]) and np.array_equal(lb, lead[::-1])
+    # chunks concatenate
+    i1, l1 = f(d[:13])
+    i2, l2 = f(d[13:])
+    assert np.array_equal(np.concatenate([i1, i2]), inc)
+    assert np.array_equal(np.concatenate([l1, l2]), lead)
+
+
+def pin_twin(f, pyref):
+    """Agreement with the pure-Python statement on small random inputs."""
+    for d in random_cases(9):
+        small = d[:6]
+        inc, lead = f(small)
+        pi, pl = pyref.frontier(small.tolist())
+        assert inc.tolist() == pi and lead.tolist() == pl
+
+
+FRONTIER_PINS = [pin_golden, pin_stall, pin_telescoping, pin_slack_identity,
+                 pin_single_rank, pin_props, pin_stability, pin_bruteforce,
+                 pin_permutation, pin_structure]
+
+
+# ----------------------------------------------------------------------------
+# window-summary pins
+
+
+def _expected_counts(lead, R, t0, t1):
+    """Leader histogram of steps [t0, t1) per stage with np.bincount."""
+    S = lead.shape[1]
+    out = np.zeros((S, R), dtype=np.int64)
+    for s in range(S):
+        v = lead[t0:t1, s]
+        v = v[(v >= 0) & (v < R)]
+        out[s] = np.bincount(v, minlength=R)[:R]
+    return out
+
+
+def pin_summary_mass(f, g):
+    """Counts sum to the window length; exposed totals sum to the window's
+    exposed makespan (Theorem 1 summed over the window); the last window
+    is the remainder."""
+    for d in random_cases(10):
+        T, S, R = d.shape
+        inc, lead = f(d)
+        for window in (1, 7, T, T + 3):
+            ex, cnt, top2 = g(inc, lead, R, window)
+            W = -(-T // window)
+            assert ex.shape == (W, S) and cnt.shape == (W, S, R) and top2.shape == (W, 2, 2)
+            for w in range(W):
+                t0, t1 = w * window, min((w + 1) * window, T)
+                assert (cnt[w].sum(axis=1) == t1 - t0).all()
+                assert int(ex[w].sum()) == int(rank_totals(d[t0:t1]).max(axis=1).sum())
+                assert np.array_equal(ex[w], inc[t0:t1].sum(axis=0))
+                assert np.array_equal(cnt[w], _expected_counts(lead, R, t0, t1))
+
+
+def pin_summary_top2(f, g):
+    """Top-2 routing on constructed windows: order by exposed total, lower
+    stage on ties; modal leader, lower rank on ties, -1 with no leader."""
+    R = 4
+    # one window of 6 steps, S = 4; exposed totals (5, 9, 9, 1) by construction
+    inc = np.array([[5, 9, 9, 1]] + [[0, 0, 0, 0]] * 5, dtype=np.int64)
+    lead = np.array([[0, 1, 3, 0],
+                     [0, 2, 3, 0],
+                     [1, 2, 0, 0],
+                     [1, 1, 0, 0],
+                     [2, 3, 0, 0],
+                     [2, 3, 0, 0]], dtype=np.int32)
+    ex, cnt, top2 = g(inc, lead, R, 6)
+    assert ex.tolist() == [[5, 9, 9, 1]]
+    # stage 1 (tie with 2 at 9 -> lower index) counts r1:2 r2:2 r3:2 -> r1
+    # stage 2 counts r0:4 r3:2 -> r0
+    assert top2.tolist() == [[[1, 1], [2, 0]]]
+    # S = 1: the second pair is padding
+    ex, cnt, top2 = g(np.array([[3], [4]], dtype=np.int64), np.array([[2], [2]], dtype=np.int32), 3, 5)
+    assert top2.tolist() == [[[0, 2], [-1, -1]]]
+    # all-zero exposed: stages 0 and 1; leaders outside [0, R) are not counted
+    inc = np.zeros((3, 3), dtype=np.int64)
+    lead = np.array([[-1, 5, 0], [7, 1, 0], [-2, 1, 0]], dtype=np.int32)
+    ex, cnt, top2 = g(inc, lead, 2, 3)
+    assert cnt[0].tolist() == [[0, 0], [0, 2], [3, 0]]
+    assert top2.tolist() == [[[0, -1], [1, 1]]]
+    # the stall case routes to the data stage and the stalled rank
+    d = np.repeat(stall_case(), 10, axis=0)
+    d[5:, 0, 2] -= 30 * MS          # the stall on only half of the steps
+    d[5:, 2, [0, 1, 3]] -= 30 * MS
+    inc, lead = f(d)
+    ex, cnt, top2 = g(inc, lead, 4, 10)
+    # data: the stalled rank leads the 5 stalled steps; the 5 clean steps
+    # are four-way ties that go to rank 0
+    assert cnt[0, 0].tolist() == [5, 0, 5, 0]
+    assert ex[0, 0] == 5 * 50 * MS + 5 * 20 * MS
+    # bwd is a four-way tie on every step: never charged to the waiting ranks
+    assert cnt[0, 2].tolist() == [10, 0, 0, 0]
+    assert ex[0, 2] == 10 * 120 * MS
+
+
+def pin_summary_bruteforce(f, g):
+    """Every leader pattern of a tiny window set against bincount."""
+    R, S, T = 2, 2, 3
+    inc = np.arange(T * S, dtype=np.int64).reshape(T, S) * 3 + 1
+    for flat in itertools.product(range(R), repeat=T * S):
+        lead = np.array(flat, dtype=np.int32).reshape(T, S)
+        for window in (1, 2, 3):
+            ex, cnt, top2 = g(inc, lead, R, window)
+            for w in range(-(-T // window)):
+                t0, t1 = w * window, min((w + 1) * window, T)
+                c = _expected_counts(lead, R, t0, t1)
+                assert np.array_equal(cnt[w], c)
+                e = inc[t0:t1].sum(axis=0)
+                order = np.lexsort((np.arange(S), -e))
+                for k in range(2):
+                    sk = int(order[k])
+                    rk = int(np.argmax(c[sk])) if c[sk].max() > 0 else -1
+                    assert top2[w, k].tolist() == [sk, rk]
+
+
+def pin_summary_twin(f, g, pyref):
+    for d in random_cases(11):
+        small = d[:9]
+        T, S, R = small.shape
+        inc, lead = f(small)
+        for window in (2, 4, 9):
+            ex, cnt, top2 = g(inc, lead, R, window)
+            pe, pc, pt = pyref.window_summary(inc.tolist(), lead.tolist(), R, window)
+            assert ex.tolist() == pe and cnt.tolist() == pc and top2.tolist() == pt
+
+
+SUMMARY_PINS = [pin_summary_mass, pin_summary_top2, pin_summary_bruteforce]

@@ -1,0 +1,55 @@
+"""The oracle against facts that do not come from the oracle (CPU only)."""
+import numpy as np
+import pytest
+
+import oracle
+import pins
+
+
+@pytest.mark.parametrize("pin", pins.FRONTIER_PINS, ids=lambda p: p.__name__)
+def test_frontier_pin(pin):
+    pin(oracle.frontier)
+
+
+@pytest.mark.parametrize("pin", pins.SUMMARY_PINS, ids=lambda p: p.__name__)
+def test_summary_pin(pin):
+    pin(oracle.frontier, oracle.window_summary)
+
+
+def test_twin_frontier():
+    pins.pin_twin(oracle.frontier, oracle.pyref)
+
+
+def test_twin_summary():
+    pins.pin_summary_twin(oracle.frontier, oracle.window_summary, oracle.pyref)
+
+
+def test_pyref_against_pins():
+    """The pure-Python twin passes the same printed examples."""
+    def f(d):
+        inc, lead = oracle.pyref.frontier(np.asarray(d).tolist())
+        return np.array(inc, dtype=np.int64), np.array(lead, dtype=np.int32)
+    pins.pin_golden(f)
+    pins.pin_stall(f)
+
+
+def test_empty_and_degenerate():
+    inc, lead = oracle.frontier(np.zeros((0, 3, 4), dtype=np.int64))
+    assert inc.shape == (0, 3) and lead.shape == (0, 3)
+    ex, cnt, top2 = oracle.window_summary(inc, lead, 4, 10)
+    assert ex.shape == (0, 3) and cnt.shape == (0, 3, 4) and top2.shape == (0, 2, 2)
+    # all-zero durations: zero advances, every boundary a full tie -> rank 0
+    inc, lead = oracle.frontier(np.zeros((2, 3, 5), dtype=np.int64))
+    assert (inc == 0).all() and (lead == 0).all()
+
+
+def test_largest_prefix_is_exact():
+    """int64 arithmetic stays exact up to the documented prefix bound."""
+    big = (1 << 47) - 1
+    d = np.zeros((1, 3, 3), dtype=np.int64)
+    d[0, 0, 1] = big - 5
+    d[0, 2, 1] = 5
+    d[0, 1, 2] = big
+    inc, lead = oracle.frontier(d)
+    assert inc[0].tolist() == [big - 5, 5, 0]
+    assert lead[0].tolist() == [1, 2, 1]
