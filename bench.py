@@ -1,0 +1,236 @@
+"""Benchmark of the StageFrontier hot path on one MI355X.
+
+One step = one pass of the whole path over the workload's input, which is
+already resident in HBM: sf_frontier over every step-axis chunk, then
+sf_window_summary over all steps.  The default workload is the largest one
+(16384 ranks x 12 stages x 20000 steps, 31.5 GB of int64 durations, two
+chunks, windows of 1000 steps).
+
+Prints ONE JSON line with the throughput (rank-stage samples per second),
+the roofline of the dominant kernel (the frontier kernel, HBM bound), and the
+CPU oracle timed on the host on the same bytes.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "rank·stage samples/sec and achieved HBM GB/s (% of peak), bit-exact"
+UNIT = "rank·stage samples/s"
+PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E, AMD published peak
+DEFAULT_WORKLOAD = "r16384_s12_t20k"
+KERNEL_SRC = os.path.join(ROOT, "paper_2606_06751_amd", "csrc", "stagefrontier.hip")
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "k_frontier_%s_hbm_counters.txt")
+
+
+def log(msg: str) -> None:
+    print("[bench %s] %s" % (time.strftime("%H:%M:%S"), msg), file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per frontier launch from the committed counter summary, or
+    None when there is none or the kernel source changed since."""
+    path = PMC_SUMMARY % workload
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="budget of the CPU oracle baseline (0: skip)")
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="also run a plain 1 GiB copy kernel (for counter scaling)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        return 2
+
+    import torch
+
+    import synth
+    from paper_2606_06751_amd import stagefrontier as sf
+
+    wl = synth.WORKLOADS[args.workload]
+    T, S, R = wl.T, wl.S, wl.R
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    bounds = wl.chunk_bounds()
+
+    # ---- input: generated on the host chunk by chunk, copied into HBM
+    log("workload %s T=%d S=%d R=%d window=%d chunks=%d (%.2f GB)"
+        % (wl.name, T, S, R, wl.window, len(bounds), wl.input_bytes / 1e9))
+    d = torch.empty((T, S, R), dtype=torch.int64, device=dev)
+    # a pinned staging buffer of about 1 GB, refilled piece by piece
+    piece = max(1, min(T, (1 << 30) // (S * R * 8)))
+    host = torch.empty((piece, S, R), dtype=torch.int64, pin_memory=True)
+    host_np = host.numpy()
+    cpu_budget = args.cpu_seconds
+    oracle_steps, oracle_time, oracle_out = 0, 0.0, []
+    gen_time = h2d_time = 0.0
+    for t0 in range(0, T, piece):
+        t1 = min(T, t0 + piece)
+        n = t1 - t0
+        tg = time.perf_counter()
+        synth.generate(wl, t0, t1, out=host_np[:n])
+        gen_time += time.perf_counter() - tg
+        th = time.perf_counter()
+        d[t0:t1].copy_(host[:n])
+        torch.cuda.synchronize(dev)
+        h2d_time += time.perf_counter() - th
+        # CPU baseline: the oracle, single thread, on the same bytes, until
+        # its time budget is spent
+        if cpu_budget > 0 and oracle_time < cpu_budget:
+            import oracle
+            tc = time.perf_counter()
+            oi, ol = oracle.frontier(host_np[:n])
+            oracle_time += time.perf_counter() - tc
+            oracle_out.append((t0, oi, ol))
+            oracle_steps += n
+    log("input: generated in %.1f s, H2D %.2f GB in %.1f s, oracle %d steps in %.1f s"
+        % (gen_time, wl.input_bytes / 1e9, h2d_time, oracle_steps, oracle_time))
+    del host, host_np
+
+    inc = torch.empty((T, S), dtype=torch.int64, device=dev)
+    lead = torch.empty((T, S), dtype=torch.int32, device=dev)
+    W = sf.sf_num_windows(T, wl.window)
+    ex = torch.empty((W, S), dtype=torch.int64, device=dev)
+    cnt = torch.empty((W, S, R), dtype=torch.int32, device=dev)
+    top2 = torch.empty((W, 2, 2), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    views = [(d[t0:t1], inc[t0:t1], lead[t0:t1]) for t0, t1 in bounds]
+
+    def step():
+        for dv, iv, lv in views:
+            sf.sf_frontier(dv, iv, lv, stream=stream)
+        sf.sf_window_summary(inc, lead, R, wl.window, ex, cnt, top2, stream=stream)
+
+    if args.calibration_copy:
+        src = torch.ones(1 << 27, dtype=torch.int64, device=dev)   # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            torch.bitwise_not(src, out=dst)
+        torch.cuda.synchronize(dev)
+        del src, dst
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+
+    # ---- timed region: K steps; events on the stream the kernels run on
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    t_start = time.perf_counter()
+    for e0, e1, e2 in ev:
+        e0.record(stream)
+        for dv, iv, lv in views:
+            sf.sf_frontier(dv, iv, lv, stream=stream)
+        e1.record(stream)
+        sf.sf_window_summary(inc, lead, R, wl.window, ex, cnt, top2, stream=stream)
+        e2.record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t_start
+    ms_per_step = wall * 1e3 / args.steps
+    frontier_ms = [e0.elapsed_time(e1) for e0, e1, _ in ev]
+    summary_ms = [e1.elapsed_time(e2) for _, e1, e2 in ev]
+    launches = len(bounds)
+    frontier_launch_ms = float(np.mean(frontier_ms)) / launches
+
+    # ---- parity of the sampled steps against the oracle outputs
+    bit_exact = None
+    if oracle_out:
+        gi, gl = inc.cpu().numpy(), lead.cpu().numpy()
+        bit_exact = all(np.array_equal(gi[t:t + len(oi)], oi) and np.array_equal(gl[t:t + len(ol)], ol)
+                        for t, oi, ol in oracle_out)
+
+    samples = T * S * R
+    value = samples / (ms_per_step / 1e3)
+    step_bytes = 8 * samples + 12 * T * S + 12 * T * S + W * S * (8 + 4 * R) + 16 * W
+    # algorithmic bytes of one frontier launch: its chunk's durations read
+    # once, its increments and leaders written once
+    launch_bytes = (8 * samples + 12 * T * S) / launches
+    achieved = launch_bytes / (frontier_launch_ms / 1e3) / 1e9
+    traffic = measured_traffic(wl.name)
+    rec = {
+        "metric": METRIC,
+        "value": value,
+        "unit": UNIT,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "ranks": R, "stages": S, "steps_per_pass": T,
+                   "window": wl.window, "chunks": launches, "input_bytes": 8 * samples},
+        "hbm_gbps": step_bytes / (ms_per_step / 1e3) / 1e9,
+        "hbm_frac_of_peak": step_bytes / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBPS,
+        "bit_exact": bit_exact,
+        "roofline": {
+            "kernel": "k_frontier",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBPS,
+            "traffic": traffic,
+            "launch_ms": frontier_launch_ms,
+            "algorithmic_bytes_per_launch": launch_bytes,
+        },
+        "summary_kernels_ms": float(np.mean(summary_ms)),
+        "h2d_gbps_pcie_context": wl.input_bytes / h2d_time / 1e9,
+        "kernel_source_sha256_16": kernel_source_hash(),
+    }
+    if oracle_steps:
+        rec["cpu_baseline"] = {
+            "value": oracle_steps * S * R / oracle_time,
+            "unit": UNIT,
+            "cores": 1,
+            "kind": "oracle",
+            "sample": "sf_frontier oracle (single thread) on steps of the same workload: "
+                      "%d of %d steps, %.1f s" % (oracle_steps, T, oracle_time),
+        }
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -54,8 +54,9 @@ enum {
 /* Largest rank count: the leader is carried in 16 bits of a packed
  * (prefix, rank) key. */
 #define SF_MAX_R 65536
-/* Largest stage count per call. */
-#define SF_MAX_S 1024
+/* Largest stage count per call (per-stage partial maxima are staged in
+ * on-chip memory). */
+#define SF_MAX_S 512
 /* Every rank-local prefix P[t][r][s] must be below this many ns (about
  * 39 hours) so that the packed key fits in 64 bits. */
 #define SF_MAX_PREFIX_NS ((int64_t)1 << 47)
@@ -120,8 +121,10 @@ int64_t sf_num_windows(int64_t T, int64_t window);
  *                      the second pair is {-1, -1}.
  *   stream             HIP stream.
  *
- * The sums are exact in int64 as long as they do not overflow (they cannot
- * under the sf_frontier preconditions and W*window*SF_MAX_PREFIX_NS < 2^63).
+ * The sums are exact in int64 unless they overflow: a window total is at
+ * most window * max F, so any window below 65536 steps is exact at the
+ * prefix bound, and any window below 2^28 steps with step times under
+ * 2^35 ns (about 34 s).
  *
  * Returns SF_OK, SF_EINVAL or SF_EHIP.
  */

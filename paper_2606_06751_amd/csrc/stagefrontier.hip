@@ -1,0 +1,438 @@
+// stagefrontier.hip -- HIP kernels for gfx950 (MI355X) and the C ABI of
+// libstagefrontier: StageFrontier frontier accounting (Sec. 3, Eq. (1) and
+// Eq. (2); top-2 routing of Sec. 4).
+//
+// Data layout in HBM: durations [T][S][R] int64 (rank fastest), per-step
+// outputs [T][S], window outputs [W][S], [W][S][R] and [W][2][2].
+//
+// Frontier kernel.  Every step is independent (Sec. 3 streams one step at a
+// time), so the grid walks the step axis; inside a step, a group of G lanes
+// owns the step and each lane owns K ranks of a tile of G*K ranks.  The lane
+// keeps the running prefix of each of its ranks in registers as a packed key
+//     q = (P << 16) | (0xFFFF - r)
+// so that an unsigned 64-bit max over keys yields the largest prefix and, on
+// equal prefixes, the lowest rank.  Adding a duration shifted left by 16
+// advances P without touching the rank field, so the key is built once per
+// rank and then only added to.  Per stage, a lane takes the max of its K
+// keys, the group reduces with DPP lane moves (quad_perm, row mirrors,
+// row broadcasts: no LDS traffic), and the last lane of each 64-lane (or
+// smaller) sub-group stores the partial max in LDS.  After the last stage
+// the workgroup decodes F and the leader per (step, stage), takes the
+// advance F[s] - F[s-1] and writes [T][S] rows with contiguous stores.
+// Durations are read exactly once, with 16-byte loads when R is even.
+//
+// Window kernels.  One workgroup per (window, stage, rank chunk) builds the
+// leader histogram of the window in LDS with LDS atomics and sums the
+// advances; one workgroup per window then picks the two largest stages and
+// their most frequent leaders.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "stagefrontier.h"
+
+#define SF_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+typedef unsigned long long u64;
+typedef long long v2i64 __attribute__((ext_vector_type(2)));
+
+constexpr int kRankBits = 16;
+constexpr u64 kRankMask = 0xFFFFull;
+
+__device__ __forceinline__ u64 umax64(u64 a, u64 b) { return a > b ? a : b; }
+
+// One DPP lane move of a 64-bit value.  Lanes outside ROW_MASK, and lanes
+// whose source is out of range, keep their own value, which is neutral for
+// a max.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ u64 dpp_move(u64 v)
+{
+    const int lo = (int)(uint32_t)v;
+    const int hi = (int)(uint32_t)(v >> 32);
+    const uint32_t nlo = (uint32_t)__builtin_amdgcn_update_dpp(lo, lo, CTRL, ROW_MASK, 0xF, false);
+    const uint32_t nhi = (uint32_t)__builtin_amdgcn_update_dpp(hi, hi, CTRL, ROW_MASK, 0xF, false);
+    return ((u64)nhi << 32) | nlo;
+}
+
+// Max over aligned groups of SUB lanes (SUB a power of two <= 64).  The
+// result is valid in the last lane of each group (in every lane of the
+// group for SUB <= 16).
+template <int SUB>
+__device__ __forceinline__ u64 group_max(u64 v)
+{
+    if (SUB >= 2) v = umax64(v, dpp_move<0xB1, 0xF>(v));   // quad_perm [1,0,3,2]
+    if (SUB >= 4) v = umax64(v, dpp_move<0x4E, 0xF>(v));   // quad_perm [2,3,0,1]
+    if (SUB >= 8) v = umax64(v, dpp_move<0x141, 0xF>(v));  // row_half_mirror
+    if (SUB >= 16) v = umax64(v, dpp_move<0x140, 0xF>(v)); // row_mirror
+    if (SUB >= 32) v = umax64(v, dpp_move<0x142, 0xA>(v)); // row_bcast:15 -> rows 1, 3
+    if (SUB >= 64) v = umax64(v, dpp_move<0x143, 0xC>(v)); // row_bcast:31 -> rows 2, 3
+    return v;
+}
+
+// ---------------------------------------------------------------------------
+// frontier kernel
+
+// VEC: int64 elements per load (2: 16-byte loads, needs even R and a 16-byte
+//      aligned base); K: ranks per lane per tile; G: lanes per step;
+// WG:  threads per workgroup (WG / G steps per workgroup).
+template <int VEC, int K, int G, int WG>
+__global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, int64_t T,
+                                                 int R, int S, int64_t* __restrict__ inc,
+                                                 int32_t* __restrict__ lead)
+{
+    static_assert(K % VEC == 0, "K must be a multiple of VEC");
+    static_assert(WG % G == 0 || G == WG, "a workgroup holds whole steps");
+    constexpr int SUB = G < 64 ? G : 64;  // lanes per DPP reduction group
+    constexpr int SPW = WG / G;           // steps per workgroup
+    constexpr int SPS = G / SUB;          // LDS slots per step
+    constexpr int NLD = K / VEC;          // loads per lane per stage row
+    constexpr int RT = G * K;             // ranks per tile
+
+    extern __shared__ u64 tab[];          // [WG / SUB][S] partial maxima
+
+    const int tid = threadIdx.x;
+    const int gl = tid % G;
+    const int j = tid / G;
+    const int slot = tid / SUB;
+    const bool writer = (tid % SUB) == SUB - 1;
+    const int64_t t = (int64_t)blockIdx.x * SPW + j;
+
+    if (t < T) {  // uniform over the step group
+        const int64_t* dt = d + t * (int64_t)S * R;
+        for (int r0 = 0; r0 < R; r0 += RT) {
+            u64 q[K];
+            bool ok[NLD];
+#pragma unroll
+            for (int l = 0; l < NLD; ++l) {
+                const int r = r0 + (l * G + gl) * VEC;
+                ok[l] = r < R;
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    q[l * VEC + e] = ok[l] ? (kRankMask - (u64)(r + e)) : 0ull;
+            }
+            int64_t v[K];
+            auto load_row = [&](int s) {
+                const int64_t* row = dt + (int64_t)s * R + r0;
+                // A lane slot past R reads the tile's first rank instead (in
+                // bounds, no branch).  Its key starts with rank field 0, so it
+                // tracks that rank's prefix with a key strictly below the
+                // rank's own key and can never be the maximum.
+#pragma unroll
+                for (int l = 0; l < NLD; ++l) {
+                    const int idx = ok[l] ? (l * G + gl) * VEC : 0;
+                    if (VEC == 2) {
+                        const v2i64 x = __builtin_nontemporal_load(reinterpret_cast<const v2i64*>(row + idx));
+                        v[2 * l] = x.x;
+                        v[2 * l + 1] = x.y;
+                    } else {
+                        v[l] = __builtin_nontemporal_load(row + idx);
+                    }
+                }
+            };
+            load_row(0);
+            for (int s = 0; s < S; ++s) {
+                u64 m = 0;
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    q[k] += (u64)v[k] << kRankBits;
+                    m = umax64(m, q[k]);
+                }
+                if (s + 1 < S) load_row(s + 1);
+                m = group_max<SUB>(m);
+                if (writer) {
+                    u64* p = &tab[slot * S + s];
+                    *p = (r0 == 0) ? m : umax64(*p, m);
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    // decode F and the leader per (step, stage); rows of out are contiguous
+    const int64_t tb = (int64_t)blockIdx.x * SPW;
+    for (int i = tid; i < SPW * S; i += WG) {
+        const int jj = i / S;
+        const int s = i - jj * S;
+        const int64_t tt = tb + jj;
+        if (tt >= T) break;
+        u64 key = 0, kprev = 0;
+#pragma unroll
+        for (int qd = 0; qd < SPS; ++qd) {
+            key = umax64(key, tab[(jj * SPS + qd) * S + s]);
+            if (s > 0) kprev = umax64(kprev, tab[(jj * SPS + qd) * S + s - 1]);
+        }
+        const int64_t F = (int64_t)(key >> kRankBits);
+        const int64_t Fp = (int64_t)(kprev >> kRankBits);
+        inc[tt * S + s] = F - Fp;
+        lead[tt * S + s] = (int32_t)(kRankMask - (key & kRankMask));
+    }
+}
+
+typedef void (*frontier_fn)(const int64_t*, int64_t, int, int, int64_t*, int32_t*);
+
+struct FrontierVariant {
+    const void* fn;
+    int K, G, WG;
+};
+
+template <int VEC, int K, int G, int WG>
+FrontierVariant variant()
+{
+    return FrontierVariant{reinterpret_cast<const void*>(&k_frontier<VEC, K, G, WG>), K, G, WG};
+}
+
+// Launch shape by rank count: the tile G*K covers R (up to 4096 ranks) so
+// that each lane keeps K ranks in registers; larger R loops over tiles.
+template <int VEC>
+FrontierVariant pick_frontier(int R)
+{
+    if (R <= 8) return variant<VEC, 2, 4, 64>();
+    if (R <= 16) return variant<VEC, 2, 8, 128>();
+    if (R <= 32) return variant<VEC, 4, 8, 128>();
+    if (R <= 64) return variant<VEC, 4, 16, 256>();
+    if (R <= 128) return variant<VEC, 8, 16, 256>();
+    if (R <= 256) return variant<VEC, 8, 32, 256>();
+    if (R <= 512) return variant<VEC, 8, 64, 256>();
+    if (R <= 1024) return variant<VEC, 16, 64, 256>();
+    if (R <= 2048) return variant<VEC, 16, 128, 128>();
+    return variant<VEC, 16, 256, 256>();
+}
+
+// ---------------------------------------------------------------------------
+// window kernels
+
+constexpr int kHistChunk = 16384;  // ranks per histogram workgroup (64 KB LDS)
+constexpr int kSumWG = 256;
+
+__device__ __forceinline__ int64_t wave_sum64(int64_t v)
+{
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+// One workgroup per (window, stage, rank chunk); grid-stride over them.
+__global__ __launch_bounds__(kSumWG) void k_window_counts(
+    const int64_t* __restrict__ inc, const int32_t* __restrict__ lead, int64_t T, int R, int S,
+    int64_t window, int64_t W, int nchunk, int64_t* __restrict__ exposed,
+    int32_t* __restrict__ counts)
+{
+    extern __shared__ int32_t hist[];  // [min(R, kHistChunk)]
+    __shared__ int64_t part[kSumWG / 64];
+    const int tid = threadIdx.x;
+    const int64_t total = W * S * nchunk;
+    for (int64_t id = blockIdx.x; id < total; id += gridDim.x) {
+        const int c = (int)(id % nchunk);
+        const int64_t ws = id / nchunk;
+        const int s = (int)(ws % S);
+        const int64_t w = ws / S;
+        const int lo = c * kHistChunk;
+        const int n = min(kHistChunk, R - lo);
+        const int64_t t0 = w * window;
+        const int64_t t1 = min(t0 + window, T);
+
+        for (int i = tid; i < n; i += kSumWG) hist[i] = 0;
+        __syncthreads();
+        for (int64_t t = t0 + tid; t < t1; t += kSumWG) {
+            const int64_t r = (int64_t)lead[t * S + s] - lo;
+            if (r >= 0 && r < n) atomicAdd(&hist[r], 1);
+        }
+        if (c == 0) {
+            int64_t sum = 0;
+            for (int64_t t = t0 + tid; t < t1; t += kSumWG) sum += inc[t * S + s];
+            sum = wave_sum64(sum);
+            if ((tid & 63) == 0) part[tid >> 6] = sum;
+        }
+        __syncthreads();
+        if (c == 0 && tid == 0) {
+            int64_t sum = 0;
+            for (int i = 0; i < kSumWG / 64; ++i) sum += part[i];
+            exposed[w * S + s] = sum;
+        }
+        int32_t* out = counts + (w * S + s) * (int64_t)R + lo;
+        for (int i = tid; i < n; i += kSumWG) out[i] = hist[i];
+        __syncthreads();  // hist and part are reused by the next id
+    }
+}
+
+constexpr int kTopWG = 256;
+
+// Block-wide max of a 64-bit key; every thread gets the result.
+__device__ __forceinline__ u64 block_max64(u64 v, u64* sh)
+{
+    for (int off = 32; off > 0; off >>= 1) {
+        const u64 o = __shfl_xor(v, off, 64);
+        v = umax64(v, o);
+    }
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+    __syncthreads();
+    u64 r = sh[0];
+    for (int i = 1; i < kTopWG / 64; ++i) r = umax64(r, sh[i]);
+    __syncthreads();
+    return r;
+}
+
+// One workgroup per window; grid-stride.
+__global__ __launch_bounds__(kTopWG) void k_window_top2(const int64_t* __restrict__ exposed,
+                                                        const int32_t* __restrict__ counts,
+                                                        int R, int S, int64_t W,
+                                                        int32_t* __restrict__ top2)
+{
+    __shared__ u64 sh[kTopWG / 64];
+    const int tid = threadIdx.x;
+    for (int64_t w = blockIdx.x; w < W; w += gridDim.x) {
+        const int64_t* ex = exposed + w * S;
+        int pick[2] = {-1, -1};
+        for (int k = 0; k < 2; ++k) {
+            // order: larger exposed total first, then lower stage index
+            int64_t be = 0;
+            int bs = -1;
+            for (int s = tid; s < S; s += kTopWG) {
+                if (s == pick[0]) continue;
+                const int64_t e = ex[s];
+                if (bs < 0 || e > be) { be = e; bs = s; }
+            }
+            // reduce (be, bs) over the block in two passes: the largest total
+            // (sign bit flipped: order-preserving as unsigned), then the lowest
+            // stage among the threads that hold it.  Threads without a stage
+            // cannot win the second pass.
+            const u64 ekey = bs < 0 ? 0ull : ((u64)be ^ 0x8000000000000000ull);
+            const u64 emax = block_max64(ekey, sh);
+            const u64 skey = (bs >= 0 && ekey == emax) ? (u64)(0xFFFFFFFFu - (uint32_t)bs) + 1ull : 0ull;
+            const u64 smax = block_max64(skey, sh);
+            pick[k] = smax ? (int)(0xFFFFFFFFu - (uint32_t)(smax - 1ull)) : -1;
+        }
+        int rank[2] = {-1, -1};
+        for (int k = 0; k < 2; ++k) {
+            if (pick[k] < 0) continue;
+            const int32_t* c = counts + (w * S + pick[k]) * (int64_t)R;
+            u64 best = 0;
+            for (int r = tid; r < R; r += kTopWG)
+                best = umax64(best, ((u64)(uint32_t)c[r] << 32) | (u64)(0xFFFFFFFFu - (uint32_t)r));
+            const u64 m = block_max64(best, sh);
+            rank[k] = (m >> 32) ? (int)(0xFFFFFFFFu - (uint32_t)(m & 0xFFFFFFFFull)) : -1;
+        }
+        if (tid == 0) {
+            top2[w * 4 + 0] = pick[0];
+            top2[w * 4 + 1] = rank[0];
+            top2[w * 4 + 2] = pick[1];
+            top2[w * 4 + 3] = rank[1];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// host helpers
+
+bool disjoint(const void* a, int64_t na, const void* b, int64_t nb)
+{
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return x + (uintptr_t)na <= y || y + (uintptr_t)nb <= x;
+}
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+// true if n1 * n2 * n3 * bytes fits in int64
+bool fits(int64_t n1, int64_t n2, int64_t n3, int64_t bytes)
+{
+    const int64_t lim = INT64_MAX;
+    if (n1 == 0) return true;
+    return n1 <= lim / n2 / n3 / bytes;
+}
+
+int launch(const void* fn, dim3 grid, dim3 block, void** args, size_t lds, sf_stream_t stream)
+{
+    const hipError_t e = hipLaunchKernel(fn, grid, block, args, lds, (hipStream_t)stream);
+    return e == hipSuccess ? SF_OK : SF_EHIP;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+
+SF_API int sf_frontier(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                       int64_t* out_increment, int32_t* out_leader, sf_stream_t stream)
+{
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S) return SF_EINVAL;
+    if (!fits(T, S, R, 8)) return SF_EINVAL;
+    if (T == 0) return SF_OK;
+    if (!durations || !out_increment || !out_leader) return SF_EINVAL;
+    if (!aligned(durations, 8) || !aligned(out_increment, 8) || !aligned(out_leader, 4))
+        return SF_EINVAL;
+    const int64_t nd = T * S * (int64_t)R * 8, ni = T * S * 8, nl = T * S * 4;
+    if (!disjoint(durations, nd, out_increment, ni) || !disjoint(durations, nd, out_leader, nl) ||
+        !disjoint(out_increment, ni, out_leader, nl))
+        return SF_EINVAL;
+
+    const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
+    const FrontierVariant v = vec2 ? pick_frontier<2>(R) : pick_frontier<1>(R);
+    const int spw = v.WG / v.G;
+    const int sub = v.G < 64 ? v.G : 64;
+    const int64_t blocks = (T + spw - 1) / spw;
+    if (blocks > INT32_MAX) return SF_EINVAL;
+    const size_t lds = (size_t)(v.WG / sub) * S * sizeof(u64);
+    int Ri = R, Si = S;
+    void* args[] = {(void*)&durations, (void*)&T, (void*)&Ri, (void*)&Si, (void*)&out_increment,
+                    (void*)&out_leader};
+    return launch(v.fn, dim3((unsigned)blocks), dim3(v.WG), args, lds, stream);
+}
+
+SF_API int64_t sf_num_windows(int64_t T, int64_t window)
+{
+    if (T < 0 || window < 1) return -1;
+    return T / window + (T % window != 0);
+}
+
+SF_API int sf_window_summary(const int64_t* increment, const int32_t* leader, int64_t T,
+                             int32_t R, int32_t S, int64_t window, int64_t* out_stage_exposed,
+                             int32_t* out_lead_counts, int32_t* out_top2, sf_stream_t stream)
+{
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S || window < 1) return SF_EINVAL;
+    if (!fits(T, S, 1, 8)) return SF_EINVAL;
+    if (T == 0) return SF_OK;
+    const int64_t W = sf_num_windows(T, window);
+    if (!fits(W, S, R, 4)) return SF_EINVAL;
+    if (!increment || !leader || !out_stage_exposed || !out_lead_counts || !out_top2)
+        return SF_EINVAL;
+    if (!aligned(increment, 8) || !aligned(leader, 4) || !aligned(out_stage_exposed, 8) ||
+        !aligned(out_lead_counts, 4) || !aligned(out_top2, 4))
+        return SF_EINVAL;
+    const void* bufs[5] = {increment, leader, out_stage_exposed, out_lead_counts, out_top2};
+    const int64_t sizes[5] = {T * S * 8, T * S * 4, W * S * 8, W * S * (int64_t)R * 4, W * 16};
+    for (int a = 0; a < 5; ++a)
+        for (int b = (a < 2 ? 2 : a + 1); b < 5; ++b)
+            if (!disjoint(bufs[a], sizes[a], bufs[b], sizes[b])) return SF_EINVAL;
+
+    const int nchunk = (R + kHistChunk - 1) / kHistChunk;
+    const int64_t items = W * S * nchunk;
+    const unsigned g1 = (unsigned)(items < 1048576 ? items : 1048576);
+    const size_t lds = (size_t)(R < kHistChunk ? R : kHistChunk) * sizeof(int32_t);
+    int Ri = R, Si = S;
+    int64_t Wl = W;
+    void* a1[] = {(void*)&increment, (void*)&leader, (void*)&T, (void*)&Ri, (void*)&Si,
+                  (void*)&window, (void*)&Wl, (void*)&nchunk, (void*)&out_stage_exposed,
+                  (void*)&out_lead_counts};
+    int rc = launch(reinterpret_cast<const void*>(&k_window_counts), dim3(g1), dim3(kSumWG), a1,
+                    lds, stream);
+    if (rc != SF_OK) return rc;
+    const unsigned g2 = (unsigned)(W < 65536 ? W : 65536);
+    void* a2[] = {(void*)&out_stage_exposed, (void*)&out_lead_counts, (void*)&Ri, (void*)&Si,
+                  (void*)&Wl, (void*)&out_top2};
+    return launch(reinterpret_cast<const void*>(&k_window_top2), dim3(g2), dim3(kTopWG), a2, 0,
+                  stream);
+}
+
+SF_API const char* sf_strerror(int status)
+{
+    switch (status) {
+    case SF_OK: return "success";
+    case SF_EINVAL: return "invalid argument";
+    case SF_ERANGE: return "value out of range";
+    case SF_EHIP: return "HIP kernel launch failed";
+    default: return "unknown status";
+    }
+}
+
+SF_API const char* sf_version(void) { return "libstagefrontier 0.1.0 (gfx950)"; }

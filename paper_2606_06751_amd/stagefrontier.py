@@ -1,0 +1,150 @@
+"""Python binding of libstagefrontier (ctypes; argument marshalling only).
+
+Every function has the name of the C entry point it wraps (declared in
+``include/stagefrontier.h``).  Arrays are torch tensors on the GPU; torch is
+used for device memory and streams only, and every step of the computation
+runs in the library's HIP kernels.  There is no fallback: if the library is
+missing, importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # loaded first so that the library binds to torch's HIP runtime
+
+from . import build as _build
+
+SF_OK, SF_EINVAL, SF_ERANGE, SF_EHIP = 0, 1, 2, 3
+SF_MAX_R = 65536
+SF_MAX_S = 512
+SF_MAX_PREFIX_NS = 1 << 47
+
+LIB_PATH = _build.LIB
+
+
+class StageFrontierError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (where, sf_strerror(status), status))
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            "libstagefrontier.so is not built (expected at %s); run "
+            "`python -c 'import __graft_entry__ as g; g.build()'` first" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+    lib.sf_frontier.argtypes = [vp, i64, i32, i32, vp, vp, vp]
+    lib.sf_frontier.restype = ctypes.c_int
+    lib.sf_num_windows.argtypes = [i64, i64]
+    lib.sf_num_windows.restype = i64
+    lib.sf_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp]
+    lib.sf_window_summary.restype = ctypes.c_int
+    lib.sf_strerror.argtypes = [ctypes.c_int]
+    lib.sf_strerror.restype = ctypes.c_char_p
+    lib.sf_version.argtypes = []
+    lib.sf_version.restype = ctypes.c_char_p
+    return lib
+
+
+_lib = _load()
+
+
+def sf_strerror(status: int) -> str:
+    return _lib.sf_strerror(status).decode()
+
+
+def sf_version() -> str:
+    return _lib.sf_version().decode()
+
+
+def sf_num_windows(T: int, window: int) -> int:
+    return int(_lib.sf_num_windows(T, window))
+
+
+def _stream_handle(stream, device) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _check(t: torch.Tensor, name: str, dtype, shape):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if t.device.type != "cuda":
+        raise ValueError("%s must be a GPU tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
+
+
+def sf_frontier(durations: torch.Tensor, out_increment: torch.Tensor | None = None,
+                out_leader: torch.Tensor | None = None, stream=None):
+    """Frontier advances and leaders of every step (``sf_frontier``).
+
+    ``durations``: int64 GPU tensor [T, S, R] (ns).  Returns
+    ``(out_increment [T, S] int64, out_leader [T, S] int32)``, allocated
+    here when not given.  Asynchronous on ``stream`` (default: the current
+    torch stream of the tensor's device).
+    """
+    if durations.dim() != 3:
+        raise ValueError("durations must be [T, S, R]")
+    T, S, R = durations.shape
+    _check(durations, "durations", torch.int64, (T, S, R))
+    dev = durations.device
+    if out_increment is None:
+        out_increment = torch.empty((T, S), dtype=torch.int64, device=dev)
+    if out_leader is None:
+        out_leader = torch.empty((T, S), dtype=torch.int32, device=dev)
+    _check(out_increment, "out_increment", torch.int64, (T, S))
+    _check(out_leader, "out_leader", torch.int32, (T, S))
+    rc = _lib.sf_frontier(durations.data_ptr(), T, R, S, out_increment.data_ptr(),
+                          out_leader.data_ptr(), _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_frontier")
+    return out_increment, out_leader
+
+
+def sf_window_summary(increment: torch.Tensor, leader: torch.Tensor, R: int, window: int,
+                      out_stage_exposed: torch.Tensor | None = None,
+                      out_lead_counts: torch.Tensor | None = None,
+                      out_top2: torch.Tensor | None = None, stream=None):
+    """Window reduction of per-step results (``sf_window_summary``).
+
+    Returns ``(out_stage_exposed [W, S] int64, out_lead_counts [W, S, R]
+    int32, out_top2 [W, 2, 2] int32)``.
+    """
+    if increment.dim() != 2:
+        raise ValueError("increment must be [T, S]")
+    T, S = increment.shape
+    _check(increment, "increment", torch.int64, (T, S))
+    _check(leader, "leader", torch.int32, (T, S))
+    W = sf_num_windows(T, window)
+    if W < 0:
+        raise StageFrontierError(SF_EINVAL, "sf_window_summary")
+    dev = increment.device
+    if out_stage_exposed is None:
+        out_stage_exposed = torch.empty((W, S), dtype=torch.int64, device=dev)
+    if out_lead_counts is None:
+        out_lead_counts = torch.empty((W, S, R), dtype=torch.int32, device=dev)
+    if out_top2 is None:
+        out_top2 = torch.empty((W, 2, 2), dtype=torch.int32, device=dev)
+    _check(out_stage_exposed, "out_stage_exposed", torch.int64, (W, S))
+    _check(out_lead_counts, "out_lead_counts", torch.int32, (W, S, R))
+    _check(out_top2, "out_top2", torch.int32, (W, 2, 2))
+    rc = _lib.sf_window_summary(increment.data_ptr(), leader.data_ptr(), T, R, S, window,
+                                out_stage_exposed.data_ptr(), out_lead_counts.data_ptr(),
+                                out_top2.data_ptr(), _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_window_summary")
+    return out_stage_exposed, out_lead_counts, out_top2
+
+
+def raw_library() -> ctypes.CDLL:
+    """The loaded ctypes library, for callers that pass raw device pointers."""
+    return _lib

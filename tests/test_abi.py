@@ -1,0 +1,135 @@
+"""The C-ABI library loads, exports every declared entry point, and rejects
+bad arguments on the host before any device work (CPU only: no call here
+reaches a kernel)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "stagefrontier.h")
+
+
+def declared_functions():
+    with open(HEADER) as fh:
+        text = fh.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sf_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def sf():
+    import torch  # noqa: F401  (binding order: torch's HIP runtime first)
+    from paper_2606_06751_amd import stagefrontier
+    return stagefrontier
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == ["sf_frontier", "sf_num_windows", "sf_strerror",
+                                    "sf_version", "sf_window_summary"]
+
+
+def test_every_declared_symbol_is_exported(sf):
+    lib = sf.raw_library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+        assert hasattr(sf, name), "binding lacks %s" % name
+
+
+def test_constants_match_header(sf):
+    with open(HEADER) as fh:
+        text = fh.read()
+    assert "#define SF_MAX_R %d" % sf.SF_MAX_R in text
+    assert "#define SF_MAX_S %d" % sf.SF_MAX_S in text
+    for name in ("SF_OK", "SF_EINVAL", "SF_ERANGE", "SF_EHIP"):
+        assert re.search(r"%s = %d" % (name, getattr(sf, name)), text), name
+
+
+def test_host_only_calls(sf):
+    assert sf.sf_version().startswith("libstagefrontier")
+    assert sf.sf_strerror(sf.SF_OK) == "success"
+    assert sf.sf_strerror(sf.SF_EINVAL) == "invalid argument"
+    assert sf.sf_strerror(12345) == "unknown status"
+    assert sf.sf_num_windows(0, 10) == 0
+    assert sf.sf_num_windows(1000, 100) == 10
+    assert sf.sf_num_windows(1001, 100) == 11
+    assert sf.sf_num_windows(5, 1) == 5
+    assert sf.sf_num_windows(-1, 1) == -1
+    assert sf.sf_num_windows(10, 0) == -1
+
+
+# fake, never-dereferenced device addresses for host-side validation
+A = 1 << 40
+B = 2 << 40
+C = 3 << 40
+
+
+def test_frontier_argument_checks(sf):
+    lib = sf.raw_library()
+    ok_args = dict(d=A, T=10, R=8, S=6, inc=B, lead=C)
+
+    def call(**kw):
+        a = dict(ok_args, **kw)
+        return lib.sf_frontier(a["d"], a["T"], a["R"], a["S"], a["inc"], a["lead"], None)
+
+    assert call(T=0, d=None, inc=None, lead=None) == sf.SF_OK   # empty input: no-op
+    assert call(T=-1) == sf.SF_EINVAL
+    assert call(R=0) == sf.SF_EINVAL
+    assert call(R=sf.SF_MAX_R + 1) == sf.SF_EINVAL
+    assert call(S=0) == sf.SF_EINVAL
+    assert call(S=sf.SF_MAX_S + 1) == sf.SF_EINVAL
+    assert call(d=None) == sf.SF_EINVAL
+    assert call(inc=None) == sf.SF_EINVAL
+    assert call(lead=None) == sf.SF_EINVAL
+    assert call(d=A + 4) == sf.SF_EINVAL          # misaligned int64
+    assert call(inc=B + 4) == sf.SF_EINVAL
+    assert call(lead=C + 2) == sf.SF_EINVAL
+    assert call(inc=A + 8) == sf.SF_EINVAL        # output overlaps input
+    assert call(lead=B + 16) == sf.SF_EINVAL      # outputs overlap
+    assert call(T=1 << 50, R=sf.SF_MAX_R, S=sf.SF_MAX_S) == sf.SF_EINVAL  # size overflow
+
+
+def test_summary_argument_checks(sf):
+    lib = sf.raw_library()
+    D = 4 << 40
+    E = 5 << 40
+    ok_args = dict(inc=A, lead=B, T=100, R=8, S=6, window=10, ex=C, cnt=D, top=E)
+
+    def call(**kw):
+        a = dict(ok_args, **kw)
+        return lib.sf_window_summary(a["inc"], a["lead"], a["T"], a["R"], a["S"], a["window"],
+                                     a["ex"], a["cnt"], a["top"], None)
+
+    assert call(T=0, inc=None, lead=None, ex=None, cnt=None, top=None) == sf.SF_OK
+    assert call(window=0) == sf.SF_EINVAL
+    assert call(T=-5) == sf.SF_EINVAL
+    assert call(R=0) == sf.SF_EINVAL
+    assert call(S=sf.SF_MAX_S + 1) == sf.SF_EINVAL
+    assert call(cnt=None) == sf.SF_EINVAL
+    assert call(top=E + 2) == sf.SF_EINVAL
+    assert call(ex=A + 8) == sf.SF_EINVAL         # output overlaps input
+    assert call(top=D + 4) == sf.SF_EINVAL        # outputs overlap
+
+
+def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
+    """The binding has no CPU fallback: a missing library is an ImportError."""
+    import importlib
+
+    import torch  # noqa: F401
+    from paper_2606_06751_amd import build as b
+    monkeypatch.setattr(b, "LIB", str(tmp_path / "missing.so"))
+    import paper_2606_06751_amd.stagefrontier as mod
+    try:
+        with pytest.raises(ImportError):
+            importlib.reload(mod)
+    finally:
+        monkeypatch.undo()
+        importlib.reload(mod)
+
+
+def test_ctypes_argtypes_cover_header(sf):
+    lib = sf.raw_library()
+    assert len(lib.sf_frontier.argtypes) == 7
+    assert len(lib.sf_window_summary.argtypes) == 10
+    assert lib.sf_num_windows.restype is ctypes.c_int64

@@ -1,0 +1,230 @@
+"""GPU path against the CPU oracle, element by element (bit-exact: every
+output is integer ns or an index).  Shapes sweep every launch variant of the
+frontier kernel (tile widths, 8- and 16-byte loads, several tiles per rank
+row, ragged rank and step counts), the window kernels (ragged last window,
+several rank chunks, leaders outside [0, R)), and the degenerate cases."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def sf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_06751_amd import stagefrontier
+    return stagefrontier
+
+
+DEV = "cuda:0"
+
+
+def gpu_frontier(sf, d: np.ndarray):
+    dd = torch.from_numpy(np.ascontiguousarray(d)).to(DEV)
+    inc, lead = sf.sf_frontier(dd)
+    torch.cuda.synchronize()
+    return inc.cpu().numpy(), lead.cpu().numpy()
+
+
+def gpu_summary(sf, inc: np.ndarray, lead: np.ndarray, R: int, window: int):
+    ti = torch.from_numpy(np.ascontiguousarray(inc)).to(DEV)
+    tl = torch.from_numpy(np.ascontiguousarray(lead)).to(DEV)
+    ex, cnt, top2 = sf.sf_window_summary(ti, tl, R, window)
+    torch.cuda.synchronize()
+    return ex.cpu().numpy(), cnt.cpu().numpy(), top2.cpu().numpy()
+
+
+def assert_frontier_equal(sf, d):
+    gi, gl = gpu_frontier(sf, d)
+    oi, ol = oracle.frontier(d)
+    np.testing.assert_array_equal(gi, oi)
+    np.testing.assert_array_equal(gl, ol)
+    return oi, ol
+
+
+def assert_summary_equal(sf, inc, lead, R, window):
+    ge, gc, gt = gpu_summary(sf, inc, lead, R, window)
+    oe, oc, ot = oracle.window_summary(inc, lead, R, window)
+    np.testing.assert_array_equal(ge, oe)
+    np.testing.assert_array_equal(gc, oc)
+    np.testing.assert_array_equal(gt, ot)
+
+
+# rank counts at and around every tile boundary of the launch table, odd
+# counts (8-byte loads), several tiles per row (R > 4096) and the maximum
+RANKS = [1, 2, 3, 7, 8, 9, 16, 17, 31, 32, 33, 63, 64, 65, 127, 128, 129, 255, 256, 257,
+         511, 512, 513, 1000, 1023, 1024, 1025, 2047, 2048, 2049, 4095, 4096, 4097,
+         8192, 12289, 16384]
+
+
+@pytest.mark.parametrize("R", RANKS)
+def test_frontier_rank_sweep(sf, R):
+    T = max(3, min(70, 200000 // (R * 6)))
+    for S, hi in [(6, 10**9), (5, 3)]:          # tie-free-ish and tie-heavy
+        d = synth.random_durations(T, S, R, seed=R * 31 + S, hi=hi)
+        print("case R=%d S=%d T=%d hi=%d" % (R, S, T, hi), flush=True)
+        assert_frontier_equal(sf, d)
+
+
+@pytest.mark.parametrize("S", [1, 2, 3, 12, 13, 64, 200, 512])
+def test_frontier_stage_sweep(sf, S):
+    for R in (8, 128, 1024, 5000):
+        T = max(2, min(40, 400000 // (R * S)))
+        d = synth.random_durations(T, S, R, seed=S * 7 + R, hi=10**6)
+        print("case R=%d S=%d T=%d" % (R, S, T), flush=True)
+        assert_frontier_equal(sf, d)
+
+
+@pytest.mark.parametrize("T", [1, 2, 3, 5, 15, 16, 17, 63, 65, 257])
+def test_frontier_ragged_steps(sf, T):
+    for R in (8, 24, 128, 300):
+        d = synth.random_durations(T, 6, R, seed=T * 13 + R, hi=50)
+        assert_frontier_equal(sf, d)
+
+
+def test_frontier_max_ranks(sf):
+    R = sf.SF_MAX_R
+    d = synth.random_durations(3, 4, R, seed=11, hi=2)   # heavy ties over 65536 ranks
+    d[1, :, R - 1] = 5                                   # last rank leads step 1
+    oi, ol = assert_frontier_equal(sf, d)
+    assert (ol[1] == R - 1).all()
+
+
+def test_frontier_all_zero_and_single_rank(sf):
+    d = np.zeros((9, 4, 300), dtype=np.int64)
+    gi, gl = gpu_frontier(sf, d)
+    assert (gi == 0).all() and (gl == 0).all()
+    d1 = synth.random_durations(50, 7, 1, seed=3)
+    gi, gl = gpu_frontier(sf, d1)
+    np.testing.assert_array_equal(gi, d1[:, :, 0])
+    assert (gl == 0).all()
+
+
+def test_frontier_large_values(sf):
+    """Prefixes close to the documented bound stay exact."""
+    big = sf.SF_MAX_PREFIX_NS - 1
+    d = np.zeros((2, 3, 130), dtype=np.int64)
+    d[0, 0, 77] = big - 5
+    d[0, 2, 77] = 5
+    d[1, 1, 129] = big
+    d[1, 0, 3] = big - 1
+    assert_frontier_equal(sf, d)
+
+
+def test_frontier_golden_examples(sf):
+    import pins
+    for name in pins.GOLDEN_FILES:
+        g = pins.load_golden(name)
+        gi, gl = gpu_frontier(sf, g["d"])
+        assert gi[0].tolist() == g["inc"] and gl[0].tolist() == g["lead"]
+    gi, gl = gpu_frontier(sf, pins.stall_case())
+    assert gl[0].tolist() == [2, 2, 0, 0, 0, 0]
+
+
+def test_frontier_misaligned_base_uses_narrow_loads(sf):
+    """A base that is 8- but not 16-byte aligned takes the 8-byte-load path."""
+    T, S, R = 20, 6, 256
+    d = synth.random_durations(T, S, R, seed=5, hi=1000)
+    flat = torch.zeros(T * S * R + 1, dtype=torch.int64, device=DEV)
+    flat[1:] = torch.from_numpy(d.reshape(-1)).to(DEV)
+    view = flat[1:].view(T, S, R)
+    assert view.data_ptr() % 16 == 8
+    inc, lead = sf.sf_frontier(view)
+    torch.cuda.synchronize()
+    oi, ol = oracle.frontier(d)
+    np.testing.assert_array_equal(inc.cpu().numpy(), oi)
+    np.testing.assert_array_equal(lead.cpu().numpy(), ol)
+
+
+def test_frontier_chunks_compose(sf):
+    """Step-axis chunks written into one output equal a single call."""
+    T, S, R = 101, 12, 640
+    d = synth.random_durations(T, S, R, seed=17, hi=10**5)
+    dd = torch.from_numpy(d).to(DEV)
+    inc = torch.full((T, S), -7, dtype=torch.int64, device=DEV)
+    lead = torch.full((T, S), -7, dtype=torch.int32, device=DEV)
+    for t0, t1 in [(0, 37), (37, 38), (38, 101)]:
+        sf.sf_frontier(dd[t0:t1], inc[t0:t1], lead[t0:t1])
+    torch.cuda.synchronize()
+    oi, ol = oracle.frontier(d)
+    np.testing.assert_array_equal(inc.cpu().numpy(), oi)
+    np.testing.assert_array_equal(lead.cpu().numpy(), ol)
+
+
+def test_frontier_empty(sf):
+    dd = torch.empty((0, 6, 8), dtype=torch.int64, device=DEV)
+    inc, lead = sf.sf_frontier(dd)
+    assert inc.shape == (0, 6)
+
+
+def test_frontier_repeatable(sf):
+    """Integer outputs of repeated runs are identical (no lane races)."""
+    d = synth.random_durations(64, 12, 4096, seed=23, hi=4)
+    dd = torch.from_numpy(d).to(DEV)
+    first = [x.clone() for x in sf.sf_frontier(dd)]
+    for _ in range(5):
+        again = sf.sf_frontier(dd)
+        assert all(torch.equal(a, b) for a, b in zip(first, again))
+
+
+@pytest.mark.parametrize("R,S,T,window", [
+    (8, 6, 1000, 100), (8, 6, 1001, 100), (3, 1, 17, 4), (128, 6, 3000, 1000),
+    (1024, 8, 1200, 500), (5, 13, 40, 1), (4096, 12, 600, 250), (16384, 12, 80, 7),
+    (20000, 3, 50, 50), (40000, 2, 30, 16), (65536, 2, 10, 3)])
+def test_summary_from_oracle_steps(sf, R, S, T, window):
+    """Window summary of seeded per-step arrays (hot leaders, ties)."""
+    rng = np.random.Generator(np.random.PCG64(R + S + T))
+    inc = rng.integers(0, 10**9, size=(T, S), dtype=np.int64)
+    # leaders concentrated on a few ranks so that counts and ties matter
+    hot = rng.integers(0, R, size=4)
+    lead = np.where(rng.random((T, S)) < 0.7, hot[rng.integers(0, 4, size=(T, S))],
+                    rng.integers(0, R, size=(T, S))).astype(np.int32)
+    print("case R=%d S=%d T=%d window=%d" % (R, S, T, window), flush=True)
+    assert_summary_equal(sf, inc, lead, R, window)
+
+
+def test_summary_ties_and_out_of_range_leaders(sf):
+    T, S, R = 60, 5, 9
+    inc = np.zeros((T, S), dtype=np.int64)
+    inc[:, 1] = 5
+    inc[:, 3] = 5                       # stages 1 and 3 tie on exposed
+    lead = np.tile(np.array([0, 4, 2, 7, 1], dtype=np.int32), (T, 1))
+    lead[::2, 1] = 6                    # ranks 4 and 6 tie on counts
+    lead[::3, 0] = -1                   # not counted
+    lead[::5, 2] = 9                    # == R: not counted
+    lead[1::7, 4] = np.iinfo(np.int32).min
+    for window in (1, 6, 7, 60, 61):
+        assert_summary_equal(sf, inc, lead, R, window)
+
+
+def test_end_to_end_small_workload(sf):
+    """sf_frontier then sf_window_summary, as the benchmark chains them."""
+    wl = synth.WORKLOADS["r8_s6_t1k"]
+    d = synth.generate(wl)
+    oi, ol = assert_frontier_equal(sf, d)
+    dd = torch.from_numpy(d).to(DEV)
+    inc, lead = sf.sf_frontier(dd)
+    ex, cnt, top2 = sf.sf_window_summary(inc, lead, wl.R, wl.window)
+    torch.cuda.synchronize()
+    oe, oc, ot = oracle.window_summary(oi, ol, wl.R, wl.window)
+    np.testing.assert_array_equal(ex.cpu().numpy(), oe)
+    np.testing.assert_array_equal(cnt.cpu().numpy(), oc)
+    np.testing.assert_array_equal(top2.cpu().numpy(), ot)
+
+
+def test_bad_arguments_raise(sf):
+    d = torch.zeros((4, 3, 8), dtype=torch.int32, device=DEV)
+    with pytest.raises(TypeError):
+        sf.sf_frontier(d)
+    with pytest.raises(ValueError):
+        sf.sf_frontier(torch.zeros((4, 3, 8), dtype=torch.int64))   # host tensor
+    dd = torch.zeros((4, 3, 8), dtype=torch.int64, device=DEV)
+    inc = torch.zeros((4, 3), dtype=torch.int64, device=DEV)
+    with pytest.raises(sf.StageFrontierError):
+        sf.sf_frontier(dd, inc, inc.view(torch.int32).view(-1)[:12].view(4, 3))  # overlap

@@ -1,0 +1,75 @@
+"""The five full-size workloads, run exactly as the benchmark runs them
+(the 16384-rank workload in two step-axis chunks), against the oracle over
+every step and every window: bit-exact."""
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def sf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_06751_amd import stagefrontier
+    return stagefrontier
+
+
+def log(msg):
+    print("[%s] %s" % (time.strftime("%H:%M:%S"), msg), flush=True)
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workload_full_parity(sf, name):
+    wl = synth.WORKLOADS[name]
+    T, S, R = wl.T, wl.S, wl.R
+    dev = torch.device("cuda:0")
+    log("workload %s: T=%d S=%d R=%d window=%d chunks=%d (%.2f GB)"
+        % (name, T, S, R, wl.window, wl.chunks, wl.input_bytes / 1e9))
+    d = torch.empty((T, S, R), dtype=torch.int64, device=dev)
+    oi = np.empty((T, S), dtype=np.int64)
+    ol = np.empty((T, S), dtype=np.int32)
+    bounds = wl.chunk_bounds()
+    buf = np.empty((max(t1 - t0 for t0, t1 in bounds), S, R), dtype=np.int64)
+    for t0, t1 in bounds:
+        x = buf[: t1 - t0]
+        synth.generate(wl, t0, t1, out=x)
+        d[t0:t1].copy_(torch.from_numpy(x))
+        oi[t0:t1], ol[t0:t1] = oracle.frontier(x)
+        log("chunk [%d, %d) generated, copied, oracle done" % (t0, t1))
+    del buf
+    oe, oc, ot = oracle.window_summary(oi, ol, R, wl.window)
+
+    inc = torch.empty((T, S), dtype=torch.int64, device=dev)
+    lead = torch.empty((T, S), dtype=torch.int32, device=dev)
+    for t0, t1 in bounds:
+        sf.sf_frontier(d[t0:t1], inc[t0:t1], lead[t0:t1])
+    ex, cnt, top2 = sf.sf_window_summary(inc, lead, R, wl.window)
+    torch.cuda.synchronize()
+    log("gpu done")
+    np.testing.assert_array_equal(inc.cpu().numpy(), oi)
+    np.testing.assert_array_equal(lead.cpu().numpy(), ol)
+    np.testing.assert_array_equal(ex.cpu().numpy(), oe)
+    np.testing.assert_array_equal(cnt.cpu().numpy(), oc)
+    np.testing.assert_array_equal(top2.cpu().numpy(), ot)
+    # the workloads exercise what they are meant to: ties at the frontier
+    # in the tie workload, leaders spread over ranks in the others
+    if wl.tie_frac:
+        P_ties = 0
+        for t, kind, (s, r1, r2, _) in synth.injections(wl)[:50]:
+            x = synth.generate(wl, t, t + 1)[0]
+            P = x[: s + 1].sum(axis=0)
+            if P[r1] == P[r2] == P.max():
+                assert ol[t, s] == min(r1, r2)
+                P_ties += 1
+        assert P_ties > 10
+    log("parity ok: %s" % name)
+    del d, inc, lead, ex, cnt, top2
+    torch.cuda.empty_cache()
