@@ -178,6 +178,20 @@ def main() -> int:
         bit_exact = all(np.array_equal(gi[t:t + len(oi)], oi) and np.array_equal(gl[t:t + len(ol)], ol)
                         for t, oi, ol in oracle_out)
 
+    # context: what a library read-reduction (torch.sum over the first
+    # chunk's int64 durations) reaches on this device
+    t0, t1 = bounds[0]
+    rd = []
+    for _ in range(3):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        torch.sum(d[t0:t1])
+        b.record(stream)
+        rd.append((a, b))
+    torch.cuda.synchronize(dev)
+    read_ms = min(a.elapsed_time(b) for a, b in rd)
+    read_ceiling = (t1 - t0) * S * R * 8 / (read_ms / 1e3) / 1e9
+
     samples = T * S * R
     value = samples / (ms_per_step / 1e3)
     step_bytes = 8 * samples + 12 * T * S + 12 * T * S + W * S * (8 + 4 * R) + 16 * W
@@ -216,6 +230,7 @@ def main() -> int:
             "algorithmic_bytes_per_launch": launch_bytes,
         },
         "summary_kernels_ms": float(np.mean(summary_ms)),
+        "read_ceiling_gbps_torch_sum": read_ceiling,
         "h2d_gbps_pcie_context": wl.input_bytes / h2d_time / 1e9,
         "kernel_source_sha256_16": kernel_source_hash(),
     }
