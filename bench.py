@@ -178,8 +178,8 @@ def main() -> int:
         bit_exact = all(np.array_equal(gi[t:t + len(oi)], oi) and np.array_equal(gl[t:t + len(ol)], ol)
                         for t, oi, ol in oracle_out)
 
-    # context: what a library read-reduction (torch.sum over the first
-    # chunk's int64 durations) reaches on this device
+    # context: the read rate of a library reduction (torch.sum) over the
+    # first chunk's int64 durations on this device
     t0, t1 = bounds[0]
     rd = []
     for _ in range(3):
@@ -230,7 +230,7 @@ def main() -> int:
             "algorithmic_bytes_per_launch": launch_bytes,
         },
         "summary_kernels_ms": float(np.mean(summary_ms)),
-        "read_ceiling_gbps_torch_sum": read_ceiling,
+        "torch_sum_read_gbps": read_ceiling,
         "h2d_gbps_pcie_context": wl.input_bytes / h2d_time / 1e9,
         "kernel_source_sha256_16": kernel_source_hash(),
     }

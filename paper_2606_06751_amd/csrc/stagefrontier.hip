@@ -170,34 +170,51 @@ __global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, 
     }
 }
 
-typedef void (*frontier_fn)(const int64_t*, int64_t, int, int, int64_t*, int32_t*);
-
 struct FrontierVariant {
     const void* fn;
     int K, G, WG;
+    int per_cu;  // resident workgroups per CU to allow (0: no cap)
 };
 
 template <int VEC, int K, int G, int WG>
-FrontierVariant variant()
+FrontierVariant variant(int per_cu)
 {
-    return FrontierVariant{reinterpret_cast<const void*>(&k_frontier<VEC, K, G, WG>), K, G, WG};
+    return FrontierVariant{reinterpret_cast<const void*>(&k_frontier<VEC, K, G, WG>), K, G, WG,
+                           per_cu};
 }
 
-// Launch shape by rank count: the tile G*K covers R (up to 4096 ranks) so
-// that each lane keeps K ranks in registers; larger R loops over tiles.
+// Launch shape by rank count, measured on MI355X over R = 16 .. 16384.
+// Wide per-lane tiles (K = 32 ranks, about 250 VGPRs) and few resident
+// workgroups per CU read HBM fastest for large R: fewer concurrent step
+// streams, each with up to 32 KB of loads in flight per wave.  A tile wider
+// than R costs no HBM traffic (lane slots past R re-read a cached rank).
 template <int VEC>
 FrontierVariant pick_frontier(int R)
 {
-    if (R <= 8) return variant<VEC, 2, 4, 64>();
-    if (R <= 16) return variant<VEC, 2, 8, 128>();
-    if (R <= 32) return variant<VEC, 4, 8, 128>();
-    if (R <= 64) return variant<VEC, 4, 16, 256>();
-    if (R <= 128) return variant<VEC, 8, 16, 256>();
-    if (R <= 256) return variant<VEC, 8, 32, 256>();
-    if (R <= 512) return variant<VEC, 8, 64, 256>();
-    if (R <= 1024) return variant<VEC, 16, 64, 256>();
-    if (R <= 2048) return variant<VEC, 16, 128, 128>();
-    return variant<VEC, 16, 256, 256>();
+    if (R <= 8) return variant<VEC, 2, 4, 64>(0);
+    if (R <= 16) return variant<VEC, 2, 8, 128>(0);
+    if (R <= 32) return variant<VEC, 4, 8, 128>(0);
+    if (R <= 64) return variant<VEC, 4, 16, 256>(6);
+    if (R <= 128) return variant<VEC, 8, 32, 256>(6);
+    if (R <= 256) return variant<VEC, 16, 32, 256>(4);
+    if (R <= 512) return variant<VEC, 4, 256, 256>(0);
+    if (R <= 1024) return variant<VEC, 32, 64, 256>(6);
+    if (R <= 2048) return variant<VEC, 8, 512, 512>(0);
+    if (R <= 4096) return variant<VEC, 32, 256, 256>(0);
+    return variant<VEC, 32, 64, 64>(3);
+}
+
+// LDS on one gfx950 CU.  Asking for LDS_PER_CU / n bytes per workgroup caps
+// residency at n workgroups per CU.
+constexpr size_t kLdsPerCu = 160 * 1024;
+constexpr size_t kLdsMaxPerWg = 64 * 1024;
+
+size_t lds_request(size_t need, int per_cu)
+{
+    if (per_cu <= 0) return need;
+    size_t cap = (kLdsPerCu / (size_t)per_cu) & ~(size_t)1023;
+    if (cap > kLdsMaxPerWg) cap = kLdsMaxPerWg;
+    return need > cap ? need : cap;
 }
 
 // ---------------------------------------------------------------------------
@@ -273,7 +290,35 @@ __device__ __forceinline__ u64 block_max64(u64 v, u64* sh)
     return r;
 }
 
-// One workgroup per window; grid-stride.
+// Largest lead count of one counts row as a packed (count, lowest rank) key;
+// every thread gets the block result.
+__device__ __forceinline__ u64 row_modal_key(const int32_t* __restrict__ c, int R, u64* sh)
+{
+    const int tid = threadIdx.x;
+    u64 b0 = 0, b1 = 0, b2 = 0, b3 = 0;
+    auto key = [](int32_t cnt, int r) {
+        return ((u64)(uint32_t)cnt << 32) | (u64)(0xFFFFFFFFu - (uint32_t)r);
+    };
+    if ((R & 3) == 0 && (((uintptr_t)c) & 15) == 0) {
+        const int4* c4 = reinterpret_cast<const int4*>(c);
+        const int n4 = R >> 2;
+        for (int i = tid; i < n4; i += kTopWG) {
+            const int4 x = c4[i];
+            const int r = i << 2;
+            b0 = umax64(b0, key(x.x, r));
+            b1 = umax64(b1, key(x.y, r + 1));
+            b2 = umax64(b2, key(x.z, r + 2));
+            b3 = umax64(b3, key(x.w, r + 3));
+        }
+    } else {
+        for (int r = tid; r < R; r += kTopWG) b0 = umax64(b0, key(c[r], r));
+    }
+    return block_max64(umax64(umax64(b0, b1), umax64(b2, b3)), sh);
+}
+
+// One workgroup per (window, pick k in {0, 1}); grid-stride.  Both
+// workgroups of a window choose the two stages (cheap: S <= SF_MAX_S); each
+// then finds the most frequent leader of its own stage.
 __global__ __launch_bounds__(kTopWG) void k_window_top2(const int64_t* __restrict__ exposed,
                                                         const int32_t* __restrict__ counts,
                                                         int R, int S, int64_t W,
@@ -281,43 +326,38 @@ __global__ __launch_bounds__(kTopWG) void k_window_top2(const int64_t* __restric
 {
     __shared__ u64 sh[kTopWG / 64];
     const int tid = threadIdx.x;
-    for (int64_t w = blockIdx.x; w < W; w += gridDim.x) {
+    for (int64_t id = blockIdx.x; id < 2 * W; id += gridDim.x) {
+        const int64_t w = id >> 1;
+        const int k = (int)(id & 1);
         const int64_t* ex = exposed + w * S;
-        int pick[2] = {-1, -1};
-        for (int k = 0; k < 2; ++k) {
-            // order: larger exposed total first, then lower stage index
+        int pick0 = -1, pick = -1;
+        for (int kk = 0; kk <= k; ++kk) {
+            // larger exposed total first, then lower stage index
             int64_t be = 0;
             int bs = -1;
             for (int s = tid; s < S; s += kTopWG) {
-                if (s == pick[0]) continue;
+                if (s == pick0) continue;
                 const int64_t e = ex[s];
                 if (bs < 0 || e > be) { be = e; bs = s; }
             }
-            // reduce (be, bs) over the block in two passes: the largest total
-            // (sign bit flipped: order-preserving as unsigned), then the lowest
-            // stage among the threads that hold it.  Threads without a stage
-            // cannot win the second pass.
+            // two block maxima: the largest total (sign bit flipped, so that
+            // unsigned order is signed order), then the lowest stage among
+            // the threads holding it; threads without a stage cannot win
             const u64 ekey = bs < 0 ? 0ull : ((u64)be ^ 0x8000000000000000ull);
             const u64 emax = block_max64(ekey, sh);
             const u64 skey = (bs >= 0 && ekey == emax) ? (u64)(0xFFFFFFFFu - (uint32_t)bs) + 1ull : 0ull;
             const u64 smax = block_max64(skey, sh);
-            pick[k] = smax ? (int)(0xFFFFFFFFu - (uint32_t)(smax - 1ull)) : -1;
+            pick = smax ? (int)(0xFFFFFFFFu - (uint32_t)(smax - 1ull)) : -1;
+            pick0 = pick;
         }
-        int rank[2] = {-1, -1};
-        for (int k = 0; k < 2; ++k) {
-            if (pick[k] < 0) continue;
-            const int32_t* c = counts + (w * S + pick[k]) * (int64_t)R;
-            u64 best = 0;
-            for (int r = tid; r < R; r += kTopWG)
-                best = umax64(best, ((u64)(uint32_t)c[r] << 32) | (u64)(0xFFFFFFFFu - (uint32_t)r));
-            const u64 m = block_max64(best, sh);
-            rank[k] = (m >> 32) ? (int)(0xFFFFFFFFu - (uint32_t)(m & 0xFFFFFFFFull)) : -1;
+        int rank = -1;
+        if (pick >= 0) {
+            const u64 m = row_modal_key(counts + (w * S + pick) * (int64_t)R, R, sh);
+            rank = (m >> 32) ? (int)(0xFFFFFFFFu - (uint32_t)(m & 0xFFFFFFFFull)) : -1;
         }
         if (tid == 0) {
-            top2[w * 4 + 0] = pick[0];
-            top2[w * 4 + 1] = rank[0];
-            top2[w * 4 + 2] = pick[1];
-            top2[w * 4 + 3] = rank[1];
+            top2[w * 4 + 2 * k] = pick;
+            top2[w * 4 + 2 * k + 1] = rank;
         }
     }
 }
@@ -372,7 +412,7 @@ SF_API int sf_frontier(const int64_t* durations, int64_t T, int32_t R, int32_t S
     const int sub = v.G < 64 ? v.G : 64;
     const int64_t blocks = (T + spw - 1) / spw;
     if (blocks > INT32_MAX) return SF_EINVAL;
-    const size_t lds = (size_t)(v.WG / sub) * S * sizeof(u64);
+    const size_t lds = lds_request((size_t)(v.WG / sub) * S * sizeof(u64), v.per_cu);
     int Ri = R, Si = S;
     void* args[] = {(void*)&durations, (void*)&T, (void*)&Ri, (void*)&Si, (void*)&out_increment,
                     (void*)&out_leader};
@@ -417,7 +457,7 @@ SF_API int sf_window_summary(const int64_t* increment, const int32_t* leader, in
     int rc = launch(reinterpret_cast<const void*>(&k_window_counts), dim3(g1), dim3(kSumWG), a1,
                     lds, stream);
     if (rc != SF_OK) return rc;
-    const unsigned g2 = (unsigned)(W < 65536 ? W : 65536);
+    const unsigned g2 = (unsigned)(2 * W < 65536 ? 2 * W : 65536);
     void* a2[] = {(void*)&out_stage_exposed, (void*)&out_lead_counts, (void*)&Ri, (void*)&Si,
                   (void*)&Wl, (void*)&out_top2};
     return launch(reinterpret_cast<const void*>(&k_window_top2), dim3(g2), dim3(kTopWG), a2, 0,
