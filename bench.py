@@ -37,9 +37,18 @@ def log(msg: str) -> None:
     print("[bench %s] %s" % (time.strftime("%H:%M:%S"), msg), file=sys.stderr, flush=True)
 
 
+# k_frontier and everything it depends on (includes, lane helpers, launch
+# table) precede this section header in the source; later sections hold
+# other kernels and the C ABI.
+FRONTIER_SECTION_END = b"// window kernels"
+
+
 def kernel_source_hash() -> str:
+    """Hash of the source text k_frontier is built from."""
     with open(KERNEL_SRC, "rb") as fh:
-        return hashlib.sha256(fh.read()).hexdigest()[:16]
+        text = fh.read()
+    cut = text.find(FRONTIER_SECTION_END)
+    return hashlib.sha256(text[:cut] if cut >= 0 else text).hexdigest()[:16]
 
 
 def measured_traffic(workload: str):

@@ -5,7 +5,8 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 the GPU path and the oracle share no code.
 
 Two independent statements of the same definitions (Sec. 3, Eq. (1) and
-Eq. (2); top-2 routing of Sec. 4):
+Eq. (2); top-2 routing and the localization evidence of Sec. 4; the
+per-stage baselines of Props. 1-2):
 
 * ``frontier`` / ``window_summary`` -- plain C nested loops in
   ``sf_oracle.c`` (fast enough for the full workloads on sampled steps),
@@ -48,6 +49,8 @@ class COracle:
         lib.sfo_frontier.restype = ctypes.c_int
         lib.sfo_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp]
         lib.sfo_window_summary.restype = None
+        lib.sfo_frontier_evidence.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp]
+        lib.sfo_frontier_evidence.restype = ctypes.c_int
         self.lib = lib
         self.path = path
 
@@ -69,6 +72,27 @@ class COracle:
             if rc != 0:
                 raise MemoryError("oracle prefix scratch allocation failed")
         return inc, lead
+
+    def frontier_evidence(self, d: np.ndarray):
+        """Eq. (1) plus the localization evidence of Sec. 4 and the
+        per-stage baselines of Props. 1-2, for every boundary.
+
+        Returns a dict of [T, S] arrays: ``inc``, ``lead``, ``gap`` (int64),
+        ``ties`` (int32), ``stage_max``, ``stage_sum`` (int64).
+        """
+        d = np.ascontiguousarray(d, dtype=np.int64)
+        if d.ndim != 3:
+            raise ValueError("durations must be [T, S, R]")
+        T, S, R = d.shape
+        out = {k: np.empty((T, S), dtype=np.int32 if k in ("lead", "ties") else np.int64)
+               for k in ("inc", "lead", "gap", "ties", "stage_max", "stage_sum")}
+        if T and S and R:
+            rc = self.lib.sfo_frontier_evidence(
+                d.ctypes.data, T, R, S, *(out[k].ctypes.data for k in
+                                          ("inc", "lead", "gap", "ties", "stage_max", "stage_sum")))
+            if rc != 0:
+                raise MemoryError("oracle prefix scratch allocation failed")
+        return out
 
     def window_summary(self, inc: np.ndarray, lead: np.ndarray, R: int, window: int):
         """Window reduction of per-step results.
@@ -114,6 +138,11 @@ def window_summary(inc: np.ndarray, lead: np.ndarray, R: int, window: int):
     return _get().window_summary(inc, lead, R, window)
 
 
+def frontier_evidence(d: np.ndarray):
+    return _get().frontier_evidence(d)
+
+
 from . import pyref  # noqa: E402  (pure-Python twin, no compiled code)
 
-__all__ = ["build", "COracle", "frontier", "window_summary", "num_windows", "pyref"]
+__all__ = ["build", "COracle", "frontier", "frontier_evidence", "window_summary",
+           "num_windows", "pyref"]

@@ -54,3 +54,30 @@ def window_summary(inc, lead, R, window):
         counts.append(c_w)
         top2.append(t2)
     return exposed, counts, top2
+
+
+def frontier_evidence(d):
+    """``d[t][s][r]`` -> dict of [t][s] lists: inc, lead, gap, ties,
+    stage_max, stage_sum (same readings as the C oracle)."""
+    out = {k: [] for k in ("inc", "lead", "gap", "ties", "stage_max", "stage_sum")}
+    for step in d:
+        S = len(step)
+        R = len(step[0])
+        P = [0] * R
+        F_prev = 0
+        rows = {k: [] for k in out}
+        for s in range(S):
+            P = [P[r] + step[s][r] for r in range(R)]
+            F = max(P)
+            leader = P.index(F)
+            others = sorted(P[:leader] + P[leader + 1:])
+            rows["inc"].append(F - F_prev)
+            rows["lead"].append(leader)
+            rows["gap"].append(F - others[-1] if others else -1)
+            rows["ties"].append(P.count(F))
+            rows["stage_max"].append(max(step[s]))
+            rows["stage_sum"].append(sum(step[s]))
+            F_prev = F
+        for k in out:
+            out[k].append(rows[k])
+    return out

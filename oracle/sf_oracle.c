@@ -17,6 +17,11 @@
  *   frontier is re-taken at every boundary.
  *   Sec. 3, Eq. (2):  the window share numerator sum_{t in window} a[t,s].
  *   Sec. 4: top-2 routing = the two stages with the highest shares.
+ *   Sec. 4, localization evidence: the tie set of the frontier and the gap
+ *   between the largest and the second-largest prefix at each boundary.
+ *   Sec. 3, Props. 1 and 2: the per-stage max and mean baselines
+ *   M_t = sum_s max_r d and Mbar_t = sum_s (1/R) sum_r d, kept per stage as
+ *   max_r d[t,r,s] and sum_r d[t,r,s].
  *
  * Readings where the paper leaves a choice open (each is listed with its
  * reason in the design notes of the repository):
@@ -27,7 +32,10 @@
  *     pairs each with its most frequent leader, lower rank on ties, -1 when
  *     that stage has no counted leader;
  *   - W = ceil(T / window); the last window may be shorter;
- *   - leaders outside [0, R) are not counted.
+ *   - leaders outside [0, R) are not counted;
+ *   - the gap is F minus the second-largest prefix over ranks (0 when two or
+ *     more ranks attain F); with R = 1 there is no runner-up and the gap
+ *     is -1.
  *
  * Layout: d is [T][S][R] (rank fastest), increments and leaders [T][S],
  * exposed [W][S], counts [W][S][R], top2 [W][2][2].
@@ -123,4 +131,59 @@ void sfo_window_summary(const int64_t* inc, const int32_t* lead,
             top2[w * 4 + 2 * k + 1] = rk;
         }
     }
+}
+
+/* Localization evidence and per-stage baselines of every boundary, with the
+ * frontier advances and leaders of sfo_frontier.  Returns 0, or -1 if the
+ * prefix scratch cannot be allocated. */
+int sfo_frontier_evidence(const int64_t* d, int64_t T, int32_t R, int32_t S,
+                          int64_t* inc, int32_t* lead, int64_t* gap,
+                          int32_t* ties, int64_t* stage_max, int64_t* stage_sum)
+{
+    int64_t* P = (int64_t*)malloc(sizeof(int64_t) * (size_t)(R > 0 ? R : 1));
+    if (!P) return -1;
+    for (int64_t t = 0; t < T; ++t) {
+        for (int32_t r = 0; r < R; ++r) P[r] = 0;
+        int64_t F_prev = 0;
+        for (int32_t s = 0; s < S; ++s) {
+            const int64_t* row = d + (t * S + s) * (int64_t)R;
+            int64_t dmax = row[0], dsum = 0;
+            for (int32_t r = 0; r < R; ++r) {
+                P[r] += row[r];
+                if (row[r] > dmax) dmax = row[r];
+                dsum += row[r];
+            }
+            /* frontier and lowest leader */
+            int64_t F = P[0];
+            int32_t L = 0;
+            for (int32_t r = 1; r < R; ++r) {
+                if (P[r] > F) {
+                    F = P[r];
+                    L = r;
+                }
+            }
+            /* tie set size and runner-up: the largest prefix of any rank
+             * other than the leader */
+            int32_t n_tie = 0;
+            int64_t second = 0;
+            int have_second = 0;
+            for (int32_t r = 0; r < R; ++r) {
+                if (P[r] == F) n_tie += 1;
+                if (r != L && (!have_second || P[r] > second)) {
+                    second = P[r];
+                    have_second = 1;
+                }
+            }
+            const int64_t i = t * S + s;
+            inc[i] = F - F_prev;
+            lead[i] = L;
+            gap[i] = have_second ? F - second : -1;
+            ties[i] = n_tie;
+            stage_max[i] = dmax;
+            stage_sum[i] = dsum;
+            F_prev = F;
+        }
+    }
+    free(P);
+    return 0;
 }

@@ -415,3 +415,117 @@ def pin_summary_twin(f, g, pyref):
 
 
 SUMMARY_PINS = [pin_summary_mass, pin_summary_top2, pin_summary_bruteforce]
+
+
+# ----------------------------------------------------------------------------
+# localization evidence and per-stage baselines (Sec. 4; Props. 1-2)
+#
+# Each pin takes ``e(d) -> dict`` with [T, S] arrays inc, lead, gap, ties,
+# stage_max, stage_sum.
+
+
+def _as_frontier(e):
+    def f(d):
+        out = e(d)
+        return out["inc"], out["lead"]
+    return f
+
+
+def pin_ev_frontier_part(e):
+    """The frontier part of the evidence pass meets every frontier pin."""
+    f = _as_frontier(e)
+    for pin in FRONTIER_PINS:
+        pin(f)
+
+
+def pin_ev_golden(e):
+    g = load_golden("motivating_example.txt")
+    out = e(g["d"])
+    assert out["stage_max"][0].tolist() == g["stage_max"]
+    assert int(out["stage_max"][0].sum()) == g["stage_max_total"][0]
+
+
+def pin_ev_stall(e):
+    """The Sec. 2 pattern: a 30 ms margin at data and fwd, then a four-way
+    tie; the per-stage max of bwd counts the wait (150 ms)."""
+    out = e(stall_case())
+    assert out["gap"][0].tolist() == [30 * MS, 30 * MS, 0, 0, 0, 0]
+    assert out["ties"][0].tolist() == [1, 1, 4, 4, 4, 4]
+    assert out["stage_max"][0].tolist() == [50 * MS, 60 * MS, 150 * MS, 2 * MS, 15 * MS, 3 * MS]
+    assert out["stage_sum"][0].tolist() == [110 * MS, 240 * MS, 570 * MS, 8 * MS, 60 * MS, 12 * MS]
+
+
+def pin_ev_bruteforce(e):
+    """Every d in {0,1,2}^(S x R) for four small shapes: prefixes summed
+    from scratch, sorted; the gap is the difference of the two largest, the
+    tie count the multiplicity of the largest."""
+    for (R, S) in [(2, 2), (2, 3), (3, 2), (3, 3)]:
+        cases = list(itertools.product(range(3), repeat=R * S))
+        d = np.array(cases, dtype=np.int64).reshape(len(cases), S, R)
+        out = e(d)
+        for i, flat in enumerate(cases):
+            case = [list(flat[s * R:(s + 1) * R]) for s in range(S)]
+            for s in range(S):
+                sums = sorted((sum(case[j][r] for j in range(s + 1)) for r in range(R)), reverse=True)
+                assert out["gap"][i, s] == sums[0] - sums[1], (case, s)
+                assert out["ties"][i, s] == sums.count(sums[0]), (case, s)
+                assert out["stage_max"][i, s] == max(case[s])
+                assert out["stage_sum"][i, s] == sum(case[s])
+
+
+def pin_ev_props(e):
+    """Props. 1 and 2 on the baselines this pass reports, with the tight
+    constructions of Appendix D."""
+    for d in random_cases(12):
+        out = e(d)
+        T, S, R = d.shape
+        F = out["inc"].sum(axis=1)
+        M = out["stage_max"].sum(axis=1)
+        tot = out["stage_sum"].sum(axis=1)                     # = R * Mbar
+        assert (F <= M).all() and (M <= min(R, S) * F).all()
+        assert (F <= tot).all() and (tot <= R * F).all()
+        assert np.array_equal(out["stage_sum"], d.sum(axis=2))    # library sum
+        assert np.array_equal(out["stage_max"], d.max(axis=2))    # library max
+    for R, S in [(3, 5), (6, 4)]:
+        d = np.zeros((1, S, R), dtype=np.int64)
+        for k in range(min(R, S)):
+            d[0, k, k] = 9 * MS
+        out = e(d)
+        assert int(out["stage_max"].sum()) == min(R, S) * int(out["inc"].sum())
+    d = np.zeros((1, 4, 5), dtype=np.int64)
+    d[0, :, 2] = [1 * MS, 2 * MS, 3 * MS, 4 * MS]
+    out = e(d)
+    assert int(out["stage_sum"].sum()) == int(out["inc"].sum())  # Mbar = F / R
+    assert out["gap"][0].tolist() == [1 * MS, 3 * MS, 6 * MS, 10 * MS]
+
+
+def pin_ev_invariants(e):
+    """Relabelling ranks leaves the evidence unchanged; gap 0 exactly at
+    ties; R = 1 has no runner-up."""
+    rng = np.random.Generator(np.random.PCG64(13))
+    for d in random_cases(14):
+        T, S, R = d.shape
+        out = e(d)
+        assert (out["ties"] >= 1).all()
+        if R >= 2:
+            assert (out["gap"] >= 0).all()
+            assert np.array_equal(out["gap"] == 0, out["ties"] >= 2)
+        else:
+            assert (out["gap"] == -1).all() and (out["ties"] == 1).all()
+        perm = rng.permutation(R)
+        out2 = e(d[:, :, perm])
+        for k in ("inc", "gap", "ties", "stage_max", "stage_sum"):
+            assert np.array_equal(out[k], out2[k]), k
+
+
+def pin_ev_twin(e, pyref):
+    for d in random_cases(15):
+        small = d[:5]
+        out = e(small)
+        ref = pyref.frontier_evidence(small.tolist())
+        for k, v in ref.items():
+            assert out[k].tolist() == v, k
+
+
+EVIDENCE_PINS = [pin_ev_frontier_part, pin_ev_golden, pin_ev_stall, pin_ev_bruteforce,
+                 pin_ev_props, pin_ev_invariants]

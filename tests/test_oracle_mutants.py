@@ -14,31 +14,66 @@ import pins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "sf_oracle.c")
 
+# (function, anchor, replacement): the anchor must occur exactly once in the
+# body of that function
 MUTANTS = {
     # frontier
-    "tie_to_highest_rank": ("if (P[r] > F) {", "if (P[r] >= F) {"),
-    "no_prefix_reset": ("for (int32_t r = 0; r < R; ++r) P[r] = 0;", ""),
-    "stage_max_not_prefix": ("P[r] += row[r];", "P[r] = row[r];"),
-    "transposed_layout": ("P[r] += row[r];", "P[r] += d[(t * R + r) * (int64_t)S + s];"),
-    "absolute_not_advance": ("F_prev = F;", ""),
-    "sign_flip": ("inc[t * S + s] = F - F_prev;", "inc[t * S + s] = F_prev - F;"),
-    "rank_relabel": ("L = r;", "L = R - 1 - r;"),
-    "start_leader_minus_one": ("int32_t L = 0;", "int32_t L = -1;"),
-    "skip_first_rank_in_prefix": ("for (int32_t r = 0; r < R; ++r) P[r] += row[r];",
+    "tie_to_highest_rank": ("sfo_frontier", "if (P[r] > F) {", "if (P[r] >= F) {"),
+    "no_prefix_reset": ("sfo_frontier", "for (int32_t r = 0; r < R; ++r) P[r] = 0;", ""),
+    "stage_max_not_prefix": ("sfo_frontier", "for (int32_t r = 0; r < R; ++r) P[r] += row[r];",
+                             "for (int32_t r = 0; r < R; ++r) P[r] = row[r];"),
+    "transposed_layout": ("sfo_frontier", "for (int32_t r = 0; r < R; ++r) P[r] += row[r];",
+                          "for (int32_t r = 0; r < R; ++r) P[r] += d[(t * R + r) * (int64_t)S + s];"),
+    "absolute_not_advance": ("sfo_frontier", "F_prev = F;", ""),
+    "sign_flip": ("sfo_frontier", "inc[t * S + s] = F - F_prev;", "inc[t * S + s] = F_prev - F;"),
+    "rank_relabel": ("sfo_frontier", "L = r;", "L = R - 1 - r;"),
+    "start_leader_minus_one": ("sfo_frontier", "int32_t L = 0;", "int32_t L = -1;"),
+    "skip_first_rank_in_prefix": ("sfo_frontier", "for (int32_t r = 0; r < R; ++r) P[r] += row[r];",
                                   "for (int32_t r = 1; r < R; ++r) P[r] += row[r];"),
     # window summary
-    "last_window_short": ("int64_t t1 = t0 + window < T ? t0 + window : T;",
+    "last_window_short": ("sfo_window_summary", "int64_t t1 = t0 + window < T ? t0 + window : T;",
                           "int64_t t1 = t0 + window < T ? t0 + window : T - 1;"),
-    "exposed_drops_first_step": ("for (int64_t t = t0; t < t1; ++t) sum += inc[t * S + s];",
+    "exposed_drops_first_step": ("sfo_window_summary",
+                                 "for (int64_t t = t0; t < t1; ++t) sum += inc[t * S + s];",
                                  "for (int64_t t = t0 + 1; t < t1; ++t) sum += inc[t * S + s];"),
-    "rank0_not_counted": ("if (r >= 0 && r < R) c[r] += 1;", "if (r > 0 && r < R) c[r] += 1;"),
-    "top_stage_tie_to_higher": ("if (exposed[w * S + s] > exposed[w * S + s1]) s1 = s;",
+    "rank0_not_counted": ("sfo_window_summary", "if (r >= 0 && r < R) c[r] += 1;",
+                          "if (r > 0 && r < R) c[r] += 1;"),
+    "top_stage_tie_to_higher": ("sfo_window_summary",
+                                "if (exposed[w * S + s] > exposed[w * S + s1]) s1 = s;",
                                 "if (exposed[w * S + s] >= exposed[w * S + s1]) s1 = s;"),
-    "second_stage_may_repeat_first": ("if (s == s1) continue;", ""),
-    "modal_rank_tie_to_higher": ("if (c[r] > best) {", "if (c[r] >= best && c[r] > 0) {"),
-    "top2_ascending": ("if (s2 < 0 || exposed[w * S + s] > exposed[w * S + s2]) s2 = s;",
+    "second_stage_may_repeat_first": ("sfo_window_summary", "if (s == s1) continue;", ""),
+    "modal_rank_tie_to_higher": ("sfo_window_summary", "if (c[r] > best) {",
+                                 "if (c[r] >= best && c[r] > 0) {"),
+    "top2_ascending": ("sfo_window_summary",
+                       "if (s2 < 0 || exposed[w * S + s] > exposed[w * S + s2]) s2 = s;",
                        "if (s2 < 0 || exposed[w * S + s] < exposed[w * S + s2]) s2 = s;"),
+    # localization evidence and baselines
+    "ev_tie_to_highest_rank": ("sfo_frontier_evidence", "if (P[r] > F) {", "if (P[r] >= F) {"),
+    "ev_no_prefix_reset": ("sfo_frontier_evidence", "for (int32_t r = 0; r < R; ++r) P[r] = 0;", ""),
+    "ev_absolute_not_advance": ("sfo_frontier_evidence", "F_prev = F;", ""),
+    "ev_tie_count_excludes_leader": ("sfo_frontier_evidence", "if (P[r] == F) n_tie += 1;",
+                                     "if (P[r] == F && r != L) n_tie += 1;"),
+    "ev_runner_up_may_be_leader": ("sfo_frontier_evidence",
+                                   "if (r != L && (!have_second || P[r] > second)) {",
+                                   "if (!have_second || P[r] > second) {"),
+    "ev_gap_sign": ("sfo_frontier_evidence", "gap[i] = have_second ? F - second : -1;",
+                    "gap[i] = have_second ? second - F : -1;"),
+    "ev_single_rank_gap_zero": ("sfo_frontier_evidence", "gap[i] = have_second ? F - second : -1;",
+                                "gap[i] = have_second ? F - second : 0;"),
+    "ev_stage_max_of_prefix": ("sfo_frontier_evidence", "if (row[r] > dmax) dmax = row[r];",
+                               "if (P[r] > dmax) dmax = P[r];"),
+    "ev_stage_sum_skips_rank0": ("sfo_frontier_evidence", "dsum += row[r];",
+                                 "if (r) dsum += row[r];"),
 }
+
+
+def _function_span(source, name):
+    """[start, end) of the definition of C function ``name`` in ``source``."""
+    import re
+    m = re.search(r"^\w[^\n;]*\b%s\(" % name, source, flags=re.M)
+    assert m, name
+    end = source.index("\n}\n", m.start()) + 3
+    return m.start(), end
 
 
 def _run_all(o):
@@ -52,6 +87,11 @@ def _run_all(o):
     for pin in pins.SUMMARY_PINS:
         try:
             pin(o.frontier, o.window_summary)
+        except AssertionError:
+            failed.append(pin.__name__)
+    for pin in pins.EVIDENCE_PINS:
+        try:
+            pin(o.frontier_evidence)
         except AssertionError:
             failed.append(pin.__name__)
     return failed
@@ -72,10 +112,12 @@ def test_unmutated_copy_passes(source, tmp_path):
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_mutant_is_caught(name, source, tmp_path):
-    old, new = MUTANTS[name]
-    assert source.count(old) == 1, "mutation anchor must occur exactly once: %r" % old
+    func, old, new = MUTANTS[name]
+    a, b = _function_span(source, func)
+    body = source[a:b]
+    assert body.count(old) == 1, "mutation anchor must occur once in %s: %r" % (func, old)
     src = tmp_path / ("%s.c" % name)
-    src.write_text(source.replace(old, new))
+    src.write_text(source[:a] + body.replace(old, new) + source[b:])
     lib = oracle.build(force=True, src=str(src), out=str(tmp_path / ("lib%s.so" % name)))
     failed = _run_all(oracle.COracle(lib))
     assert failed, "mutant %s passed every pin" % name

@@ -16,6 +16,15 @@ def test_summary_pin(pin):
     pin(oracle.frontier, oracle.window_summary)
 
 
+@pytest.mark.parametrize("pin", pins.EVIDENCE_PINS, ids=lambda p: p.__name__)
+def test_evidence_pin(pin):
+    pin(oracle.frontier_evidence)
+
+
+def test_twin_evidence():
+    pins.pin_ev_twin(oracle.frontier_evidence, oracle.pyref)
+
+
 def test_twin_frontier():
     pins.pin_twin(oracle.frontier, oracle.pyref)
 
