@@ -79,6 +79,8 @@ def main() -> int:
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU oracle baseline (0: skip)")
+    ap.add_argument("--no-next", action="store_true",
+                    help="skip timing the next-row passes (localization evidence)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="also run a plain 1 GiB copy kernel (for counter scaling)")
     args = ap.parse_args()
@@ -201,6 +203,51 @@ def main() -> int:
     read_ms = min(a.elapsed_time(b) for a, b in rd)
     read_ceiling = (t1 - t0) * S * R * 8 / (read_ms / 1e3) / 1e9
 
+    # next row: the evidence pass (frontier + runner-up gap, tie-set size,
+    # per-stage max and sum) over the same chunks, timed the same way
+    next_rows = {}
+    if not args.no_next:
+        ev_out = {k: torch.empty((T, S), dtype=torch.int32 if k in ("leader", "ties") else torch.int64,
+                                 device=dev) for k in sf.EVIDENCE_FIELDS}
+        ev_views = [(d[t0:t1], {k: v[t0:t1] for k, v in ev_out.items()}) for t0, t1 in bounds]
+        for dv, ov in ev_views:
+            sf.sf_frontier_evidence(dv, ov, stream=stream)
+        evs = []
+        for _ in range(max(3, args.steps // 2)):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for dv, ov in ev_views:
+                sf.sf_frontier_evidence(dv, ov, stream=stream)
+            b.record(stream)
+            evs.append((a, b))
+        torch.cuda.synchronize(dev)
+        ev_ms = float(np.mean([a.elapsed_time(b) for a, b in evs])) / len(bounds)
+        ev_bytes = (8 * T * S * R + 40 * T * S) / len(bounds)
+        ev_exact = None
+        if oracle_out:
+            import oracle
+            t0c = oracle_out[0][0]
+            n_chk = min(len(oracle_out[0][1]), 64)
+            # the first sampled steps, regenerated from the seed for the oracle
+            x = synth.generate(wl, t0c, t0c + n_chk)
+            o = oracle.frontier_evidence(x)
+            ev_exact = all(np.array_equal(ev_out[k][t0c:t0c + n_chk].cpu().numpy(), o[ok])
+                           for k, ok in (("increment", "inc"), ("leader", "lead"), ("gap", "gap"),
+                                         ("ties", "ties"), ("stage_max", "stage_max"),
+                                         ("stage_sum", "stage_sum")))
+        next_rows["frontier_evidence"] = {
+            "kernel": "k_frontier_evidence",
+            "bound": "hbm",
+            "launch_ms": ev_ms,
+            "algorithmic_bytes_per_launch": ev_bytes,
+            "achieved": ev_bytes / (ev_ms / 1e3) / 1e9,
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": ev_bytes / (ev_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+            "bit_exact_first_steps": ev_exact,
+        }
+        del ev_out, ev_views
+
     samples = T * S * R
     value = samples / (ms_per_step / 1e3)
     step_bytes = 8 * samples + 12 * T * S + 12 * T * S + W * S * (8 + 4 * R) + 16 * W
@@ -240,6 +287,7 @@ def main() -> int:
         },
         "summary_kernels_ms": float(np.mean(summary_ms)),
         "torch_sum_read_gbps": read_ceiling,
+        "next_rows": next_rows,
         "h2d_gbps_pcie_context": wl.input_bytes / h2d_time / 1e9,
         "kernel_source_sha256_16": kernel_source_hash(),
     }

@@ -90,6 +90,35 @@ int sf_frontier(const int64_t* durations, int64_t T, int32_t R, int32_t S,
                 sf_stream_t stream);
 
 /*
+ * sf_frontier_evidence -- the sf_frontier pass plus, at every boundary, the
+ * localization evidence of Sec. 4 (the frontier tie set and the gap between
+ * the largest and second-largest prefix) and the per-stage terms of the
+ * max and mean baselines that Props. 1 and 2 compare the frontier with
+ * (M_t = sum_s max_r d, Mbar_t = sum_s (1/R) sum_r d).  One read of the
+ * durations produces all six outputs.
+ *
+ *   durations, T, R, S, out_increment, out_leader: as for sf_frontier (the
+ *                  outputs are identical to sf_frontier's).
+ *   out_gap        [T][S] int64, ns: F[t][s] minus the second-largest prefix
+ *                  over ranks (0 exactly when two or more ranks attain F);
+ *                  -1 when R == 1 (no runner-up).
+ *   out_ties       [T][S] int32: number of ranks r with P[t][r][s] == F[t][s]
+ *                  (>= 1); the leader is the lowest of them.
+ *   out_stage_max  [T][S] int64, ns: max over r of d[t][s][r].
+ *   out_stage_sum  [T][S] int64, ns: sum over r of d[t][s][r].
+ *   stream         HIP stream.
+ *
+ * Preconditions, alignment (element size), chunking and overlap rules as
+ * for sf_frontier; additionally T <= INT32_MAX.  Returns SF_OK, SF_EINVAL or
+ * SF_EHIP.
+ */
+int sf_frontier_evidence(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                         int64_t* out_increment, int32_t* out_leader,
+                         int64_t* out_gap, int32_t* out_ties,
+                         int64_t* out_stage_max, int64_t* out_stage_sum,
+                         sf_stream_t stream);
+
+/*
  * sf_num_windows -- number of windows W = ceil(T / window) that
  * sf_window_summary produces; the last window holds the remaining
  * T - (W-1)*window steps.  Returns -1 when T < 0 or window < 1.

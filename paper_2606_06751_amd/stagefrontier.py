@@ -38,6 +38,8 @@ def _load() -> ctypes.CDLL:
     i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
     lib.sf_frontier.argtypes = [vp, i64, i32, i32, vp, vp, vp]
     lib.sf_frontier.restype = ctypes.c_int
+    lib.sf_frontier_evidence.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+    lib.sf_frontier_evidence.restype = ctypes.c_int
     lib.sf_num_windows.argtypes = [i64, i64]
     lib.sf_num_windows.restype = i64
     lib.sf_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp]
@@ -108,6 +110,35 @@ def sf_frontier(durations: torch.Tensor, out_increment: torch.Tensor | None = No
     if rc != SF_OK:
         raise StageFrontierError(rc, "sf_frontier")
     return out_increment, out_leader
+
+
+EVIDENCE_FIELDS = ("increment", "leader", "gap", "ties", "stage_max", "stage_sum")
+
+
+def sf_frontier_evidence(durations: torch.Tensor, out: dict | None = None, stream=None) -> dict:
+    """The frontier pass plus localization evidence and per-stage baselines
+    (``sf_frontier_evidence``).
+
+    ``durations``: int64 GPU tensor [T, S, R].  Returns a dict of [T, S]
+    tensors keyed by ``EVIDENCE_FIELDS`` (``leader`` and ``ties`` int32,
+    the others int64); ``out`` may supply any of them.
+    """
+    if durations.dim() != 3:
+        raise ValueError("durations must be [T, S, R]")
+    T, S, R = durations.shape
+    _check(durations, "durations", torch.int64, (T, S, R))
+    out = dict(out or {})
+    for k in EVIDENCE_FIELDS:
+        dt = torch.int32 if k in ("leader", "ties") else torch.int64
+        if k not in out:
+            out[k] = torch.empty((T, S), dtype=dt, device=durations.device)
+        _check(out[k], k, dt, (T, S))
+    rc = _lib.sf_frontier_evidence(durations.data_ptr(), T, R, S,
+                                   *(out[k].data_ptr() for k in EVIDENCE_FIELDS),
+                                   _stream_handle(stream, durations.device))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_frontier_evidence")
+    return out
 
 
 def sf_window_summary(increment: torch.Tensor, leader: torch.Tensor, R: int, window: int,

@@ -26,8 +26,8 @@ def sf():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["sf_frontier", "sf_num_windows", "sf_strerror",
-                                    "sf_version", "sf_window_summary"]
+    assert declared_functions() == ["sf_frontier", "sf_frontier_evidence", "sf_num_windows",
+                                    "sf_strerror", "sf_version", "sf_window_summary"]
 
 
 def test_every_declared_symbol_is_exported(sf):
@@ -90,6 +90,29 @@ def test_frontier_argument_checks(sf):
     assert call(T=1 << 50, R=sf.SF_MAX_R, S=sf.SF_MAX_S) == sf.SF_EINVAL  # size overflow
 
 
+def test_evidence_argument_checks(sf):
+    lib = sf.raw_library()
+    names = ["d", "inc", "lead", "gap", "ties", "smax", "ssum"]
+    base = {n: (i + 1) << 40 for i, n in enumerate(names)}
+    ok_args = dict(base, T=10, R=8, S=6)
+
+    def call(**kw):
+        a = dict(ok_args, **kw)
+        return lib.sf_frontier_evidence(a["d"], a["T"], a["R"], a["S"],
+                                        *(a[n] for n in names[1:]), None)
+
+    assert call(T=0, **{n: None for n in names}) == sf.SF_OK
+    assert call(R=0) == sf.SF_EINVAL
+    assert call(S=sf.SF_MAX_S + 1) == sf.SF_EINVAL
+    for n in names:
+        assert call(**{n: None}) == sf.SF_EINVAL, n
+    assert call(ties=base["ties"] + 2) == sf.SF_EINVAL       # misaligned int32
+    assert call(gap=base["gap"] + 4) == sf.SF_EINVAL         # misaligned int64
+    assert call(ssum=base["d"] + 64) == sf.SF_EINVAL         # output overlaps input
+    assert call(ties=base["gap"] + 8) == sf.SF_EINVAL        # outputs overlap
+    assert call(T=1 << 33, R=1, S=1) == sf.SF_EINVAL         # one workgroup per step
+
+
 def test_summary_argument_checks(sf):
     lib = sf.raw_library()
     D = 4 << 40
@@ -131,5 +154,6 @@ def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
 def test_ctypes_argtypes_cover_header(sf):
     lib = sf.raw_library()
     assert len(lib.sf_frontier.argtypes) == 7
+    assert len(lib.sf_frontier_evidence.argtypes) == 11
     assert len(lib.sf_window_summary.argtypes) == 10
     assert lib.sf_num_windows.restype is ctypes.c_int64

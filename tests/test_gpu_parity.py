@@ -228,3 +228,74 @@ def test_bad_arguments_raise(sf):
     inc = torch.zeros((4, 3), dtype=torch.int64, device=DEV)
     with pytest.raises(sf.StageFrontierError):
         sf.sf_frontier(dd, inc, inc.view(torch.int32).view(-1)[:12].view(4, 3))  # overlap
+
+
+# ----------------------------------------------------------------------------
+# localization evidence and per-stage baselines (sf_frontier_evidence)
+
+EV_KEYS = {"increment": "inc", "leader": "lead", "gap": "gap", "ties": "ties",
+           "stage_max": "stage_max", "stage_sum": "stage_sum"}
+
+
+def gpu_evidence(sf, d):
+    out = sf.sf_frontier_evidence(torch.from_numpy(np.ascontiguousarray(d)).to(DEV))
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def assert_evidence_equal(sf, d):
+    g = gpu_evidence(sf, d)
+    o = oracle.frontier_evidence(d)
+    for gk, ok in EV_KEYS.items():
+        np.testing.assert_array_equal(g[gk], o[ok], err_msg=gk)
+    # the frontier part equals sf_frontier's
+    gi, gl = gpu_frontier(sf, d)
+    np.testing.assert_array_equal(g["increment"], gi)
+    np.testing.assert_array_equal(g["leader"], gl)
+
+
+EV_RANKS = [1, 2, 3, 8, 63, 64, 65, 127, 128, 129, 300, 512, 513, 1000, 1024, 1025, 2048,
+            2049, 4096, 5000, 16384]
+
+
+@pytest.mark.parametrize("R", EV_RANKS)
+def test_evidence_rank_sweep(sf, R):
+    T = max(3, min(60, 200000 // (R * 6)))
+    for S, hi in [(6, 10**9), (5, 2)]:
+        d = synth.random_durations(T, S, R, seed=R * 17 + S, hi=hi)
+        print("case R=%d S=%d T=%d hi=%d" % (R, S, T, hi), flush=True)
+        assert_evidence_equal(sf, d)
+
+
+@pytest.mark.parametrize("S", [1, 2, 13, 100, 512])
+def test_evidence_stage_sweep(sf, S):
+    for R in (8, 130, 3000):
+        T = max(2, min(30, 300000 // (R * S)))
+        d = synth.random_durations(T, S, R, seed=S * 5 + R, hi=10**5)
+        print("case R=%d S=%d T=%d" % (R, S, T), flush=True)
+        assert_evidence_equal(sf, d)
+
+
+def test_evidence_max_ranks_and_odd_base(sf):
+    d = synth.random_durations(2, 3, sf.SF_MAX_R, seed=19, hi=1)
+    assert_evidence_equal(sf, d)
+    # 8- but not 16-byte aligned base: narrow loads
+    T, S, R = 9, 4, 1030
+    d = synth.random_durations(T, S, R, seed=21, hi=3)
+    flat = torch.zeros(T * S * R + 1, dtype=torch.int64, device=DEV)
+    flat[1:] = torch.from_numpy(d.reshape(-1)).to(DEV)
+    out = sf.sf_frontier_evidence(flat[1:].view(T, S, R))
+    torch.cuda.synchronize()
+    o = oracle.frontier_evidence(d)
+    for gk, ok in EV_KEYS.items():
+        np.testing.assert_array_equal(out[gk].cpu().numpy(), o[ok], err_msg=gk)
+
+
+def test_evidence_golden_and_stall(sf):
+    import pins
+    g = pins.load_golden("motivating_example.txt")
+    out = gpu_evidence(sf, g["d"])
+    assert out["stage_max"][0].tolist() == g["stage_max"]
+    out = gpu_evidence(sf, pins.stall_case())
+    assert out["ties"][0].tolist() == [1, 1, 4, 4, 4, 4]
+    assert out["gap"][0].tolist() == [30 * pins.MS, 30 * pins.MS, 0, 0, 0, 0]

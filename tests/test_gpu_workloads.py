@@ -73,3 +73,30 @@ def test_workload_full_parity(sf, name):
     log("parity ok: %s" % name)
     del d, inc, lead, ex, cnt, top2
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workload_evidence_full_parity(sf, name):
+    """sf_frontier_evidence over every step of every workload (per chunk)."""
+    wl = synth.WORKLOADS[name]
+    T, S, R = wl.T, wl.S, wl.R
+    dev = torch.device("cuda:0")
+    log("evidence %s" % name)
+    bounds = wl.chunk_bounds()
+    n_max = max(t1 - t0 for t0, t1 in bounds)
+    d = torch.empty((n_max, S, R), dtype=torch.int64, device=dev)
+    buf = np.empty((n_max, S, R), dtype=np.int64)
+    keys = {"increment": "inc", "leader": "lead", "gap": "gap", "ties": "ties",
+            "stage_max": "stage_max", "stage_sum": "stage_sum"}
+    for t0, t1 in bounds:
+        n = t1 - t0
+        synth.generate(wl, t0, t1, out=buf[:n])
+        d[:n].copy_(torch.from_numpy(buf[:n]))
+        out = sf.sf_frontier_evidence(d[:n])
+        o = oracle.frontier_evidence(buf[:n])
+        torch.cuda.synchronize()
+        for gk, ok in keys.items():
+            np.testing.assert_array_equal(out[gk].cpu().numpy(), o[ok], err_msg=gk)
+        log("evidence chunk [%d, %d) ok" % (t0, t1))
+    del d, out
+    torch.cuda.empty_cache()
