@@ -579,30 +579,44 @@ __global__ __launch_bounds__(WG) void k_frontier_evidence(
 struct EvidenceVariant {
     const void* fn;
     int K, G, WG;
+    int per_cu;  // resident workgroups per CU to allow (0: no cap)
 };
 
 template <int VEC, int K, int G, int WG>
-EvidenceVariant ev_variant()
+EvidenceVariant ev_variant(int per_cu)
 {
     return EvidenceVariant{reinterpret_cast<const void*>(&k_frontier_evidence<VEC, K, G, WG>), K,
-                           G, WG};
+                           G, WG, per_cu};
 }
 
-// Up to 1024 ranks one group of at most 64 lanes covers a step (direct
-// writes, no LDS); beyond that two waves share a step and loop over
-// 2048-rank tiles, with at most 2 LDS slots (80 * S bytes of LDS).
-template <int VEC>
-EvidenceVariant pick_evidence(int R)
+// LDS bytes a variant needs: none when one group of <= 64 lanes covers the
+// step's ranks, else 5 arrays of [WG / min(G, 64)][S] u64.
+size_t ev_lds_need(const EvidenceVariant& v, int R, int S)
 {
-    if (R <= 8) return ev_variant<VEC, 2, 4, 64>();
-    if (R <= 16) return ev_variant<VEC, 2, 8, 64>();
-    if (R <= 32) return ev_variant<VEC, 4, 8, 64>();
-    if (R <= 64) return ev_variant<VEC, 4, 16, 64>();
-    if (R <= 128) return ev_variant<VEC, 8, 16, 64>();
-    if (R <= 256) return ev_variant<VEC, 8, 32, 64>();
-    if (R <= 512) return ev_variant<VEC, 8, 64, 64>();
-    if (R <= 1024) return ev_variant<VEC, 16, 64, 64>();
-    return ev_variant<VEC, 16, 128, 128>();
+    const int sub = v.G < 64 ? v.G : 64;
+    if (v.G <= 64 && R <= v.G * v.K) return 0;
+    return (size_t)5 * (v.WG / sub) * S * 8;
+}
+
+// Launch shape by rank count, measured on MI355X; a shape whose LDS would
+// exceed 64 KB at this S falls back to two 64-lane slots per step
+// (80 * S bytes, at most 40 KB).
+template <int VEC>
+EvidenceVariant pick_evidence(int R, int S)
+{
+    EvidenceVariant v;
+    if (R <= 8) v = ev_variant<VEC, 2, 4, 64>(0);
+    else if (R <= 16) v = ev_variant<VEC, 2, 8, 64>(0);
+    else if (R <= 32) v = ev_variant<VEC, 4, 8, 64>(0);
+    else if (R <= 64) v = ev_variant<VEC, 4, 16, 64>(0);
+    else if (R <= 128) v = ev_variant<VEC, 8, 16, 256>(8);
+    else if (R <= 256) v = ev_variant<VEC, 8, 16, 256>(8);
+    else if (R <= 512) v = ev_variant<VEC, 16, 32, 64>(0);
+    else if (R <= 1024) v = ev_variant<VEC, 16, 32, 64>(8);
+    else if (R <= 4096) v = ev_variant<VEC, 16, 256, 256>(2);
+    else v = ev_variant<VEC, 32, 256, 256>(0);
+    if (ev_lds_need(v, R, S) > kLdsMaxPerWg) v = ev_variant<VEC, 16, 128, 128>(0);
+    return v;
 }
 
 // ---------------------------------------------------------------------------
@@ -683,11 +697,9 @@ SF_API int sf_frontier_evidence(const int64_t* durations, int64_t T, int32_t R, 
             if (!disjoint(bufs[a], sizes[a], bufs[b], sizes[b])) return SF_EINVAL;
 
     const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
-    const EvidenceVariant v = vec2 ? pick_evidence<2>(R) : pick_evidence<1>(R);
-    const int sub = v.G < 64 ? v.G : 64;
+    const EvidenceVariant v = vec2 ? pick_evidence<2>(R, S) : pick_evidence<1>(R, S);
     const int spw = v.WG / v.G;
-    const bool direct = v.G <= 64 && R <= v.G * v.K;
-    const size_t lds = direct ? 0 : (size_t)5 * (v.WG / sub) * S * sizeof(u64);
+    const size_t lds = lds_request(ev_lds_need(v, R, S), v.per_cu);
     const int64_t blocks = (T + spw - 1) / spw;
     int Ri = R, Si = S;
     void* args[] = {(void*)&durations, (void*)&T, (void*)&Ri, (void*)&Si,
