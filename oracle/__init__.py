@@ -5,8 +5,9 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 the GPU path and the oracle share no code.
 
 Two independent statements of the same definitions (Sec. 3, Eq. (1) and
-Eq. (2); top-2 routing and the localization evidence of Sec. 4; the
-per-stage baselines of Props. 1-2):
+Eq. (2); top-2 routing, the routing candidate set and the localization
+evidence of Sec. 4; the per-stage baselines of Props. 1-2; the closure of
+Appendix A):
 
 * ``frontier`` / ``window_summary`` -- plain C nested loops in
   ``sf_oracle.c`` (fast enough for the full workloads on sampled steps),
@@ -51,6 +52,10 @@ class COracle:
         lib.sfo_window_summary.restype = None
         lib.sfo_frontier_evidence.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp]
         lib.sfo_frontier_evidence.restype = ctypes.c_int
+        lib.sfo_ingest.argtypes = [vp, vp, i64, i32, i32, vp, vp]
+        lib.sfo_ingest.restype = None
+        lib.sfo_route.argtypes = [vp, i64, i32, i64, i64, vp, vp]
+        lib.sfo_route.restype = None
         self.lib = lib
         self.path = path
 
@@ -93,6 +98,33 @@ class COracle:
             if rc != 0:
                 raise MemoryError("oracle prefix scratch allocation failed")
         return out
+
+    def ingest(self, x: np.ndarray, w: np.ndarray):
+        """Appendix A closure and the transpose to [T][S][R].
+
+        ``x``: int64 [R, T, K] explicit stage durations per rank; ``w``: int64
+        [R, T] step wall times.  Returns ``(d [T, K+1, R], o [T, R])``.
+        """
+        x = np.ascontiguousarray(x, dtype=np.int64)
+        w = np.ascontiguousarray(w, dtype=np.int64)
+        R, T, K = x.shape
+        assert w.shape == (R, T)
+        d = np.empty((T, K + 1, R), dtype=np.int64)
+        o = np.empty((T, R), dtype=np.int64)
+        if R and T:
+            self.lib.sfo_ingest(x.ctypes.data, w.ctypes.data, T, R, K, d.ctypes.data, o.ctypes.data)
+        return d, o
+
+    def route(self, exposed: np.ndarray, tau_num: int = 4, tau_den: int = 5):
+        """Routing candidate set per window: ``(order [W, S], size [W])``."""
+        exposed = np.ascontiguousarray(exposed, dtype=np.int64)
+        W, S = exposed.shape
+        order = np.empty((W, S), dtype=np.int32)
+        size = np.empty((W,), dtype=np.int32)
+        if W and S:
+            self.lib.sfo_route(exposed.ctypes.data, W, S, tau_num, tau_den,
+                               order.ctypes.data, size.ctypes.data)
+        return order, size
 
     def window_summary(self, inc: np.ndarray, lead: np.ndarray, R: int, window: int):
         """Window reduction of per-step results.
@@ -142,7 +174,15 @@ def frontier_evidence(d: np.ndarray):
     return _get().frontier_evidence(d)
 
 
+def ingest(x: np.ndarray, w: np.ndarray):
+    return _get().ingest(x, w)
+
+
+def route(exposed: np.ndarray, tau_num: int = 4, tau_den: int = 5):
+    return _get().route(exposed, tau_num, tau_den)
+
+
 from . import pyref  # noqa: E402  (pure-Python twin, no compiled code)
 
-__all__ = ["build", "COracle", "frontier", "frontier_evidence", "window_summary",
-           "num_windows", "pyref"]
+__all__ = ["build", "COracle", "frontier", "frontier_evidence", "ingest", "route",
+           "window_summary", "num_windows", "pyref"]

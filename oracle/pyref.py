@@ -81,3 +81,37 @@ def frontier_evidence(d):
         for k in out:
             out[k].append(rows[k])
     return out
+
+
+def ingest(x, w):
+    """``x[r][t][k]``, ``w[r][t]`` -> ``(d[t][s][r], o[t][r])`` with the
+    residual stage appended last (Appendix A)."""
+    R = len(x)
+    T = len(x[0]) if R else 0
+    K = len(x[0][0]) if T else 0
+    d = [[[0] * R for _ in range(K + 1)] for _ in range(T)]
+    o = [[0] * R for _ in range(T)]
+    for r in range(R):
+        for t in range(T):
+            for k in range(K):
+                d[t][k][r] = x[r][t][k]
+            e = w[r][t] - sum(x[r][t])
+            d[t][K][r] = max(0, e)
+            o[t][r] = max(0, -e)
+    return d, o
+
+
+def route(exposed, tau_num=4, tau_den=5):
+    """Stage order by (exposed desc, stage asc) and the smallest prefix size
+    whose exposed sum reaches tau_num / tau_den of the total."""
+    order, size = [], []
+    for ex in exposed:
+        ordw = sorted(range(len(ex)), key=lambda s: (-ex[s], s))
+        total = sum(ex)
+        k, cum = 0, 0
+        while k < len(ex) and tau_den * cum < tau_num * total:
+            cum += ex[ordw[k]]
+            k += 1
+        order.append(ordw)
+        size.append(k)
+    return order, size

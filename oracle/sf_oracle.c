@@ -19,6 +19,11 @@
  *   Sec. 4: top-2 routing = the two stages with the highest shares.
  *   Sec. 4, localization evidence: the tie set of the frontier and the gap
  *   between the largest and the second-largest prefix at each boundary.
+ *   Appendix A, closure: with rank-local step wall time w[t,r] and the
+ *   explicit stage durations, e = w - sum of the explicit stages, the
+ *   residual stage is max(0, e) and the overlap error max(0, -e).
+ *   Sec. 4, routing candidate set: the smallest prefix of stages, ordered by
+ *   share, whose cumulative share reaches tau_C.
  *   Sec. 3, Props. 1 and 2: the per-stage max and mean baselines
  *   M_t = sum_s max_r d and Mbar_t = sum_s (1/R) sum_r d, kept per stage as
  *   max_r d[t,r,s] and sum_r d[t,r,s].
@@ -37,8 +42,16 @@
  *     more ranks attain F); with R = 1 there is no runner-up and the gap
  *     is -1.
  *
+ *   - the gathered per-rank buffers are [R][T][K] (each rank's steps, each
+ *     step's K explicit stages) and the residual is appended as the last
+ *     stage, S = K + 1, as in the default stage taxonomy;
+ *   - the routing set orders stages like top-2 (exposed total descending,
+ *     lower stage first) and compares shares exactly: k stages suffice when
+ *     tau_den * (their exposed sum) >= tau_num * (window total).
+ *
  * Layout: d is [T][S][R] (rank fastest), increments and leaders [T][S],
- * exposed [W][S], counts [W][S][R], top2 [W][2][2].
+ * exposed [W][S], counts [W][S][R], top2 [W][2][2], route order [W][S] and
+ * route size [W].
  *
  * Parity status: every function here is pinned by the CPU test suite
  * (printed worked examples, closed forms, brute force); see tests/.
@@ -186,4 +199,58 @@ int sfo_frontier_evidence(const int64_t* d, int64_t T, int32_t R, int32_t S,
     }
     free(P);
     return 0;
+}
+
+/* Ingest of gathered per-rank stage buffers (Appendix A closure): x is
+ * [R][T][K] explicit stage durations, w is [R][T] step wall times.  Writes
+ * d [T][K+1][R] with the residual stage last and the overlap error o [T][R]. */
+void sfo_ingest(const int64_t* x, const int64_t* w, int64_t T, int32_t R, int32_t K,
+                int64_t* d, int64_t* o)
+{
+    const int32_t S = K + 1;
+    for (int32_t r = 0; r < R; ++r) {
+        for (int64_t t = 0; t < T; ++t) {
+            const int64_t* xs = x + ((int64_t)r * T + t) * K;
+            int64_t explicit_sum = 0;
+            for (int32_t k = 0; k < K; ++k) {
+                d[(t * S + k) * R + r] = xs[k];
+                explicit_sum += xs[k];
+            }
+            const int64_t e = w[(int64_t)r * T + t] - explicit_sum;
+            d[(t * S + K) * R + r] = e > 0 ? e : 0;
+            o[t * R + r] = e < 0 ? -e : 0;
+        }
+    }
+}
+
+/* Routing candidate set per window (Sec. 4): order[w] lists the stages by
+ * exposed total, descending, lower stage first on ties; size[w] is the
+ * smallest k whose first k stages reach tau = tau_num / tau_den of the
+ * window total. */
+void sfo_route(const int64_t* exposed, int64_t W, int32_t S, int64_t tau_num,
+               int64_t tau_den, int32_t* order, int32_t* size)
+{
+    for (int64_t w = 0; w < W; ++w) {
+        const int64_t* ex = exposed + w * S;
+        int32_t* ord = order + w * S;
+        /* insertion sort by (exposed desc, stage asc) */
+        for (int32_t s = 0; s < S; ++s) {
+            int32_t j = s;
+            while (j > 0 && ex[ord[j - 1]] < ex[s]) {
+                ord[j] = ord[j - 1];
+                --j;
+            }
+            ord[j] = s;
+        }
+        __int128 total = 0;
+        for (int32_t s = 0; s < S; ++s) total += ex[s];
+        const __int128 need = (__int128)tau_num * total;
+        __int128 cum = 0;
+        int32_t k = 0;
+        while (k < S && (__int128)tau_den * cum < need) {
+            cum += ex[ord[k]];
+            ++k;
+        }
+        size[w] = k;
+    }
 }

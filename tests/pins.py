@@ -529,3 +529,122 @@ def pin_ev_twin(e, pyref):
 
 EVIDENCE_PINS = [pin_ev_frontier_part, pin_ev_golden, pin_ev_stall, pin_ev_bruteforce,
                  pin_ev_props, pin_ev_invariants]
+
+
+# ----------------------------------------------------------------------------
+# ingest (Appendix A closure) and routing candidate set (Sec. 4)
+#
+# ingest pins take ``g(x[R,T,K], w[R,T]) -> (d[T,K+1,R], o[T,R])``; route pins
+# take ``c(exposed[W,S], num, den) -> (order[W,S], size[W])``.
+
+
+def pin_ingest_closure(g):
+    """Appendix A: the residual is max(0, e), the overlap max(0, -e), with
+    e = w - (explicit stages); so the stages minus the overlap give back w,
+    and residual and overlap are never both positive."""
+    rng = np.random.Generator(np.random.PCG64(30))
+    for (R, T, K) in [(1, 5, 1), (3, 7, 5), (8, 40, 5), (33, 9, 11)]:
+        x = rng.integers(0, 10**6, size=(R, T, K), dtype=np.int64)
+        w = x.sum(axis=2) + rng.integers(-3 * 10**5, 3 * 10**5, size=(R, T), dtype=np.int64)
+        w[0, 0] = x[0, 0].sum()          # exact closure: both zero
+        d, o = g(x, w)
+        assert d.shape == (T, K + 1, R) and o.shape == (T, R)
+        assert np.array_equal(d[:, :K, :], x.transpose(1, 2, 0))    # library transpose
+        assert np.array_equal(d.sum(axis=1) - o, w.T)
+        assert (d[:, K, :] >= 0).all() and (o >= 0).all()
+        assert not ((d[:, K, :] > 0) & (o > 0)).any()
+        assert d[0, K, 0] == 0 and o[0, 0] == 0
+
+
+def pin_ingest_roundtrip(g):
+    """A [T][S][R] matrix whose last stage is the residual of the others comes
+    back unchanged from its per-rank explicit stages and rank totals."""
+    rng = np.random.Generator(np.random.PCG64(31))
+    d0 = rng.integers(0, 10**7, size=(20, 6, 13), dtype=np.int64)
+    x = d0[:, :5, :].transpose(2, 0, 1).copy()
+    w = d0.sum(axis=1).T.copy()
+    d, o = g(x, w)
+    assert np.array_equal(d, d0) and (o == 0).all()
+
+
+def pin_ingest_twin(g, pyref):
+    rng = np.random.Generator(np.random.PCG64(32))
+    x = rng.integers(0, 100, size=(4, 6, 3), dtype=np.int64)
+    w = rng.integers(0, 400, size=(4, 6), dtype=np.int64)
+    d, o = g(x, w)
+    pd, po = pyref.ingest(x.tolist(), w.tolist())
+    assert d.tolist() == pd and o.tolist() == po
+
+
+def _route_by_lexsort(ex, num, den):
+    order = np.lexsort((np.arange(len(ex)), -ex))
+    cum = np.concatenate([[0], np.cumsum(ex[order])])
+    need = num * int(ex.sum())
+    k = next(i for i in range(len(ex) + 1) if i == len(ex) or den * int(cum[i]) >= need)
+    return order, k
+
+
+def pin_route_definition(c):
+    """Sec. 4: the smallest leading-share prefix reaching tau, on constructed
+    windows and against a sort by numpy's lexsort with a cumulative sum."""
+    ex = np.array([[50, 30, 15, 5], [5, 5, 5, 5], [0, 0, 0, 0], [10, 0, 0, 0],
+                   [1, 2, 3, 4], [7, 9, 9, 1]], dtype=np.int64)
+    order, size = c(ex, 4, 5)
+    assert size.tolist() == [2, 4, 0, 1, 3, 3]
+    assert order[5].tolist() == [1, 2, 0, 3]                 # tie 9/9: lower stage first
+    rng = np.random.Generator(np.random.PCG64(33))
+    for S in (1, 2, 6, 12, 40):
+        ex = rng.integers(0, 5, size=(30, S), dtype=np.int64) * rng.integers(1, 10**6)
+        for num, den in ((4, 5), (7, 10), (9, 10), (1, 1), (0, 1), (1, 3)):
+            order, size = c(ex, num, den)
+            for w in range(len(ex)):
+                eo, ek = _route_by_lexsort(ex[w], num, den)
+                assert order[w].tolist() == eo.tolist() and size[w] == ek
+
+
+def pin_route_properties(c):
+    """Larger tau never shrinks the set; tau = 0 gives the empty set; tau = 1
+    reaches every stage with nonzero exposure; the first two stages are the
+    top-2 stages."""
+    rng = np.random.Generator(np.random.PCG64(34))
+    ex = rng.integers(0, 10**6, size=(50, 8), dtype=np.int64)
+    ex[::5, 3:] = 0
+    sizes = [c(ex, n, 10)[1] for n in range(11)]
+    for a, b in zip(sizes, sizes[1:]):
+        assert (a <= b).all()
+    assert (sizes[0] == 0).all()
+    assert np.array_equal(sizes[10], (ex > 0).sum(axis=1))
+    order, _ = c(ex, 4, 5)
+    for w in range(len(ex)):
+        first = int(np.argmax(ex[w]))
+        assert order[w, 0] == first
+
+
+def pin_route_bruteforce(c):
+    """Every exposure vector in {0,1,2,3}^4 at tau 4/5 and 1/2."""
+    vecs = np.array(list(itertools.product(range(4), repeat=4)), dtype=np.int64)
+    for num, den in ((4, 5), (1, 2)):
+        order, size = c(vecs, num, den)
+        for i, ex in enumerate(vecs):
+            best = None
+            for k in range(5):
+                for subset in itertools.combinations(range(4), k):
+                    if den * int(ex[list(subset)].sum()) >= num * int(ex.sum()):
+                        best = k
+                        break
+                if best is not None:
+                    break
+            # the smallest subset of any stages equals the smallest leading prefix
+            assert size[i] == best, (ex, num, den)
+
+
+def pin_route_twin(c, pyref):
+    rng = np.random.Generator(np.random.PCG64(35))
+    ex = rng.integers(0, 6, size=(40, 5), dtype=np.int64)
+    order, size = c(ex, 4, 5)
+    po, ps = pyref.route(ex.tolist(), 4, 5)
+    assert order.tolist() == po and size.tolist() == ps
+
+
+INGEST_PINS = [pin_ingest_closure, pin_ingest_roundtrip]
+ROUTE_PINS = [pin_route_definition, pin_route_properties, pin_route_bruteforce]

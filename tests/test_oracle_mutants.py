@@ -64,6 +64,24 @@ MUTANTS = {
                                "if (P[r] > dmax) dmax = P[r];"),
     "ev_stage_sum_skips_rank0": ("sfo_frontier_evidence", "dsum += row[r];",
                                  "if (r) dsum += row[r];"),
+    # ingest
+    "ingest_residual_unclamped": ("sfo_ingest", "d[(t * S + K) * R + r] = e > 0 ? e : 0;",
+                                  "d[(t * S + K) * R + r] = e;"),
+    "ingest_overlap_sign": ("sfo_ingest", "o[t * R + r] = e < 0 ? -e : 0;",
+                            "o[t * R + r] = e < 0 ? e : 0;"),
+    "ingest_residual_first": ("sfo_ingest", "d[(t * S + k) * R + r] = xs[k];",
+                              "d[(t * S + k + 1) * R + r] = xs[k];"),
+    "ingest_wall_of_next_rank": ("sfo_ingest", "const int64_t e = w[(int64_t)r * T + t] - explicit_sum;",
+                                 "const int64_t e = w[(int64_t)((r + 1) % R) * T + t] - explicit_sum;"),
+    # routing set
+    "route_ascending": ("sfo_route", "while (j > 0 && ex[ord[j - 1]] < ex[s]) {",
+                        "while (j > 0 && ex[ord[j - 1]] > ex[s]) {"),
+    "route_tie_to_higher_stage": ("sfo_route", "while (j > 0 && ex[ord[j - 1]] < ex[s]) {",
+                                  "while (j > 0 && ex[ord[j - 1]] <= ex[s]) {"),
+    "route_strict_threshold": ("sfo_route", "while (k < S && (__int128)tau_den * cum < need) {",
+                               "while (k < S && (__int128)tau_den * cum <= need) {"),
+    "route_tau_inverted": ("sfo_route", "const __int128 need = (__int128)tau_num * total;",
+                           "const __int128 need = (__int128)tau_den * total;"),
 }
 
 
@@ -92,6 +110,16 @@ def _run_all(o):
     for pin in pins.EVIDENCE_PINS:
         try:
             pin(o.frontier_evidence)
+        except AssertionError:
+            failed.append(pin.__name__)
+    for pin in pins.INGEST_PINS:
+        try:
+            pin(o.ingest)
+        except AssertionError:
+            failed.append(pin.__name__)
+    for pin in pins.ROUTE_PINS:
+        try:
+            pin(o.route)
         except AssertionError:
             failed.append(pin.__name__)
     return failed

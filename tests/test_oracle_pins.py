@@ -62,3 +62,18 @@ def test_largest_prefix_is_exact():
     inc, lead = oracle.frontier(d)
     assert inc[0].tolist() == [big - 5, 5, 0]
     assert lead[0].tolist() == [1, 2, 1]
+
+
+@pytest.mark.parametrize("pin", pins.INGEST_PINS, ids=lambda p: p.__name__)
+def test_ingest_pin(pin):
+    pin(oracle.ingest)
+
+
+@pytest.mark.parametrize("pin", pins.ROUTE_PINS, ids=lambda p: p.__name__)
+def test_route_pin(pin):
+    pin(oracle.route)
+
+
+def test_twin_ingest_route():
+    pins.pin_ingest_twin(oracle.ingest, oracle.pyref)
+    pins.pin_route_twin(oracle.route, oracle.pyref)
