@@ -248,6 +248,62 @@ def main() -> int:
         }
         del ev_out, ev_views
 
+        # next row: ingest (the step before the path).  The first chunk's
+        # per-rank buffers [R][n][S-1] and step wall times [R][n] are rebuilt
+        # from the resident matrix; ingesting them must give the chunk back
+        # with zero overlap error (its last stage is the residual of the rest).
+        t0, t1 = bounds[0]
+        n = t1 - t0
+        xs = d[t0:t1, : S - 1, :].permute(2, 0, 1).contiguous()
+        wall = d[t0:t1].sum(dim=1).transpose(0, 1).contiguous()
+        ing_d = torch.empty((n, S, R), dtype=torch.int64, device=dev)
+        ing_o = torch.empty((n, R), dtype=torch.int64, device=dev)
+        sf.sf_ingest(xs, wall, ing_d, ing_o, stream=stream)
+        torch.cuda.synchronize(dev)
+        roundtrip = bool(torch.equal(ing_d, d[t0:t1]) and int(ing_o.abs().max()) == 0)
+        ig = []
+        for _ in range(max(3, args.steps // 2)):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            sf.sf_ingest(xs, wall, ing_d, ing_o, stream=stream)
+            b.record(stream)
+            ig.append((a, b))
+        torch.cuda.synchronize(dev)
+        ig_ms = float(np.mean([a.elapsed_time(b) for a, b in ig]))
+        ig_bytes = 8 * R * n * (S - 1) + 8 * R * n + 8 * n * S * R + 8 * n * R
+        next_rows["ingest"] = {
+            "kernel": "k_ingest",
+            "bound": "hbm",
+            "launch_ms": ig_ms,
+            "algorithmic_bytes_per_launch": ig_bytes,
+            "achieved": ig_bytes / (ig_ms / 1e3) / 1e9,
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": ig_bytes / (ig_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+            "shape": {"ranks": R, "steps": n, "explicit_stages": S - 1},
+            "roundtrip_exact": roundtrip,
+        }
+        del xs, wall, ing_d, ing_o
+
+        # next row: routing candidate set (tau 4/5) of the path's windows
+        order = torch.empty((W, S), dtype=torch.int32, device=dev)
+        size = torch.empty((W,), dtype=torch.int32, device=dev)
+        rt = []
+        for _ in range(max(3, args.steps // 2)):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            sf.sf_route(ex, 4, 5, order, size, stream=stream)
+            b.record(stream)
+            rt.append((a, b))
+        torch.cuda.synchronize(dev)
+        next_rows["route"] = {
+            "kernel": "k_route",
+            "bound": "launch",
+            "launch_ms": float(np.mean([a.elapsed_time(b) for a, b in rt])),
+            "windows": W,
+            "candidate_sizes": np.bincount(size.cpu().numpy(), minlength=S + 1).tolist(),
+        }
+
     samples = T * S * R
     value = samples / (ms_per_step / 1e3)
     step_bytes = 8 * samples + 12 * T * S + 12 * T * S + W * S * (8 + 4 * R) + 16 * W

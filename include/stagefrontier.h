@@ -119,6 +119,55 @@ int sf_frontier_evidence(const int64_t* durations, int64_t T, int32_t R, int32_t
                          sf_stream_t stream);
 
 /*
+ * sf_ingest -- the step before the path: gathered per-rank stage buffers to
+ * the [T][S][R] layout, with the closure of Appendix A.  For each rank r and
+ * step t, with w[r][t] the rank-local step wall time and x[r][t][k] the K
+ * explicit stage durations, e = w - sum_k x; the residual stage
+ * ("step.other", last in the default taxonomy) is max(0, e) and the
+ * overlap error is max(0, -e).
+ *
+ *   stages         [R][T][K] int64 ns, each rank's buffer as gathered
+ *                  (steps, then explicit stages).  May be NULL when K == 0.
+ *   wall           [R][T] int64 ns.
+ *   T, R, K        0 <= T, 1 <= R <= SF_MAX_R, 0 <= K, K + 1 <= SF_MAX_S.
+ *                  T == 0 is a no-op.
+ *   out_durations  [T][K+1][R] int64: stage k < K is x, stage K the residual.
+ *   out_overlap    [T][R] int64.
+ *   stream         HIP stream.
+ *
+ * Pointers 8-byte aligned; outputs must not overlap inputs or each other.
+ * Returns SF_OK, SF_EINVAL or SF_EHIP.
+ */
+int sf_ingest(const int64_t* stages, const int64_t* wall, int64_t T, int32_t R,
+              int32_t K, int64_t* out_durations, int64_t* out_overlap,
+              sf_stream_t stream);
+
+/*
+ * sf_route -- the routing candidate set of Sec. 4 per window: the smallest
+ * prefix of stages, ordered by share, whose cumulative share reaches
+ * tau_C = tau_num / tau_den (the paper's default is 0.80 = 4/5).  Shares of
+ * a window have a common denominator (Eq. (2)), so the order and the test
+ * use the exposed totals of sf_window_summary directly:
+ * k stages suffice when tau_den * (sum of their totals) >= tau_num * (sum of
+ * all totals), evaluated exactly in 128-bit integers.
+ *
+ *   stage_exposed  [W][S] int64 (out_stage_exposed of sf_window_summary).
+ *   W, S           0 <= W, 1 <= S <= SF_MAX_S.  W == 0 is a no-op.
+ *   tau_num, tau_den  0 <= tau_num <= tau_den, 1 <= tau_den <= INT32_MAX.
+ *   out_order      [W][S] int32: stages by total, descending; the lower
+ *                  stage first on ties (so the first two are the top-2
+ *                  stages of sf_window_summary).
+ *   out_size       [W] int32: the candidate-set size k (0 when the window
+ *                  total is 0 or tau is 0); the set is out_order[w][0..k).
+ *   stream         HIP stream.
+ *
+ * Returns SF_OK, SF_EINVAL or SF_EHIP.
+ */
+int sf_route(const int64_t* stage_exposed, int64_t W, int32_t S, int64_t tau_num,
+             int64_t tau_den, int32_t* out_order, int32_t* out_size,
+             sf_stream_t stream);
+
+/*
  * sf_num_windows -- number of windows W = ceil(T / window) that
  * sf_window_summary produces; the last window holds the remaining
  * T - (W-1)*window steps.  Returns -1 when T < 0 or window < 1.

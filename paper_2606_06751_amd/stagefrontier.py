@@ -40,6 +40,10 @@ def _load() -> ctypes.CDLL:
     lib.sf_frontier.restype = ctypes.c_int
     lib.sf_frontier_evidence.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp]
     lib.sf_frontier_evidence.restype = ctypes.c_int
+    lib.sf_ingest.argtypes = [vp, vp, i64, i32, i32, vp, vp, vp]
+    lib.sf_ingest.restype = ctypes.c_int
+    lib.sf_route.argtypes = [vp, i64, i32, i64, i64, vp, vp, vp]
+    lib.sf_route.restype = ctypes.c_int
     lib.sf_num_windows.argtypes = [i64, i64]
     lib.sf_num_windows.restype = i64
     lib.sf_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp]
@@ -174,6 +178,56 @@ def sf_window_summary(increment: torch.Tensor, leader: torch.Tensor, R: int, win
     if rc != SF_OK:
         raise StageFrontierError(rc, "sf_window_summary")
     return out_stage_exposed, out_lead_counts, out_top2
+
+
+def sf_ingest(stages: torch.Tensor, wall: torch.Tensor, out_durations: torch.Tensor | None = None,
+              out_overlap: torch.Tensor | None = None, stream=None):
+    """Gathered per-rank buffers to [T][K+1][R] with the Appendix A closure
+    (``sf_ingest``).
+
+    ``stages``: int64 GPU tensor [R, T, K]; ``wall``: int64 [R, T].  Returns
+    ``(out_durations [T, K+1, R], out_overlap [T, R])``.
+    """
+    if stages.dim() != 3:
+        raise ValueError("stages must be [R, T, K]")
+    R, T, K = stages.shape
+    _check(stages, "stages", torch.int64, (R, T, K))
+    _check(wall, "wall", torch.int64, (R, T))
+    dev = stages.device
+    if out_durations is None:
+        out_durations = torch.empty((T, K + 1, R), dtype=torch.int64, device=dev)
+    if out_overlap is None:
+        out_overlap = torch.empty((T, R), dtype=torch.int64, device=dev)
+    _check(out_durations, "out_durations", torch.int64, (T, K + 1, R))
+    _check(out_overlap, "out_overlap", torch.int64, (T, R))
+    rc = _lib.sf_ingest(stages.data_ptr(), wall.data_ptr(), T, R, K, out_durations.data_ptr(),
+                        out_overlap.data_ptr(), _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_ingest")
+    return out_durations, out_overlap
+
+
+def sf_route(stage_exposed: torch.Tensor, tau_num: int = 4, tau_den: int = 5,
+             out_order: torch.Tensor | None = None, out_size: torch.Tensor | None = None,
+             stream=None):
+    """Routing candidate set per window (``sf_route``); tau = num / den
+    (default 4/5 = 0.80).  Returns ``(out_order [W, S], out_size [W])``."""
+    if stage_exposed.dim() != 2:
+        raise ValueError("stage_exposed must be [W, S]")
+    W, S = stage_exposed.shape
+    _check(stage_exposed, "stage_exposed", torch.int64, (W, S))
+    dev = stage_exposed.device
+    if out_order is None:
+        out_order = torch.empty((W, S), dtype=torch.int32, device=dev)
+    if out_size is None:
+        out_size = torch.empty((W,), dtype=torch.int32, device=dev)
+    _check(out_order, "out_order", torch.int32, (W, S))
+    _check(out_size, "out_size", torch.int32, (W,))
+    rc = _lib.sf_route(stage_exposed.data_ptr(), W, S, tau_num, tau_den, out_order.data_ptr(),
+                       out_size.data_ptr(), _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_route")
+    return out_order, out_size
 
 
 def raw_library() -> ctypes.CDLL:

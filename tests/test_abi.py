@@ -26,8 +26,9 @@ def sf():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["sf_frontier", "sf_frontier_evidence", "sf_num_windows",
-                                    "sf_strerror", "sf_version", "sf_window_summary"]
+    assert declared_functions() == ["sf_frontier", "sf_frontier_evidence", "sf_ingest",
+                                    "sf_num_windows", "sf_route", "sf_strerror", "sf_version",
+                                    "sf_window_summary"]
 
 
 def test_every_declared_symbol_is_exported(sf):
@@ -113,6 +114,36 @@ def test_evidence_argument_checks(sf):
     assert call(T=1 << 33, R=1, S=1) == sf.SF_EINVAL         # one workgroup per step
 
 
+def test_ingest_and_route_argument_checks(sf):
+    lib = sf.raw_library()
+    X, Wl, D, O = 1 << 40, 2 << 40, 3 << 40, 4 << 40
+
+    def ingest(**kw):
+        a = dict(dict(x=X, w=Wl, T=10, R=8, K=5, d=D, o=O), **kw)
+        return lib.sf_ingest(a["x"], a["w"], a["T"], a["R"], a["K"], a["d"], a["o"], None)
+
+    assert ingest(T=0, x=None, w=None, d=None, o=None) == sf.SF_OK
+    assert ingest(K=-1) == sf.SF_EINVAL
+    assert ingest(K=sf.SF_MAX_S) == sf.SF_EINVAL            # K + 1 > SF_MAX_S
+    assert ingest(R=0) == sf.SF_EINVAL
+    assert ingest(w=None) == sf.SF_EINVAL
+    assert ingest(d=X + 8) == sf.SF_EINVAL                  # output overlaps input
+    assert ingest(o=D + 16) == sf.SF_EINVAL                 # outputs overlap
+    assert ingest(o=O + 4) == sf.SF_EINVAL                  # misaligned
+
+    def route(**kw):
+        a = dict(dict(e=X, W=10, S=6, num=4, den=5, order=D, size=O), **kw)
+        return lib.sf_route(a["e"], a["W"], a["S"], a["num"], a["den"], a["order"], a["size"], None)
+
+    assert route(W=0, e=None, order=None, size=None) == sf.SF_OK
+    assert route(den=0) == sf.SF_EINVAL
+    assert route(num=6) == sf.SF_EINVAL                     # tau > 1
+    assert route(num=-1) == sf.SF_EINVAL
+    assert route(S=0) == sf.SF_EINVAL
+    assert route(order=X + 8) == sf.SF_EINVAL
+    assert route(size=D + 4) == sf.SF_EINVAL
+
+
 def test_summary_argument_checks(sf):
     lib = sf.raw_library()
     D = 4 << 40
@@ -155,5 +186,7 @@ def test_ctypes_argtypes_cover_header(sf):
     lib = sf.raw_library()
     assert len(lib.sf_frontier.argtypes) == 7
     assert len(lib.sf_frontier_evidence.argtypes) == 11
+    assert len(lib.sf_ingest.argtypes) == 8
+    assert len(lib.sf_route.argtypes) == 8
     assert len(lib.sf_window_summary.argtypes) == 10
     assert lib.sf_num_windows.restype is ctypes.c_int64

@@ -299,3 +299,76 @@ def test_evidence_golden_and_stall(sf):
     out = gpu_evidence(sf, pins.stall_case())
     assert out["ties"][0].tolist() == [1, 1, 4, 4, 4, 4]
     assert out["gap"][0].tolist() == [30 * pins.MS, 30 * pins.MS, 0, 0, 0, 0]
+
+
+# ----------------------------------------------------------------------------
+# ingest (Appendix A closure) and routing candidate set (Sec. 4)
+
+def _ingest_inputs(R, T, K, seed, slack=10**5):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    x = rng.integers(0, 10**6, size=(R, T, K), dtype=np.int64)
+    w = x.sum(axis=2) + rng.integers(-slack, slack + 1, size=(R, T), dtype=np.int64)
+    return x, w
+
+
+@pytest.mark.parametrize("R,T,K", [(1, 1, 0), (1, 9, 5), (8, 100, 5), (7, 33, 1), (64, 64, 5),
+                                   (65, 17, 11), (130, 50, 7), (1000, 12, 63), (3, 5, 64),
+                                   (40, 3, 127), (17, 2, 255), (9, 2, 511), (65536, 2, 3),
+                                   (4099, 19, 11)])
+def test_ingest_matches_oracle(sf, R, T, K):
+    x, w = _ingest_inputs(R, T, K, seed=R * 7 + T + K)
+    print("case R=%d T=%d K=%d" % (R, T, K), flush=True)
+    gd, go = sf.sf_ingest(torch.from_numpy(x).to(DEV), torch.from_numpy(w).to(DEV))
+    torch.cuda.synchronize()
+    od, oo = oracle.ingest(x, w)
+    np.testing.assert_array_equal(gd.cpu().numpy(), od)
+    np.testing.assert_array_equal(go.cpu().numpy(), oo)
+
+
+def test_ingest_feeds_the_frontier(sf):
+    """Ingested buffers give the same frontier as the matrix they came from."""
+    wl = synth.WORKLOADS["r128_s6_t100k"]
+    d0 = synth.generate(wl, 0, 500)
+    x = d0[:, :-1, :].transpose(2, 0, 1).copy()
+    w = d0.sum(axis=1).T.copy()
+    gd, go = sf.sf_ingest(torch.from_numpy(x).to(DEV), torch.from_numpy(w).to(DEV))
+    inc, lead = sf.sf_frontier(gd)
+    torch.cuda.synchronize()
+    assert np.array_equal(gd.cpu().numpy(), d0) and int(go.abs().sum()) == 0
+    oi, ol = oracle.frontier(d0)
+    np.testing.assert_array_equal(inc.cpu().numpy(), oi)
+    np.testing.assert_array_equal(lead.cpu().numpy(), ol)
+
+
+@pytest.mark.parametrize("S", [1, 2, 3, 6, 12, 64, 100, 511, 512])
+def test_route_matches_oracle(sf, S):
+    rng = np.random.Generator(np.random.PCG64(S))
+    W = 37
+    ex = rng.integers(0, 6, size=(W, S), dtype=np.int64) * rng.integers(1, 10**9)
+    ex[0] = 0                                   # empty window total
+    ex[1, :] = 7                                # all tied
+    if S > 3:
+        ex[2, 3] = 1 << 61                      # one dominant stage, large values
+    te = torch.from_numpy(ex).to(DEV)
+    for num, den in ((4, 5), (7, 10), (9, 10), (0, 1), (1, 1), (1, 3), (2147483646, 2147483647)):
+        go, gs = sf.sf_route(te, num, den)
+        torch.cuda.synchronize()
+        oo, os_ = oracle.route(ex, num, den)
+        np.testing.assert_array_equal(go.cpu().numpy(), oo)
+        np.testing.assert_array_equal(gs.cpu().numpy(), os_)
+
+
+def test_route_after_window_summary(sf):
+    """Chained on the GPU: the first two routed stages are the top-2 stages."""
+    wl = synth.WORKLOADS["r8_s6_t1k"]
+    d = synth.generate(wl)
+    inc, lead = sf.sf_frontier(torch.from_numpy(d).to(DEV))
+    ex, cnt, top2 = sf.sf_window_summary(inc, lead, wl.R, wl.window)
+    order, size = sf.sf_route(ex)
+    torch.cuda.synchronize()
+    oi, ol = oracle.frontier(d)
+    oe, _, _ = oracle.window_summary(oi, ol, wl.R, wl.window)
+    oo, os_ = oracle.route(oe)
+    np.testing.assert_array_equal(order.cpu().numpy(), oo)
+    np.testing.assert_array_equal(size.cpu().numpy(), os_)
+    assert np.array_equal(order.cpu().numpy()[:, :2], top2.cpu().numpy()[:, :, 0])

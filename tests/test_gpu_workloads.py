@@ -100,3 +100,36 @@ def test_workload_evidence_full_parity(sf, name):
         log("evidence chunk [%d, %d) ok" % (t0, t1))
     del d, out
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workload_ingest_and_route(sf, name):
+    """Ingest of the workload's per-rank buffers (first steps, up to 2000)
+    against the oracle, and the routing set of all its windows."""
+    wl = synth.WORKLOADS[name]
+    T, S, R = wl.T, wl.S, wl.R
+    n = min(T, 2000 if R <= 1024 else 400)
+    d0 = synth.generate(wl, 0, n)
+    x = d0[:, :-1, :].transpose(2, 0, 1).copy()        # per-rank [R][n][S-1]
+    rng = np.random.Generator(np.random.PCG64(wl.seed))
+    w = d0.sum(axis=1).T.copy() + rng.integers(-10**6, 10**6, size=(R, n), dtype=np.int64)
+    gd, go = sf.sf_ingest(torch.from_numpy(x).to("cuda:0"), torch.from_numpy(w).to("cuda:0"))
+    torch.cuda.synchronize()
+    od, oo = oracle.ingest(x, w)
+    np.testing.assert_array_equal(gd.cpu().numpy(), od)
+    np.testing.assert_array_equal(go.cpu().numpy(), oo)
+    log("ingest ok: %s, %d steps" % (name, n))
+    # routing set over every window of the workload (exposed totals from
+    # the oracle's own pass over the generated steps)
+    ex = np.empty((wl.num_windows, S), dtype=np.int64)
+    for w0 in range(0, T, wl.window * max(1, 2000 // wl.window)):
+        t1 = min(T, w0 + wl.window * max(1, 2000 // wl.window))
+        oi, ol = oracle.frontier(synth.generate(wl, w0, t1))
+        e, _, _ = oracle.window_summary(oi, ol, R, wl.window)
+        ex[w0 // wl.window: w0 // wl.window + len(e)] = e
+    go2, gs2 = sf.sf_route(torch.from_numpy(ex).to("cuda:0"))
+    torch.cuda.synchronize()
+    oo2, os2 = oracle.route(ex)
+    np.testing.assert_array_equal(go2.cpu().numpy(), oo2)
+    np.testing.assert_array_equal(gs2.cpu().numpy(), os2)
+    log("route ok: %s, %d windows, sizes %s" % (name, len(ex), np.bincount(os2).tolist()))
