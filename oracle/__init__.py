@@ -6,8 +6,8 @@ the GPU path and the oracle share no code.
 
 Two independent statements of the same definitions (Sec. 3, Eq. (1) and
 Eq. (2); top-2 routing, the routing candidate set and the localization
-evidence of Sec. 4; the per-stage baselines of Props. 1-2; the closure of
-Appendix A):
+evidence of Sec. 4; the direct-exposure gain of Eq. (4); the per-stage
+baselines of Props. 1-2; the closure of Appendix A):
 
 * ``frontier`` / ``window_summary`` -- plain C nested loops in
   ``sf_oracle.c`` (fast enough for the full workloads on sampled steps),
@@ -56,6 +56,8 @@ class COracle:
         lib.sfo_ingest.restype = None
         lib.sfo_route.argtypes = [vp, i64, i32, i64, i64, vp, vp]
         lib.sfo_route.restype = None
+        lib.sfo_exposure_gain.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp]
+        lib.sfo_exposure_gain.restype = ctypes.c_int
         self.lib = lib
         self.path = path
 
@@ -126,6 +128,30 @@ class COracle:
                                order.ctypes.data, size.ctypes.data)
         return order, size
 
+    def exposure_gain(self, d: np.ndarray, btilde: np.ndarray, window: int):
+        """Eq. (4) numerators and denominators.
+
+        ``d``: int64 [T, S, R]; ``btilde``: int64 [W, S, R] baseline per
+        window.  Returns a dict: ``gain`` [T, S], ``makespan`` [T],
+        ``window_gain`` [W, S], ``window_makespan`` [W] (all int64).
+        """
+        d = np.ascontiguousarray(d, dtype=np.int64)
+        btilde = np.ascontiguousarray(btilde, dtype=np.int64)
+        T, S, R = d.shape
+        W = num_windows(T, window)
+        assert btilde.shape == (W, S, R)
+        out = {"gain": np.empty((T, S), np.int64), "makespan": np.empty((T,), np.int64),
+               "window_gain": np.empty((W, S), np.int64),
+               "window_makespan": np.empty((W,), np.int64)}
+        if T:
+            rc = self.lib.sfo_exposure_gain(
+                d.ctypes.data, btilde.ctypes.data, T, R, S, window,
+                *(out[k].ctypes.data for k in ("gain", "makespan", "window_gain",
+                                               "window_makespan")))
+            if rc != 0:
+                raise MemoryError("oracle scratch allocation failed")
+        return out
+
     def window_summary(self, inc: np.ndarray, lead: np.ndarray, R: int, window: int):
         """Window reduction of per-step results.
 
@@ -182,7 +208,11 @@ def route(exposed: np.ndarray, tau_num: int = 4, tau_den: int = 5):
     return _get().route(exposed, tau_num, tau_den)
 
 
+def exposure_gain(d: np.ndarray, btilde: np.ndarray, window: int):
+    return _get().exposure_gain(d, btilde, window)
+
+
 from . import pyref  # noqa: E402  (pure-Python twin, no compiled code)
 
-__all__ = ["build", "COracle", "frontier", "frontier_evidence", "ingest", "route",
+__all__ = ["build", "COracle", "frontier", "frontier_evidence", "ingest", "route", "exposure_gain",
            "window_summary", "num_windows", "pyref"]

@@ -115,3 +115,29 @@ def route(exposed, tau_num=4, tau_den=5):
         order.append(ordw)
         size.append(k)
     return order, size
+
+
+def exposure_gain(d, btilde, window):
+    """Eq. (4) on nested lists: d[t][s][r], btilde[w][s][r] -> dict of
+    gain[t][s], makespan[t], window_gain[w][s], window_makespan[w]."""
+    def last_frontier(step):
+        return max(sum(step[s][r] for s in range(len(step))) for r in range(len(step[0])))
+
+    T = len(d)
+    S = len(d[0]) if T else 0
+    W = (T + window - 1) // window
+    out = {"gain": [], "makespan": [], "window_gain": [[0] * S for _ in range(W)],
+           "window_makespan": [0] * W}
+    for t, step in enumerate(d):
+        w = t // window
+        F = last_frontier(step)
+        g = []
+        for s in range(S):
+            m = [row[:] for row in step]
+            m[s] = [min(v, b) for v, b in zip(step[s], btilde[w][s])]
+            g.append(F - last_frontier(m))
+            out["window_gain"][w][s] += g[-1]
+        out["gain"].append(g)
+        out["makespan"].append(F)
+        out["window_makespan"][w] += F
+    return out

@@ -24,6 +24,10 @@
  *   residual stage is max(0, e) and the overlap error max(0, -e).
  *   Sec. 4, routing candidate set: the smallest prefix of stages, ordered by
  *   share, whose cumulative share reaches tau_C.
+ *   Sec. 4, Eq. (4), direct exposure: replace stage s on every rank by the
+ *   clipped baseline b = min(d, btilde), recompute the frontier, and take
+ *   F[t,S] - F^(s<-b)[t,S]; G_s is its window sum over the window sum of
+ *   F[t,S].
  *   Sec. 3, Props. 1 and 2: the per-stage max and mean baselines
  *   M_t = sum_s max_r d and Mbar_t = sum_s (1/R) sum_r d, kept per stage as
  *   max_r d[t,r,s] and sum_r d[t,r,s].
@@ -45,6 +49,10 @@
  *   - the gathered per-rank buffers are [R][T][K] (each rank's steps, each
  *     step's K explicit stages) and the residual is appended as the last
  *     stage, S = K + 1, as in the default stage taxonomy;
+ *   - the baseline btilde of Eq. (4) is given per window, per stage and per
+ *     rank ([W][S][R]), which covers a per-rank window median, a cohort
+ *     median or a no-stall reference; the library returns the numerators
+ *     and the denominator of G_s as int64 sums, never their quotient;
  *   - the routing set orders stages like top-2 (exposed total descending,
  *     lower stage first) and compares shares exactly: k stages suffice when
  *     tau_den * (their exposed sum) >= tau_num * (window total).
@@ -253,4 +261,63 @@ void sfo_route(const int64_t* exposed, int64_t W, int32_t S, int64_t tau_num,
         }
         size[w] = k;
     }
+}
+
+/* Frontier at the last boundary of one step, F[t,S] = max over ranks of the
+ * rank's total, from its own running prefixes (Eq. (1)). */
+static int64_t last_frontier(const int64_t* m, int32_t R, int32_t S, int64_t* P)
+{
+    for (int32_t r = 0; r < R; ++r) P[r] = 0;
+    int64_t F = 0;
+    for (int32_t s = 0; s < S; ++s) {
+        for (int32_t r = 0; r < R; ++r) P[r] += m[(int64_t)s * R + r];
+        F = P[0];
+        for (int32_t r = 1; r < R; ++r)
+            if (P[r] > F) F = P[r];
+    }
+    return F;
+}
+
+/* Direct-exposure gain, Eq. (4): for every step and stage s, the frontier is
+ * recomputed on a copy of the step whose stage s holds min(d, btilde) on
+ * every rank.  Per step: gain[t][s] = F[t,S] - F^(s<-b)[t,S] and
+ * makespan[t] = F[t,S]; per window w: wgain[w][s] and wmakespan[w] are their
+ * sums.  Returns 0, or -1 if scratch cannot be allocated. */
+int sfo_exposure_gain(const int64_t* d, const int64_t* btilde, int64_t T, int32_t R,
+                      int32_t S, int64_t window, int64_t* gain, int64_t* makespan,
+                      int64_t* wgain, int64_t* wmakespan)
+{
+    const int64_t n = (int64_t)S * R;
+    int64_t* m = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t* P = (int64_t*)malloc(sizeof(int64_t) * (size_t)(R > 0 ? R : 1));
+    if (!m || !P) {
+        free(m);
+        free(P);
+        return -1;
+    }
+    const int64_t W = (T + window - 1) / window;
+    for (int64_t i = 0; i < W * S; ++i) wgain[i] = 0;
+    for (int64_t i = 0; i < W; ++i) wmakespan[i] = 0;
+    for (int64_t t = 0; t < T; ++t) {
+        const int64_t w = t / window;
+        const int64_t* step = d + t * n;
+        const int64_t F = last_frontier(step, R, S, P);
+        makespan[t] = F;
+        wmakespan[w] += F;
+        for (int32_t s = 0; s < S; ++s) {
+            /* the step with stage s replaced by the clipped baseline */
+            for (int64_t i = 0; i < n; ++i) m[i] = step[i];
+            for (int32_t r = 0; r < R; ++r) {
+                const int64_t b = btilde[(w * S + s) * R + r];
+                int64_t* cell = m + (int64_t)s * R + r;
+                if (b < *cell) *cell = b;
+            }
+            const int64_t g = F - last_frontier(m, R, S, P);
+            gain[t * S + s] = g;
+            wgain[w * S + s] += g;
+        }
+    }
+    free(m);
+    free(P);
+    return 0;
 }

@@ -648,3 +648,110 @@ def pin_route_twin(c, pyref):
 
 INGEST_PINS = [pin_ingest_closure, pin_ingest_roundtrip]
 ROUTE_PINS = [pin_route_definition, pin_route_properties, pin_route_bruteforce]
+
+
+# ----------------------------------------------------------------------------
+# direct-exposure gain, Eq. (4)
+#
+# Pins take ``x(d[T,S,R], btilde[W,S,R], window) -> dict`` with gain [T,S],
+# makespan [T], window_gain [W,S], window_makespan [W].
+
+_BASE6 = np.array([20, 60, 120, 2, 15, 3], dtype=np.int64) * MS
+
+
+def _gain_by_numpy(d, btilde, window):
+    """F[t,S] is the largest rank total (Theorem 1); replacing stage s by
+    min(d, btilde) changes each rank's total only through that stage."""
+    T, S, R = d.shape
+    F = d.sum(axis=1).max(axis=1)
+    gain = np.empty((T, S), dtype=np.int64)
+    for t in range(T):
+        b = btilde[t // window]
+        for s in range(S):
+            m = d[t].copy()
+            m[s] = np.minimum(m[s], b[s])
+            gain[t, s] = F[t] - m.sum(axis=0).max()
+    return F, gain
+
+
+def pin_gain_sync_wait(x):
+    """Sec. 4: the Sec. 2 stall has a large data share but no single-stage
+    gain against a no-stall baseline, because the other ranks' wait stays in
+    place when only one stage is replaced."""
+    d = stall_case()
+    bt = np.repeat(_BASE6[:, None], 4, axis=1)[None]
+    out = x(d, bt, 1)
+    assert out["gain"][0].tolist() == [0] * 6
+    assert out["makespan"][0] == 250 * MS
+
+
+def pin_gain_direct(x):
+    """A delay no other rank waits for is directly exposed: replacing that
+    stage removes it from the makespan."""
+    d = np.repeat(np.repeat(_BASE6[:, None], 4, axis=1)[None], 3, axis=0)
+    d[:, 4, 1] += 50 * MS                      # rank 1's optimizer, every step
+    d[1, 0, 3] += 7 * MS                       # and a small data delay on step 1
+    bt = np.repeat(_BASE6[:, None], 4, axis=1)[None]
+    out = x(d, bt, 3)
+    assert out["gain"].tolist() == [[0, 0, 0, 0, 50 * MS, 0],
+                                    [0, 0, 0, 0, 43 * MS, 0],
+                                    [0, 0, 0, 0, 50 * MS, 0]]
+    assert out["makespan"].tolist() == [270 * MS, 270 * MS, 270 * MS]
+    assert out["window_gain"][0].tolist() == [0, 0, 0, 0, 143 * MS, 0]
+    assert out["window_makespan"].tolist() == [810 * MS]
+
+
+def pin_gain_bounds(x):
+    """0 <= gain <= the largest reduction of any rank at that stage; a
+    baseline at or above every duration gives 0; a zero baseline removes the
+    stage; window sums are the sums of the steps."""
+    rng = np.random.Generator(np.random.PCG64(40))
+    for (T, S, R, window) in [(20, 6, 8, 7), (9, 3, 1, 4), (12, 12, 33, 12), (5, 2, 64, 1)]:
+        d = rng.integers(0, 10**6, size=(T, S, R), dtype=np.int64)
+        W = -(-T // window)
+        bt = rng.integers(0, 10**6, size=(W, S, R), dtype=np.int64)
+        out = x(d, bt, window)
+        F, g = _gain_by_numpy(d, bt, window)
+        assert np.array_equal(out["makespan"], F) and np.array_equal(out["gain"], g)
+        for t in range(T):
+            red = np.maximum(0, d[t] - bt[t // window]).max(axis=1)
+            assert (out["gain"][t] >= 0).all() and (out["gain"][t] <= red).all()
+        for w in range(W):
+            sl = slice(w * window, min(T, (w + 1) * window))
+            assert np.array_equal(out["window_gain"][w], out["gain"][sl].sum(axis=0))
+            assert out["window_makespan"][w] == out["makespan"][sl].sum()
+        hi = np.full_like(bt, 10**7)
+        assert (x(d, hi, window)["gain"] == 0).all()
+        zero = np.zeros_like(bt)
+        gz = x(d, zero, window)["gain"]
+        tot = d.sum(axis=1)
+        for s in range(S):
+            assert np.array_equal(gz[:, s], F - (tot - d[:, s]).max(axis=1))
+
+
+def pin_gain_bruteforce(x):
+    """Every d and btilde in {0,1,2}^(S x R) for R = S = 2 (6561 pairs)."""
+    R, S = 2, 2
+    mats = np.array(list(itertools.product(range(3), repeat=R * S)), dtype=np.int64).reshape(-1, S, R)
+    n = len(mats)
+    d = np.repeat(mats, n, axis=0)
+    bt = np.tile(mats, (n, 1, 1))
+    out = x(d, bt, 1)
+    F = d.sum(axis=1).max(axis=1)
+    for s in range(S):
+        m = d.copy()
+        m[:, s] = np.minimum(d[:, s], bt[:, s])
+        assert np.array_equal(out["gain"][:, s], F - m.sum(axis=1).max(axis=1))
+
+
+def pin_gain_twin(x, pyref):
+    rng = np.random.Generator(np.random.PCG64(41))
+    d = rng.integers(0, 50, size=(7, 4, 5), dtype=np.int64)
+    bt = rng.integers(0, 50, size=(3, 4, 5), dtype=np.int64)
+    out = x(d, bt, 3)
+    ref = pyref.exposure_gain(d.tolist(), bt.tolist(), 3)
+    for k, v in ref.items():
+        assert out[k].tolist() == v, k
+
+
+GAIN_PINS = [pin_gain_sync_wait, pin_gain_direct, pin_gain_bounds, pin_gain_bruteforce]

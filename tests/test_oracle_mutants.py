@@ -82,6 +82,16 @@ MUTANTS = {
                                "while (k < S && (__int128)tau_den * cum <= need) {"),
     "route_tau_inverted": ("sfo_route", "const __int128 need = (__int128)tau_num * total;",
                            "const __int128 need = (__int128)tau_den * total;"),
+    # direct-exposure gain
+    "gain_unclipped": ("sfo_exposure_gain", "if (b < *cell) *cell = b;", "*cell = b;"),
+    "gain_replaces_next_stage": ("sfo_exposure_gain", "int64_t* cell = m + (int64_t)s * R + r;",
+                                 "int64_t* cell = m + (int64_t)((s + 1) % S) * R + r;"),
+    "gain_baseline_of_window0": ("sfo_exposure_gain", "const int64_t b = btilde[(w * S + s) * R + r];",
+                                 "const int64_t b = btilde[(0 * S + s) * R + r];"),
+    "gain_window_sum_skips_first": ("sfo_exposure_gain", "wgain[w * S + s] += g;",
+                                    "if (t % window) wgain[w * S + s] += g;"),
+    "gain_frontier_misses_last_stage": ("last_frontier", "for (int32_t s = 0; s < S; ++s) {",
+                                        "for (int32_t s = 0; s < S - 1; ++s) {"),
 }
 
 
@@ -120,6 +130,11 @@ def _run_all(o):
     for pin in pins.ROUTE_PINS:
         try:
             pin(o.route)
+        except AssertionError:
+            failed.append(pin.__name__)
+    for pin in pins.GAIN_PINS:
+        try:
+            pin(o.exposure_gain)
         except AssertionError:
             failed.append(pin.__name__)
     return failed

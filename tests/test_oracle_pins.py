@@ -77,3 +77,12 @@ def test_route_pin(pin):
 def test_twin_ingest_route():
     pins.pin_ingest_twin(oracle.ingest, oracle.pyref)
     pins.pin_route_twin(oracle.route, oracle.pyref)
+
+
+@pytest.mark.parametrize("pin", pins.GAIN_PINS, ids=lambda p: p.__name__)
+def test_gain_pin(pin):
+    pin(oracle.exposure_gain)
+
+
+def test_twin_gain():
+    pins.pin_gain_twin(oracle.exposure_gain, oracle.pyref)
