@@ -285,6 +285,60 @@ def main() -> int:
         }
         del xs, wall, ing_d, ing_o
 
+        # next row: direct-exposure gain, Eq. (4), against a no-stall baseline
+        # (every rank's stage median of the workload's recipe), per chunk
+        base = torch.tensor([b * synth.MS for b in wl.base_ms], dtype=torch.int64, device=dev)
+        btilde = base.view(1, S, 1).expand(W, S, R).contiguous()
+        g_out = {"gain": torch.empty((T, S), dtype=torch.int64, device=dev),
+                 "makespan": torch.empty((T,), dtype=torch.int64, device=dev),
+                 "window_gain": torch.empty((W, S), dtype=torch.int64, device=dev),
+                 "window_makespan": torch.empty((W,), dtype=torch.int64, device=dev)}
+        g_views = []
+        for t0, t1 in bounds:
+            w0, w1 = t0 // wl.window, -(-t1 // wl.window)
+            g_views.append((d[t0:t1], btilde[w0:w1],
+                            {"gain": g_out["gain"][t0:t1], "makespan": g_out["makespan"][t0:t1],
+                             "window_gain": g_out["window_gain"][w0:w1],
+                             "window_makespan": g_out["window_makespan"][w0:w1]}))
+        for dv, bv, ov in g_views:
+            sf.sf_exposure_gain(dv, bv, wl.window, ov, stream=stream)
+        gt = []
+        for _ in range(max(3, args.steps // 2)):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for dv, bv, ov in g_views:
+                sf.sf_exposure_gain(dv, bv, wl.window, ov, stream=stream)
+            b.record(stream)
+            gt.append((a, b))
+        torch.cuda.synchronize(dev)
+        g_ms = float(np.mean([a.elapsed_time(b) for a, b in gt])) / len(bounds)
+        n_per = T / len(bounds)
+        g_bytes = (8 * T * S * R + 8 * W * S * R + 8 * T * S + 8 * T + 8 * W * S + 8 * W) / len(bounds)
+        g_exact = None
+        if oracle_out:
+            import oracle
+            n_chk = min(16, T)
+            x = synth.generate(wl, 0, n_chk)
+            o = oracle.exposure_gain(x, btilde[:1].cpu().numpy(), wl.window)
+            g_exact = bool(np.array_equal(g_out["gain"][:n_chk].cpu().numpy(), o["gain"]) and
+                           np.array_equal(g_out["makespan"][:n_chk].cpu().numpy(), o["makespan"]))
+        wg = g_out["window_gain"].sum(dim=0).double()
+        wm = float(g_out["window_makespan"].sum())
+        next_rows["exposure_gain"] = {
+            "kernel": "k_exposure_gain (+ k_window_sum)",
+            "bound": "hbm",
+            "launch_ms": g_ms,
+            "algorithmic_bytes_per_launch": g_bytes,
+            "achieved": g_bytes / (g_ms / 1e3) / 1e9,
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": g_bytes / (g_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+            "steps_per_launch": n_per,
+            "G_s_all_windows": [round(float(v) / wm, 6) for v in wg],
+            "bit_exact_first_steps": g_exact,
+        }
+        del btilde, g_out, g_views
+
         # next row: routing candidate set (tau 4/5) of the path's windows
         order = torch.empty((W, S), dtype=torch.int32, device=dev)
         size = torch.empty((W,), dtype=torch.int32, device=dev)

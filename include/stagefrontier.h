@@ -57,6 +57,9 @@ enum {
 /* Largest stage count per call (per-stage partial maxima are staged in
  * on-chip memory). */
 #define SF_MAX_S 512
+/* Largest stage count of sf_exposure_gain (its per-stage reductions are
+ * kept in registers). */
+#define SF_MAX_S_GAIN 64
 /* Every rank-local prefix P[t][r][s] must be below this many ns (about
  * 39 hours) so that the packed key fits in 64 bits. */
 #define SF_MAX_PREFIX_NS ((int64_t)1 << 47)
@@ -166,6 +169,33 @@ int sf_ingest(const int64_t* stages, const int64_t* wall, int64_t T, int32_t R,
 int sf_route(const int64_t* stage_exposed, int64_t W, int32_t S, int64_t tau_num,
              int64_t tau_den, int32_t* out_order, int32_t* out_size,
              sf_stream_t stream);
+
+/*
+ * sf_exposure_gain -- the direct-exposure score of Eq. (4) (Sec. 4).  For
+ * every step t and stage s, stage s of every rank is replaced by the clipped
+ * baseline b = min(d, btilde) and the frontier is recomputed; the gain is
+ * F[t][S-1] - F^(s<-b)[t][S-1] >= 0.  Per window, G_s = out_window_gain[w][s]
+ * / out_window_makespan[w]; the quotient is left to the caller.
+ *
+ *   durations            [T][S][R] int64 ns (as for sf_frontier).
+ *   baseline             [W][S][R] int64 ns: btilde for the steps of window
+ *                        w (a per-rank window median, a cohort median, a
+ *                        no-stall reference, ...).
+ *   T, R, S, window      as for sf_window_summary; S <= SF_MAX_S_GAIN.
+ *   out_gain             [T][S] int64: the gain of each step and stage.
+ *   out_makespan         [T] int64: F[t][S-1], the step's exposed makespan.
+ *   out_window_gain      [W][S] int64: window sums of out_gain.
+ *   out_window_makespan  [W] int64: window sums of out_makespan.
+ *   stream               HIP stream.
+ *
+ * Preconditions as for sf_frontier, and every baseline value must lie in
+ * [0, SF_MAX_PREFIX_NS).  Pointers 8-byte aligned; outputs must not overlap
+ * inputs or each other.  Returns SF_OK, SF_EINVAL or SF_EHIP.
+ */
+int sf_exposure_gain(const int64_t* durations, const int64_t* baseline, int64_t T,
+                     int32_t R, int32_t S, int64_t window, int64_t* out_gain,
+                     int64_t* out_makespan, int64_t* out_window_gain,
+                     int64_t* out_window_makespan, sf_stream_t stream);
 
 /*
  * sf_num_windows -- number of windows W = ceil(T / window) that

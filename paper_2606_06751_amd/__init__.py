@@ -8,9 +8,10 @@ paper_2606_06751_amd`` alone loads nothing.
 __version__ = "0.1.0"
 
 _BINDING_NAMES = ("sf_frontier", "sf_frontier_evidence", "sf_window_summary", "sf_ingest",
-                  "sf_route", "sf_num_windows",
+                  "sf_route", "sf_exposure_gain", "sf_num_windows",
                   "sf_strerror", "sf_version", "StageFrontierError", "SF_OK", "SF_EINVAL", "SF_ERANGE",
-                  "SF_EHIP", "SF_MAX_R", "SF_MAX_S", "SF_MAX_PREFIX_NS")
+                  "SF_EHIP", "SF_MAX_R", "SF_MAX_S", "SF_MAX_S_GAIN",
+                  "SF_MAX_PREFIX_NS")
 
 
 def __getattr__(name):

@@ -18,6 +18,7 @@ from . import build as _build
 SF_OK, SF_EINVAL, SF_ERANGE, SF_EHIP = 0, 1, 2, 3
 SF_MAX_R = 65536
 SF_MAX_S = 512
+SF_MAX_S_GAIN = 64
 SF_MAX_PREFIX_NS = 1 << 47
 
 LIB_PATH = _build.LIB
@@ -44,6 +45,8 @@ def _load() -> ctypes.CDLL:
     lib.sf_ingest.restype = ctypes.c_int
     lib.sf_route.argtypes = [vp, i64, i32, i64, i64, vp, vp, vp]
     lib.sf_route.restype = ctypes.c_int
+    lib.sf_exposure_gain.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp, vp]
+    lib.sf_exposure_gain.restype = ctypes.c_int
     lib.sf_num_windows.argtypes = [i64, i64]
     lib.sf_num_windows.restype = i64
     lib.sf_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp]
@@ -228,6 +231,40 @@ def sf_route(stage_exposed: torch.Tensor, tau_num: int = 4, tau_den: int = 5,
     if rc != SF_OK:
         raise StageFrontierError(rc, "sf_route")
     return out_order, out_size
+
+
+GAIN_FIELDS = ("gain", "makespan", "window_gain", "window_makespan")
+
+
+def sf_exposure_gain(durations: torch.Tensor, baseline: torch.Tensor, window: int,
+                     out: dict | None = None, stream=None) -> dict:
+    """Direct-exposure gain of Eq. (4) (``sf_exposure_gain``).
+
+    ``durations``: int64 GPU tensor [T, S, R]; ``baseline``: int64 [W, S, R]
+    (btilde per window).  Returns a dict keyed by ``GAIN_FIELDS``: ``gain``
+    [T, S], ``makespan`` [T], ``window_gain`` [W, S], ``window_makespan`` [W].
+    G_s of window w is window_gain[w, s] / window_makespan[w].
+    """
+    if durations.dim() != 3:
+        raise ValueError("durations must be [T, S, R]")
+    T, S, R = durations.shape
+    W = sf_num_windows(T, window)
+    if W < 0:
+        raise StageFrontierError(SF_EINVAL, "sf_exposure_gain")
+    _check(durations, "durations", torch.int64, (T, S, R))
+    _check(baseline, "baseline", torch.int64, (W, S, R))
+    shapes = {"gain": (T, S), "makespan": (T,), "window_gain": (W, S), "window_makespan": (W,)}
+    out = dict(out or {})
+    for k, shp in shapes.items():
+        if k not in out:
+            out[k] = torch.empty(shp, dtype=torch.int64, device=durations.device)
+        _check(out[k], k, torch.int64, shp)
+    rc = _lib.sf_exposure_gain(durations.data_ptr(), baseline.data_ptr(), T, R, S, window,
+                               *(out[k].data_ptr() for k in GAIN_FIELDS),
+                               _stream_handle(stream, durations.device))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_exposure_gain")
+    return out
 
 
 def raw_library() -> ctypes.CDLL:

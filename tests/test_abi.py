@@ -26,9 +26,9 @@ def sf():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["sf_frontier", "sf_frontier_evidence", "sf_ingest",
-                                    "sf_num_windows", "sf_route", "sf_strerror", "sf_version",
-                                    "sf_window_summary"]
+    assert declared_functions() == ["sf_exposure_gain", "sf_frontier", "sf_frontier_evidence",
+                                    "sf_ingest", "sf_num_windows", "sf_route", "sf_strerror",
+                                    "sf_version", "sf_window_summary"]
 
 
 def test_every_declared_symbol_is_exported(sf):
@@ -43,6 +43,7 @@ def test_constants_match_header(sf):
         text = fh.read()
     assert "#define SF_MAX_R %d" % sf.SF_MAX_R in text
     assert "#define SF_MAX_S %d" % sf.SF_MAX_S in text
+    assert "#define SF_MAX_S_GAIN %d" % sf.SF_MAX_S_GAIN in text
     for name in ("SF_OK", "SF_EINVAL", "SF_ERANGE", "SF_EHIP"):
         assert re.search(r"%s = %d" % (name, getattr(sf, name)), text), name
 
@@ -144,6 +145,26 @@ def test_ingest_and_route_argument_checks(sf):
     assert route(size=D + 4) == sf.SF_EINVAL
 
 
+def test_gain_argument_checks(sf):
+    lib = sf.raw_library()
+    names = ["d", "b", "g", "m", "wg", "wm"]
+    base = {n: (i + 1) << 40 for i, n in enumerate(names)}
+
+    def call(**kw):
+        a = dict(dict(base, T=100, R=8, S=6, window=10), **kw)
+        return lib.sf_exposure_gain(a["d"], a["b"], a["T"], a["R"], a["S"], a["window"],
+                                    *(a[n] for n in names[2:]), None)
+
+    assert call(T=0) == sf.SF_OK
+    assert call(S=sf.SF_MAX_S_GAIN + 1) == sf.SF_EINVAL
+    assert call(window=0) == sf.SF_EINVAL
+    for n in names:
+        assert call(**{n: None}) == sf.SF_EINVAL, n
+    assert call(b=base["b"] + 4) == sf.SF_EINVAL            # misaligned
+    assert call(g=base["d"] + 8) == sf.SF_EINVAL            # output overlaps input
+    assert call(wm=base["wg"] + 8) == sf.SF_EINVAL          # outputs overlap
+
+
 def test_summary_argument_checks(sf):
     lib = sf.raw_library()
     D = 4 << 40
@@ -187,6 +208,7 @@ def test_ctypes_argtypes_cover_header(sf):
     assert len(lib.sf_frontier.argtypes) == 7
     assert len(lib.sf_frontier_evidence.argtypes) == 11
     assert len(lib.sf_ingest.argtypes) == 8
+    assert len(lib.sf_exposure_gain.argtypes) == 11
     assert len(lib.sf_route.argtypes) == 8
     assert len(lib.sf_window_summary.argtypes) == 10
     assert lib.sf_num_windows.restype is ctypes.c_int64

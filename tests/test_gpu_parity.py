@@ -372,3 +372,68 @@ def test_route_after_window_summary(sf):
     np.testing.assert_array_equal(order.cpu().numpy(), oo)
     np.testing.assert_array_equal(size.cpu().numpy(), os_)
     assert np.array_equal(order.cpu().numpy()[:, :2], top2.cpu().numpy()[:, :, 0])
+
+
+# ----------------------------------------------------------------------------
+# direct-exposure gain, Eq. (4)
+
+GAIN_KEYS = ("gain", "makespan", "window_gain", "window_makespan")
+
+
+def assert_gain_equal(sf, d, bt, window):
+    out = sf.sf_exposure_gain(torch.from_numpy(np.ascontiguousarray(d)).to(DEV),
+                              torch.from_numpy(np.ascontiguousarray(bt)).to(DEV), window)
+    torch.cuda.synchronize()
+    o = oracle.exposure_gain(d, bt, window)
+    for k in GAIN_KEYS:
+        np.testing.assert_array_equal(out[k].cpu().numpy(), o[k], err_msg=k)
+
+
+@pytest.mark.parametrize("R", [1, 2, 3, 15, 16, 17, 31, 64, 65, 127, 128, 129, 255, 256, 257,
+                               1000, 1024, 1025, 4096, 5000, 16384])
+def test_gain_rank_sweep(sf, R):
+    rng = np.random.Generator(np.random.PCG64(R))
+    for S, window in [(6, 4), (12, 5)]:
+        T = max(2, min(24, 60000 // (R * S)))
+        d = rng.integers(0, 10**6, size=(T, S, R), dtype=np.int64)
+        W = -(-T // window)
+        bt = rng.integers(0, 10**6, size=(W, S, R), dtype=np.int64)
+        print("case R=%d S=%d T=%d" % (R, S, T), flush=True)
+        assert_gain_equal(sf, d, bt, window)
+
+
+@pytest.mark.parametrize("S", [1, 2, 7, 8, 9, 16, 17, 32, 33, 64])
+def test_gain_stage_sweep(sf, S):
+    rng = np.random.Generator(np.random.PCG64(S + 100))
+    for R in (8, 200, 1030):
+        T = max(2, min(12, 40000 // (R * S)))
+        d = rng.integers(0, 4, size=(T, S, R), dtype=np.int64)        # heavy ties
+        bt = rng.integers(0, 4, size=(-(-T // 3), S, R), dtype=np.int64)
+        print("case R=%d S=%d T=%d" % (R, S, T), flush=True)
+        assert_gain_equal(sf, d, bt, 3)
+
+
+def test_gain_golden_cases(sf):
+    import pins
+    pins.pin_gain_sync_wait(lambda d, b, w: {k: v.cpu().numpy() for k, v in sf.sf_exposure_gain(
+        torch.from_numpy(d).to(DEV), torch.from_numpy(np.ascontiguousarray(b)).to(DEV), w).items()})
+    pins.pin_gain_direct(lambda d, b, w: {k: v.cpu().numpy() for k, v in sf.sf_exposure_gain(
+        torch.from_numpy(d).to(DEV), torch.from_numpy(np.ascontiguousarray(b)).to(DEV), w).items()})
+
+
+def test_gain_odd_rank_count_and_misaligned(sf):
+    rng = np.random.Generator(np.random.PCG64(7))
+    T, S, R = 10, 6, 301
+    d = rng.integers(0, 10**6, size=(T, S, R), dtype=np.int64)
+    bt = rng.integers(0, 10**6, size=(2, S, R), dtype=np.int64)
+    assert_gain_equal(sf, d, bt, 5)
+    R = 300
+    d = rng.integers(0, 10**6, size=(T, S, R), dtype=np.int64)
+    bt = rng.integers(0, 10**6, size=(2, S, R), dtype=np.int64)
+    flat = torch.zeros(T * S * R + 1, dtype=torch.int64, device=DEV)
+    flat[1:] = torch.from_numpy(d.reshape(-1)).to(DEV)
+    out = sf.sf_exposure_gain(flat[1:].view(T, S, R), torch.from_numpy(bt).to(DEV), 5)
+    torch.cuda.synchronize()
+    o = oracle.exposure_gain(d, bt, 5)
+    for k in GAIN_KEYS:
+        np.testing.assert_array_equal(out[k].cpu().numpy(), o[k], err_msg=k)
