@@ -959,20 +959,22 @@ GainVariant gain_variant()
     return GainVariant{reinterpret_cast<const void*>(&k_exposure_gain<VEC, K, G, WG, SMAX>), G, WG};
 }
 
-// K * SMAX <= 64 keeps the deltas in registers; G covers R in one tile up to
-// 256 * K ranks, larger R loops over tiles.
+// Two ranks per lane keep the deltas of up to 32 stages in registers
+// (K = 1 at 64); G covers R in one tile up to 256 * K ranks, larger R loops
+// over tiles.  Chosen by measurement on MI355X (wider K held more registers
+// and ran up to 2x slower).
 template <int VEC, int K, int SMAX>
 GainVariant pick_gain_g(int R)
 {
     if (R <= 16 * K) return gain_variant<VEC, K, 16, 64, SMAX>();
-    if (R <= 64 * K) return gain_variant<VEC, K, 64, 64, SMAX>();
+    if (R <= 64 * K) return gain_variant<VEC, K, 64, 256, SMAX>();
     return gain_variant<VEC, K, 256, 256, SMAX>();
 }
 
 GainVariant pick_gain(int R, int S, bool vec2)
 {
-    if (S <= 8) return vec2 ? pick_gain_g<2, 8, 8>(R) : pick_gain_g<1, 8, 8>(R);
-    if (S <= 16) return vec2 ? pick_gain_g<2, 4, 16>(R) : pick_gain_g<1, 4, 16>(R);
+    if (S <= 8) return vec2 ? pick_gain_g<2, 2, 8>(R) : pick_gain_g<1, 2, 8>(R);
+    if (S <= 16) return vec2 ? pick_gain_g<2, 2, 16>(R) : pick_gain_g<1, 2, 16>(R);
     if (S <= 32) return vec2 ? pick_gain_g<2, 2, 32>(R) : pick_gain_g<1, 2, 32>(R);
     return pick_gain_g<1, 1, 64>(R);
 }
