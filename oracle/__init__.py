@@ -5,8 +5,8 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 the GPU path and the oracle share no code.
 
 Two independent statements of the same definitions (Sec. 3, Eq. (1) and
-Eq. (2); top-2 routing, the routing candidate set and the localization
-evidence of Sec. 4; the direct-exposure gain of Eq. (4); the per-stage
+Eq. (2); top-2 routing, the routing candidate set, the lag and the
+localization evidence of Sec. 4; the direct-exposure gain of Eq. (4); the per-stage
 baselines of Props. 1-2; the closure of Appendix A):
 
 * ``frontier`` / ``window_summary`` -- plain C nested loops in
@@ -58,6 +58,8 @@ class COracle:
         lib.sfo_route.restype = None
         lib.sfo_exposure_gain.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp]
         lib.sfo_exposure_gain.restype = ctypes.c_int
+        lib.sfo_frontier_lag.argtypes = [vp, i64, i32, i32, vp, vp]
+        lib.sfo_frontier_lag.restype = ctypes.c_int
         self.lib = lib
         self.path = path
 
@@ -127,6 +129,18 @@ class COracle:
             self.lib.sfo_route(exposed.ctypes.data, W, S, tau_num, tau_den,
                                order.ctypes.data, size.ctypes.data)
         return order, size
+
+    def frontier_lag(self, d: np.ndarray):
+        """Lag of the frontier over the (lower) median rank and its
+        increment, [T, S] int64 each (Sec. 4)."""
+        d = np.ascontiguousarray(d, dtype=np.int64)
+        T, S, R = d.shape
+        lag = np.empty((T, S), dtype=np.int64)
+        inc = np.empty((T, S), dtype=np.int64)
+        if T and S and R:
+            if self.lib.sfo_frontier_lag(d.ctypes.data, T, R, S, lag.ctypes.data, inc.ctypes.data):
+                raise MemoryError("oracle scratch allocation failed")
+        return lag, inc
 
     def exposure_gain(self, d: np.ndarray, btilde: np.ndarray, window: int):
         """Eq. (4) numerators and denominators.
@@ -212,7 +226,12 @@ def exposure_gain(d: np.ndarray, btilde: np.ndarray, window: int):
     return _get().exposure_gain(d, btilde, window)
 
 
+def frontier_lag(d: np.ndarray):
+    return _get().frontier_lag(d)
+
+
 from . import pyref  # noqa: E402  (pure-Python twin, no compiled code)
 
-__all__ = ["build", "COracle", "frontier", "frontier_evidence", "ingest", "route", "exposure_gain",
+__all__ = ["build", "COracle", "frontier", "frontier_evidence", "frontier_lag", "ingest", "route",
+           "exposure_gain",
            "window_summary", "num_windows", "pyref"]

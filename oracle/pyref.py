@@ -141,3 +141,23 @@ def exposure_gain(d, btilde, window):
         out["makespan"].append(F)
         out["window_makespan"][w] += F
     return out
+
+
+def frontier_lag(d):
+    """d[t][s][r] -> (lag[t][s], lag_inc[t][s]) with the lower median."""
+    lag, inc = [], []
+    for step in d:
+        R = len(step[0])
+        P = [0] * R
+        prev = 0
+        lt, it = [], []
+        for row in step:
+            P = [p + v for p, v in zip(P, row)]
+            srt = sorted(P)
+            L = srt[-1] - srt[(R - 1) // 2]
+            lt.append(L)
+            it.append(L - prev)
+            prev = L
+        lag.append(lt)
+        inc.append(it)
+    return lag, inc

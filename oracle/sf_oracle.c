@@ -24,6 +24,8 @@
  *   residual stage is max(0, e) and the overlap error max(0, -e).
  *   Sec. 4, routing candidate set: the smallest prefix of stages, ordered by
  *   share, whose cumulative share reaches tau_C.
+ *   Sec. 4, lag: L[t,s] = max_r P[t,r,s] - median_r P[t,r,s] and its
+ *   increment L[t,s] - L[t,s-1] (L[t,-1] = 0, like F).
  *   Sec. 4, Eq. (4), direct exposure: replace stage s on every rank by the
  *   clipped baseline b = min(d, btilde), recompute the frontier, and take
  *   F[t,S] - F^(s<-b)[t,S]; G_s is its window sum over the window sum of
@@ -53,6 +55,9 @@
  *     rank ([W][S][R]), which covers a per-rank window median, a cohort
  *     median or a no-stall reference; the library returns the numerators
  *     and the denominator of G_s as int64 sums, never their quotient;
+ *   - the median of the lag is the lower median, the element of rank
+ *     floor((R - 1) / 2) in ascending order (the middle element for odd R;
+ *     the lower middle for even R, which keeps the lag integer);
  *   - the routing set orders stages like top-2 (exposed total descending,
  *     lower stage first) and compares shares exactly: k stages suffice when
  *     tau_den * (their exposed sum) >= tau_num * (window total).
@@ -66,6 +71,7 @@
  */
 #include <stdint.h>
 #include <stdlib.h>
+#include <string.h>
 
 /* Frontier advances and leaders, Eq. (1).  Returns 0, or -1 if the prefix
  * scratch cannot be allocated. */
@@ -319,5 +325,45 @@ int sfo_exposure_gain(const int64_t* d, const int64_t* btilde, int64_t T, int32_
     }
     free(m);
     free(P);
+    return 0;
+}
+
+static int cmp_i64(const void* a, const void* b)
+{
+    const int64_t x = *(const int64_t*)a, y = *(const int64_t*)b;
+    return (x > y) - (x < y);
+}
+
+/* Lag of the frontier over the median rank (Sec. 4) and its increment.
+ * The median is taken with a library sort of a copy of the prefixes.
+ * Returns 0, or -1 if scratch cannot be allocated. */
+int sfo_frontier_lag(const int64_t* d, int64_t T, int32_t R, int32_t S, int64_t* lag,
+                     int64_t* lag_inc)
+{
+    int64_t* P = (int64_t*)malloc(sizeof(int64_t) * (size_t)(R > 0 ? R : 1));
+    int64_t* sorted = (int64_t*)malloc(sizeof(int64_t) * (size_t)(R > 0 ? R : 1));
+    if (!P || !sorted) {
+        free(P);
+        free(sorted);
+        return -1;
+    }
+    for (int64_t t = 0; t < T; ++t) {
+        for (int32_t r = 0; r < R; ++r) P[r] = 0;
+        int64_t L_prev = 0;
+        for (int32_t s = 0; s < S; ++s) {
+            const int64_t* row = d + (t * S + s) * (int64_t)R;
+            for (int32_t r = 0; r < R; ++r) P[r] += row[r];
+            memcpy(sorted, P, sizeof(int64_t) * (size_t)R);
+            qsort(sorted, (size_t)R, sizeof(int64_t), cmp_i64);
+            const int64_t F = sorted[R - 1];
+            const int64_t median = sorted[(R - 1) / 2];
+            const int64_t L = F - median;
+            lag[t * S + s] = L;
+            lag_inc[t * S + s] = L - L_prev;
+            L_prev = L;
+        }
+    }
+    free(P);
+    free(sorted);
     return 0;
 }

@@ -755,3 +755,80 @@ def pin_gain_twin(x, pyref):
 
 
 GAIN_PINS = [pin_gain_sync_wait, pin_gain_direct, pin_gain_bounds, pin_gain_bruteforce]
+
+
+# ----------------------------------------------------------------------------
+# lag of the frontier over the median rank (Sec. 4)
+#
+# Pins take ``l(d[T,S,R]) -> (lag[T,S], lag_inc[T,S])``.
+
+
+def pin_lag_stall(l):
+    """The Sec. 2 pattern: the stalled rank opens a 30 ms lag at data that
+    closes (-30 ms increment) at bwd, where the others' wait levels them."""
+    lag, inc = l(stall_case())
+    assert lag[0].tolist() == [30 * MS, 30 * MS, 0, 0, 0, 0]
+    assert inc[0].tolist() == [30 * MS, 0, -30 * MS, 0, 0, 0]
+
+
+def pin_lag_library_median(l):
+    """Odd R: numpy's median; even R: the lower middle of numpy's sort."""
+    rng = np.random.Generator(np.random.PCG64(50))
+    for (T, S, R) in [(20, 6, 7), (15, 5, 8), (10, 4, 1), (8, 3, 2), (6, 12, 129), (5, 6, 1000),
+                      (12, 4, 3)]:
+        for hi in (10**9, 3):
+            d = rng.integers(0, hi + 1, size=(T, S, R), dtype=np.int64)
+            lag, inc = l(d)
+            P = np.cumsum(d, axis=1)
+            F = P.max(axis=2)
+            if R % 2:
+                med = np.median(P, axis=2).astype(np.int64)
+            else:
+                med = np.sort(P, axis=2)[:, :, (R - 1) // 2]
+            assert np.array_equal(lag, F - med)
+            assert np.array_equal(np.cumsum(inc, axis=1), lag)
+            assert (lag >= 0).all()
+            if R == 1:
+                assert (lag == 0).all()
+            if R == 2:
+                assert np.array_equal(lag, P.max(axis=2) - P.min(axis=2))
+
+
+def pin_lag_invariants(l):
+    """Relabelling ranks and adding one constant to a stage of every rank
+    leave the lag unchanged; scaling scales it."""
+    rng = np.random.Generator(np.random.PCG64(51))
+    d = rng.integers(0, 10**6, size=(30, 6, 33), dtype=np.int64)
+    lag, inc = l(d)
+    lag2, _ = l(d[:, :, rng.permutation(33)])
+    assert np.array_equal(lag, lag2)
+    dc = d.copy()
+    dc[:, 3] += 777
+    assert np.array_equal(l(dc)[0], lag)
+    assert np.array_equal(l(5 * d)[0], 5 * lag)
+
+
+def pin_lag_bruteforce(l):
+    """Every d in {0,1,2}^(S x R) for (R, S) in {(3, 2), (4, 2), (2, 3)}."""
+    for (R, S) in [(3, 2), (4, 2), (2, 3)]:
+        cases = list(itertools.product(range(3), repeat=R * S))
+        d = np.array(cases, dtype=np.int64).reshape(len(cases), S, R)
+        lag, inc = l(d)
+        for i, flat in enumerate(cases):
+            prev = 0
+            for s in range(S):
+                sums = sorted(sum(flat[j * R + r] for j in range(s + 1)) for r in range(R))
+                L = sums[-1] - sums[(R - 1) // 2]
+                assert lag[i, s] == L and inc[i, s] == L - prev
+                prev = L
+
+
+def pin_lag_twin(l, pyref):
+    rng = np.random.Generator(np.random.PCG64(52))
+    d = rng.integers(0, 20, size=(6, 5, 9), dtype=np.int64)
+    lag, inc = l(d)
+    pl, pi = pyref.frontier_lag(d.tolist())
+    assert lag.tolist() == pl and inc.tolist() == pi
+
+
+LAG_PINS = [pin_lag_stall, pin_lag_library_median, pin_lag_invariants, pin_lag_bruteforce]

@@ -92,6 +92,15 @@ MUTANTS = {
                                     "if (t % window) wgain[w * S + s] += g;"),
     "gain_frontier_misses_last_stage": ("last_frontier", "for (int32_t s = 0; s < S; ++s) {",
                                         "for (int32_t s = 0; s < S - 1; ++s) {"),
+    # lag
+    "lag_upper_median": ("sfo_frontier_lag", "const int64_t median = sorted[(R - 1) / 2];",
+                         "const int64_t median = sorted[R / 2];"),
+    "lag_of_durations": ("sfo_frontier_lag", "memcpy(sorted, P, sizeof(int64_t) * (size_t)R);",
+                         "memcpy(sorted, row, sizeof(int64_t) * (size_t)R);"),
+    "lag_increment_not_reset": ("sfo_frontier_lag", "int64_t L_prev = 0;",
+                                "static int64_t L_prev = 0;"),
+    "lag_against_min": ("sfo_frontier_lag", "const int64_t median = sorted[(R - 1) / 2];",
+                        "const int64_t median = sorted[0];"),
 }
 
 
@@ -135,6 +144,11 @@ def _run_all(o):
     for pin in pins.GAIN_PINS:
         try:
             pin(o.exposure_gain)
+        except AssertionError:
+            failed.append(pin.__name__)
+    for pin in pins.LAG_PINS:
+        try:
+            pin(o.frontier_lag)
         except AssertionError:
             failed.append(pin.__name__)
     return failed

@@ -86,3 +86,12 @@ def test_gain_pin(pin):
 
 def test_twin_gain():
     pins.pin_gain_twin(oracle.exposure_gain, oracle.pyref)
+
+
+@pytest.mark.parametrize("pin", pins.LAG_PINS, ids=lambda p: p.__name__)
+def test_lag_pin(pin):
+    pin(oracle.frontier_lag)
+
+
+def test_twin_lag():
+    pins.pin_lag_twin(oracle.frontier_lag, oracle.pyref)
