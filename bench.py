@@ -339,6 +339,44 @@ def main() -> int:
         }
         del btilde, g_out, g_views
 
+        # next row: lag over the median rank (exact radix select per boundary)
+        if R <= sf.SF_MAX_R_LAG:
+            lg = torch.empty((T, S), dtype=torch.int64, device=dev)
+            lgi = torch.empty((T, S), dtype=torch.int64, device=dev)
+            l_views = [(d[t0:t1], lg[t0:t1], lgi[t0:t1]) for t0, t1 in bounds]
+            for dv, a1, a2 in l_views:
+                sf.sf_frontier_lag(dv, a1, a2, stream=stream)
+            lt = []
+            for _ in range(3):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                for dv, a1, a2 in l_views:
+                    sf.sf_frontier_lag(dv, a1, a2, stream=stream)
+                b.record(stream)
+                lt.append((a, b))
+            torch.cuda.synchronize(dev)
+            l_ms = float(np.mean([a.elapsed_time(b) for a, b in lt])) / len(bounds)
+            l_bytes = (8 * T * S * R + 16 * T * S) / len(bounds)
+            l_exact = None
+            if oracle_out:
+                import oracle
+                x = synth.generate(wl, 0, 8)
+                ol, oi = oracle.frontier_lag(x)
+                l_exact = bool(np.array_equal(lg[:8].cpu().numpy(), ol) and
+                               np.array_equal(lgi[:8].cpu().numpy(), oi))
+            next_rows["lag"] = {
+                "kernel": "k_frontier_lag",
+                "bound": "lds (radix select)",
+                "launch_ms": l_ms,
+                "algorithmic_bytes_per_launch": l_bytes,
+                "achieved": l_bytes / (l_ms / 1e3) / 1e9,
+                "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s",
+                "frac": l_bytes / (l_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                "bit_exact_first_steps": l_exact,
+            }
+            del lg, lgi, l_views
+
         # next row: routing candidate set (tau 4/5) of the path's windows
         order = torch.empty((W, S), dtype=torch.int32, device=dev)
         size = torch.empty((W,), dtype=torch.int32, device=dev)

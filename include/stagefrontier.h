@@ -57,6 +57,9 @@ enum {
 /* Largest stage count per call (per-stage partial maxima are staged in
  * on-chip memory). */
 #define SF_MAX_S 512
+/* Largest rank count of sf_frontier_lag (all prefixes of a step are held
+ * on chip at once). */
+#define SF_MAX_R_LAG 16384
 /* Largest stage count of sf_exposure_gain (its per-stage reductions are
  * kept in registers). */
 #define SF_MAX_S_GAIN 64
@@ -196,6 +199,26 @@ int sf_exposure_gain(const int64_t* durations, const int64_t* baseline, int64_t 
                      int32_t R, int32_t S, int64_t window, int64_t* out_gain,
                      int64_t* out_makespan, int64_t* out_window_gain,
                      int64_t* out_window_makespan, sf_stream_t stream);
+
+/*
+ * sf_frontier_lag -- the lag of the frontier over the median rank, one of
+ * the localization signals of Sec. 4: L[t][s] = F[t][s] - median_r P[t][r][s],
+ * and its increment L[t][s] - L[t][s-1] (L[t][-1] = 0).  The median is the
+ * lower median: the prefix of rank floor((R - 1) / 2) in ascending order
+ * (the middle one for odd R), so the lag is an exact integer.
+ *
+ *   durations      [T][S][R] int64 ns (as for sf_frontier).
+ *   T, R, S        0 <= T <= INT32_MAX, 1 <= R <= SF_MAX_R_LAG,
+ *                  1 <= S <= SF_MAX_S.  T == 0 is a no-op.
+ *   out_lag        [T][S] int64 ns, >= 0.
+ *   out_lag_inc    [T][S] int64 ns.
+ *   stream         HIP stream.
+ *
+ * Preconditions, alignment, chunking and overlap rules as for sf_frontier.
+ * Returns SF_OK, SF_EINVAL or SF_EHIP.
+ */
+int sf_frontier_lag(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                    int64_t* out_lag, int64_t* out_lag_inc, sf_stream_t stream);
 
 /*
  * sf_num_windows -- number of windows W = ceil(T / window) that

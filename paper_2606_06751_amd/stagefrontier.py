@@ -19,6 +19,7 @@ SF_OK, SF_EINVAL, SF_ERANGE, SF_EHIP = 0, 1, 2, 3
 SF_MAX_R = 65536
 SF_MAX_S = 512
 SF_MAX_S_GAIN = 64
+SF_MAX_R_LAG = 16384
 SF_MAX_PREFIX_NS = 1 << 47
 
 LIB_PATH = _build.LIB
@@ -47,6 +48,8 @@ def _load() -> ctypes.CDLL:
     lib.sf_route.restype = ctypes.c_int
     lib.sf_exposure_gain.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp, vp]
     lib.sf_exposure_gain.restype = ctypes.c_int
+    lib.sf_frontier_lag.argtypes = [vp, i64, i32, i32, vp, vp, vp]
+    lib.sf_frontier_lag.restype = ctypes.c_int
     lib.sf_num_windows.argtypes = [i64, i64]
     lib.sf_num_windows.restype = i64
     lib.sf_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp]
@@ -265,6 +268,28 @@ def sf_exposure_gain(durations: torch.Tensor, baseline: torch.Tensor, window: in
     if rc != SF_OK:
         raise StageFrontierError(rc, "sf_exposure_gain")
     return out
+
+
+def sf_frontier_lag(durations: torch.Tensor, out_lag: torch.Tensor | None = None,
+                    out_lag_inc: torch.Tensor | None = None, stream=None):
+    """Lag of the frontier over the (lower) median rank and its increment
+    (``sf_frontier_lag``).  Returns ``(out_lag [T, S], out_lag_inc [T, S])``."""
+    if durations.dim() != 3:
+        raise ValueError("durations must be [T, S, R]")
+    T, S, R = durations.shape
+    _check(durations, "durations", torch.int64, (T, S, R))
+    dev = durations.device
+    if out_lag is None:
+        out_lag = torch.empty((T, S), dtype=torch.int64, device=dev)
+    if out_lag_inc is None:
+        out_lag_inc = torch.empty((T, S), dtype=torch.int64, device=dev)
+    _check(out_lag, "out_lag", torch.int64, (T, S))
+    _check(out_lag_inc, "out_lag_inc", torch.int64, (T, S))
+    rc = _lib.sf_frontier_lag(durations.data_ptr(), T, R, S, out_lag.data_ptr(),
+                              out_lag_inc.data_ptr(), _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_frontier_lag")
+    return out_lag, out_lag_inc
 
 
 def raw_library() -> ctypes.CDLL:

@@ -27,8 +27,8 @@ def sf():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == ["sf_exposure_gain", "sf_frontier", "sf_frontier_evidence",
-                                    "sf_ingest", "sf_num_windows", "sf_route", "sf_strerror",
-                                    "sf_version", "sf_window_summary"]
+                                    "sf_frontier_lag", "sf_ingest", "sf_num_windows", "sf_route",
+                                    "sf_strerror", "sf_version", "sf_window_summary"]
 
 
 def test_every_declared_symbol_is_exported(sf):
@@ -44,6 +44,7 @@ def test_constants_match_header(sf):
     assert "#define SF_MAX_R %d" % sf.SF_MAX_R in text
     assert "#define SF_MAX_S %d" % sf.SF_MAX_S in text
     assert "#define SF_MAX_S_GAIN %d" % sf.SF_MAX_S_GAIN in text
+    assert "#define SF_MAX_R_LAG %d" % sf.SF_MAX_R_LAG in text
     for name in ("SF_OK", "SF_EINVAL", "SF_ERANGE", "SF_EHIP"):
         assert re.search(r"%s = %d" % (name, getattr(sf, name)), text), name
 
@@ -165,6 +166,23 @@ def test_gain_argument_checks(sf):
     assert call(wm=base["wg"] + 8) == sf.SF_EINVAL          # outputs overlap
 
 
+def test_lag_argument_checks(sf):
+    lib = sf.raw_library()
+
+    def call(**kw):
+        a = dict(dict(d=A, T=10, R=8, S=6, lag=B, inc=C), **kw)
+        return lib.sf_frontier_lag(a["d"], a["T"], a["R"], a["S"], a["lag"], a["inc"], None)
+
+    assert call(T=0, d=None, lag=None, inc=None) == sf.SF_OK
+    assert call(R=sf.SF_MAX_R_LAG + 1) == sf.SF_EINVAL
+    assert call(S=0) == sf.SF_EINVAL
+    assert call(inc=None) == sf.SF_EINVAL
+    assert call(lag=B + 4) == sf.SF_EINVAL
+    assert call(lag=A + 8) == sf.SF_EINVAL                  # output overlaps input
+    assert call(inc=B + 8) == sf.SF_EINVAL                  # outputs overlap
+    assert call(T=1 << 32, R=1, S=1) == sf.SF_EINVAL        # one workgroup per step
+
+
 def test_summary_argument_checks(sf):
     lib = sf.raw_library()
     D = 4 << 40
@@ -209,6 +227,7 @@ def test_ctypes_argtypes_cover_header(sf):
     assert len(lib.sf_frontier_evidence.argtypes) == 11
     assert len(lib.sf_ingest.argtypes) == 8
     assert len(lib.sf_exposure_gain.argtypes) == 11
+    assert len(lib.sf_frontier_lag.argtypes) == 7
     assert len(lib.sf_route.argtypes) == 8
     assert len(lib.sf_window_summary.argtypes) == 10
     assert lib.sf_num_windows.restype is ctypes.c_int64

@@ -437,3 +437,53 @@ def test_gain_odd_rank_count_and_misaligned(sf):
     o = oracle.exposure_gain(d, bt, 5)
     for k in GAIN_KEYS:
         np.testing.assert_array_equal(out[k].cpu().numpy(), o[k], err_msg=k)
+
+
+# ----------------------------------------------------------------------------
+# lag over the median rank (Sec. 4)
+
+def assert_lag_equal(sf, d):
+    lag, inc = sf.sf_frontier_lag(torch.from_numpy(np.ascontiguousarray(d)).to(DEV))
+    torch.cuda.synchronize()
+    ol, oi = oracle.frontier_lag(d)
+    np.testing.assert_array_equal(lag.cpu().numpy(), ol)
+    np.testing.assert_array_equal(inc.cpu().numpy(), oi)
+
+
+@pytest.mark.parametrize("R", [1, 2, 3, 7, 64, 65, 127, 128, 129, 256, 300, 512, 513, 1000,
+                               1024, 2047, 4096, 5000, 8192, 10001, 16384])
+def test_lag_rank_sweep(sf, R):
+    rng = np.random.Generator(np.random.PCG64(R + 7))
+    T = max(2, min(40, 200000 // (R * 6)))
+    for hi in (3, 10**6, 1 << 40):               # ties, moderate, wide range (6 radix passes)
+        d = rng.integers(0, hi + 1, size=(T, 6, R), dtype=np.int64)
+        d[0] = 5                                 # a step where every prefix is equal
+        if R > 2:
+            d[1, 2, R // 3] += 1 << 44           # one outlier rank
+        print("case R=%d hi=%d T=%d" % (R, hi, T), flush=True)
+        assert_lag_equal(sf, d)
+
+
+@pytest.mark.parametrize("S", [1, 2, 12, 100, 512])
+def test_lag_stage_sweep(sf, S):
+    rng = np.random.Generator(np.random.PCG64(S + 11))
+    for R in (9, 1030):
+        T = max(2, min(16, 100000 // (R * S)))
+        d = rng.integers(0, 10**7, size=(T, S, R), dtype=np.int64)
+        assert_lag_equal(sf, d)
+
+
+def test_lag_stall_and_odd_base(sf):
+    import pins
+    lag, inc = sf.sf_frontier_lag(torch.from_numpy(pins.stall_case()).to(DEV))
+    torch.cuda.synchronize()
+    assert lag.cpu().numpy()[0].tolist() == [30 * pins.MS, 30 * pins.MS, 0, 0, 0, 0]
+    T, S, R = 7, 5, 402
+    d = synth.random_durations(T, S, R, seed=3, hi=10**5)
+    flat = torch.zeros(T * S * R + 1, dtype=torch.int64, device=DEV)
+    flat[1:] = torch.from_numpy(d.reshape(-1)).to(DEV)
+    lag, inc = sf.sf_frontier_lag(flat[1:].view(T, S, R))
+    torch.cuda.synchronize()
+    ol, oi = oracle.frontier_lag(d)
+    np.testing.assert_array_equal(lag.cpu().numpy(), ol)
+    np.testing.assert_array_equal(inc.cpu().numpy(), oi)

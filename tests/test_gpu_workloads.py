@@ -133,3 +133,19 @@ def test_workload_ingest_and_route(sf, name):
     np.testing.assert_array_equal(go2.cpu().numpy(), oo2)
     np.testing.assert_array_equal(gs2.cpu().numpy(), os2)
     log("route ok: %s, %d windows, sizes %s" % (name, len(ex), np.bincount(os2).tolist()))
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workload_lag(sf, name):
+    """The lag over the median rank on sampled step ranges of every
+    workload (the oracle sorts R prefixes per boundary)."""
+    wl = synth.WORKLOADS[name]
+    n = min(wl.T, 600 if wl.R <= 1024 else 60)
+    for t0 in sorted({0, wl.T // 2, wl.T - n}):
+        x = synth.generate(wl, t0, t0 + n)
+        lag, inc = sf.sf_frontier_lag(torch.from_numpy(x).to("cuda:0"))
+        torch.cuda.synchronize()
+        ol, oi = oracle.frontier_lag(x)
+        np.testing.assert_array_equal(lag.cpu().numpy(), ol)
+        np.testing.assert_array_equal(inc.cpu().numpy(), oi)
+    log("lag ok: %s (%d steps x 3 ranges)" % (name, n))
