@@ -29,7 +29,10 @@ METRIC = "rank·stage samples/sec and achieved HBM GB/s (% of peak), bit-exact"
 UNIT = "rank·stage samples/s"
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E, AMD published peak
 DEFAULT_WORKLOAD = "r16384_s12_t20k"
-KERNEL_SRC = os.path.join(ROOT, "paper_2606_06751_amd", "csrc", "stagefrontier.hip")
+CSRC = os.path.join(ROOT, "paper_2606_06751_amd", "csrc")
+# the source k_frontier is built from: its translation unit and the headers
+# it includes
+FRONTIER_SOURCES = [os.path.join(CSRC, f) for f in ("frontier.hip", "sf_device.h", "sf_host.h")]
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "k_frontier_%s_hbm_counters.txt")
 
 
@@ -37,18 +40,13 @@ def log(msg: str) -> None:
     print("[bench %s] %s" % (time.strftime("%H:%M:%S"), msg), file=sys.stderr, flush=True)
 
 
-# k_frontier and everything it depends on (includes, lane helpers, launch
-# table) precede this section header in the source; later sections hold
-# other kernels and the C ABI.
-FRONTIER_SECTION_END = b"// window kernels"
-
-
 def kernel_source_hash() -> str:
     """Hash of the source text k_frontier is built from."""
-    with open(KERNEL_SRC, "rb") as fh:
-        text = fh.read()
-    cut = text.find(FRONTIER_SECTION_END)
-    return hashlib.sha256(text[:cut] if cut >= 0 else text).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in FRONTIER_SOURCES:
+        with open(path, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(workload: str):

@@ -1,0 +1,190 @@
+// gain.hip -- direct-exposure gain, Eq. (4).  Replacing stage s of every rank by
+// b = min(d, btilde) changes the last frontier F[t,S] = max_r P[t,r,S] only
+// through the rank totals: F^(s<-b)[t,S] = max_r (P[t,r,S] - delta[r,s]) with
+// delta = max(0, d - btilde).  Step group layout as in k_frontier; each lane
+// keeps its ranks' totals and the deltas of all stages in registers (the
+// stage loop is unrolled to SMAX, rows past S re-read row 0 and are
+// ignored), then every stage's candidate max and the plain max go through
+// the idempotent DPP max, so lane slots past R (which re-read rank r0) need
+// no masking.  Partial maxima of several tiles or groups meet in LDS.
+
+#include "sf_device.h"
+#include "sf_host.h"
+
+namespace sfk {
+
+template <int VEC, int K, int G, int WG, int SMAX>
+__global__ __launch_bounds__(WG) void k_exposure_gain(
+    const int64_t* __restrict__ d, const int64_t* __restrict__ btilde, int64_t T, int R, int S,
+    int64_t window, int64_t* __restrict__ gain, int64_t* __restrict__ makespan)
+{
+    static_assert(K % VEC == 0 && (WG % G == 0 || G == WG), "shape");
+    constexpr int SUB = G < 64 ? G : 64;
+    constexpr int SPW = WG / G;
+    constexpr int SPS = G / SUB;
+    constexpr int NLD = K / VEC;
+    constexpr int RT = G * K;
+    constexpr int NCOL = SMAX + 1;  // SMAX replaced-stage maxima, then F
+
+    __shared__ u64 tab[(WG / SUB) * NCOL];
+
+    const int tid = threadIdx.x;
+    const int gl = tid % G;
+    const int slot = tid / SUB;
+    const bool writer = (tid % SUB) == SUB - 1;
+    const int64_t tb = (int64_t)blockIdx.x * SPW;
+    const int64_t t = tb + tid / G;
+
+    if (t < T) {
+        const int64_t* dt = d + t * (int64_t)S * R;
+        const int64_t* bw = btilde + (t / window) * (int64_t)S * R;
+        for (int r0 = 0; r0 < R; r0 += RT) {
+            int idx[NLD];
+#pragma unroll
+            for (int l = 0; l < NLD; ++l) {
+                const int r = r0 + (l * G + gl) * VEC;
+                idx[l] = r < R ? r : r0;
+            }
+            int64_t tot[K];
+            int64_t dl[K][SMAX];
+#pragma unroll
+            for (int k = 0; k < K; ++k) tot[k] = 0;
+#pragma unroll
+            for (int s = 0; s < SMAX; ++s) {
+                const int sr = s < S ? s : 0;
+                const int64_t* row = dt + (int64_t)sr * R;
+                const int64_t* brow = bw + (int64_t)sr * R;
+#pragma unroll
+                for (int l = 0; l < NLD; ++l) {
+                    int64_t x[VEC], y[VEC];
+                    if (VEC == 2) {
+                        const v2i64 a = __builtin_nontemporal_load(reinterpret_cast<const v2i64*>(row + idx[l]));
+                        const v2i64 b = *reinterpret_cast<const v2i64*>(brow + idx[l]);
+                        x[0] = a.x;
+                        x[VEC - 1] = a.y;
+                        y[0] = b.x;
+                        y[VEC - 1] = b.y;
+                    } else {
+                        x[0] = __builtin_nontemporal_load(row + idx[l]);
+                        y[0] = brow[idx[l]];
+                    }
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) {
+                        const int k = l * VEC + e;
+                        const int64_t red = x[e] - y[e];
+                        dl[k][s] = red > 0 ? red : 0;
+                        if (s < S) tot[k] += x[e];
+                    }
+                }
+            }
+            u64 fmax = 0;
+#pragma unroll
+            for (int k = 0; k < K; ++k) fmax = umax64(fmax, (u64)tot[k]);
+            fmax = group_max<SUB>(fmax);
+            if (writer) {
+                u64* p = &tab[slot * NCOL + SMAX];
+                *p = (r0 == 0) ? fmax : umax64(*p, fmax);
+            }
+#pragma unroll
+            for (int s = 0; s < SMAX; ++s) {
+                if (s < S) {
+                    u64 m = 0;
+#pragma unroll
+                    for (int k = 0; k < K; ++k) m = umax64(m, (u64)(tot[k] - dl[k][s]));
+                    m = group_max<SUB>(m);
+                    if (writer) {
+                        u64* p = &tab[slot * NCOL + s];
+                        *p = (r0 == 0) ? m : umax64(*p, m);
+                    }
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    for (int i = tid; i < SPW * S; i += WG) {
+        const int jj = i / S;
+        const int s = i - jj * S;
+        const int64_t tt = tb + jj;
+        if (tt >= T) break;
+        u64 F = 0, Fr = 0;
+#pragma unroll
+        for (int qd = 0; qd < SPS; ++qd) {
+            F = umax64(F, tab[(jj * SPS + qd) * NCOL + SMAX]);
+            Fr = umax64(Fr, tab[(jj * SPS + qd) * NCOL + s]);
+        }
+        gain[tt * S + s] = (int64_t)F - (int64_t)Fr;
+        if (s == 0) makespan[tt] = (int64_t)F;
+    }
+}
+
+struct GainVariant {
+    const void* fn;
+    int G, WG;
+};
+
+template <int VEC, int K, int G, int WG, int SMAX>
+GainVariant gain_variant()
+{
+    return GainVariant{reinterpret_cast<const void*>(&k_exposure_gain<VEC, K, G, WG, SMAX>), G, WG};
+}
+
+// Two ranks per lane keep the deltas of up to 32 stages in registers
+// (K = 1 at 64); G covers R in one tile up to 256 * K ranks, larger R loops
+// over tiles.  Chosen by measurement on MI355X (wider K held more registers
+// and ran up to 2x slower).
+template <int VEC, int K, int SMAX>
+GainVariant pick_gain_g(int R)
+{
+    if (R <= 16 * K) return gain_variant<VEC, K, 16, 64, SMAX>();
+    if (R <= 64 * K) return gain_variant<VEC, K, 64, 256, SMAX>();
+    return gain_variant<VEC, K, 256, 256, SMAX>();
+}
+
+GainVariant pick_gain(int R, int S, bool vec2)
+{
+    if (S <= 8) return vec2 ? pick_gain_g<2, 2, 8>(R) : pick_gain_g<1, 2, 8>(R);
+    if (S <= 16) return vec2 ? pick_gain_g<2, 2, 16>(R) : pick_gain_g<1, 2, 16>(R);
+    if (S <= 32) return vec2 ? pick_gain_g<2, 2, 32>(R) : pick_gain_g<1, 2, 32>(R);
+    return pick_gain_g<1, 1, 64>(R);
+}
+
+}  // namespace sfk
+
+using namespace sfk;
+
+SF_API int sf_exposure_gain(const int64_t* durations, const int64_t* baseline, int64_t T,
+                            int32_t R, int32_t S, int64_t window, int64_t* out_gain,
+                            int64_t* out_makespan, int64_t* out_window_gain,
+                            int64_t* out_window_makespan, sf_stream_t stream)
+{
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S_GAIN || window < 1)
+        return SF_EINVAL;
+    if (!fits(T, S, R, 8)) return SF_EINVAL;
+    if (T == 0) return SF_OK;
+    const int64_t W = sf_num_windows(T, window);
+    if (!fits(W, S, R, 8)) return SF_EINVAL;
+    const void* bufs[6] = {durations, baseline, out_gain, out_makespan, out_window_gain,
+                           out_window_makespan};
+    const int64_t sizes[6] = {T * S * (int64_t)R * 8, W * S * (int64_t)R * 8, T * S * 8, T * 8,
+                              W * S * 8, W * 8};
+    for (int a = 0; a < 6; ++a)
+        if (!bufs[a] || !aligned(bufs[a], 8)) return SF_EINVAL;
+    for (int a = 0; a < 6; ++a)
+        for (int b = (a < 2 ? 2 : a + 1); b < 6; ++b)
+            if (!disjoint(bufs[a], sizes[a], bufs[b], sizes[b])) return SF_EINVAL;
+
+    const bool vec2 = (R % 2 == 0) && aligned(durations, 16) && aligned(baseline, 16);
+    const GainVariant v = pick_gain(R, S, vec2);
+    const int spw = v.WG / v.G;
+    const int64_t blocks = (T + spw - 1) / spw;
+    if (blocks > INT32_MAX) return SF_EINVAL;
+    int Ri = R, Si = S;
+    void* a1[] = {(void*)&durations, (void*)&baseline, (void*)&T, (void*)&Ri, (void*)&Si,
+                  (void*)&window, (void*)&out_gain, (void*)&out_makespan};
+    int rc = launch(v.fn, dim3((unsigned)blocks), dim3(v.WG), a1, 0, stream);
+    if (rc != SF_OK) return rc;
+    rc = launch_window_sum(out_gain, T, S, window, W, out_window_gain, stream);
+    if (rc != SF_OK) return rc;
+    return launch_window_sum(out_makespan, T, 1, window, W, out_window_makespan, stream);
+}

@@ -1,0 +1,233 @@
+// window.hip -- sf_window_summary and sf_num_windows: window sums of the
+// advances (Eq. (2) numerators), leader counts and top-2 routing (Sec. 4);
+// and the generic window sum used by sf_exposure_gain.
+//
+// Window kernels.  One workgroup per (window, stage, rank chunk) builds the
+// leader histogram of the window in LDS with LDS atomics and sums the
+// advances; one workgroup per window then picks the two largest stages and
+// their most frequent leaders.
+
+#include "sf_device.h"
+#include "sf_host.h"
+
+namespace sfk {
+
+constexpr int kHistChunk = 16384;  // ranks per histogram workgroup (64 KB LDS)
+
+// One workgroup per (window, stage, rank chunk); grid-stride over them.
+__global__ __launch_bounds__(kSumWG) void k_window_counts(
+    const int64_t* __restrict__ inc, const int32_t* __restrict__ lead, int64_t T, int R, int S,
+    int64_t window, int64_t W, int nchunk, int64_t* __restrict__ exposed,
+    int32_t* __restrict__ counts)
+{
+    extern __shared__ int32_t hist[];  // [min(R, kHistChunk)]
+    __shared__ int64_t part[kSumWG / 64];
+    const int tid = threadIdx.x;
+    const int64_t total = W * S * nchunk;
+    for (int64_t id = blockIdx.x; id < total; id += gridDim.x) {
+        const int c = (int)(id % nchunk);
+        const int64_t ws = id / nchunk;
+        const int s = (int)(ws % S);
+        const int64_t w = ws / S;
+        const int lo = c * kHistChunk;
+        const int n = min(kHistChunk, R - lo);
+        const int64_t t0 = w * window;
+        const int64_t t1 = min(t0 + window, T);
+
+        for (int i = tid; i < n; i += kSumWG) hist[i] = 0;
+        __syncthreads();
+        for (int64_t t = t0 + tid; t < t1; t += kSumWG) {
+            const int64_t r = (int64_t)lead[t * S + s] - lo;
+            if (r >= 0 && r < n) atomicAdd(&hist[r], 1);
+        }
+        if (c == 0) {
+            int64_t sum = 0;
+            for (int64_t t = t0 + tid; t < t1; t += kSumWG) sum += inc[t * S + s];
+            sum = wave_sum64(sum);
+            if ((tid & 63) == 0) part[tid >> 6] = sum;
+        }
+        __syncthreads();
+        if (c == 0 && tid == 0) {
+            int64_t sum = 0;
+            for (int i = 0; i < kSumWG / 64; ++i) sum += part[i];
+            exposed[w * S + s] = sum;
+        }
+        int32_t* out = counts + (w * S + s) * (int64_t)R + lo;
+        for (int i = tid; i < n; i += kSumWG) out[i] = hist[i];
+        __syncthreads();  // hist and part are reused by the next id
+    }
+}
+
+constexpr int kTopWG = 256;
+
+// Block-wide max of a 64-bit key; every thread gets the result.
+__device__ __forceinline__ u64 block_max64(u64 v, u64* sh)
+{
+    for (int off = 32; off > 0; off >>= 1) {
+        const u64 o = __shfl_xor(v, off, 64);
+        v = umax64(v, o);
+    }
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+    __syncthreads();
+    u64 r = sh[0];
+    for (int i = 1; i < kTopWG / 64; ++i) r = umax64(r, sh[i]);
+    __syncthreads();
+    return r;
+}
+
+// Largest lead count of one counts row as a packed (count, lowest rank) key;
+// every thread gets the block result.
+__device__ __forceinline__ u64 row_modal_key(const int32_t* __restrict__ c, int R, u64* sh)
+{
+    const int tid = threadIdx.x;
+    u64 b0 = 0, b1 = 0, b2 = 0, b3 = 0;
+    auto key = [](int32_t cnt, int r) {
+        return ((u64)(uint32_t)cnt << 32) | (u64)(0xFFFFFFFFu - (uint32_t)r);
+    };
+    if ((R & 3) == 0 && (((uintptr_t)c) & 15) == 0) {
+        const int4* c4 = reinterpret_cast<const int4*>(c);
+        const int n4 = R >> 2;
+        for (int i = tid; i < n4; i += kTopWG) {
+            const int4 x = c4[i];
+            const int r = i << 2;
+            b0 = umax64(b0, key(x.x, r));
+            b1 = umax64(b1, key(x.y, r + 1));
+            b2 = umax64(b2, key(x.z, r + 2));
+            b3 = umax64(b3, key(x.w, r + 3));
+        }
+    } else {
+        for (int r = tid; r < R; r += kTopWG) b0 = umax64(b0, key(c[r], r));
+    }
+    return block_max64(umax64(umax64(b0, b1), umax64(b2, b3)), sh);
+}
+
+// One workgroup per (window, pick k in {0, 1}); grid-stride.  Both
+// workgroups of a window choose the two stages (cheap: S <= SF_MAX_S); each
+// then finds the most frequent leader of its own stage.
+__global__ __launch_bounds__(kTopWG) void k_window_top2(const int64_t* __restrict__ exposed,
+                                                        const int32_t* __restrict__ counts,
+                                                        int R, int S, int64_t W,
+                                                        int32_t* __restrict__ top2)
+{
+    __shared__ u64 sh[kTopWG / 64];
+    const int tid = threadIdx.x;
+    for (int64_t id = blockIdx.x; id < 2 * W; id += gridDim.x) {
+        const int64_t w = id >> 1;
+        const int k = (int)(id & 1);
+        const int64_t* ex = exposed + w * S;
+        int pick0 = -1, pick = -1;
+        for (int kk = 0; kk <= k; ++kk) {
+            // larger exposed total first, then lower stage index
+            int64_t be = 0;
+            int bs = -1;
+            for (int s = tid; s < S; s += kTopWG) {
+                if (s == pick0) continue;
+                const int64_t e = ex[s];
+                if (bs < 0 || e > be) { be = e; bs = s; }
+            }
+            // two block maxima: the largest total (sign bit flipped, so that
+            // unsigned order is signed order), then the lowest stage among
+            // the threads holding it; threads without a stage cannot win
+            const u64 ekey = bs < 0 ? 0ull : ((u64)be ^ 0x8000000000000000ull);
+            const u64 emax = block_max64(ekey, sh);
+            const u64 skey = (bs >= 0 && ekey == emax) ? (u64)(0xFFFFFFFFu - (uint32_t)bs) + 1ull : 0ull;
+            const u64 smax = block_max64(skey, sh);
+            pick = smax ? (int)(0xFFFFFFFFu - (uint32_t)(smax - 1ull)) : -1;
+            pick0 = pick;
+        }
+        int rank = -1;
+        if (pick >= 0) {
+            const u64 m = row_modal_key(counts + (w * S + pick) * (int64_t)R, R, sh);
+            rank = (m >> 32) ? (int)(0xFFFFFFFFu - (uint32_t)(m & 0xFFFFFFFFull)) : -1;
+        }
+        if (tid == 0) {
+            top2[w * 4 + 2 * k] = pick;
+            top2[w * 4 + 2 * k + 1] = rank;
+        }
+    }
+}
+
+// Segmented sums over windows of the columns of a [T][C] int64 array: one
+// workgroup per (window, column); grid-stride.
+__global__ __launch_bounds__(kSumWG) void k_window_sum(const int64_t* __restrict__ x, int64_t T,
+                                                       int C, int64_t window, int64_t W,
+                                                       int64_t* __restrict__ out)
+{
+    __shared__ int64_t part[kSumWG / 64];
+    const int tid = threadIdx.x;
+    for (int64_t id = blockIdx.x; id < W * C; id += gridDim.x) {
+        const int64_t w = id / C;
+        const int c = (int)(id - w * C);
+        const int64_t t0 = w * window;
+        const int64_t t1 = min(t0 + window, T);
+        int64_t sum = 0;
+        for (int64_t t = t0 + tid; t < t1; t += kSumWG) sum += x[t * C + c];
+        sum = wave_sum64(sum);
+        if ((tid & 63) == 0) part[tid >> 6] = sum;
+        __syncthreads();
+        if (tid == 0) {
+            int64_t acc = 0;
+            for (int i = 0; i < kSumWG / 64; ++i) acc += part[i];
+            out[w * C + c] = acc;
+        }
+        __syncthreads();
+    }
+}
+
+int launch_window_sum(const int64_t* x, int64_t T, int C, int64_t window, int64_t W,
+                      int64_t* out, sf_stream_t stream)
+{
+    const int64_t items = W * C;
+    void* args[] = {(void*)&x, (void*)&T, (void*)&C, (void*)&window, (void*)&W, (void*)&out};
+    return launch(reinterpret_cast<const void*>(&k_window_sum),
+                  dim3((unsigned)(items < 1048576 ? items : 1048576)), dim3(kSumWG), args, 0, stream);
+}
+
+}  // namespace sfk
+
+using namespace sfk;
+
+SF_API int64_t sf_num_windows(int64_t T, int64_t window)
+{
+    if (T < 0 || window < 1) return -1;
+    return T / window + (T % window != 0);
+}
+
+SF_API int sf_window_summary(const int64_t* increment, const int32_t* leader, int64_t T,
+                             int32_t R, int32_t S, int64_t window, int64_t* out_stage_exposed,
+                             int32_t* out_lead_counts, int32_t* out_top2, sf_stream_t stream)
+{
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S || window < 1) return SF_EINVAL;
+    if (!fits(T, S, 1, 8)) return SF_EINVAL;
+    if (T == 0) return SF_OK;
+    const int64_t W = sf_num_windows(T, window);
+    if (!fits(W, S, R, 4)) return SF_EINVAL;
+    if (!increment || !leader || !out_stage_exposed || !out_lead_counts || !out_top2)
+        return SF_EINVAL;
+    if (!aligned(increment, 8) || !aligned(leader, 4) || !aligned(out_stage_exposed, 8) ||
+        !aligned(out_lead_counts, 4) || !aligned(out_top2, 4))
+        return SF_EINVAL;
+    const void* bufs[5] = {increment, leader, out_stage_exposed, out_lead_counts, out_top2};
+    const int64_t sizes[5] = {T * S * 8, T * S * 4, W * S * 8, W * S * (int64_t)R * 4, W * 16};
+    for (int a = 0; a < 5; ++a)
+        for (int b = (a < 2 ? 2 : a + 1); b < 5; ++b)
+            if (!disjoint(bufs[a], sizes[a], bufs[b], sizes[b])) return SF_EINVAL;
+
+    const int nchunk = (R + kHistChunk - 1) / kHistChunk;
+    const int64_t items = W * S * nchunk;
+    const unsigned g1 = (unsigned)(items < 1048576 ? items : 1048576);
+    const size_t lds = (size_t)(R < kHistChunk ? R : kHistChunk) * sizeof(int32_t);
+    int Ri = R, Si = S;
+    int64_t Wl = W;
+    void* a1[] = {(void*)&increment, (void*)&leader, (void*)&T, (void*)&Ri, (void*)&Si,
+                  (void*)&window, (void*)&Wl, (void*)&nchunk, (void*)&out_stage_exposed,
+                  (void*)&out_lead_counts};
+    int rc = launch(reinterpret_cast<const void*>(&k_window_counts), dim3(g1), dim3(kSumWG), a1,
+                    lds, stream);
+    if (rc != SF_OK) return rc;
+    const unsigned g2 = (unsigned)(2 * W < 65536 ? 2 * W : 65536);
+    void* a2[] = {(void*)&out_stage_exposed, (void*)&out_lead_counts, (void*)&Ri, (void*)&Si,
+                  (void*)&Wl, (void*)&out_top2};
+    return launch(reinterpret_cast<const void*>(&k_window_top2), dim3(g2), dim3(kTopWG), a2, 0,
+                  stream);
+}
