@@ -60,6 +60,10 @@ class COracle:
         lib.sfo_exposure_gain.restype = ctypes.c_int
         lib.sfo_frontier_lag.argtypes = [vp, i64, i32, i32, vp, vp]
         lib.sfo_frontier_lag.restype = ctypes.c_int
+        lib.sfo_rank_spread.argtypes = [vp, i64, i32, i32, i64, vp, vp]
+        lib.sfo_rank_spread.restype = ctypes.c_int
+        lib.sfo_window_median.argtypes = [vp, i64, i32, i32, i64, vp]
+        lib.sfo_window_median.restype = ctypes.c_int
         self.lib = lib
         self.path = path
 
@@ -141,6 +145,32 @@ class COracle:
             if self.lib.sfo_frontier_lag(d.ctypes.data, T, R, S, lag.ctypes.data, inc.ctypes.data):
                 raise MemoryError("oracle scratch allocation failed")
         return lag, inc
+
+    def rank_spread(self, d: np.ndarray, window: int):
+        """Raw rank spread of Sec. 6.2: max_r d - (lower) median_r d per
+        step and stage, [T, S], and its window sums, [W, S] (int64)."""
+        d = np.ascontiguousarray(d, dtype=np.int64)
+        T, S, R = d.shape
+        W = num_windows(T, window)
+        spread = np.empty((T, S), dtype=np.int64)
+        wspread = np.zeros((W, S), dtype=np.int64)
+        if T and S and R:
+            if self.lib.sfo_rank_spread(d.ctypes.data, T, R, S, window, spread.ctypes.data,
+                                        wspread.ctypes.data):
+                raise MemoryError("oracle scratch allocation failed")
+        return spread, wspread
+
+    def window_median(self, d: np.ndarray, window: int):
+        """Per-rank window median (a baseline btilde of Eq. (4)): the lower
+        median over each window's steps, [W, S, R] int64."""
+        d = np.ascontiguousarray(d, dtype=np.int64)
+        T, S, R = d.shape
+        W = num_windows(T, window)
+        med = np.empty((W, S, R), dtype=np.int64)
+        if T and S and R:
+            if self.lib.sfo_window_median(d.ctypes.data, T, R, S, window, med.ctypes.data):
+                raise MemoryError("oracle scratch allocation failed")
+        return med
 
     def exposure_gain(self, d: np.ndarray, btilde: np.ndarray, window: int):
         """Eq. (4) numerators and denominators.
@@ -230,8 +260,17 @@ def frontier_lag(d: np.ndarray):
     return _get().frontier_lag(d)
 
 
+def rank_spread(d: np.ndarray, window: int):
+    return _get().rank_spread(d, window)
+
+
+def window_median(d: np.ndarray, window: int):
+    return _get().window_median(d, window)
+
+
 from . import pyref  # noqa: E402  (pure-Python twin, no compiled code)
 
-__all__ = ["build", "COracle", "frontier", "frontier_evidence", "frontier_lag", "ingest", "route",
+__all__ = ["build", "COracle", "frontier", "frontier_evidence", "frontier_lag", "rank_spread",
+           "window_median", "ingest", "route",
            "exposure_gain",
            "window_summary", "num_windows", "pyref"]

@@ -161,3 +161,29 @@ def frontier_lag(d):
         lag.append(lt)
         inc.append(it)
     return lag, inc
+
+
+def rank_spread(d, window):
+    """d[t][s][r] -> (spread[t][s], window sums[w][s]): max minus lower
+    median over ranks (Sec. 6.2)."""
+    spread = [[max(row) - sorted(row)[(len(row) - 1) // 2] for row in step] for step in d]
+    T, S = len(d), len(d[0]) if d else 0
+    W = (T + window - 1) // window
+    wsum = [[0] * S for _ in range(W)]
+    for t in range(T):
+        for s in range(S):
+            wsum[t // window][s] += spread[t][s]
+    return spread, wsum
+
+
+def window_median(d, window):
+    """d[t][s][r] -> med[w][s][r]: lower median over each window's steps
+    (the per-rank window-median baseline of Eq. (4))."""
+    T = len(d)
+    S, R = len(d[0]), len(d[0][0])
+    out = []
+    for t0 in range(0, T, window):
+        steps = d[t0:t0 + window]
+        out.append([[sorted(st[s][r] for st in steps)[(len(steps) - 1) // 2] for r in range(R)]
+                    for s in range(S)])
+    return out

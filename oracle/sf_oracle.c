@@ -33,6 +33,11 @@
  *   Sec. 3, Props. 1 and 2: the per-stage max and mean baselines
  *   M_t = sum_s max_r d and Mbar_t = sum_s (1/R) sum_r d, kept per stage as
  *   max_r d[t,r,s] and sum_r d[t,r,s].
+ *   Sec. 6.2, raw rank spread (a dispersion baseline scored on the same
+ *   window matrix): max_r d[t,r,s] - median_r d[t,r,s], summed over the
+ *   steps of a window.
+ *   Sec. 4, Eq. (4), per-rank window median: a candidate baseline btilde,
+ *   the median over the steps of a window of d[t,r,s], per stage and rank.
  *
  * Readings where the paper leaves a choice open (each is listed with its
  * reason in the design notes of the repository):
@@ -57,7 +62,9 @@
  *     and the denominator of G_s as int64 sums, never their quotient;
  *   - the median of the lag is the lower median, the element of rank
  *     floor((R - 1) / 2) in ascending order (the middle element for odd R;
- *     the lower middle for even R, which keeps the lag integer);
+ *     the lower middle for even R, which keeps the lag integer); the raw
+ *     rank spread and the window median take the lower median likewise
+ *     (over ranks, and over the n steps of a window: rank floor((n-1)/2));
  *   - the routing set orders stages like top-2 (exposed total descending,
  *     lower stage first) and compares shares exactly: k stages suffice when
  *     tau_den * (their exposed sum) >= tau_num * (window total).
@@ -365,5 +372,57 @@ int sfo_frontier_lag(const int64_t* d, int64_t T, int32_t R, int32_t S, int64_t*
     }
     free(P);
     free(sorted);
+    return 0;
+}
+
+/* Raw rank spread of Sec. 6.2: spread[t][s] = max_r d - median_r d at every
+ * step and stage (lower median, by a library sort of a copy of the row),
+ * and its sums over the steps of each window, wspread[W][S].
+ * Returns 0, or -1 if scratch cannot be allocated. */
+int sfo_rank_spread(const int64_t* d, int64_t T, int32_t R, int32_t S, int64_t window,
+                    int64_t* spread, int64_t* wspread)
+{
+    int64_t* sorted = (int64_t*)malloc(sizeof(int64_t) * (size_t)(R > 0 ? R : 1));
+    if (!sorted) return -1;
+    const int64_t W = T / window + (T % window != 0);
+    for (int64_t i = 0; i < W * S; ++i) wspread[i] = 0;
+    for (int64_t t = 0; t < T; ++t) {
+        const int64_t w = t / window;
+        for (int32_t s = 0; s < S; ++s) {
+            const int64_t* row = d + (t * S + s) * (int64_t)R;
+            memcpy(sorted, row, sizeof(int64_t) * (size_t)R);
+            qsort(sorted, (size_t)R, sizeof(int64_t), cmp_i64);
+            const int64_t x = sorted[R - 1] - sorted[(R - 1) / 2];
+            spread[t * S + s] = x;
+            wspread[w * S + s] += x;
+        }
+    }
+    free(sorted);
+    return 0;
+}
+
+/* Per-rank window median, a candidate baseline btilde of Eq. (4) (Sec. 4):
+ * med[w][s][r] = the lower median of d[t][s][r] over the n steps t of
+ * window w (the element of rank floor((n-1)/2) of a library sort).
+ * Returns 0, or -1 if scratch cannot be allocated. */
+int sfo_window_median(const int64_t* d, int64_t T, int32_t R, int32_t S, int64_t window,
+                      int64_t* med)
+{
+    int64_t* col = (int64_t*)malloc(sizeof(int64_t) * (size_t)(window < T ? window : (T > 0 ? T : 1)));
+    if (!col) return -1;
+    const int64_t W = T / window + (T % window != 0);
+    for (int64_t w = 0; w < W; ++w) {
+        const int64_t t0 = w * window;
+        const int64_t t1 = t0 + window < T ? t0 + window : T;
+        const int64_t n = t1 - t0;
+        for (int32_t s = 0; s < S; ++s) {
+            for (int32_t r = 0; r < R; ++r) {
+                for (int64_t t = t0; t < t1; ++t) col[t - t0] = d[(t * S + s) * (int64_t)R + r];
+                qsort(col, (size_t)n, sizeof(int64_t), cmp_i64);
+                med[(w * S + s) * (int64_t)R + r] = col[(n - 1) / 2];
+            }
+        }
+    }
+    free(col);
     return 0;
 }

@@ -832,3 +832,168 @@ def pin_lag_twin(l, pyref):
 
 
 LAG_PINS = [pin_lag_stall, pin_lag_library_median, pin_lag_invariants, pin_lag_bruteforce]
+
+
+# ----------------------------------------------------------------------------
+# raw rank spread (Sec. 6.2) and the per-rank window median (Eq. (4))
+#
+# Spread pins take ``sp(d[T,S,R], window) -> (spread[T,S], wspread[W,S])``;
+# window-median pins take ``wm(d[T,S,R], window) -> med[W,S,R]``.
+
+
+def _lower_median_by_count(xs):
+    """The lower median of ``xs`` from its defining property, without
+    sorting: the value m with #{x < m} <= k < #{x <= m}, k = (n-1)//2."""
+    k = (len(xs) - 1) // 2
+    for m in xs:
+        if sum(x < m for x in xs) <= k < sum(x <= m for x in xs):
+            return m
+    raise AssertionError("no lower median")
+
+
+def _window_sums(x, window):
+    T = x.shape[0]
+    return np.stack([x[t0:t0 + window].sum(axis=0) for t0 in range(0, T, window)])
+
+
+def pin_spread_stall(sp):
+    """The Sec. 2 pattern, by hand: at data the stalled rank is 30 ms above
+    the median of the four ranks; at bwd the three waiting ranks are 30 ms
+    above the stalled one, but they are the median, so the spread is 0."""
+    spread, wspread = sp(stall_case(), 1)
+    assert spread[0].tolist() == [30 * MS, 0, 0, 0, 0, 0]
+    assert wspread.tolist() == spread.tolist()
+
+
+def pin_spread_library(sp):
+    """numpy's max and median (odd R) or the lower middle of numpy's sort
+    (even R); window sums by numpy."""
+    rng = np.random.Generator(np.random.PCG64(60))
+    for (T, S, R, window) in [(20, 6, 7, 5), (15, 5, 8, 4), (10, 4, 1, 3), (8, 3, 2, 8),
+                              (6, 12, 129, 1), (5, 6, 1000, 2), (13, 4, 3, 20)]:
+        for hi in (10**9, 3):
+            d = rng.integers(0, hi + 1, size=(T, S, R), dtype=np.int64)
+            spread, wspread = sp(d, window)
+            if R % 2:
+                med = np.median(d, axis=2).astype(np.int64)
+            else:
+                med = np.sort(d, axis=2)[:, :, (R - 1) // 2]
+            assert np.array_equal(spread, d.max(axis=2) - med)
+            assert np.array_equal(wspread, _window_sums(spread, window))
+            assert (spread >= 0).all()
+            if R == 1:
+                assert (spread == 0).all()
+            if R == 2:
+                assert np.array_equal(spread, d.max(axis=2) - d.min(axis=2))
+
+
+def pin_spread_first_boundary_is_lag(sp, l):
+    """At the first boundary a rank's prefix is its duration, so the spread
+    of stage 0 equals the lag of stage 0; with S = 1 they agree everywhere."""
+    rng = np.random.Generator(np.random.PCG64(61))
+    d = rng.integers(0, 10**6, size=(25, 5, 31), dtype=np.int64)
+    spread, _ = sp(d, 7)
+    lag, _ = l(d)
+    assert np.array_equal(spread[:, 0], lag[:, 0])
+    assert np.array_equal(sp(d[:, :1], 7)[0], l(d[:, :1])[0])
+
+
+def pin_spread_invariants(sp):
+    """Relabelling ranks, adding one constant to every rank of a stage, and
+    reordering stages act as they must; scaling scales."""
+    rng = np.random.Generator(np.random.PCG64(62))
+    d = rng.integers(0, 10**6, size=(30, 6, 33), dtype=np.int64)
+    spread, wspread = sp(d, 10)
+    assert np.array_equal(sp(d[:, :, rng.permutation(33)], 10)[0], spread)
+    dc = d.copy()
+    dc[:, 2] += 12345
+    assert np.array_equal(sp(dc, 10)[0], spread)
+    order = rng.permutation(6)
+    assert np.array_equal(sp(d[:, order], 10)[0], spread[:, order])
+    assert np.array_equal(sp(3 * d, 10)[0], 3 * spread)
+    assert np.array_equal(sp(d, 1)[1], spread)
+    assert np.array_equal(sp(d, 1000)[1][0], spread.sum(axis=0))
+
+
+def pin_spread_bruteforce(sp):
+    """Every row in {0,1,2,3}^R for R in 1..5, the median by its counting
+    definition."""
+    for R in range(1, 6):
+        rows = list(itertools.product(range(4), repeat=R))
+        d = np.array(rows, dtype=np.int64).reshape(len(rows), 1, R)
+        spread, _ = sp(d, 1)
+        for i, row in enumerate(rows):
+            assert spread[i, 0] == max(row) - _lower_median_by_count(list(row))
+
+
+def pin_spread_twin(sp, pyref):
+    rng = np.random.Generator(np.random.PCG64(63))
+    d = rng.integers(0, 20, size=(7, 5, 9), dtype=np.int64)
+    spread, wspread = sp(d, 3)
+    ps, pw = pyref.rank_spread(d.tolist(), 3)
+    assert spread.tolist() == ps and wspread.tolist() == pw
+
+
+SPREAD_PINS = [pin_spread_stall, pin_spread_library, pin_spread_invariants, pin_spread_bruteforce]
+
+
+def pin_median_identity_window(wm):
+    """A window of one step: the median is the step itself."""
+    rng = np.random.Generator(np.random.PCG64(70))
+    d = rng.integers(0, 10**9, size=(9, 4, 5), dtype=np.int64)
+    assert np.array_equal(wm(d, 1), d)
+
+
+def pin_median_library(wm):
+    """numpy's median over each window's steps (odd n) or the lower middle
+    of numpy's sort (even n), the last window shorter."""
+    rng = np.random.Generator(np.random.PCG64(71))
+    for (T, S, R, window) in [(21, 3, 5, 7), (20, 2, 4, 8), (7, 3, 6, 100), (50, 1, 3, 2),
+                              (30, 4, 17, 10), (11, 2, 2, 3)]:
+        d = rng.integers(0, 10**9, size=(T, S, R), dtype=np.int64)
+        med = wm(d, window)
+        W = (T + window - 1) // window
+        assert med.shape == (W, S, R)
+        for w in range(W):
+            blk = d[w * window:(w + 1) * window]
+            n = blk.shape[0]
+            want = (np.median(blk, axis=0).astype(np.int64) if n % 2
+                    else np.sort(blk, axis=0)[(n - 1) // 2])
+            assert np.array_equal(med[w], want), (T, window, w)
+
+
+def pin_median_invariants(wm):
+    """Reordering the steps inside a window leaves its medians unchanged;
+    a shift or a positive scale of the data moves them alike; a constant
+    series is its own median; the median lies within the window's range."""
+    rng = np.random.Generator(np.random.PCG64(72))
+    d = rng.integers(0, 10**6, size=(40, 3, 6), dtype=np.int64)
+    med = wm(d, 10)
+    perm = np.concatenate([w * 10 + rng.permutation(10) for w in range(4)])
+    assert np.array_equal(wm(d[perm], 10), med)
+    assert np.array_equal(wm(d + 999, 10), med + 999)
+    assert np.array_equal(wm(7 * d, 10), 7 * med)
+    c = np.full((12, 2, 3), 42, dtype=np.int64)
+    assert (wm(c, 5) == 42).all()
+    blocks = d.reshape(4, 10, 3, 6)
+    assert (med >= blocks.min(axis=1)).all() and (med <= blocks.max(axis=1)).all()
+
+
+def pin_median_bruteforce(wm):
+    """Every sequence in {0,1,2,3}^n for n in 1..6 (one stage, one rank), the
+    median by its counting definition."""
+    for n in range(1, 7):
+        seqs = list(itertools.product(range(4), repeat=n))
+        for seq in seqs:
+            d = np.array(seq, dtype=np.int64).reshape(n, 1, 1)
+            assert wm(d, n)[0, 0, 0] == _lower_median_by_count(list(seq))
+
+
+def pin_median_twin(wm, pyref):
+    rng = np.random.Generator(np.random.PCG64(73))
+    d = rng.integers(0, 30, size=(11, 3, 4), dtype=np.int64)
+    assert wm(d, 4).tolist() == pyref.window_median(d.tolist(), 4)
+
+
+MEDIAN_PINS = [pin_median_identity_window, pin_median_library, pin_median_invariants,
+               pin_median_bruteforce]

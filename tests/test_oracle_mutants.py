@@ -101,6 +101,23 @@ MUTANTS = {
                                 "static int64_t L_prev = 0;"),
     "lag_against_min": ("sfo_frontier_lag", "const int64_t median = sorted[(R - 1) / 2];",
                         "const int64_t median = sorted[0];"),
+    # raw rank spread
+    "spread_upper_median": ("sfo_rank_spread", "sorted[R - 1] - sorted[(R - 1) / 2];",
+                            "sorted[R - 1] - sorted[R / 2];"),
+    "spread_from_min": ("sfo_rank_spread", "sorted[R - 1] - sorted[(R - 1) / 2];",
+                        "sorted[(R - 1) / 2] - sorted[0];"),
+    "spread_window_overwrites": ("sfo_rank_spread", "wspread[w * S + s] += x;",
+                                 "wspread[w * S + s] = x;"),
+    "spread_drops_last_rank": ("sfo_rank_spread", "qsort(sorted, (size_t)R, sizeof(int64_t), cmp_i64);",
+                               "qsort(sorted, (size_t)(R > 1 ? R - 1 : R), sizeof(int64_t), cmp_i64);"),
+    # per-rank window median
+    "median_upper": ("sfo_window_median", "med[(w * S + s) * (int64_t)R + r] = col[(n - 1) / 2];",
+                     "med[(w * S + s) * (int64_t)R + r] = col[n / 2];"),
+    "median_drops_last_step": ("sfo_window_median", "const int64_t n = t1 - t0;",
+                               "const int64_t n = t1 - t0 - (t1 - t0 > 1);"),
+    "median_stage_zero_only": ("sfo_window_median", "col[t - t0] = d[(t * S + s) * (int64_t)R + r];",
+                               "col[t - t0] = d[(t * S + 0) * (int64_t)R + r];"),
+    "median_unsorted": ("sfo_window_median", "qsort(col, (size_t)n, sizeof(int64_t), cmp_i64);", ""),
 }
 
 
@@ -149,6 +166,20 @@ def _run_all(o):
     for pin in pins.LAG_PINS:
         try:
             pin(o.frontier_lag)
+        except AssertionError:
+            failed.append(pin.__name__)
+    for pin in pins.SPREAD_PINS:
+        try:
+            pin(o.rank_spread)
+        except AssertionError:
+            failed.append(pin.__name__)
+    try:
+        pins.pin_spread_first_boundary_is_lag(o.rank_spread, o.frontier_lag)
+    except AssertionError:
+        failed.append("pin_spread_first_boundary_is_lag")
+    for pin in pins.MEDIAN_PINS:
+        try:
+            pin(o.window_median)
         except AssertionError:
             failed.append(pin.__name__)
     return failed

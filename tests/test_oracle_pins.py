@@ -95,3 +95,25 @@ def test_lag_pin(pin):
 
 def test_twin_lag():
     pins.pin_lag_twin(oracle.frontier_lag, oracle.pyref)
+
+
+@pytest.mark.parametrize("pin", pins.SPREAD_PINS, ids=lambda p: p.__name__)
+def test_spread_pin(pin):
+    pin(oracle.rank_spread)
+
+
+def test_spread_first_boundary_is_lag():
+    pins.pin_spread_first_boundary_is_lag(oracle.rank_spread, oracle.frontier_lag)
+
+
+def test_twin_spread():
+    pins.pin_spread_twin(oracle.rank_spread, oracle.pyref)
+
+
+@pytest.mark.parametrize("pin", pins.MEDIAN_PINS, ids=lambda p: p.__name__)
+def test_median_pin(pin):
+    pin(oracle.window_median)
+
+
+def test_twin_median():
+    pins.pin_median_twin(oracle.window_median, oracle.pyref)
