@@ -283,10 +283,57 @@ def main() -> int:
         }
         del xs, wall, ing_d, ing_o
 
-        # next row: direct-exposure gain, Eq. (4), against a no-stall baseline
-        # (every rank's stage median of the workload's recipe), per chunk
-        base = torch.tensor([b * synth.MS for b in wl.base_ms], dtype=torch.int64, device=dev)
-        btilde = base.view(1, S, 1).expand(W, S, R).contiguous()
+        # next row: the per-rank window median (a baseline btilde of Eq. (4)),
+        # per chunk (the chunks are whole windows)
+        btilde = None
+        if min(wl.window, T) <= sf.SF_MAX_WINDOW_MEDIAN:
+            btilde = torch.empty((W, S, R), dtype=torch.int64, device=dev)
+            m_views = []
+            for t0, t1 in bounds:
+                w0, w1 = t0 // wl.window, -(-t1 // wl.window)
+                m_views.append((d[t0:t1], btilde[w0:w1]))
+            for dv, mv in m_views:
+                sf.sf_window_median(dv, wl.window, mv, stream=stream)
+            mt = []
+            for _ in range(max(3, args.steps // 2)):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                for dv, mv in m_views:
+                    sf.sf_window_median(dv, wl.window, mv, stream=stream)
+                b.record(stream)
+                mt.append((a, b))
+            torch.cuda.synchronize(dev)
+            m_ms = float(np.mean([a.elapsed_time(b) for a, b in mt])) / len(bounds)
+            m_bytes = (8 * T * S * R + 8 * W * S * R) / len(bounds)
+            m_exact = None
+            if oracle_out:
+                import oracle
+                # window 0, ranks [0, 256): ranks are independent
+                x = synth.generate(wl, 0, min(T, wl.window))
+                rs = min(R, 256)
+                om = oracle.window_median(np.ascontiguousarray(x[:, :, :rs]), wl.window)
+                m_exact = bool(np.array_equal(btilde[:1, :, :rs].cpu().numpy(), om))
+            next_rows["window_median"] = {
+                "kernel": "k_window_median",
+                "bound": "hbm",
+                "launch_ms": m_ms,
+                "algorithmic_bytes_per_launch": m_bytes,
+                "achieved": m_bytes / (m_ms / 1e3) / 1e9,
+                "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s",
+                "frac": m_bytes / (m_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                "bit_exact_window0_ranks": m_exact,
+            }
+            del m_views
+
+        # next row: direct-exposure gain, Eq. (4), with the per-rank window
+        # median as btilde (else the workload recipe's no-stall stage medians)
+        if btilde is None:
+            base = torch.tensor([b * synth.MS for b in wl.base_ms], dtype=torch.int64, device=dev)
+            btilde = base.view(1, S, 1).expand(W, S, R).contiguous()
+            g_baseline = "no-stall stage medians of the recipe"
+        else:
+            g_baseline = "per-rank window median (sf_window_median)"
         g_out = {"gain": torch.empty((T, S), dtype=torch.int64, device=dev),
                  "makespan": torch.empty((T,), dtype=torch.int64, device=dev),
                  "window_gain": torch.empty((W, S), dtype=torch.int64, device=dev),
@@ -315,11 +362,21 @@ def main() -> int:
         g_exact = None
         if oracle_out:
             import oracle
+            # the chain window median -> gain on the first 16 steps as one
+            # window of 16, on the GPU and (independently) in the oracle
             n_chk = min(16, T)
             x = synth.generate(wl, 0, n_chk)
-            o = oracle.exposure_gain(x, btilde[:1].cpu().numpy(), wl.window)
-            g_exact = bool(np.array_equal(g_out["gain"][:n_chk].cpu().numpy(), o["gain"]) and
-                           np.array_equal(g_out["makespan"][:n_chk].cpu().numpy(), o["makespan"]))
+            xd = torch.from_numpy(x).to(dev)
+            if n_chk <= sf.SF_MAX_WINDOW_MEDIAN:
+                gb = sf.sf_window_median(xd, n_chk, stream=stream)
+                ob = oracle.window_median(x, n_chk)
+            else:
+                gb, ob = btilde[:1].contiguous(), btilde[:1].cpu().numpy()
+            go = sf.sf_exposure_gain(xd, gb, n_chk, stream=stream)
+            torch.cuda.synchronize(dev)
+            o = oracle.exposure_gain(x, ob, n_chk)
+            g_exact = bool(all(np.array_equal(go[k].cpu().numpy(), o[k]) for k in sf.GAIN_FIELDS))
+            del xd, gb, go
         wg = g_out["window_gain"].sum(dim=0).double()
         wm = float(g_out["window_makespan"].sum())
         next_rows["exposure_gain"] = {
@@ -332,6 +389,7 @@ def main() -> int:
             "unit": "GB/s",
             "frac": g_bytes / (g_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
             "steps_per_launch": n_per,
+            "baseline": g_baseline,
             "G_s_all_windows": [round(float(v) / wm, 6) for v in wg],
             "bit_exact_first_steps": g_exact,
         }
@@ -363,7 +421,7 @@ def main() -> int:
                 l_exact = bool(np.array_equal(lg[:8].cpu().numpy(), ol) and
                                np.array_equal(lgi[:8].cpu().numpy(), oi))
             next_rows["lag"] = {
-                "kernel": "k_frontier_lag",
+                "kernel": "k_median_spread<prefix>",
                 "bound": "lds (radix select)",
                 "launch_ms": l_ms,
                 "algorithmic_bytes_per_launch": l_bytes,
@@ -374,6 +432,50 @@ def main() -> int:
                 "bit_exact_first_steps": l_exact,
             }
             del lg, lgi, l_views
+
+        # next row: raw rank spread (the dispersion baseline of Sec. 6.2),
+        # the lag's selection on each stage's durations
+        if R <= sf.SF_MAX_R_LAG:
+            sp = torch.empty((T, S), dtype=torch.int64, device=dev)
+            wsp = torch.empty((W, S), dtype=torch.int64, device=dev)
+            s_views = []
+            for t0, t1 in bounds:
+                w0, w1 = t0 // wl.window, -(-t1 // wl.window)
+                s_views.append((d[t0:t1], sp[t0:t1], wsp[w0:w1]))
+            for dv, a1, a2 in s_views:
+                sf.sf_rank_spread(dv, wl.window, a1, a2, stream=stream)
+            st = []
+            for _ in range(3):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                for dv, a1, a2 in s_views:
+                    sf.sf_rank_spread(dv, wl.window, a1, a2, stream=stream)
+                b.record(stream)
+                st.append((a, b))
+            torch.cuda.synchronize(dev)
+            s_ms = float(np.mean([a.elapsed_time(b) for a, b in st])) / len(bounds)
+            s_bytes = (8 * T * S * R + 8 * T * S + 8 * W * S) / len(bounds)
+            s_exact = None
+            if oracle_out:
+                import oracle
+                x = synth.generate(wl, 0, 8)
+                osp, _ = oracle.rank_spread(x, wl.window)
+                s_exact = bool(np.array_equal(sp[:8].cpu().numpy(), osp))
+            wsum = wsp.sum(dim=0).double()
+            next_rows["rank_spread"] = {
+                "kernel": "k_median_spread<raw> (+ k_window_sum)",
+                "bound": "lds (radix select)",
+                "launch_ms": s_ms,
+                "algorithmic_bytes_per_launch": s_bytes,
+                "achieved": s_bytes / (s_ms / 1e3) / 1e9,
+                "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s",
+                "frac": s_bytes / (s_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                "spread_share_all_windows": [round(float(v) / float(wsum.sum()), 6) for v in wsum]
+                if float(wsum.sum()) > 0 else None,
+                "bit_exact_first_steps": s_exact,
+            }
+            del sp, wsp, s_views
 
         # next row: routing candidate set (tau 4/5) of the path's windows
         order = torch.empty((W, S), dtype=torch.int32, device=dev)

@@ -63,6 +63,9 @@ enum {
 /* Largest stage count of sf_exposure_gain (its per-stage reductions are
  * kept in registers). */
 #define SF_MAX_S_GAIN 64
+/* Longest window of sf_window_median (a window's values for 16 ranks are
+ * held on chip at once). */
+#define SF_MAX_WINDOW_MEDIAN 1024
 /* Every rank-local prefix P[t][r][s] must be below this many ns (about
  * 39 hours) so that the packed key fits in 64 bits. */
 #define SF_MAX_PREFIX_NS ((int64_t)1 << 47)
@@ -219,6 +222,50 @@ int sf_exposure_gain(const int64_t* durations, const int64_t* baseline, int64_t 
  */
 int sf_frontier_lag(const int64_t* durations, int64_t T, int32_t R, int32_t S,
                     int64_t* out_lag, int64_t* out_lag_inc, sf_stream_t stream);
+
+/*
+ * sf_rank_spread -- the raw rank spread, the dispersion baseline of Sec. 6.2
+ * that ranks stages by sum over steps of (max_r d - median_r d):
+ * spread[t][s] = max_r d[t][s][r] - the lower median over r of d[t][s][r]
+ * (rank floor((R - 1) / 2) in ascending order, as for sf_frontier_lag), and
+ * its sums over the steps of each window.
+ *
+ *   durations          [T][S][R] int64 ns (as for sf_frontier).
+ *   T, R, S            0 <= T <= INT32_MAX, 1 <= R <= SF_MAX_R_LAG,
+ *                      1 <= S <= SF_MAX_S.  T == 0 is a no-op.
+ *   window             steps per window, >= 1 (windows as for
+ *                      sf_window_summary).
+ *   out_spread         [T][S] int64 ns, >= 0.
+ *   out_window_spread  [W][S] int64 ns: window sums of out_spread.
+ *   stream             HIP stream.
+ *
+ * Preconditions and alignment as for sf_frontier; outputs must not overlap
+ * the input or each other.  Returns SF_OK, SF_EINVAL or SF_EHIP.
+ */
+int sf_rank_spread(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                   int64_t window, int64_t* out_spread, int64_t* out_window_spread,
+                   sf_stream_t stream);
+
+/*
+ * sf_window_median -- the per-rank window median, a candidate baseline
+ * btilde of Eq. (4) (Sec. 4): out_median[w][s][r] is the lower median of
+ * d[t][s][r] over the n steps t of window w (the value of rank
+ * floor((n - 1) / 2) in ascending order).  Its output is laid out as the
+ * baseline argument of sf_exposure_gain.
+ *
+ *   durations   [T][S][R] int64 ns (as for sf_frontier).
+ *   T, R, S     0 <= T, 1 <= R <= SF_MAX_R, 1 <= S <= SF_MAX_S.  T == 0 is a
+ *               no-op.
+ *   window      steps per window, >= 1 (windows as for sf_window_summary);
+ *               min(window, T) <= SF_MAX_WINDOW_MEDIAN.
+ *   out_median  [W][S][R] int64 ns.
+ *   stream      HIP stream.
+ *
+ * Pointers 8-byte aligned; the output must not overlap the input.  Returns
+ * SF_OK, SF_EINVAL or SF_EHIP.
+ */
+int sf_window_median(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                     int64_t window, int64_t* out_median, sf_stream_t stream);
 
 /*
  * sf_num_windows -- number of windows W = ceil(T / window) that

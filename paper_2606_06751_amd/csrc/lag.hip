@@ -1,5 +1,7 @@
 // lag.hip -- lag kernel (Sec. 4): L[t,s] = max_r P - median_r P with the lower median
-// (rank floor((R-1)/2) in ascending order) and its increment.
+// (rank floor((R-1)/2) in ascending order) and its increment; and, by the
+// same selection applied to each stage's durations instead of the prefixes,
+// the raw rank spread max_r d - median_r d of Sec. 6.2.
 //
 // One workgroup per step holds all R prefixes in registers (K per lane), and
 // the next stage's durations are loaded while the current boundary is
@@ -13,78 +15,25 @@
 
 #include "sf_device.h"
 #include "sf_host.h"
+#include "sf_select.h"
 
 namespace sfk {
 
-constexpr int kLagBins = 256;                // bins per histogram (8-bit digits)
-constexpr int kLagPerLane = kLagBins / 64;   // bins scanned by each lane of wave 0
-// bin b lives at word b + b / kLagPerLane: the bins a lane of wave 0 scans
-// start kLagPerLane + 1 (odd) words after the previous lane's, so the scan
-// reads hit distinct banks
-constexpr int kLagWords = kLagBins + kLagBins / kLagPerLane;
-
-__device__ __forceinline__ int lag_slot(int b) { return b + b / kLagPerLane; }
-
-// DPP lane move of a 32-bit value in which lanes outside the row/bank masks,
-// and lanes whose source lies outside their row, read 0
-template <int CTRL, int ROW_MASK = 0xF, int BANK_MASK = 0xF>
-__device__ __forceinline__ uint32_t dpp0(uint32_t v)
-{
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROW_MASK, BANK_MASK, true);
-}
-
-// inclusive prefix sum over the 64 lanes: row_shr 1..3 of the input, then
-// row_shr 4 and 8 of the partial sums, then the row totals carried across
-// rows by row_bcast 15 and 31
-__device__ __forceinline__ uint32_t wave_scan_incl(uint32_t v)
-{
-    uint32_t t = v + dpp0<0x111>(v);
-    t += dpp0<0x112>(v);
-    t += dpp0<0x113>(v);
-    t += dpp0<0x114, 0xF, 0xE>(t);
-    t += dpp0<0x118, 0xF, 0xC>(t);
-    t += dpp0<0x142, 0xA>(t);
-    t += dpp0<0x143, 0xC>(t);
-    return t;
-}
+constexpr int kLagWords = kSelWords;
 
 // lane 0's value, in every lane
-__device__ __forceinline__ u64 lane0(u64 v)
-{
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 0);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 0);
-    return ((u64)hi << 32) | lo;
-}
+__device__ __forceinline__ u64 lane0(u64 v) { return lane_value(v, 0); }
 
-// Add the active lanes' bins (-1: none) to the histogram.  When every active
-// lane has the same bin one lane adds them all, so they do not serialise on
-// one word.
-__device__ __forceinline__ void lag_hist_add(uint32_t* h, int bin)
-{
-    const int first = __builtin_amdgcn_readfirstlane(bin);
-    if (__ballot(bin != first) == 0) {
-        const u64 active = __ballot(1);
-        if (first >= 0 && (int)(threadIdx.x & 63) == __builtin_ctzll(active))
-            atomicAdd(&h[lag_slot(first)], (uint32_t)__popcll(active));
-    } else if (bin >= 0) {
-        atomicAdd(&h[lag_slot(bin)], 1u);
-    }
-}
-
-// Selection state: the candidates are the values u with u >> hi == prefix,
-// and a pass histograms their bits [lo, hi) (hi - lo <= 8).  Returns the
-// digit, or -1 for a value that is not a candidate.
-__device__ __forceinline__ int lag_bin(u64 u, int lo, int hi, u64 prefix)
-{
-    const bool match = hi >= 64 || (u >> hi) == prefix;
-    return match ? (int)((u >> lo) & ((1u << (hi - lo)) - 1u)) : -1;
-}
-
-// LCAP: capacity of the candidate list (0: every pass reads the registers)
-template <int VEC, int K, int WG, int LCAP>
-__global__ __launch_bounds__(WG) void k_frontier_lag(const int64_t* __restrict__ d, int64_t T,
-                                                     int R, int S, int64_t* __restrict__ lag,
-                                                     int64_t* __restrict__ lag_inc)
+// One step per workgroup: at every stage, out[t][s] = max - lower median
+// over ranks of the prefixes (PREFIX: the lag, and out_inc gets its
+// increment) or of the stage's durations themselves (the raw rank spread;
+// out_inc is not written).  LCAP: capacity of the candidate list (0: every
+// pass reads the registers).  At least 4 waves per SIMD, so at most 128
+// VGPRs: without the cap the raw spread's allocation lands above it.
+template <bool PREFIX, int VEC, int K, int WG, int LCAP>
+__global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_median_spread(const int64_t* __restrict__ d, int64_t T,
+                                                      int R, int S, int64_t* __restrict__ out,
+                                                      int64_t* __restrict__ out_inc)
 {
     static_assert(K % VEC == 0 && WG % 64 == 0 && WG / 64 <= 16, "shape");
     constexpr int NW = WG / 64;
@@ -147,7 +96,7 @@ __global__ __launch_bounds__(WG) void k_frontier_lag(const int64_t* __restrict__
 #pragma unroll
         for (int k = 0; k < K; ++k) {
             if (ok[k / VEC]) {
-                P[k] += (u64)nx[k];
+                P[k] = PREFIX ? P[k] + (u64)nx[k] : (u64)nx[k];
                 lmax = umax64(lmax, P[k]);
                 lmin = umin64(lmin, P[k]);
             }
@@ -174,9 +123,7 @@ __global__ __launch_bounds__(WG) void k_frontier_lag(const int64_t* __restrict__
         for (int k = 0; k < K; ++k) P[k] -= Pmin;
         u64 um = 0;  // u of the median (0 when every u is 0)
         if (range != 0) {
-            // 256 bins of width 2^lo cover [0, range]
-            const int nbits = 64 - __builtin_clzll(range);
-            int lo = nbits > 8 ? nbits - 8 : 0, hi = lo + 8;
+            int lo = sel_first_lo(range), hi = lo + 8;
             u64 prefix = 0;
             uint32_t kk = target;
             bool in_list = false;
@@ -185,21 +132,21 @@ __global__ __launch_bounds__(WG) void k_frontier_lag(const int64_t* __restrict__
                 // histogram of the next digit of the candidates
                 uint32_t* h = hist[cur];
                 if (LCAP > 0 && in_list) {
-                    for (uint32_t i = tid; i < n; i += WG) lag_hist_add(h, lag_bin(list[i], lo, hi, prefix));
+                    for (uint32_t i = tid; i < n; i += WG) sel_hist_add(h, sel_bin(list[i], lo, hi, prefix));
                 } else {
 #pragma unroll
                     for (int k = 0; k < K; ++k)
-                        lag_hist_add(h, ok[k / VEC] ? lag_bin(P[k], lo, hi, prefix) : -1);
+                        sel_hist_add(h, ok[k / VEC] ? sel_bin(P[k], lo, hi, prefix) : -1);
                 }
                 __syncthreads();
                 if (wave == 0) {
-                    // scan of the bins, kLagPerLane per lane; the lane
+                    // scan of the bins, kSelPerLane per lane; the lane
                     // whose bins hold the target rank names the bin
-                    uint32_t c[kLagPerLane];
-                    const uint32_t* hl = h + lane * (kLagPerLane + 1);  // lag_slot(lane * kLagPerLane)
+                    uint32_t c[kSelPerLane];
+                    const uint32_t* hl = h + lane * (kSelPerLane + 1);  // sel_slot(lane * kSelPerLane)
                     uint32_t part = 0;
 #pragma unroll
-                    for (int i = 0; i < kLagPerLane; ++i) {
+                    for (int i = 0; i < kSelPerLane; ++i) {
                         c[i] = hl[i];
                         part += c[i];
                     }
@@ -208,10 +155,10 @@ __global__ __launch_bounds__(WG) void k_frontier_lag(const int64_t* __restrict__
                     if (cum <= kk && kk < incl) {
                         bool found = false;
 #pragma unroll
-                        for (int i = 0; i < kLagPerLane; ++i) {
+                        for (int i = 0; i < kSelPerLane; ++i) {
                             if (!found && kk < cum + c[i]) {
                                 found = true;
-                                sel[0] = (u64)(lane * kLagPerLane + i);
+                                sel[0] = (u64)(lane * kSelPerLane + i);
                                 sel[1] = (u64)(kk - cum);
                                 sel[2] = (u64)c[i];
                             }
@@ -241,11 +188,11 @@ __global__ __launch_bounds__(WG) void k_frontier_lag(const int64_t* __restrict__
                     // one value has the chosen digits: its lane publishes it
                     if (LCAP > 0 && in_list) {
                         for (uint32_t i = tid; i < n; i += WG)
-                            if (lag_bin(list[i], lo, hi, prefix) >= 0) found_u = list[i];
+                            if (sel_bin(list[i], lo, hi, prefix) >= 0) found_u = list[i];
                     } else {
 #pragma unroll
                         for (int k = 0; k < K; ++k)
-                            if (ok[k / VEC] && lag_bin(P[k], lo, hi, prefix) >= 0) found_u = P[k];
+                            if (ok[k / VEC] && sel_bin(P[k], lo, hi, prefix) >= 0) found_u = P[k];
                     }
                     __syncthreads();
                     prefix = found_u;
@@ -257,7 +204,7 @@ __global__ __launch_bounds__(WG) void k_frontier_lag(const int64_t* __restrict__
                     uint32_t cand = 0;  // bit k: P[k] is a candidate
 #pragma unroll
                     for (int k = 0; k < K; ++k)
-                        cand |= (ok[k / VEC] && lag_bin(P[k], lo, hi, prefix) >= 0) ? (1u << k) : 0u;
+                        cand |= (ok[k / VEC] && sel_bin(P[k], lo, hi, prefix) >= 0) ? (1u << k) : 0u;
                     const uint32_t nc = (uint32_t)__popc(cand);
                     const uint32_t incl = wave_scan_incl(nc);
                     const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
@@ -286,8 +233,8 @@ __global__ __launch_bounds__(WG) void k_frontier_lag(const int64_t* __restrict__
         }
         const int64_t L = (int64_t)(range - um);
         if (tid == 0) {
-            lag[t * S + s] = L;
-            lag_inc[t * S + s] = L - L_prev;
+            out[t * S + s] = L;
+            if (PREFIX) out_inc[t * S + s] = L - L_prev;
         }
         L_prev = L;
     }
@@ -298,29 +245,29 @@ struct LagVariant {
     int WG;
 };
 
-template <int VEC, int K, int WG>
+template <bool PREFIX, int VEC, int K, int WG>
 LagVariant lag_variant()
 {
     // candidate list: a quarter of the slots, at most 32 KB; none when a
     // lane holds so few values that the registers are as cheap to re-read
     constexpr int LCAP = K <= 2 ? 0 : (K * WG / 4 < 4096 ? K * WG / 4 : 4096);
-    return LagVariant{reinterpret_cast<const void*>(&k_frontier_lag<VEC, K, WG, LCAP>), WG};
+    return LagVariant{reinterpret_cast<const void*>(&k_median_spread<PREFIX, VEC, K, WG, LCAP>), WG};
 }
 
 // One step per workgroup with all R prefixes in registers, as few waves as
 // the registers allow: a wave spends less time at barriers than a lane does
 // on 4x the prefixes (measured on the 128- to 16384-rank workloads).
-template <int VEC>
+template <bool PREFIX, int VEC>
 LagVariant pick_lag(int R)
 {
-    if (R <= 128) return lag_variant<VEC, 2, 64>();
-    if (R <= 256) return lag_variant<VEC, 4, 64>();
-    if (R <= 512) return lag_variant<VEC, 8, 64>();
-    if (R <= 1024) return lag_variant<VEC, 16, 64>();
-    if (R <= 2048) return lag_variant<VEC, 16, 128>();
-    if (R <= 4096) return lag_variant<VEC, 16, 256>();
-    if (R <= 8192) return lag_variant<VEC, 16, 512>();
-    return lag_variant<VEC, 16, 1024>();  // R <= SF_MAX_R_LAG = 16384
+    if (R <= 128) return lag_variant<PREFIX, VEC, 2, 64>();
+    if (R <= 256) return lag_variant<PREFIX, VEC, 4, 64>();
+    if (R <= 512) return lag_variant<PREFIX, VEC, 8, 64>();
+    if (R <= 1024) return lag_variant<PREFIX, VEC, 16, 64>();
+    if (R <= 2048) return lag_variant<PREFIX, VEC, 16, 128>();
+    if (R <= 4096) return lag_variant<PREFIX, VEC, 16, 256>();
+    if (R <= 8192) return lag_variant<PREFIX, VEC, 16, 512>();
+    return lag_variant<PREFIX, VEC, 16, 1024>();  // R <= SF_MAX_R_LAG = 16384
 }
 
 }  // namespace sfk
@@ -342,9 +289,37 @@ SF_API int sf_frontier_lag(const int64_t* durations, int64_t T, int32_t R, int32
         !disjoint(out_lag, no, out_lag_inc, no))
         return SF_EINVAL;
     const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
-    const LagVariant v = vec2 ? pick_lag<2>(R) : pick_lag<1>(R);
+    const LagVariant v = vec2 ? pick_lag<true, 2>(R) : pick_lag<true, 1>(R);
     int Ri = R, Si = S;
     void* args[] = {(void*)&durations, (void*)&T, (void*)&Ri, (void*)&Si, (void*)&out_lag,
                     (void*)&out_lag_inc};
     return launch(v.fn, dim3((unsigned)T), dim3(v.WG), args, 0, stream);
+}
+
+SF_API int sf_rank_spread(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                          int64_t window, int64_t* out_spread, int64_t* out_window_spread,
+                          sf_stream_t stream)
+{
+    if (T < 0 || R < 1 || R > SF_MAX_R_LAG || S < 1 || S > SF_MAX_S || window < 1)
+        return SF_EINVAL;
+    if (!fits(T, S, R, 8)) return SF_EINVAL;
+    if (T == 0) return SF_OK;
+    if (T > INT32_MAX) return SF_EINVAL;  // one workgroup per step
+    if (!durations || !out_spread || !out_window_spread) return SF_EINVAL;
+    if (!aligned(durations, 8) || !aligned(out_spread, 8) || !aligned(out_window_spread, 8))
+        return SF_EINVAL;
+    const int64_t W = sf_num_windows(T, window);
+    const int64_t nd = T * S * (int64_t)R * 8, no = T * S * 8, nw = W * S * 8;
+    if (!disjoint(durations, nd, out_spread, no) || !disjoint(durations, nd, out_window_spread, nw) ||
+        !disjoint(out_spread, no, out_window_spread, nw))
+        return SF_EINVAL;
+    const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
+    const LagVariant v = vec2 ? pick_lag<false, 2>(R) : pick_lag<false, 1>(R);
+    int Ri = R, Si = S;
+    int64_t* unused = nullptr;
+    void* args[] = {(void*)&durations, (void*)&T, (void*)&Ri, (void*)&Si, (void*)&out_spread,
+                    (void*)&unused};
+    const int rc = launch(v.fn, dim3((unsigned)T), dim3(v.WG), args, 0, stream);
+    if (rc != SF_OK) return rc;
+    return launch_window_sum(out_spread, T, S, window, W, out_window_spread, stream);
 }

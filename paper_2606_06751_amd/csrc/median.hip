@@ -1,0 +1,239 @@
+// median.hip -- per-rank window median, a candidate baseline btilde of Eq. (4)
+// (Sec. 4): med[w][s][r] = the lower median over the n steps t of window w of
+// d[t][s][r] (the value of rank floor((n-1)/2) in ascending order).
+//
+// One workgroup per (window, stage, RPW adjacent ranks).  Its n x RPW tile
+// is read once along the rank rows (8 * RPW contiguous bytes per step, in
+// 16-byte loads) and transposed through LDS, where the low and high words
+// sit in separate planes with a row stride of RPW + 1 words, so that a wave
+// reading one rank's column hits distinct banks.  Each wave then takes one
+// rank: its n values (K per lane) go to registers, and an exact radix select
+// (a 256-bin histogram of the first digit fitted to the range's top bits,
+// then 8 bits at a time of the values left) finds the lower median.  The
+// histogram is private to the wave and a wave's LDS operations complete in
+// issue order, so the waves need no barrier between them.
+
+#include "sf_device.h"
+#include "sf_host.h"
+#include "sf_select.h"
+
+namespace sfk {
+
+// orders this wave's LDS accesses before the ones that follow (a wave's LDS
+// operations complete in issue order; this keeps the compiler from moving
+// them across)
+__device__ __forceinline__ void wave_lds_fence()
+{
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
+template <int VEC, int K, int RPW>
+__global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __restrict__ d,
+                                                            int64_t T, int R, int S,
+                                                            int64_t window, int nchunk,
+                                                            int64_t* __restrict__ med)
+{
+    constexpr int WG = 64 * RPW;
+    constexpr int ROWS = 64 * K;     // tile rows (steps), >= n
+    constexpr int STRIDE = RPW + 1;  // words per tile row in each plane
+    constexpr int TPR = RPW / 2;     // threads per tile row, two ranks each
+    constexpr int RPS = WG / TPR;    // rows per load sweep
+    constexpr int NSW = ROWS / RPS;  // load sweeps
+    static_assert(RPW % 2 == 0 && ROWS % RPS == 0, "shape");
+    __shared__ uint32_t tlo[ROWS * STRIDE], thi[ROWS * STRIDE];
+    __shared__ uint32_t hist[RPW][kSelWords];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    // block -> (window, stage, rank chunk), the chunk fastest so that
+    // neighbouring blocks read neighbouring pieces of the same rows
+    const int64_t b = blockIdx.x;
+    const int chunk = (int)(b % nchunk);
+    const int64_t wsi = b / nchunk;
+    const int s = (int)(wsi % S);
+    const int64_t w = wsi / S;
+    const int64_t t0 = w * window;
+    const int n = (int)((t0 + window < T ? t0 + window : T) - t0);  // 1 <= n <= ROWS
+    const int r0 = chunk * RPW;
+
+    // the tile: thread (row i, pair c) loads ranks r0 + c and r0 + c + 1
+    {
+        const int c = (tid % TPR) * 2;
+        const int r = r0 + c;
+        int64_t x0[NSW], x1[NSW];
+#pragma unroll
+        for (int j = 0; j < NSW; ++j) {
+            const int i = tid / TPR + j * RPS;
+            x0[j] = 0;
+            x1[j] = 0;
+            if (i < n) {
+                const int64_t* p = d + ((t0 + i) * S + s) * (int64_t)R + r;
+                if (VEC == 2) {
+                    if (r < R) {  // R even: r + 1 < R too
+                        const v2i64 v = __builtin_nontemporal_load(reinterpret_cast<const v2i64*>(p));
+                        x0[j] = v.x;
+                        x1[j] = v.y;
+                    }
+                } else {
+                    if (r < R) x0[j] = __builtin_nontemporal_load(p);
+                    if (r + 1 < R) x1[j] = __builtin_nontemporal_load(p + 1);
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < NSW; ++j) {
+            const int i = tid / TPR + j * RPS;
+            tlo[i * STRIDE + c] = (uint32_t)x0[j];
+            thi[i * STRIDE + c] = (uint32_t)((u64)x0[j] >> 32);
+            tlo[i * STRIDE + c + 1] = (uint32_t)x1[j];
+            thi[i * STRIDE + c + 1] = (uint32_t)((u64)x1[j] >> 32);
+        }
+    }
+    uint32_t* h = hist[wave];
+    for (int i = lane; i < kSelWords; i += 64) h[i] = 0;
+    __syncthreads();
+
+    // one rank per wave; no barrier follows
+    const int r = r0 + wave;
+    if (r >= R) return;
+    u64 v[K];
+    bool ok[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int i = k * 64 + lane;
+        ok[k] = i < n;
+        v[k] = ((u64)thi[i * STRIDE + wave] << 32) | tlo[i * STRIDE + wave];
+    }
+    u64 vmax = 0, vmin = ~0ull;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        if (ok[k]) {
+            vmax = umax64(vmax, v[k]);
+            vmin = umin64(vmin, v[k]);
+        }
+    }
+    vmax = lane_value(group_max<64>(vmax), 63);
+    vmin = ~lane_value(group_max<64>(~vmin), 63);
+    const u64 range = vmax - vmin;
+    u64 um = 0;  // the median minus vmin
+    if (range != 0) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) v[k] -= vmin;
+        int lo = sel_first_lo(range), hi = lo + 8;
+        u64 prefix = 0;
+        uint32_t kk = (uint32_t)((n - 1) / 2);
+        for (;;) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) sel_hist_add(h, ok[k] ? sel_bin(v[k], lo, hi, prefix) : -1);
+            wave_lds_fence();
+            // scan of the bins, kSelPerLane per lane; the lane whose bins hold
+            // the target rank names the bin, and every lane clears its bins
+            uint32_t c[kSelPerLane];
+            uint32_t* hl = h + lane * (kSelPerLane + 1);  // sel_slot(lane * kSelPerLane)
+            uint32_t part = 0;
+#pragma unroll
+            for (int i = 0; i < kSelPerLane; ++i) {
+                c[i] = hl[i];
+                part += c[i];
+            }
+            const uint32_t incl = wave_scan_incl(part);
+            uint32_t cum = incl - part;
+            int fd = -1;
+            uint32_t fk = 0, fc = 0;
+            if (cum <= kk && kk < incl) {
+#pragma unroll
+                for (int i = 0; i < kSelPerLane; ++i) {
+                    if (fd < 0 && kk < cum + c[i]) {
+                        fd = lane * kSelPerLane + i;
+                        fk = kk - cum;
+                        fc = c[i];
+                    }
+                    cum += c[i];
+                }
+            }
+#pragma unroll
+            for (int i = 0; i <= kSelPerLane; ++i) hl[i] = 0;
+            wave_lds_fence();
+            // the candidates hold the target rank, so exactly one lane found it
+            const u64 fm = __ballot(fd >= 0);
+            const int src = fm ? __builtin_ctzll(fm) : 0;
+            const int digit = __builtin_amdgcn_readlane(fd, src);
+            kk = (uint32_t)__builtin_amdgcn_readlane((int)fk, src);
+            const uint32_t count = (uint32_t)__builtin_amdgcn_readlane((int)fc, src);
+            prefix = (prefix << (hi - lo)) | (u64)(uint32_t)digit;
+            hi = lo;
+            if (hi == 0) break;  // every bit chosen: u == prefix
+            lo = lo > 8 ? lo - 8 : 0;
+            if (count == 1) {
+                // one value has the chosen digits: its lane hands it over
+                u64 x = 0;
+                bool has = false;
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    if (ok[k] && sel_bin(v[k], lo, hi, prefix) >= 0) {
+                        x = v[k];
+                        has = true;
+                    }
+                }
+                const u64 hm = __ballot(has);
+                prefix = lane_value(x, hm ? __builtin_ctzll(hm) : 0);
+                break;
+            }
+        }
+        um = prefix;
+    }
+    if (lane == 0) med[(w * S + s) * (int64_t)R + r] = (int64_t)(vmin + um);
+}
+
+struct MedianVariant {
+    const void* fn;
+    int WG, RPW;
+};
+
+template <int VEC, int K, int RPW>
+MedianVariant median_variant()
+{
+    return MedianVariant{reinterpret_cast<const void*>(&k_window_median<VEC, K, RPW>), 64 * RPW, RPW};
+}
+
+// K values per lane for windows up to 64 K steps, 16 ranks per workgroup
+// (128-byte rows; the 1024-step tile fills 156 KB of LDS)
+template <int VEC>
+MedianVariant pick_median(int64_t n)
+{
+    if (n <= 128) return median_variant<VEC, 2, 16>();
+    if (n <= 256) return median_variant<VEC, 4, 16>();
+    if (n <= 512) return median_variant<VEC, 8, 16>();
+    return median_variant<VEC, 16, 16>();  // n <= SF_MAX_WINDOW_MEDIAN = 1024
+}
+
+}  // namespace sfk
+
+using namespace sfk;
+
+SF_API int sf_window_median(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                            int64_t window, int64_t* out_median, sf_stream_t stream)
+{
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S || window < 1) return SF_EINVAL;
+    if (!fits(T, S, R, 8)) return SF_EINVAL;
+    if (T == 0) return SF_OK;
+    const int64_t n_max = window < T ? window : T;
+    if (n_max > SF_MAX_WINDOW_MEDIAN) return SF_EINVAL;
+    const int64_t W = sf_num_windows(T, window);
+    if (!fits(W, S, R, 8)) return SF_EINVAL;
+    if (!durations || !out_median) return SF_EINVAL;
+    if (!aligned(durations, 8) || !aligned(out_median, 8)) return SF_EINVAL;
+    if (!disjoint(durations, T * S * (int64_t)R * 8, out_median, W * S * (int64_t)R * 8))
+        return SF_EINVAL;
+    const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
+    const MedianVariant v = vec2 ? pick_median<2>(n_max) : pick_median<1>(n_max);
+    const int nchunk = (R + v.RPW - 1) / v.RPW;
+    const int64_t blocks = W * S * (int64_t)nchunk;
+    if (blocks > INT32_MAX) return SF_EINVAL;
+    int Ri = R, Si = S;
+    void* args[] = {(void*)&durations, (void*)&T,      (void*)&Ri,        (void*)&Si,
+                    (void*)&window,    (void*)&nchunk, (void*)&out_median};
+    return launch(v.fn, dim3((unsigned)blocks), dim3(v.WG), args, 0, stream);
+}

@@ -20,6 +20,7 @@ SF_MAX_R = 65536
 SF_MAX_S = 512
 SF_MAX_S_GAIN = 64
 SF_MAX_R_LAG = 16384
+SF_MAX_WINDOW_MEDIAN = 1024
 SF_MAX_PREFIX_NS = 1 << 47
 
 LIB_PATH = _build.LIB
@@ -50,6 +51,10 @@ def _load() -> ctypes.CDLL:
     lib.sf_exposure_gain.restype = ctypes.c_int
     lib.sf_frontier_lag.argtypes = [vp, i64, i32, i32, vp, vp, vp]
     lib.sf_frontier_lag.restype = ctypes.c_int
+    lib.sf_rank_spread.argtypes = [vp, i64, i32, i32, i64, vp, vp, vp]
+    lib.sf_rank_spread.restype = ctypes.c_int
+    lib.sf_window_median.argtypes = [vp, i64, i32, i32, i64, vp, vp]
+    lib.sf_window_median.restype = ctypes.c_int
     lib.sf_num_windows.argtypes = [i64, i64]
     lib.sf_num_windows.restype = i64
     lib.sf_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp]
@@ -290,6 +295,54 @@ def sf_frontier_lag(durations: torch.Tensor, out_lag: torch.Tensor | None = None
     if rc != SF_OK:
         raise StageFrontierError(rc, "sf_frontier_lag")
     return out_lag, out_lag_inc
+
+
+def sf_rank_spread(durations: torch.Tensor, window: int, out_spread: torch.Tensor | None = None,
+                   out_window_spread: torch.Tensor | None = None, stream=None):
+    """Raw rank spread, max_r d - (lower) median_r d, and its window sums
+    (``sf_rank_spread``).  Returns ``(out_spread [T, S], out_window_spread
+    [W, S])``."""
+    if durations.dim() != 3:
+        raise ValueError("durations must be [T, S, R]")
+    T, S, R = durations.shape
+    W = sf_num_windows(T, window)
+    if W < 0:
+        raise StageFrontierError(SF_EINVAL, "sf_rank_spread")
+    _check(durations, "durations", torch.int64, (T, S, R))
+    dev = durations.device
+    if out_spread is None:
+        out_spread = torch.empty((T, S), dtype=torch.int64, device=dev)
+    if out_window_spread is None:
+        out_window_spread = torch.empty((W, S), dtype=torch.int64, device=dev)
+    _check(out_spread, "out_spread", torch.int64, (T, S))
+    _check(out_window_spread, "out_window_spread", torch.int64, (W, S))
+    rc = _lib.sf_rank_spread(durations.data_ptr(), T, R, S, window, out_spread.data_ptr(),
+                             out_window_spread.data_ptr(), _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_rank_spread")
+    return out_spread, out_window_spread
+
+
+def sf_window_median(durations: torch.Tensor, window: int, out_median: torch.Tensor | None = None,
+                     stream=None) -> torch.Tensor:
+    """Per-rank window median (``sf_window_median``), the baseline argument
+    of ``sf_exposure_gain``.  Returns ``out_median [W, S, R]``."""
+    if durations.dim() != 3:
+        raise ValueError("durations must be [T, S, R]")
+    T, S, R = durations.shape
+    W = sf_num_windows(T, window)
+    if W < 0:
+        raise StageFrontierError(SF_EINVAL, "sf_window_median")
+    _check(durations, "durations", torch.int64, (T, S, R))
+    dev = durations.device
+    if out_median is None:
+        out_median = torch.empty((W, S, R), dtype=torch.int64, device=dev)
+    _check(out_median, "out_median", torch.int64, (W, S, R))
+    rc = _lib.sf_window_median(durations.data_ptr(), T, R, S, window, out_median.data_ptr(),
+                               _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_window_median")
+    return out_median
 
 
 def raw_library() -> ctypes.CDLL:

@@ -27,8 +27,9 @@ def sf():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == ["sf_exposure_gain", "sf_frontier", "sf_frontier_evidence",
-                                    "sf_frontier_lag", "sf_ingest", "sf_num_windows", "sf_route",
-                                    "sf_strerror", "sf_version", "sf_window_summary"]
+                                    "sf_frontier_lag", "sf_ingest", "sf_num_windows",
+                                    "sf_rank_spread", "sf_route", "sf_strerror", "sf_version",
+                                    "sf_window_median", "sf_window_summary"]
 
 
 def test_every_declared_symbol_is_exported(sf):
@@ -45,6 +46,7 @@ def test_constants_match_header(sf):
     assert "#define SF_MAX_S %d" % sf.SF_MAX_S in text
     assert "#define SF_MAX_S_GAIN %d" % sf.SF_MAX_S_GAIN in text
     assert "#define SF_MAX_R_LAG %d" % sf.SF_MAX_R_LAG in text
+    assert "#define SF_MAX_WINDOW_MEDIAN %d" % sf.SF_MAX_WINDOW_MEDIAN in text
     for name in ("SF_OK", "SF_EINVAL", "SF_ERANGE", "SF_EHIP"):
         assert re.search(r"%s = %d" % (name, getattr(sf, name)), text), name
 
@@ -183,6 +185,42 @@ def test_lag_argument_checks(sf):
     assert call(T=1 << 32, R=1, S=1) == sf.SF_EINVAL        # one workgroup per step
 
 
+def test_spread_argument_checks(sf):
+    lib = sf.raw_library()
+
+    def call(**kw):
+        a = dict(dict(d=A, T=10, R=8, S=6, window=4, sp=B, wsp=C), **kw)
+        return lib.sf_rank_spread(a["d"], a["T"], a["R"], a["S"], a["window"], a["sp"], a["wsp"],
+                                  None)
+
+    assert call(T=0, d=None, sp=None, wsp=None) == sf.SF_OK
+    assert call(R=sf.SF_MAX_R_LAG + 1) == sf.SF_EINVAL
+    assert call(S=0) == sf.SF_EINVAL
+    assert call(window=0) == sf.SF_EINVAL
+    assert call(wsp=None) == sf.SF_EINVAL
+    assert call(sp=B + 4) == sf.SF_EINVAL                   # misaligned
+    assert call(sp=A + 8) == sf.SF_EINVAL                   # output overlaps input
+    assert call(wsp=B + 8) == sf.SF_EINVAL                  # outputs overlap
+    assert call(T=1 << 32, R=1, S=1) == sf.SF_EINVAL        # one workgroup per step
+
+
+def test_window_median_argument_checks(sf):
+    lib = sf.raw_library()
+
+    def call(**kw):
+        a = dict(dict(d=A, T=100, R=8, S=6, window=10, m=B), **kw)
+        return lib.sf_window_median(a["d"], a["T"], a["R"], a["S"], a["window"], a["m"], None)
+
+    assert call(T=0, d=None, m=None) == sf.SF_OK
+    assert call(R=0) == sf.SF_EINVAL
+    assert call(R=sf.SF_MAX_R + 1) == sf.SF_EINVAL
+    assert call(window=0) == sf.SF_EINVAL
+    assert call(T=5000, window=sf.SF_MAX_WINDOW_MEDIAN + 1) == sf.SF_EINVAL
+    assert call(m=None) == sf.SF_EINVAL
+    assert call(m=B + 4) == sf.SF_EINVAL                    # misaligned
+    assert call(m=A + 8) == sf.SF_EINVAL                    # output overlaps input
+
+
 def test_summary_argument_checks(sf):
     lib = sf.raw_library()
     D = 4 << 40
@@ -228,6 +266,8 @@ def test_ctypes_argtypes_cover_header(sf):
     assert len(lib.sf_ingest.argtypes) == 8
     assert len(lib.sf_exposure_gain.argtypes) == 11
     assert len(lib.sf_frontier_lag.argtypes) == 7
+    assert len(lib.sf_rank_spread.argtypes) == 8
+    assert len(lib.sf_window_median.argtypes) == 7
     assert len(lib.sf_route.argtypes) == 8
     assert len(lib.sf_window_summary.argtypes) == 10
     assert lib.sf_num_windows.restype is ctypes.c_int64

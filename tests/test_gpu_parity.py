@@ -487,3 +487,117 @@ def test_lag_stall_and_odd_base(sf):
     ol, oi = oracle.frontier_lag(d)
     np.testing.assert_array_equal(lag.cpu().numpy(), ol)
     np.testing.assert_array_equal(inc.cpu().numpy(), oi)
+
+
+# ----------------------------------------------------------------------------
+# raw rank spread (Sec. 6.2)
+
+def _spread_fn(sf):
+    def f(d, window):
+        sp, wsp = sf.sf_rank_spread(torch.from_numpy(np.ascontiguousarray(d)).to(DEV), window)
+        torch.cuda.synchronize()
+        return sp.cpu().numpy(), wsp.cpu().numpy()
+    return f
+
+
+def assert_spread_equal(sf, d, window):
+    sp, wsp = _spread_fn(sf)(d, window)
+    osp, owsp = oracle.rank_spread(d, window)
+    np.testing.assert_array_equal(sp, osp)
+    np.testing.assert_array_equal(wsp, owsp)
+
+
+@pytest.mark.parametrize("R", [1, 2, 3, 7, 64, 127, 128, 129, 256, 300, 513, 1000, 1024, 2047,
+                               4096, 5000, 8192, 10001, 16384])
+def test_spread_rank_sweep(sf, R):
+    rng = np.random.Generator(np.random.PCG64(R + 17))
+    T = max(2, min(40, 200000 // (R * 6)))
+    for hi in (3, 10**6, 1 << 40):
+        d = rng.integers(0, hi + 1, size=(T, 6, R), dtype=np.int64)
+        d[0] = 5                                 # a step where every duration is equal
+        if R > 2:
+            d[1, 2, R // 3] += 1 << 44           # one outlier rank
+        print("case R=%d hi=%d T=%d" % (R, hi, T), flush=True)
+        assert_spread_equal(sf, d, 7)
+
+
+def test_spread_pins_and_layouts(sf):
+    import pins
+    f = _spread_fn(sf)
+    pins.pin_spread_stall(f)
+    pins.pin_spread_invariants(f)
+    pins.pin_spread_first_boundary_is_lag(
+        f, lambda d: tuple(x.cpu().numpy() for x in sf.sf_frontier_lag(torch.from_numpy(d).to(DEV))))
+    for S in (1, 12, 512):
+        d = synth.random_durations(3, S, 33, seed=S, hi=10**6)
+        assert_spread_equal(sf, d, 2)
+    T, S, R = 7, 5, 402                          # 8-byte aligned base: 8-byte loads
+    d = synth.random_durations(T, S, R, seed=4, hi=10**5)
+    flat = torch.zeros(T * S * R + 1, dtype=torch.int64, device=DEV)
+    flat[1:] = torch.from_numpy(d.reshape(-1)).to(DEV)
+    sp, wsp = sf.sf_rank_spread(flat[1:].view(T, S, R), 3)
+    torch.cuda.synchronize()
+    osp, owsp = oracle.rank_spread(d, 3)
+    np.testing.assert_array_equal(sp.cpu().numpy(), osp)
+    np.testing.assert_array_equal(wsp.cpu().numpy(), owsp)
+
+
+# ----------------------------------------------------------------------------
+# per-rank window median, the baseline of Eq. (4)
+
+def _median_fn(sf):
+    def f(d, window):
+        m = sf.sf_window_median(torch.from_numpy(np.ascontiguousarray(d)).to(DEV), window)
+        torch.cuda.synchronize()
+        return m.cpu().numpy()
+    return f
+
+
+def assert_median_equal(sf, d, window):
+    np.testing.assert_array_equal(_median_fn(sf)(d, window), oracle.window_median(d, window))
+
+
+@pytest.mark.parametrize("window", [1, 2, 3, 64, 100, 127, 128, 129, 250, 256, 257, 500, 512, 513,
+                                    1000, 1024])
+def test_median_window_sweep(sf, window):
+    rng = np.random.Generator(np.random.PCG64(window + 23))
+    T = 2 * window + window // 3 + 1             # a ragged last window
+    for R, hi in ((16, 3), (33, 10**6), (5, 1 << 40)):
+        d = rng.integers(0, hi + 1, size=(T, 3, R), dtype=np.int64)
+        d[:, 1, 0] = 9                           # a constant series
+        d[min(T - 1, 3), 2, R // 2] += 1 << 44   # an outlier step
+        print("case window=%d R=%d hi=%d T=%d" % (window, R, hi, T), flush=True)
+        assert_median_equal(sf, d, window)
+
+
+@pytest.mark.parametrize("R", [1, 2, 15, 16, 17, 31, 1000, 4097])
+def test_median_rank_sweep(sf, R):
+    d = synth.random_durations(250, 2, R, seed=R, hi=10**7)
+    assert_median_equal(sf, d, 100)
+
+
+def test_median_pins_and_layouts(sf):
+    import pins
+    f = _median_fn(sf)
+    for pin in pins.MEDIAN_PINS:
+        pin(f)
+    T, S, R = 40, 3, 30                          # 8-byte aligned base, even R
+    d = synth.random_durations(T, S, R, seed=5, hi=10**8)
+    flat = torch.zeros(T * S * R + 1, dtype=torch.int64, device=DEV)
+    flat[1:] = torch.from_numpy(d.reshape(-1)).to(DEV)
+    m = sf.sf_window_median(flat[1:].view(T, S, R), 16)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(m.cpu().numpy(), oracle.window_median(d, 16))
+    assert_median_equal(sf, synth.random_durations(5, 512, 3, seed=6, hi=100), 2)
+
+
+def test_median_feeds_gain(sf):
+    """The window median as the baseline of the direct-exposure gain."""
+    d = synth.random_durations(60, 6, 40, seed=7, hi=10**7)
+    dd = torch.from_numpy(d).to(DEV)
+    m = sf.sf_window_median(dd, 20)
+    out = sf.sf_exposure_gain(dd, m, 20)
+    torch.cuda.synchronize()
+    o = oracle.exposure_gain(d, oracle.window_median(d, 20), 20)
+    for k in GAIN_KEYS:
+        np.testing.assert_array_equal(out[k].cpu().numpy(), o[k])

@@ -149,3 +149,40 @@ def test_workload_lag(sf, name):
         np.testing.assert_array_equal(lag.cpu().numpy(), ol)
         np.testing.assert_array_equal(inc.cpu().numpy(), oi)
     log("lag ok: %s (%d steps x 3 ranges)" % (name, n))
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workload_spread(sf, name):
+    """The raw rank spread on sampled step ranges of every workload."""
+    wl = synth.WORKLOADS[name]
+    n = min(wl.T, 600 if wl.R <= 1024 else 60)
+    for t0 in sorted({0, wl.T // 2, wl.T - n}):
+        x = synth.generate(wl, t0, t0 + n)
+        sp, wsp = sf.sf_rank_spread(torch.from_numpy(x).to("cuda:0"), wl.window)
+        torch.cuda.synchronize()
+        osp, owsp = oracle.rank_spread(x, wl.window)
+        np.testing.assert_array_equal(sp.cpu().numpy(), osp)
+        np.testing.assert_array_equal(wsp.cpu().numpy(), owsp)
+    log("spread ok: %s (%d steps x 3 ranges)" % (name, n))
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workload_window_median(sf, name):
+    """The per-rank window median of the first and the last window of every
+    workload, in the launch shape the benchmark uses (one full window);
+    above 1024 ranks the oracle checks slices of 512 ranks at both ends
+    and in the middle (ranks are independent)."""
+    wl = synth.WORKLOADS[name]
+    T, S, R = wl.T, wl.S, wl.R
+    W = wl.num_windows
+    for w in sorted({0, W - 1}):
+        t0, t1 = w * wl.window, min(T, (w + 1) * wl.window)
+        x = synth.generate(wl, t0, t1)
+        m = sf.sf_window_median(torch.from_numpy(x).to("cuda:0"), wl.window)
+        torch.cuda.synchronize()
+        m = m.cpu().numpy()
+        slices = [(0, R)] if R <= 1024 else [(0, 512), (R // 2 - 256, R // 2 + 256), (R - 512, R)]
+        for r0, r1 in slices:
+            om = oracle.window_median(np.ascontiguousarray(x[:, :, r0:r1]), wl.window)
+            np.testing.assert_array_equal(m[:, :, r0:r1], om)
+        log("window median ok: %s window %d (%d steps, ranks %s)" % (name, w, t1 - t0, slices))
