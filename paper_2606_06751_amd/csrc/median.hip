@@ -2,16 +2,20 @@
 // (Sec. 4): med[w][s][r] = the lower median over the n steps t of window w of
 // d[t][s][r] (the value of rank floor((n-1)/2) in ascending order).
 //
-// One workgroup per (window, stage, RPW adjacent ranks).  Its n x RPW tile
-// is read once along the rank rows (8 * RPW contiguous bytes per step, in
-// 16-byte loads) and transposed through LDS, where the low and high words
-// sit in separate planes with a row stride of RPW + 1 words, so that a wave
-// reading one rank's column hits distinct banks.  Each wave then takes one
-// rank: its n values (K per lane) go to registers, and an exact radix select
-// (a 256-bin histogram of the first digit fitted to the range's top bits,
-// then 8 bits at a time of the values left) finds the lower median.  The
-// histogram is private to the wave and a wave's LDS operations complete in
-// issue order, so the waves need no barrier between them.
+// A tile is (window, stage, RPW adjacent ranks).  Persistent workgroups walk
+// the tiles; each tile is read once along the rank rows (8 * RPW contiguous
+// bytes per step, in 16-byte loads) into registers, while the previous tile
+// is being resolved, and is then transposed through LDS, where the low and
+// high words sit in separate planes with a row stride of RPW + 1 words so
+// that a wave reading one rank's column hits distinct banks.  Each wave then
+// takes one rank: its n values (K per lane) go to registers, and an exact
+// radix select (a 256-bin histogram of the first digit fitted to the range's
+// top bits, then 8 bits at a time of the values left) finds the lower
+// median.  Once at most 64 values are left they are compacted, one per lane,
+// through the wave's own (already read) tile column, so later passes handle
+// one value per lane.  The histogram is private to the wave and a wave's LDS
+// operations complete in issue order, so the waves need no barrier between
+// them during the selection.
 
 #include "sf_device.h"
 #include "sf_host.h"
@@ -32,6 +36,7 @@ template <int VEC, int K, int RPW>
 __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __restrict__ d,
                                                             int64_t T, int R, int S,
                                                             int64_t window, int nchunk,
+                                                            int64_t ntiles,
                                                             int64_t* __restrict__ med)
 {
     constexpr int WG = 64 * RPW;
@@ -40,36 +45,45 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
     constexpr int TPR = RPW / 2;     // threads per tile row, two ranks each
     constexpr int RPS = WG / TPR;    // rows per load sweep
     constexpr int NSW = ROWS / RPS;  // load sweeps
-    static_assert(RPW % 2 == 0 && ROWS % RPS == 0, "shape");
+    constexpr int LIST = 64;         // values left that are compacted
+    static_assert(RPW % 2 == 0 && ROWS % RPS == 0 && ROWS >= LIST, "shape");
     __shared__ uint32_t tlo[ROWS * STRIDE], thi[ROWS * STRIDE];
     __shared__ uint32_t hist[RPW][kSelWords];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    // block -> (window, stage, rank chunk), the chunk fastest so that
-    // neighbouring blocks read neighbouring pieces of the same rows
-    const int64_t b = blockIdx.x;
-    const int chunk = (int)(b % nchunk);
-    const int64_t wsi = b / nchunk;
-    const int s = (int)(wsi % S);
-    const int64_t w = wsi / S;
-    const int64_t t0 = w * window;
-    const int n = (int)((t0 + window < T ? t0 + window : T) - t0);  // 1 <= n <= ROWS
-    const int r0 = chunk * RPW;
+    const int c = (tid % TPR) * 2;  // this thread's rank pair within a tile row
+    uint32_t* h = hist[wave];
+    for (int i = lane; i < kSelWords; i += 64) h[i] = 0;  // cleared again by every scan
 
-    // the tile: thread (row i, pair c) loads ranks r0 + c and r0 + c + 1
-    {
-        const int c = (tid % TPR) * 2;
-        const int r = r0 + c;
-        int64_t x0[NSW], x1[NSW];
+    // tile b -> (window, stage, rank chunk), the chunk fastest so that
+    // neighbouring workgroups read neighbouring pieces of the same rows
+    struct Tile {
+        int64_t w, t0;
+        int s, n, r0;
+    };
+    auto tile = [&](int64_t b) {
+        Tile x;
+        const int64_t wsi = b / nchunk;
+        x.r0 = (int)(b - wsi * nchunk) * RPW;
+        x.s = (int)(wsi % S);
+        x.w = wsi / S;
+        x.t0 = x.w * window;
+        x.n = (int)((x.t0 + window < T ? x.t0 + window : T) - x.t0);  // 1 <= n <= ROWS
+        return x;
+    };
+    // the next tile in flight: thread (row i, pair c) holds ranks r0 + c, r0 + c + 1
+    int64_t x0[NSW], x1[NSW];
+    auto load = [&](const Tile& q) {
+        const int r = q.r0 + c;
 #pragma unroll
         for (int j = 0; j < NSW; ++j) {
             const int i = tid / TPR + j * RPS;
             x0[j] = 0;
             x1[j] = 0;
-            if (i < n) {
-                const int64_t* p = d + ((t0 + i) * S + s) * (int64_t)R + r;
+            if (i < q.n) {
+                const int64_t* p = d + ((q.t0 + i) * S + q.s) * (int64_t)R + r;
                 if (VEC == 2) {
                     if (r < R) {  // R even: r + 1 < R too
                         const v2i64 v = __builtin_nontemporal_load(reinterpret_cast<const v2i64*>(p));
@@ -82,6 +96,13 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
                 }
             }
         }
+    };
+
+    int64_t b = blockIdx.x;  // the grid is at most ntiles
+    load(tile(b));
+    for (; b < ntiles; b += gridDim.x) {
+        const Tile q = tile(b);
+        __syncthreads();  // every wave is done with the previous tile's columns
 #pragma unroll
         for (int j = 0; j < NSW; ++j) {
             const int i = tid / TPR + j * RPS;
@@ -90,101 +111,138 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
             tlo[i * STRIDE + c + 1] = (uint32_t)x1[j];
             thi[i * STRIDE + c + 1] = (uint32_t)((u64)x1[j] >> 32);
         }
-    }
-    uint32_t* h = hist[wave];
-    for (int i = lane; i < kSelWords; i += 64) h[i] = 0;
-    __syncthreads();
-
-    // one rank per wave; no barrier follows
-    const int r = r0 + wave;
-    if (r >= R) return;
-    u64 v[K];
-    bool ok[K];
+        __syncthreads();
+        // this wave's rank: its column to registers
+        u64 v[K];
+        bool ok[K];
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
-        const int i = k * 64 + lane;
-        ok[k] = i < n;
-        v[k] = ((u64)thi[i * STRIDE + wave] << 32) | tlo[i * STRIDE + wave];
-    }
-    u64 vmax = 0, vmin = ~0ull;
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-        if (ok[k]) {
-            vmax = umax64(vmax, v[k]);
-            vmin = umin64(vmin, v[k]);
+        for (int k = 0; k < K; ++k) {
+            const int i = k * 64 + lane;
+            ok[k] = i < q.n;
+            v[k] = ((u64)thi[i * STRIDE + wave] << 32) | tlo[i * STRIDE + wave];
         }
-    }
-    vmax = lane_value(group_max<64>(vmax), 63);
-    vmin = ~lane_value(group_max<64>(~vmin), 63);
-    const u64 range = vmax - vmin;
-    u64 um = 0;  // the median minus vmin
-    if (range != 0) {
+        // the next tile's loads fly while this one is resolved
+        if (b + gridDim.x < ntiles) load(tile(b + gridDim.x));
+        const int r = q.r0 + wave;
+        if (r >= R) continue;  // the barriers are at the top of the loop
+
+        u64 vmax = 0, vmin = ~0ull;
 #pragma unroll
-        for (int k = 0; k < K; ++k) v[k] -= vmin;
-        int lo = sel_first_lo(range), hi = lo + 8;
-        u64 prefix = 0;
-        uint32_t kk = (uint32_t)((n - 1) / 2);
-        for (;;) {
-#pragma unroll
-            for (int k = 0; k < K; ++k) sel_hist_add(h, ok[k] ? sel_bin(v[k], lo, hi, prefix) : -1);
-            wave_lds_fence();
-            // scan of the bins, kSelPerLane per lane; the lane whose bins hold
-            // the target rank names the bin, and every lane clears its bins
-            uint32_t c[kSelPerLane];
-            uint32_t* hl = h + lane * (kSelPerLane + 1);  // sel_slot(lane * kSelPerLane)
-            uint32_t part = 0;
-#pragma unroll
-            for (int i = 0; i < kSelPerLane; ++i) {
-                c[i] = hl[i];
-                part += c[i];
+        for (int k = 0; k < K; ++k) {
+            if (ok[k]) {
+                vmax = umax64(vmax, v[k]);
+                vmin = umin64(vmin, v[k]);
             }
-            const uint32_t incl = wave_scan_incl(part);
-            uint32_t cum = incl - part;
-            int fd = -1;
-            uint32_t fk = 0, fc = 0;
-            if (cum <= kk && kk < incl) {
+        }
+        vmax = lane_value(group_max<64>(vmax), 63);
+        vmin = ~lane_value(group_max<64>(~vmin), 63);
+        const u64 range = vmax - vmin;
+        u64 um = 0;  // the median minus vmin
+        if (range != 0) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) v[k] -= vmin;
+            int lo = sel_first_lo(range), hi = lo + 8;
+            u64 prefix = 0;
+            uint32_t kk = (uint32_t)((q.n - 1) / 2);
+            bool compact = false;  // the values left are one per lane in (c1, ok1)
+            u64 c1 = 0;
+            bool ok1 = false;
+            for (;;) {
+                if (compact) {
+                    sel_hist_add(h, ok1 ? sel_bin(c1, lo, hi, prefix) : -1);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < K; ++k) sel_hist_add(h, ok[k] ? sel_bin(v[k], lo, hi, prefix) : -1);
+                }
+                wave_lds_fence();
+                // scan of the bins, kSelPerLane per lane; the lane whose bins
+                // hold the target rank names the bin, and every lane clears
+                // its bins
+                uint32_t cnt[kSelPerLane];
+                uint32_t* hl = h + lane * (kSelPerLane + 1);  // sel_slot(lane * kSelPerLane)
+                uint32_t part = 0;
 #pragma unroll
                 for (int i = 0; i < kSelPerLane; ++i) {
-                    if (fd < 0 && kk < cum + c[i]) {
-                        fd = lane * kSelPerLane + i;
-                        fk = kk - cum;
-                        fc = c[i];
-                    }
-                    cum += c[i];
+                    cnt[i] = hl[i];
+                    part += cnt[i];
                 }
-            }
+                const uint32_t incl = wave_scan_incl(part);
+                uint32_t cum = incl - part;
+                int fd = -1;
+                uint32_t fk = 0, fc = 0;
+                if (cum <= kk && kk < incl) {
 #pragma unroll
-            for (int i = 0; i <= kSelPerLane; ++i) hl[i] = 0;
-            wave_lds_fence();
-            // the candidates hold the target rank, so exactly one lane found it
-            const u64 fm = __ballot(fd >= 0);
-            const int src = fm ? __builtin_ctzll(fm) : 0;
-            const int digit = __builtin_amdgcn_readlane(fd, src);
-            kk = (uint32_t)__builtin_amdgcn_readlane((int)fk, src);
-            const uint32_t count = (uint32_t)__builtin_amdgcn_readlane((int)fc, src);
-            prefix = (prefix << (hi - lo)) | (u64)(uint32_t)digit;
-            hi = lo;
-            if (hi == 0) break;  // every bit chosen: u == prefix
-            lo = lo > 8 ? lo - 8 : 0;
-            if (count == 1) {
-                // one value has the chosen digits: its lane hands it over
-                u64 x = 0;
-                bool has = false;
-#pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    if (ok[k] && sel_bin(v[k], lo, hi, prefix) >= 0) {
-                        x = v[k];
-                        has = true;
+                    for (int i = 0; i < kSelPerLane; ++i) {
+                        if (fd < 0 && kk < cum + cnt[i]) {
+                            fd = lane * kSelPerLane + i;
+                            fk = kk - cum;
+                            fc = cnt[i];
+                        }
+                        cum += cnt[i];
                     }
                 }
-                const u64 hm = __ballot(has);
-                prefix = lane_value(x, hm ? __builtin_ctzll(hm) : 0);
-                break;
+#pragma unroll
+                for (int i = 0; i <= kSelPerLane; ++i) hl[i] = 0;
+                wave_lds_fence();
+                // the candidates hold the target rank, so exactly one lane found it
+                const u64 fm = __ballot(fd >= 0);
+                const int src = fm ? __builtin_ctzll(fm) : 0;
+                const int digit = __builtin_amdgcn_readlane(fd, src);
+                kk = (uint32_t)__builtin_amdgcn_readlane((int)fk, src);
+                const uint32_t count = (uint32_t)__builtin_amdgcn_readlane((int)fc, src);
+                prefix = (prefix << (hi - lo)) | (u64)(uint32_t)digit;
+                hi = lo;
+                if (hi == 0) break;  // every bit chosen: u == prefix
+                lo = lo > 8 ? lo - 8 : 0;
+                if (count == 1) {
+                    // one value has the chosen digits: its lane hands it over
+                    u64 x = 0;
+                    bool has = false;
+                    if (compact) {
+                        has = ok1 && sel_bin(c1, lo, hi, prefix) >= 0;
+                        x = c1;
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < K; ++k) {
+                            if (ok[k] && sel_bin(v[k], lo, hi, prefix) >= 0) {
+                                x = v[k];
+                                has = true;
+                            }
+                        }
+                    }
+                    const u64 hm = __ballot(has);
+                    prefix = lane_value(x, hm ? __builtin_ctzll(hm) : 0);
+                    break;
+                }
+                if (!compact && count <= (uint32_t)LIST) {
+                    // the values left, one per lane, through rows [0, count)
+                    // of this wave's tile column (read already)
+                    uint32_t cand = 0;  // bit k: v[k] is left
+#pragma unroll
+                    for (int k = 0; k < K; ++k)
+                        cand |= (ok[k] && sel_bin(v[k], lo, hi, prefix) >= 0) ? (1u << k) : 0u;
+                    const uint32_t nc = (uint32_t)__popc(cand);
+                    uint32_t pos = wave_scan_incl(nc) - nc;
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        if ((cand >> k) & 1u) {
+                            if (pos < (uint32_t)LIST) {  // always, as count <= LIST
+                                tlo[pos * STRIDE + wave] = (uint32_t)v[k];
+                                thi[pos * STRIDE + wave] = (uint32_t)(v[k] >> 32);
+                            }
+                            ++pos;
+                        }
+                    }
+                    wave_lds_fence();
+                    ok1 = (uint32_t)lane < count;
+                    c1 = ok1 ? (((u64)thi[lane * STRIDE + wave] << 32) | tlo[lane * STRIDE + wave]) : 0ull;
+                    compact = true;
+                }
             }
+            um = prefix;
         }
-        um = prefix;
+        if (lane == 0) med[(q.w * S + q.s) * (int64_t)R + r] = (int64_t)(vmin + um);
     }
-    if (lane == 0) med[(w * S + s) * (int64_t)R + r] = (int64_t)(vmin + um);
 }
 
 struct MedianVariant {
@@ -230,10 +288,17 @@ SF_API int sf_window_median(const int64_t* durations, int64_t T, int32_t R, int3
     const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
     const MedianVariant v = vec2 ? pick_median<2>(n_max) : pick_median<1>(n_max);
     const int nchunk = (R + v.RPW - 1) / v.RPW;
-    const int64_t blocks = W * S * (int64_t)nchunk;
-    if (blocks > INT32_MAX) return SF_EINVAL;
+    int64_t ntiles = W * S * (int64_t)nchunk;
+    // persistent workgroups: as many as are resident at once
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, v.fn, v.WG, 0) != hipSuccess)
+        return SF_EHIP;
+    int64_t grid = (int64_t)(cus > 0 ? cus : 1) * (per_cu > 0 ? per_cu : 1);
+    if (grid > ntiles) grid = ntiles;
     int Ri = R, Si = S;
-    void* args[] = {(void*)&durations, (void*)&T,      (void*)&Ri,        (void*)&Si,
-                    (void*)&window,    (void*)&nchunk, (void*)&out_median};
-    return launch(v.fn, dim3((unsigned)blocks), dim3(v.WG), args, 0, stream);
+    void* args[] = {(void*)&durations, (void*)&T,      (void*)&Ri,     (void*)&Si,
+                    (void*)&window,    (void*)&nchunk, (void*)&ntiles, (void*)&out_median};
+    return launch(v.fn, dim3((unsigned)grid), dim3(v.WG), args, 0, stream);
 }
