@@ -64,6 +64,8 @@ class COracle:
         lib.sfo_rank_spread.restype = ctypes.c_int
         lib.sfo_window_median.argtypes = [vp, i64, i32, i32, i64, vp]
         lib.sfo_window_median.restype = ctypes.c_int
+        lib.sfo_range_status.argtypes = [vp, i64, i32, i32]
+        lib.sfo_range_status.restype = ctypes.c_int
         self.lib = lib
         self.path = path
 
@@ -172,6 +174,19 @@ class COracle:
                 raise MemoryError("oracle scratch allocation failed")
         return med
 
+    def range_status(self, d: np.ndarray) -> int:
+        """2 (SF_ERANGE) if some duration is negative or some prefix reaches
+        2^47 ns, else 0 (the data contract of Sec. 3 with the library's
+        prefix bound)."""
+        d = np.ascontiguousarray(d, dtype=np.int64)
+        T, S, R = d.shape
+        if not (T and S and R):
+            return 0
+        st = self.lib.sfo_range_status(d.ctypes.data, T, R, S)
+        if st < 0:
+            raise MemoryError("oracle scratch allocation failed")
+        return st
+
     def exposure_gain(self, d: np.ndarray, btilde: np.ndarray, window: int):
         """Eq. (4) numerators and denominators.
 
@@ -268,9 +283,13 @@ def window_median(d: np.ndarray, window: int):
     return _get().window_median(d, window)
 
 
+def range_status(d: np.ndarray) -> int:
+    return _get().range_status(d)
+
+
 from . import pyref  # noqa: E402  (pure-Python twin, no compiled code)
 
 __all__ = ["build", "COracle", "frontier", "frontier_evidence", "frontier_lag", "rank_spread",
-           "window_median", "ingest", "route",
+           "window_median", "range_status", "ingest", "route",
            "exposure_gain",
            "window_summary", "num_windows", "pyref"]

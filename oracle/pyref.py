@@ -187,3 +187,17 @@ def window_median(d, window):
         out.append([[sorted(st[s][r] for st in steps)[(len(steps) - 1) // 2] for r in range(R)]
                     for s in range(S)])
     return out
+
+
+def range_status(d):
+    """2 if some duration is negative or some prefix reaches 2**47, else 0."""
+    for step in d:
+        P = [0] * len(step[0])
+        for row in step:
+            for r, x in enumerate(row):
+                if x < 0:
+                    return 2
+                P[r] += x
+                if P[r] >= 1 << 47:
+                    return 2
+    return 0

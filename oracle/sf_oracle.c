@@ -38,6 +38,10 @@
  *   steps of a window.
  *   Sec. 4, Eq. (4), per-rank window median: a candidate baseline btilde,
  *   the median over the steps of a window of d[t,r,s], per stage and rank.
+ *   Sec. 3, the data contract: durations are nonnegative; with the
+ *   library's packed keys every prefix must also stay below 2^47 ns.  The
+ *   range status is 2 (SF_ERANGE) when some d < 0 or some prefix of
+ *   nonnegative durations reaches 2^47, else 0.
  *
  * Readings where the paper leaves a choice open (each is listed with its
  * reason in the design notes of the repository):
@@ -425,4 +429,32 @@ int sfo_window_median(const int64_t* d, int64_t T, int32_t R, int32_t S, int64_t
     }
     free(col);
     return 0;
+}
+
+/* Range status of the data contract (Sec. 3: nonnegative durations; prefixes
+ * below 2^47 ns for the library's packed keys): 2 (SF_ERANGE) if some
+ * d[t][s][r] < 0 or some prefix P[t][r][s] >= 2^47, else 0.  A rank stops
+ * accumulating once it is flagged, so nothing overflows.
+ * Returns the status, or -1 if scratch cannot be allocated. */
+int sfo_range_status(const int64_t* d, int64_t T, int32_t R, int32_t S)
+{
+    const int64_t limit = (int64_t)1 << 47;
+    int64_t* P = (int64_t*)malloc(sizeof(int64_t) * (size_t)(R > 0 ? R : 1));
+    if (!P) return -1;
+    int status = 0;
+    for (int64_t t = 0; t < T && status == 0; ++t) {
+        for (int32_t r = 0; r < R; ++r) P[r] = 0;
+        for (int32_t s = 0; s < S && status == 0; ++s) {
+            const int64_t* row = d + (t * S + s) * (int64_t)R;
+            for (int32_t r = 0; r < R; ++r) {
+                if (row[r] < 0 || row[r] >= limit - P[r]) {
+                    status = 2;
+                    break;
+                }
+                P[r] += row[r];
+            }
+        }
+    }
+    free(P);
+    return status;
 }

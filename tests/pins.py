@@ -997,3 +997,56 @@ def pin_median_twin(wm, pyref):
 
 MEDIAN_PINS = [pin_median_identity_window, pin_median_library, pin_median_invariants,
                pin_median_bruteforce]
+
+
+# ----------------------------------------------------------------------------
+# range status of the data contract (Sec. 3: d >= 0; prefixes below 2^47)
+#
+# Pins take ``rs(d[T,S,R]) -> 0 or 2``.
+
+LIMIT = 1 << 47
+
+
+def pin_range_edges(rs):
+    """The bound is exclusive, on prefixes as well as on single durations."""
+    z = np.zeros((2, 3, 4), dtype=np.int64)
+    assert rs(z) == 0
+    d = z.copy(); d[1, 2, 3] = -1
+    assert rs(d) == 2                                   # one negative duration
+    d = z.copy(); d[0, 0, 0] = LIMIT - 1
+    assert rs(d) == 0                                   # largest allowed prefix
+    d = z.copy(); d[0, 0, 0] = LIMIT
+    assert rs(d) == 2                                   # one duration at the bound
+    d = z.copy(); d[0, :, 2] = [LIMIT // 2, LIMIT // 4, LIMIT // 4 - 1]
+    assert rs(d) == 0                                   # a prefix of 2^47 - 1
+    d[0, 2, 2] += 1
+    assert rs(d) == 2                                   # the same prefix reaching 2^47
+    d = z.copy(); d[:, :, 1] = LIMIT // 3               # each step's prefix is 3 * floor(2^47 / 3)
+    assert rs(d) == 0                                   # steps are separate: no carry across steps
+    d = z.copy(); d[0, 0, 0] = np.iinfo(np.int64).max
+    assert rs(d) == 2
+    d = z.copy(); d[0, 0, 0] = np.iinfo(np.int64).min
+    assert rs(d) == 2
+
+
+def pin_range_library(rs):
+    """numpy's cumulative sums (exact here: every value is small or the
+    first prefix already crosses) and sign test on random inputs."""
+    rng = np.random.Generator(np.random.PCG64(80))
+    for _ in range(40):
+        T, S, R = rng.integers(1, 6, size=3)
+        d = rng.integers(0, 1 << 46, size=(T, S, R), dtype=np.int64)
+        if rng.random() < 0.3:
+            d[rng.integers(T), rng.integers(S), rng.integers(R)] = -int(rng.integers(1, 10))
+        want = 2 if ((d < 0).any() or (np.cumsum(np.maximum(d, 0), axis=1) >= LIMIT).any()) else 0
+        assert rs(d) == want
+
+
+def pin_range_twin(rs, pyref):
+    rng = np.random.Generator(np.random.PCG64(81))
+    for _ in range(20):
+        d = rng.integers(-2, 1 << 45, size=(3, 6, 5), dtype=np.int64)
+        assert rs(d) == pyref.range_status(d.tolist())
+
+
+RANGE_PINS = [pin_range_edges, pin_range_library]

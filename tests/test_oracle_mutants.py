@@ -110,6 +110,13 @@ MUTANTS = {
                                  "wspread[w * S + s] = x;"),
     "spread_drops_last_rank": ("sfo_rank_spread", "qsort(sorted, (size_t)R, sizeof(int64_t), cmp_i64);",
                                "qsort(sorted, (size_t)(R > 1 ? R - 1 : R), sizeof(int64_t), cmp_i64);"),
+    # range status
+    "range_inclusive_bound": ("sfo_range_status", "if (row[r] < 0 || row[r] >= limit - P[r]) {",
+                              "if (row[r] < 0 || row[r] > limit - P[r]) {"),
+    "range_ignores_negative": ("sfo_range_status", "if (row[r] < 0 || row[r] >= limit - P[r]) {",
+                               "if (row[r] >= limit - P[r]) {"),
+    "range_durations_not_prefixes": ("sfo_range_status", "P[r] += row[r];", ""),
+    "range_carries_across_steps": ("sfo_range_status", "for (int32_t r = 0; r < R; ++r) P[r] = 0;", ""),
     # per-rank window median
     "median_upper": ("sfo_window_median", "med[(w * S + s) * (int64_t)R + r] = col[(n - 1) / 2];",
                      "med[(w * S + s) * (int64_t)R + r] = col[n / 2];"),
@@ -180,6 +187,11 @@ def _run_all(o):
     for pin in pins.MEDIAN_PINS:
         try:
             pin(o.window_median)
+        except AssertionError:
+            failed.append(pin.__name__)
+    for pin in pins.RANGE_PINS:
+        try:
+            pin(o.range_status)
         except AssertionError:
             failed.append(pin.__name__)
     return failed

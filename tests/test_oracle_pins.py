@@ -117,3 +117,12 @@ def test_median_pin(pin):
 
 def test_twin_median():
     pins.pin_median_twin(oracle.window_median, oracle.pyref)
+
+
+@pytest.mark.parametrize("pin", pins.RANGE_PINS, ids=lambda p: p.__name__)
+def test_range_pin(pin):
+    pin(oracle.range_status)
+
+
+def test_twin_range():
+    pins.pin_range_twin(oracle.range_status, oracle.pyref)
