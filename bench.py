@@ -246,6 +246,39 @@ def main() -> int:
         }
         del ev_out, ev_views
 
+        # next row: the checked frontier pass (the data contract verified on
+        # the same read), same chunks; its outputs must equal the path's
+        ck_inc = torch.empty((T, S), dtype=torch.int64, device=dev)
+        ck_lead = torch.empty((T, S), dtype=torch.int32, device=dev)
+        ck_status = torch.zeros((1,), dtype=torch.int32, device=dev)
+        ck_views = [(d[t0:t1], ck_inc[t0:t1], ck_lead[t0:t1]) for t0, t1 in bounds]
+        for dv, a1, a2 in ck_views:
+            sf.sf_frontier_checked(dv, a1, a2, ck_status, stream=stream)
+        cks = []
+        for _ in range(max(3, args.steps // 2)):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for dv, a1, a2 in ck_views:
+                sf.sf_frontier_checked(dv, a1, a2, ck_status, stream=stream)
+            b.record(stream)
+            cks.append((a, b))
+        torch.cuda.synchronize(dev)
+        ck_ms = float(np.mean([a.elapsed_time(b) for a, b in cks])) / len(bounds)
+        ck_bytes = (8 * T * S * R + 12 * T * S) / len(bounds)
+        next_rows["frontier_checked"] = {
+            "kernel": "k_frontier<..., check>",
+            "bound": "hbm",
+            "launch_ms": ck_ms,
+            "algorithmic_bytes_per_launch": ck_bytes,
+            "achieved": ck_bytes / (ck_ms / 1e3) / 1e9,
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": ck_bytes / (ck_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+            "status": int(ck_status.cpu()[0]),
+            "outputs_equal_path": bool(torch.equal(ck_inc, inc) and torch.equal(ck_lead, lead)),
+        }
+        del ck_inc, ck_lead, ck_status, ck_views
+
         # next row: ingest (the step before the path).  The first chunk's
         # per-rank buffers [R][n][S-1] and step wall times [R][n] are rebuilt
         # from the resident matrix; ingesting them must give the chunk back

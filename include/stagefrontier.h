@@ -47,7 +47,8 @@ enum {
     SF_OK = 0,
     SF_EINVAL = 1, /* bad argument: NULL pointer, size out of range,
                       misaligned pointer, overlapping outputs, overflow   */
-    SF_ERANGE = 2, /* reserved for data-range errors                     */
+    SF_ERANGE = 2, /* data outside the contract (sf_frontier_checked's
+                      status word; never returned by a call)             */
     SF_EHIP = 3    /* the HIP runtime rejected a kernel launch            */
 };
 
@@ -97,6 +98,27 @@ enum {
 int sf_frontier(const int64_t* durations, int64_t T, int32_t R, int32_t S,
                 int64_t* out_increment, int32_t* out_leader,
                 sf_stream_t stream);
+
+/*
+ * sf_frontier_checked -- sf_frontier, verifying the data contract on the
+ * same pass: if some duration lies outside [0, SF_MAX_PREFIX_NS) or some
+ * prefix P[t][r][s] reaches SF_MAX_PREFIX_NS, SF_ERANGE is OR-ed into
+ * *status.  The word is the caller's: the library never clears it, so one
+ * word can collect several calls; clear it before the first.  Where the
+ * contract holds the outputs equal sf_frontier's, and *status is untouched.
+ *
+ *   durations, T, R, S, out_increment, out_leader, stream: as for
+ *                  sf_frontier.
+ *   status         device uint32, 4-byte aligned, overlapping no array of
+ *                  the call.
+ *
+ * Data errors are reported only through *status, once the stream has
+ * reached this call.  Returns SF_OK, SF_EINVAL (also for a NULL status) or
+ * SF_EHIP.
+ */
+int sf_frontier_checked(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                        int64_t* out_increment, int32_t* out_leader, uint32_t* status,
+                        sf_stream_t stream);
 
 /*
  * sf_frontier_evidence -- the sf_frontier pass plus, at every boundary, the

@@ -20,6 +20,13 @@
 // advance F[s] - F[s-1] and writes [T][S] rows with contiguous stores.
 // Durations are read exactly once, with 16-byte loads when R is even.
 //
+// The checked variant also verifies the data contract on the way: every
+// duration in [0, 2^47) (its high word below 2^15) and every prefix below
+// 2^47 (the top bit of every key clear: while all durations are below 2^47
+// a prefix that first reaches 2^47 is still below 2^48, so its key's top bit
+// is set at that stage).  A wave that sees a violation ORs SF_ERANGE into the
+// caller's status word.
+//
 
 #include "sf_device.h"
 #include "sf_host.h"
@@ -28,11 +35,13 @@ namespace sfk {
 
 // VEC: int64 elements per load (2: 16-byte loads, needs even R and a 16-byte
 //      aligned base); K: ranks per lane per tile; G: lanes per step;
-// WG:  threads per workgroup (WG / G steps per workgroup).
-template <int VEC, int K, int G, int WG>
+// WG:  threads per workgroup (WG / G steps per workgroup); CHECK: verify the
+//      data contract into *status.
+template <int VEC, int K, int G, int WG, bool CHECK>
 __global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, int64_t T,
                                                  int R, int S, int64_t* __restrict__ inc,
-                                                 int32_t* __restrict__ lead)
+                                                 int32_t* __restrict__ lead,
+                                                 uint32_t* __restrict__ status)
 {
     static_assert(K % VEC == 0, "K must be a multiple of VEC");
     static_assert(WG % G == 0 || G == WG, "a workgroup holds whole steps");
@@ -50,6 +59,7 @@ __global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, 
     const int slot = tid / SUB;
     const bool writer = (tid % SUB) == SUB - 1;
     const int64_t t = (int64_t)blockIdx.x * SPW + j;
+    uint32_t dhi = 0, khi = 0;  // CHECK: OR of the durations' and the keys' high words
 
     if (t < T) {  // uniform over the step group
         const int64_t* dt = d + t * (int64_t)S * R;
@@ -90,7 +100,9 @@ __global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, 
                 for (int k = 0; k < K; ++k) {
                     q[k] += (u64)v[k] << kRankBits;
                     m = umax64(m, q[k]);
+                    if (CHECK) dhi |= (uint32_t)((u64)v[k] >> 32);
                 }
+                if (CHECK) khi |= (uint32_t)(m >> 32);
                 if (s + 1 < S) load_row(s + 1);
                 m = group_max<SUB>(m);
                 if (writer) {
@@ -99,6 +111,10 @@ __global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, 
                 }
             }
         }
+    }
+    if (CHECK) {
+        const u64 bad = __ballot((dhi >> 15) != 0 || (khi >> 31) != 0);
+        if (bad != 0 && (tid & 63) == __builtin_ctzll(bad)) atomicOr(status, (uint32_t)SF_ERANGE);
     }
     __syncthreads();
 
@@ -128,11 +144,11 @@ struct FrontierVariant {
     int per_cu;  // resident workgroups per CU to allow (0: no cap)
 };
 
-template <int VEC, int K, int G, int WG>
+template <int VEC, bool CHECK, int K, int G, int WG>
 FrontierVariant variant(int per_cu)
 {
-    return FrontierVariant{reinterpret_cast<const void*>(&k_frontier<VEC, K, G, WG>), K, G, WG,
-                           per_cu};
+    return FrontierVariant{reinterpret_cast<const void*>(&k_frontier<VEC, K, G, WG, CHECK>), K, G,
+                           WG, per_cu};
 }
 
 // Launch shape by rank count, measured on MI355X over R = 16 .. 16384.
@@ -140,28 +156,25 @@ FrontierVariant variant(int per_cu)
 // workgroups per CU read HBM fastest for large R: fewer concurrent step
 // streams, each with up to 32 KB of loads in flight per wave.  A tile wider
 // than R costs no HBM traffic (lane slots past R re-read a cached rank).
-template <int VEC>
+template <int VEC, bool CHECK>
 FrontierVariant pick_frontier(int R)
 {
-    if (R <= 8) return variant<VEC, 2, 4, 64>(0);
-    if (R <= 16) return variant<VEC, 2, 8, 128>(0);
-    if (R <= 32) return variant<VEC, 4, 8, 128>(0);
-    if (R <= 64) return variant<VEC, 4, 16, 256>(6);
-    if (R <= 128) return variant<VEC, 8, 32, 256>(6);
-    if (R <= 256) return variant<VEC, 16, 32, 256>(4);
-    if (R <= 512) return variant<VEC, 4, 256, 256>(0);
-    if (R <= 1024) return variant<VEC, 32, 64, 256>(6);
-    if (R <= 2048) return variant<VEC, 8, 512, 512>(0);
-    if (R <= 4096) return variant<VEC, 32, 256, 256>(0);
-    return variant<VEC, 32, 64, 64>(3);
+    if (R <= 8) return variant<VEC, CHECK, 2, 4, 64>(0);
+    if (R <= 16) return variant<VEC, CHECK, 2, 8, 128>(0);
+    if (R <= 32) return variant<VEC, CHECK, 4, 8, 128>(0);
+    if (R <= 64) return variant<VEC, CHECK, 4, 16, 256>(6);
+    if (R <= 128) return variant<VEC, CHECK, 8, 32, 256>(6);
+    if (R <= 256) return variant<VEC, CHECK, 16, 32, 256>(4);
+    if (R <= 512) return variant<VEC, CHECK, 4, 256, 256>(0);
+    if (R <= 1024) return variant<VEC, CHECK, 32, 64, 256>(6);
+    if (R <= 2048) return variant<VEC, CHECK, 8, 512, 512>(0);
+    if (R <= 4096) return variant<VEC, CHECK, 32, 256, 256>(0);
+    return variant<VEC, CHECK, 32, 64, 64>(3);
 }
 
-}  // namespace sfk
-
-using namespace sfk;
-
-SF_API int sf_frontier(const int64_t* durations, int64_t T, int32_t R, int32_t S,
-                       int64_t* out_increment, int32_t* out_leader, sf_stream_t stream)
+static int frontier_launch(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                           int64_t* out_increment, int32_t* out_leader, uint32_t* status,
+                           sf_stream_t stream)
 {
     if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S) return SF_EINVAL;
     if (!fits(T, S, R, 8)) return SF_EINVAL;
@@ -173,16 +186,38 @@ SF_API int sf_frontier(const int64_t* durations, int64_t T, int32_t R, int32_t S
     if (!disjoint(durations, nd, out_increment, ni) || !disjoint(durations, nd, out_leader, nl) ||
         !disjoint(out_increment, ni, out_leader, nl))
         return SF_EINVAL;
+    if (status && (!aligned(status, 4) || !disjoint(status, 4, durations, nd) ||
+                   !disjoint(status, 4, out_increment, ni) || !disjoint(status, 4, out_leader, nl)))
+        return SF_EINVAL;
 
     const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
-    const FrontierVariant v = vec2 ? pick_frontier<2>(R) : pick_frontier<1>(R);
+    const FrontierVariant v = status ? (vec2 ? pick_frontier<2, true>(R) : pick_frontier<1, true>(R))
+                                     : (vec2 ? pick_frontier<2, false>(R) : pick_frontier<1, false>(R));
     const int spw = v.WG / v.G;
     const int sub = v.G < 64 ? v.G : 64;
     const int64_t blocks = (T + spw - 1) / spw;
     if (blocks > INT32_MAX) return SF_EINVAL;
     const size_t lds = lds_request((size_t)(v.WG / sub) * S * sizeof(u64), v.per_cu);
     int Ri = R, Si = S;
-    void* args[] = {(void*)&durations, (void*)&T, (void*)&Ri, (void*)&Si, (void*)&out_increment,
-                    (void*)&out_leader};
+    void* args[] = {(void*)&durations,     (void*)&T,          (void*)&Ri,    (void*)&Si,
+                    (void*)&out_increment, (void*)&out_leader, (void*)&status};
     return launch(v.fn, dim3((unsigned)blocks), dim3(v.WG), args, lds, stream);
+}
+
+}  // namespace sfk
+
+using namespace sfk;
+
+SF_API int sf_frontier(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                       int64_t* out_increment, int32_t* out_leader, sf_stream_t stream)
+{
+    return frontier_launch(durations, T, R, S, out_increment, out_leader, nullptr, stream);
+}
+
+SF_API int sf_frontier_checked(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                               int64_t* out_increment, int32_t* out_leader, uint32_t* status,
+                               sf_stream_t stream)
+{
+    if (!status) return SF_EINVAL;
+    return frontier_launch(durations, T, R, S, out_increment, out_leader, status, stream);
 }

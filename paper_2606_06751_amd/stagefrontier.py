@@ -41,6 +41,8 @@ def _load() -> ctypes.CDLL:
     i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
     lib.sf_frontier.argtypes = [vp, i64, i32, i32, vp, vp, vp]
     lib.sf_frontier.restype = ctypes.c_int
+    lib.sf_frontier_checked.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp]
+    lib.sf_frontier_checked.restype = ctypes.c_int
     lib.sf_frontier_evidence.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp]
     lib.sf_frontier_evidence.restype = ctypes.c_int
     lib.sf_ingest.argtypes = [vp, vp, i64, i32, i32, vp, vp, vp]
@@ -128,6 +130,38 @@ def sf_frontier(durations: torch.Tensor, out_increment: torch.Tensor | None = No
 
 
 EVIDENCE_FIELDS = ("increment", "leader", "gap", "ties", "stage_max", "stage_sum")
+
+
+def sf_frontier_checked(durations: torch.Tensor, out_increment: torch.Tensor | None = None,
+                        out_leader: torch.Tensor | None = None, status: torch.Tensor | None = None,
+                        stream=None):
+    """``sf_frontier`` plus the data-contract check (``sf_frontier_checked``).
+
+    ``status`` is a one-element int32 tensor on the device (the bits of the
+    C ABI's uint32 word); a new zeroed one is made when none is given.  The
+    library only ORs ``SF_ERANGE`` into it.  Returns ``(out_increment,
+    out_leader, status)``.
+    """
+    if durations.dim() != 3:
+        raise ValueError("durations must be [T, S, R]")
+    T, S, R = durations.shape
+    _check(durations, "durations", torch.int64, (T, S, R))
+    dev = durations.device
+    if out_increment is None:
+        out_increment = torch.empty((T, S), dtype=torch.int64, device=dev)
+    if out_leader is None:
+        out_leader = torch.empty((T, S), dtype=torch.int32, device=dev)
+    if status is None:
+        status = torch.zeros((1,), dtype=torch.int32, device=dev)
+    _check(out_increment, "out_increment", torch.int64, (T, S))
+    _check(out_leader, "out_leader", torch.int32, (T, S))
+    _check(status, "status", torch.int32, (1,))
+    rc = _lib.sf_frontier_checked(durations.data_ptr(), T, R, S, out_increment.data_ptr(),
+                                  out_leader.data_ptr(), status.data_ptr(),
+                                  _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_frontier_checked")
+    return out_increment, out_leader, status
 
 
 def sf_frontier_evidence(durations: torch.Tensor, out: dict | None = None, stream=None) -> dict:

@@ -26,7 +26,8 @@ def sf():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["sf_exposure_gain", "sf_frontier", "sf_frontier_evidence",
+    assert declared_functions() == ["sf_exposure_gain", "sf_frontier", "sf_frontier_checked",
+                                    "sf_frontier_evidence",
                                     "sf_frontier_lag", "sf_ingest", "sf_num_windows",
                                     "sf_rank_spread", "sf_route", "sf_strerror", "sf_version",
                                     "sf_window_median", "sf_window_summary"]
@@ -93,6 +94,24 @@ def test_frontier_argument_checks(sf):
     assert call(inc=A + 8) == sf.SF_EINVAL        # output overlaps input
     assert call(lead=B + 16) == sf.SF_EINVAL      # outputs overlap
     assert call(T=1 << 50, R=sf.SF_MAX_R, S=sf.SF_MAX_S) == sf.SF_EINVAL  # size overflow
+
+
+def test_checked_argument_checks(sf):
+    lib = sf.raw_library()
+    D = 4 << 40
+
+    def call(**kw):
+        a = dict(dict(d=A, T=10, R=8, S=6, inc=B, lead=C, st=D), **kw)
+        return lib.sf_frontier_checked(a["d"], a["T"], a["R"], a["S"], a["inc"], a["lead"],
+                                       a["st"], None)
+
+    assert call(T=0, d=None, inc=None, lead=None) == sf.SF_OK
+    assert call(st=None) == sf.SF_EINVAL          # the status word is required
+    assert call(st=D + 2) == sf.SF_EINVAL         # misaligned
+    assert call(st=B + 8) == sf.SF_EINVAL         # inside an output
+    assert call(st=A + 16) == sf.SF_EINVAL        # inside the input
+    assert call(R=0) == sf.SF_EINVAL
+    assert call(inc=A + 8) == sf.SF_EINVAL        # output overlaps input
 
 
 def test_evidence_argument_checks(sf):
@@ -263,6 +282,7 @@ def test_ctypes_argtypes_cover_header(sf):
     lib = sf.raw_library()
     assert len(lib.sf_frontier.argtypes) == 7
     assert len(lib.sf_frontier_evidence.argtypes) == 11
+    assert len(lib.sf_frontier_checked.argtypes) == 8
     assert len(lib.sf_ingest.argtypes) == 8
     assert len(lib.sf_exposure_gain.argtypes) == 11
     assert len(lib.sf_frontier_lag.argtypes) == 7

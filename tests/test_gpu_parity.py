@@ -601,3 +601,59 @@ def test_median_feeds_gain(sf):
     o = oracle.exposure_gain(d, oracle.window_median(d, 20), 20)
     for k in GAIN_KEYS:
         np.testing.assert_array_equal(out[k].cpu().numpy(), o[k])
+
+
+# ----------------------------------------------------------------------------
+# the checked frontier pass: outputs of sf_frontier, plus the data contract
+
+def checked(sf, d, status=None):
+    inc, lead, st = sf.sf_frontier_checked(torch.from_numpy(np.ascontiguousarray(d)).to(DEV),
+                                           status=status)
+    torch.cuda.synchronize()
+    return inc.cpu().numpy(), lead.cpu().numpy(), int(st.cpu()[0])
+
+
+@pytest.mark.parametrize("R", [1, 3, 8, 16, 31, 64, 100, 128, 255, 256, 511, 512, 1000, 1024,
+                               2047, 2048, 4095, 4096, 5000, 16384])
+def test_checked_rank_sweep(sf, R):
+    """Every launch shape: clean data gives sf_frontier's outputs and a
+    clear status; one violation at the last step, stage and rank is seen."""
+    T, S = 5, 4
+    d = synth.random_durations(T, S, R, seed=R + 3, hi=10**9)
+    oi, ol = oracle.frontier(d)
+    inc, lead, st = checked(sf, d)
+    np.testing.assert_array_equal(inc, oi)
+    np.testing.assert_array_equal(lead, ol)
+    assert st == oracle.range_status(d) == 0
+    for bad in (-1, 1 << 47, np.iinfo(np.int64).min):
+        e = d.copy()
+        e[T - 1, S - 1, R - 1] = bad
+        assert checked(sf, e)[2] == oracle.range_status(e) == sf.SF_ERANGE, (R, bad)
+
+
+def test_checked_prefix_bound(sf):
+    """A prefix of 2^47 - 1 passes and the same prefix reaching 2^47 is
+    flagged, on a rank in the middle of a several-tile row; the status word
+    collects across calls and is never cleared by the library."""
+    T, S, R = 3, 5, 3001
+    lim = 1 << 47
+    d = np.zeros((T, S, R), dtype=np.int64)
+    d[1, :, 1777] = [lim // 4, lim // 4, lim // 4, lim // 8, lim // 8 - 1]
+    assert checked(sf, d)[2] == oracle.range_status(d) == 0
+    oi, ol = oracle.frontier(d)
+    inc, lead, _ = checked(sf, d)
+    np.testing.assert_array_equal(inc, oi)
+    np.testing.assert_array_equal(lead, ol)
+    e = d.copy()
+    e[1, 4, 1777] += 1
+    st = torch.zeros((1,), dtype=torch.int32, device=DEV)
+    assert checked(sf, e, st)[2] == oracle.range_status(e) == sf.SF_ERANGE
+    assert checked(sf, d, st)[2] == sf.SF_ERANGE          # kept, not cleared
+    for pin in (pins_range_edges_gpu,):
+        pin(sf)
+
+
+def pins_range_edges_gpu(sf):
+    import pins
+    pins.pin_range_edges(lambda d: checked(sf, d)[2])
+    pins.pin_range_library(lambda d: checked(sf, d)[2])
