@@ -657,3 +657,15 @@ def pins_range_edges_gpu(sf):
     import pins
     pins.pin_range_edges(lambda d: checked(sf, d)[2])
     pins.pin_range_library(lambda d: checked(sf, d)[2])
+
+
+def test_median_window_longer_than_input(sf):
+    """A window longer than the input is one window of all T steps; the
+    limit applies to min(window, T), so a 5000-step window over 1000 steps
+    is accepted and one over 1025 steps is not."""
+    for T, window, R in ((300, 1024, 20), (1000, 5000, 33), (1, 7, 5), (129, 10**9, 2)):
+        d = synth.random_durations(T, 3, R, seed=T + R, hi=10**8)
+        assert_median_equal(sf, d, window)
+    d = torch.zeros((1025, 1, 4), dtype=torch.int64, device=DEV)
+    with pytest.raises(sf.StageFrontierError):
+        sf.sf_window_median(d, 5000)
