@@ -79,9 +79,16 @@ def main() -> int:
                     help="budget of the CPU oracle baseline (0: skip)")
     ap.add_argument("--no-next", action="store_true",
                     help="skip timing the next-row passes (localization evidence)")
+    ap.add_argument("--rows", default=None,
+                    help="comma-separated next rows to time (default: all), e.g. lag,rank_spread")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="also run a plain 1 GiB copy kernel (for counter scaling)")
     args = ap.parse_args()
+
+    rows = None if args.rows is None else set(args.rows.split(","))
+
+    def want(row):
+        return rows is None or row in rows
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -205,329 +212,338 @@ def main() -> int:
     # per-stage max and sum) over the same chunks, timed the same way
     next_rows = {}
     if not args.no_next:
-        ev_out = {k: torch.empty((T, S), dtype=torch.int32 if k in ("leader", "ties") else torch.int64,
-                                 device=dev) for k in sf.EVIDENCE_FIELDS}
-        ev_views = [(d[t0:t1], {k: v[t0:t1] for k, v in ev_out.items()}) for t0, t1 in bounds]
-        for dv, ov in ev_views:
-            sf.sf_frontier_evidence(dv, ov, stream=stream)
-        evs = []
-        for _ in range(max(3, args.steps // 2)):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
+        btilde = None  # the window median, when that row runs
+        if want("frontier_evidence"):
+            ev_out = {k: torch.empty((T, S), dtype=torch.int32 if k in ("leader", "ties") else torch.int64,
+                                     device=dev) for k in sf.EVIDENCE_FIELDS}
+            ev_views = [(d[t0:t1], {k: v[t0:t1] for k, v in ev_out.items()}) for t0, t1 in bounds]
             for dv, ov in ev_views:
                 sf.sf_frontier_evidence(dv, ov, stream=stream)
-            b.record(stream)
-            evs.append((a, b))
-        torch.cuda.synchronize(dev)
-        ev_ms = float(np.mean([a.elapsed_time(b) for a, b in evs])) / len(bounds)
-        ev_bytes = (8 * T * S * R + 40 * T * S) / len(bounds)
-        ev_exact = None
-        if oracle_out:
-            import oracle
-            t0c = oracle_out[0][0]
-            n_chk = min(len(oracle_out[0][1]), 64)
-            # the first sampled steps, regenerated from the seed for the oracle
-            x = synth.generate(wl, t0c, t0c + n_chk)
-            o = oracle.frontier_evidence(x)
-            ev_exact = all(np.array_equal(ev_out[k][t0c:t0c + n_chk].cpu().numpy(), o[ok])
-                           for k, ok in (("increment", "inc"), ("leader", "lead"), ("gap", "gap"),
-                                         ("ties", "ties"), ("stage_max", "stage_max"),
-                                         ("stage_sum", "stage_sum")))
-        next_rows["frontier_evidence"] = {
-            "kernel": "k_frontier_evidence",
-            "bound": "hbm",
-            "launch_ms": ev_ms,
-            "algorithmic_bytes_per_launch": ev_bytes,
-            "achieved": ev_bytes / (ev_ms / 1e3) / 1e9,
-            "peak": PEAK_HBM_GBPS,
-            "unit": "GB/s",
-            "frac": ev_bytes / (ev_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
-            "bit_exact_first_steps": ev_exact,
-        }
-        del ev_out, ev_views
+            evs = []
+            for _ in range(max(3, args.steps // 2)):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                for dv, ov in ev_views:
+                    sf.sf_frontier_evidence(dv, ov, stream=stream)
+                b.record(stream)
+                evs.append((a, b))
+            torch.cuda.synchronize(dev)
+            ev_ms = float(np.mean([a.elapsed_time(b) for a, b in evs])) / len(bounds)
+            ev_bytes = (8 * T * S * R + 40 * T * S) / len(bounds)
+            ev_exact = None
+            if oracle_out:
+                import oracle
+                t0c = oracle_out[0][0]
+                n_chk = min(len(oracle_out[0][1]), 64)
+                # the first sampled steps, regenerated from the seed for the oracle
+                x = synth.generate(wl, t0c, t0c + n_chk)
+                o = oracle.frontier_evidence(x)
+                ev_exact = all(np.array_equal(ev_out[k][t0c:t0c + n_chk].cpu().numpy(), o[ok])
+                               for k, ok in (("increment", "inc"), ("leader", "lead"), ("gap", "gap"),
+                                             ("ties", "ties"), ("stage_max", "stage_max"),
+                                             ("stage_sum", "stage_sum")))
+            next_rows["frontier_evidence"] = {
+                "kernel": "k_frontier_evidence",
+                "bound": "hbm",
+                "launch_ms": ev_ms,
+                "algorithmic_bytes_per_launch": ev_bytes,
+                "achieved": ev_bytes / (ev_ms / 1e3) / 1e9,
+                "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s",
+                "frac": ev_bytes / (ev_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                "bit_exact_first_steps": ev_exact,
+            }
+            del ev_out, ev_views
 
         # next row: the checked frontier pass (the data contract verified on
         # the same read), same chunks; its outputs must equal the path's
-        ck_inc = torch.empty((T, S), dtype=torch.int64, device=dev)
-        ck_lead = torch.empty((T, S), dtype=torch.int32, device=dev)
-        ck_status = torch.zeros((1,), dtype=torch.int32, device=dev)
-        ck_views = [(d[t0:t1], ck_inc[t0:t1], ck_lead[t0:t1]) for t0, t1 in bounds]
-        for dv, a1, a2 in ck_views:
-            sf.sf_frontier_checked(dv, a1, a2, ck_status, stream=stream)
-        cks = []
-        for _ in range(max(3, args.steps // 2)):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
+        if want("frontier_checked"):
+            ck_inc = torch.empty((T, S), dtype=torch.int64, device=dev)
+            ck_lead = torch.empty((T, S), dtype=torch.int32, device=dev)
+            ck_status = torch.zeros((1,), dtype=torch.int32, device=dev)
+            ck_views = [(d[t0:t1], ck_inc[t0:t1], ck_lead[t0:t1]) for t0, t1 in bounds]
             for dv, a1, a2 in ck_views:
                 sf.sf_frontier_checked(dv, a1, a2, ck_status, stream=stream)
-            b.record(stream)
-            cks.append((a, b))
-        torch.cuda.synchronize(dev)
-        ck_ms = float(np.mean([a.elapsed_time(b) for a, b in cks])) / len(bounds)
-        ck_bytes = (8 * T * S * R + 12 * T * S) / len(bounds)
-        next_rows["frontier_checked"] = {
-            "kernel": "k_frontier<..., check>",
-            "bound": "hbm",
-            "launch_ms": ck_ms,
-            "algorithmic_bytes_per_launch": ck_bytes,
-            "achieved": ck_bytes / (ck_ms / 1e3) / 1e9,
-            "peak": PEAK_HBM_GBPS,
-            "unit": "GB/s",
-            "frac": ck_bytes / (ck_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
-            "status": int(ck_status.cpu()[0]),
-            "outputs_equal_path": bool(torch.equal(ck_inc, inc) and torch.equal(ck_lead, lead)),
-        }
-        del ck_inc, ck_lead, ck_status, ck_views
+            cks = []
+            for _ in range(max(3, args.steps // 2)):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                for dv, a1, a2 in ck_views:
+                    sf.sf_frontier_checked(dv, a1, a2, ck_status, stream=stream)
+                b.record(stream)
+                cks.append((a, b))
+            torch.cuda.synchronize(dev)
+            ck_ms = float(np.mean([a.elapsed_time(b) for a, b in cks])) / len(bounds)
+            ck_bytes = (8 * T * S * R + 12 * T * S) / len(bounds)
+            next_rows["frontier_checked"] = {
+                "kernel": "k_frontier<..., check>",
+                "bound": "hbm",
+                "launch_ms": ck_ms,
+                "algorithmic_bytes_per_launch": ck_bytes,
+                "achieved": ck_bytes / (ck_ms / 1e3) / 1e9,
+                "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s",
+                "frac": ck_bytes / (ck_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                "status": int(ck_status.cpu()[0]),
+                "outputs_equal_path": bool(torch.equal(ck_inc, inc) and torch.equal(ck_lead, lead)),
+            }
+            del ck_inc, ck_lead, ck_status, ck_views
 
         # next row: ingest (the step before the path).  The first chunk's
         # per-rank buffers [R][n][S-1] and step wall times [R][n] are rebuilt
         # from the resident matrix; ingesting them must give the chunk back
         # with zero overlap error (its last stage is the residual of the rest).
-        t0, t1 = bounds[0]
-        n = t1 - t0
-        xs = d[t0:t1, : S - 1, :].permute(2, 0, 1).contiguous()
-        wall = d[t0:t1].sum(dim=1).transpose(0, 1).contiguous()
-        ing_d = torch.empty((n, S, R), dtype=torch.int64, device=dev)
-        ing_o = torch.empty((n, R), dtype=torch.int64, device=dev)
-        sf.sf_ingest(xs, wall, ing_d, ing_o, stream=stream)
-        torch.cuda.synchronize(dev)
-        roundtrip = bool(torch.equal(ing_d, d[t0:t1]) and int(ing_o.abs().max()) == 0)
-        ig = []
-        for _ in range(max(3, args.steps // 2)):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
+        if want("ingest"):
+            t0, t1 = bounds[0]
+            n = t1 - t0
+            xs = d[t0:t1, : S - 1, :].permute(2, 0, 1).contiguous()
+            wall = d[t0:t1].sum(dim=1).transpose(0, 1).contiguous()
+            ing_d = torch.empty((n, S, R), dtype=torch.int64, device=dev)
+            ing_o = torch.empty((n, R), dtype=torch.int64, device=dev)
             sf.sf_ingest(xs, wall, ing_d, ing_o, stream=stream)
-            b.record(stream)
-            ig.append((a, b))
-        torch.cuda.synchronize(dev)
-        ig_ms = float(np.mean([a.elapsed_time(b) for a, b in ig]))
-        ig_bytes = 8 * R * n * (S - 1) + 8 * R * n + 8 * n * S * R + 8 * n * R
-        next_rows["ingest"] = {
-            "kernel": "k_ingest",
-            "bound": "hbm",
-            "launch_ms": ig_ms,
-            "algorithmic_bytes_per_launch": ig_bytes,
-            "achieved": ig_bytes / (ig_ms / 1e3) / 1e9,
-            "peak": PEAK_HBM_GBPS,
-            "unit": "GB/s",
-            "frac": ig_bytes / (ig_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
-            "shape": {"ranks": R, "steps": n, "explicit_stages": S - 1},
-            "roundtrip_exact": roundtrip,
-        }
-        del xs, wall, ing_d, ing_o
-
-        # next row: the per-rank window median (a baseline btilde of Eq. (4)),
-        # per chunk (the chunks are whole windows)
-        btilde = None
-        if min(wl.window, T) <= sf.SF_MAX_WINDOW_MEDIAN:
-            btilde = torch.empty((W, S, R), dtype=torch.int64, device=dev)
-            m_views = []
-            for t0, t1 in bounds:
-                w0, w1 = t0 // wl.window, -(-t1 // wl.window)
-                m_views.append((d[t0:t1], btilde[w0:w1]))
-            for dv, mv in m_views:
-                sf.sf_window_median(dv, wl.window, mv, stream=stream)
-            mt = []
+            torch.cuda.synchronize(dev)
+            roundtrip = bool(torch.equal(ing_d, d[t0:t1]) and int(ing_o.abs().max()) == 0)
+            ig = []
             for _ in range(max(3, args.steps // 2)):
                 a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 a.record(stream)
-                for dv, mv in m_views:
-                    sf.sf_window_median(dv, wl.window, mv, stream=stream)
+                sf.sf_ingest(xs, wall, ing_d, ing_o, stream=stream)
                 b.record(stream)
-                mt.append((a, b))
+                ig.append((a, b))
             torch.cuda.synchronize(dev)
-            m_ms = float(np.mean([a.elapsed_time(b) for a, b in mt])) / len(bounds)
-            m_bytes = (8 * T * S * R + 8 * W * S * R) / len(bounds)
-            m_exact = None
-            if oracle_out:
-                import oracle
-                # window 0, ranks [0, 256): ranks are independent
-                x = synth.generate(wl, 0, min(T, wl.window))
-                rs = min(R, 256)
-                om = oracle.window_median(np.ascontiguousarray(x[:, :, :rs]), wl.window)
-                m_exact = bool(np.array_equal(btilde[:1, :, :rs].cpu().numpy(), om))
-            next_rows["window_median"] = {
-                "kernel": "k_window_median",
+            ig_ms = float(np.mean([a.elapsed_time(b) for a, b in ig]))
+            ig_bytes = 8 * R * n * (S - 1) + 8 * R * n + 8 * n * S * R + 8 * n * R
+            next_rows["ingest"] = {
+                "kernel": "k_ingest",
                 "bound": "hbm",
-                "launch_ms": m_ms,
-                "algorithmic_bytes_per_launch": m_bytes,
-                "achieved": m_bytes / (m_ms / 1e3) / 1e9,
+                "launch_ms": ig_ms,
+                "algorithmic_bytes_per_launch": ig_bytes,
+                "achieved": ig_bytes / (ig_ms / 1e3) / 1e9,
                 "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s",
-                "frac": m_bytes / (m_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
-                "bit_exact_window0_ranks": m_exact,
+                "frac": ig_bytes / (ig_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                "shape": {"ranks": R, "steps": n, "explicit_stages": S - 1},
+                "roundtrip_exact": roundtrip,
             }
-            del m_views
+            del xs, wall, ing_d, ing_o
+
+        # next row: the per-rank window median (a baseline btilde of Eq. (4)),
+        # per chunk (the chunks are whole windows)
+        if want("window_median"):
+            btilde = None
+            if min(wl.window, T) <= sf.SF_MAX_WINDOW_MEDIAN:
+                btilde = torch.empty((W, S, R), dtype=torch.int64, device=dev)
+                m_views = []
+                for t0, t1 in bounds:
+                    w0, w1 = t0 // wl.window, -(-t1 // wl.window)
+                    m_views.append((d[t0:t1], btilde[w0:w1]))
+                for dv, mv in m_views:
+                    sf.sf_window_median(dv, wl.window, mv, stream=stream)
+                mt = []
+                for _ in range(max(3, args.steps // 2)):
+                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a.record(stream)
+                    for dv, mv in m_views:
+                        sf.sf_window_median(dv, wl.window, mv, stream=stream)
+                    b.record(stream)
+                    mt.append((a, b))
+                torch.cuda.synchronize(dev)
+                m_ms = float(np.mean([a.elapsed_time(b) for a, b in mt])) / len(bounds)
+                m_bytes = (8 * T * S * R + 8 * W * S * R) / len(bounds)
+                m_exact = None
+                if oracle_out:
+                    import oracle
+                    # window 0, ranks [0, 256): ranks are independent
+                    x = synth.generate(wl, 0, min(T, wl.window))
+                    rs = min(R, 256)
+                    om = oracle.window_median(np.ascontiguousarray(x[:, :, :rs]), wl.window)
+                    m_exact = bool(np.array_equal(btilde[:1, :, :rs].cpu().numpy(), om))
+                next_rows["window_median"] = {
+                    "kernel": "k_window_median",
+                    "bound": "hbm",
+                    "launch_ms": m_ms,
+                    "algorithmic_bytes_per_launch": m_bytes,
+                    "achieved": m_bytes / (m_ms / 1e3) / 1e9,
+                    "peak": PEAK_HBM_GBPS,
+                    "unit": "GB/s",
+                    "frac": m_bytes / (m_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                    "bit_exact_window0_ranks": m_exact,
+                }
+                del m_views
 
         # next row: direct-exposure gain, Eq. (4), with the per-rank window
         # median as btilde (else the workload recipe's no-stall stage medians)
-        if btilde is None:
-            base = torch.tensor([b * synth.MS for b in wl.base_ms], dtype=torch.int64, device=dev)
-            btilde = base.view(1, S, 1).expand(W, S, R).contiguous()
-            g_baseline = "no-stall stage medians of the recipe"
-        else:
-            g_baseline = "per-rank window median (sf_window_median)"
-        g_out = {"gain": torch.empty((T, S), dtype=torch.int64, device=dev),
-                 "makespan": torch.empty((T,), dtype=torch.int64, device=dev),
-                 "window_gain": torch.empty((W, S), dtype=torch.int64, device=dev),
-                 "window_makespan": torch.empty((W,), dtype=torch.int64, device=dev)}
-        g_views = []
-        for t0, t1 in bounds:
-            w0, w1 = t0 // wl.window, -(-t1 // wl.window)
-            g_views.append((d[t0:t1], btilde[w0:w1],
-                            {"gain": g_out["gain"][t0:t1], "makespan": g_out["makespan"][t0:t1],
-                             "window_gain": g_out["window_gain"][w0:w1],
-                             "window_makespan": g_out["window_makespan"][w0:w1]}))
-        for dv, bv, ov in g_views:
-            sf.sf_exposure_gain(dv, bv, wl.window, ov, stream=stream)
-        gt = []
-        for _ in range(max(3, args.steps // 2)):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
+        if want("exposure_gain"):
+            if btilde is None:
+                base = torch.tensor([b * synth.MS for b in wl.base_ms], dtype=torch.int64, device=dev)
+                btilde = base.view(1, S, 1).expand(W, S, R).contiguous()
+                g_baseline = "no-stall stage medians of the recipe"
+            else:
+                g_baseline = "per-rank window median (sf_window_median)"
+            g_out = {"gain": torch.empty((T, S), dtype=torch.int64, device=dev),
+                     "makespan": torch.empty((T,), dtype=torch.int64, device=dev),
+                     "window_gain": torch.empty((W, S), dtype=torch.int64, device=dev),
+                     "window_makespan": torch.empty((W,), dtype=torch.int64, device=dev)}
+            g_views = []
+            for t0, t1 in bounds:
+                w0, w1 = t0 // wl.window, -(-t1 // wl.window)
+                g_views.append((d[t0:t1], btilde[w0:w1],
+                                {"gain": g_out["gain"][t0:t1], "makespan": g_out["makespan"][t0:t1],
+                                 "window_gain": g_out["window_gain"][w0:w1],
+                                 "window_makespan": g_out["window_makespan"][w0:w1]}))
             for dv, bv, ov in g_views:
                 sf.sf_exposure_gain(dv, bv, wl.window, ov, stream=stream)
-            b.record(stream)
-            gt.append((a, b))
-        torch.cuda.synchronize(dev)
-        g_ms = float(np.mean([a.elapsed_time(b) for a, b in gt])) / len(bounds)
-        n_per = T / len(bounds)
-        g_bytes = (8 * T * S * R + 8 * W * S * R + 8 * T * S + 8 * T + 8 * W * S + 8 * W) / len(bounds)
-        g_exact = None
-        if oracle_out:
-            import oracle
-            # the chain window median -> gain on the first 16 steps as one
-            # window of 16, on the GPU and (independently) in the oracle
-            n_chk = min(16, T)
-            x = synth.generate(wl, 0, n_chk)
-            xd = torch.from_numpy(x).to(dev)
-            if n_chk <= sf.SF_MAX_WINDOW_MEDIAN:
-                gb = sf.sf_window_median(xd, n_chk, stream=stream)
-                ob = oracle.window_median(x, n_chk)
-            else:
-                gb, ob = btilde[:1].contiguous(), btilde[:1].cpu().numpy()
-            go = sf.sf_exposure_gain(xd, gb, n_chk, stream=stream)
-            torch.cuda.synchronize(dev)
-            o = oracle.exposure_gain(x, ob, n_chk)
-            g_exact = bool(all(np.array_equal(go[k].cpu().numpy(), o[k]) for k in sf.GAIN_FIELDS))
-            del xd, gb, go
-        wg = g_out["window_gain"].sum(dim=0).double()
-        wm = float(g_out["window_makespan"].sum())
-        next_rows["exposure_gain"] = {
-            "kernel": "k_exposure_gain (+ k_window_sum)",
-            "bound": "hbm",
-            "launch_ms": g_ms,
-            "algorithmic_bytes_per_launch": g_bytes,
-            "achieved": g_bytes / (g_ms / 1e3) / 1e9,
-            "peak": PEAK_HBM_GBPS,
-            "unit": "GB/s",
-            "frac": g_bytes / (g_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
-            "steps_per_launch": n_per,
-            "baseline": g_baseline,
-            "G_s_all_windows": [round(float(v) / wm, 6) for v in wg],
-            "bit_exact_first_steps": g_exact,
-        }
-        del btilde, g_out, g_views
-
-        # next row: lag over the median rank (exact radix select per boundary)
-        if R <= sf.SF_MAX_R_LAG:
-            lg = torch.empty((T, S), dtype=torch.int64, device=dev)
-            lgi = torch.empty((T, S), dtype=torch.int64, device=dev)
-            l_views = [(d[t0:t1], lg[t0:t1], lgi[t0:t1]) for t0, t1 in bounds]
-            for dv, a1, a2 in l_views:
-                sf.sf_frontier_lag(dv, a1, a2, stream=stream)
-            lt = []
-            for _ in range(3):
+            gt = []
+            for _ in range(max(3, args.steps // 2)):
                 a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 a.record(stream)
-                for dv, a1, a2 in l_views:
-                    sf.sf_frontier_lag(dv, a1, a2, stream=stream)
+                for dv, bv, ov in g_views:
+                    sf.sf_exposure_gain(dv, bv, wl.window, ov, stream=stream)
                 b.record(stream)
-                lt.append((a, b))
+                gt.append((a, b))
             torch.cuda.synchronize(dev)
-            l_ms = float(np.mean([a.elapsed_time(b) for a, b in lt])) / len(bounds)
-            l_bytes = (8 * T * S * R + 16 * T * S) / len(bounds)
-            l_exact = None
+            g_ms = float(np.mean([a.elapsed_time(b) for a, b in gt])) / len(bounds)
+            n_per = T / len(bounds)
+            g_bytes = (8 * T * S * R + 8 * W * S * R + 8 * T * S + 8 * T + 8 * W * S + 8 * W) / len(bounds)
+            g_exact = None
             if oracle_out:
                 import oracle
-                x = synth.generate(wl, 0, 8)
-                ol, oi = oracle.frontier_lag(x)
-                l_exact = bool(np.array_equal(lg[:8].cpu().numpy(), ol) and
-                               np.array_equal(lgi[:8].cpu().numpy(), oi))
-            next_rows["lag"] = {
-                "kernel": "k_median_spread<prefix>",
-                "bound": "lds (radix select)",
-                "launch_ms": l_ms,
-                "algorithmic_bytes_per_launch": l_bytes,
-                "achieved": l_bytes / (l_ms / 1e3) / 1e9,
+                # the chain window median -> gain on the first 16 steps as one
+                # window of 16, on the GPU and (independently) in the oracle
+                n_chk = min(16, T)
+                x = synth.generate(wl, 0, n_chk)
+                xd = torch.from_numpy(x).to(dev)
+                if n_chk <= sf.SF_MAX_WINDOW_MEDIAN:
+                    gb = sf.sf_window_median(xd, n_chk, stream=stream)
+                    ob = oracle.window_median(x, n_chk)
+                else:
+                    gb, ob = btilde[:1].contiguous(), btilde[:1].cpu().numpy()
+                go = sf.sf_exposure_gain(xd, gb, n_chk, stream=stream)
+                torch.cuda.synchronize(dev)
+                o = oracle.exposure_gain(x, ob, n_chk)
+                g_exact = bool(all(np.array_equal(go[k].cpu().numpy(), o[k]) for k in sf.GAIN_FIELDS))
+                del xd, gb, go
+            wg = g_out["window_gain"].sum(dim=0).double()
+            wm = float(g_out["window_makespan"].sum())
+            next_rows["exposure_gain"] = {
+                "kernel": "k_exposure_gain (+ k_window_sum)",
+                "bound": "hbm",
+                "launch_ms": g_ms,
+                "algorithmic_bytes_per_launch": g_bytes,
+                "achieved": g_bytes / (g_ms / 1e3) / 1e9,
                 "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s",
-                "frac": l_bytes / (l_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
-                "bit_exact_first_steps": l_exact,
+                "frac": g_bytes / (g_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                "steps_per_launch": n_per,
+                "baseline": g_baseline,
+                "G_s_all_windows": [round(float(v) / wm, 6) for v in wg],
+                "bit_exact_first_steps": g_exact,
             }
-            del lg, lgi, l_views
+            del btilde, g_out, g_views
+
+        # next row: lag over the median rank (exact radix select per boundary)
+        if want("lag"):
+            if R <= sf.SF_MAX_R_LAG:
+                lg = torch.empty((T, S), dtype=torch.int64, device=dev)
+                lgi = torch.empty((T, S), dtype=torch.int64, device=dev)
+                l_views = [(d[t0:t1], lg[t0:t1], lgi[t0:t1]) for t0, t1 in bounds]
+                for dv, a1, a2 in l_views:
+                    sf.sf_frontier_lag(dv, a1, a2, stream=stream)
+                lt = []
+                for _ in range(3):
+                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a.record(stream)
+                    for dv, a1, a2 in l_views:
+                        sf.sf_frontier_lag(dv, a1, a2, stream=stream)
+                    b.record(stream)
+                    lt.append((a, b))
+                torch.cuda.synchronize(dev)
+                l_ms = float(np.mean([a.elapsed_time(b) for a, b in lt])) / len(bounds)
+                l_bytes = (8 * T * S * R + 16 * T * S) / len(bounds)
+                l_exact = None
+                if oracle_out:
+                    import oracle
+                    x = synth.generate(wl, 0, 8)
+                    ol, oi = oracle.frontier_lag(x)
+                    l_exact = bool(np.array_equal(lg[:8].cpu().numpy(), ol) and
+                                   np.array_equal(lgi[:8].cpu().numpy(), oi))
+                next_rows["lag"] = {
+                    "kernel": "k_median_spread<prefix>",
+                    "bound": "valu (radix select)",
+                    "launch_ms": l_ms,
+                    "algorithmic_bytes_per_launch": l_bytes,
+                    "achieved": l_bytes / (l_ms / 1e3) / 1e9,
+                    "peak": PEAK_HBM_GBPS,
+                    "unit": "GB/s",
+                    "frac": l_bytes / (l_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                    "bit_exact_first_steps": l_exact,
+                }
+                del lg, lgi, l_views
 
         # next row: raw rank spread (the dispersion baseline of Sec. 6.2),
         # the lag's selection on each stage's durations
-        if R <= sf.SF_MAX_R_LAG:
-            sp = torch.empty((T, S), dtype=torch.int64, device=dev)
-            wsp = torch.empty((W, S), dtype=torch.int64, device=dev)
-            s_views = []
-            for t0, t1 in bounds:
-                w0, w1 = t0 // wl.window, -(-t1 // wl.window)
-                s_views.append((d[t0:t1], sp[t0:t1], wsp[w0:w1]))
-            for dv, a1, a2 in s_views:
-                sf.sf_rank_spread(dv, wl.window, a1, a2, stream=stream)
-            st = []
-            for _ in range(3):
-                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                a.record(stream)
+        if want("rank_spread"):
+            if R <= sf.SF_MAX_R_LAG:
+                sp = torch.empty((T, S), dtype=torch.int64, device=dev)
+                wsp = torch.empty((W, S), dtype=torch.int64, device=dev)
+                s_views = []
+                for t0, t1 in bounds:
+                    w0, w1 = t0 // wl.window, -(-t1 // wl.window)
+                    s_views.append((d[t0:t1], sp[t0:t1], wsp[w0:w1]))
                 for dv, a1, a2 in s_views:
                     sf.sf_rank_spread(dv, wl.window, a1, a2, stream=stream)
-                b.record(stream)
-                st.append((a, b))
-            torch.cuda.synchronize(dev)
-            s_ms = float(np.mean([a.elapsed_time(b) for a, b in st])) / len(bounds)
-            s_bytes = (8 * T * S * R + 8 * T * S + 8 * W * S) / len(bounds)
-            s_exact = None
-            if oracle_out:
-                import oracle
-                x = synth.generate(wl, 0, 8)
-                osp, _ = oracle.rank_spread(x, wl.window)
-                s_exact = bool(np.array_equal(sp[:8].cpu().numpy(), osp))
-            wsum = wsp.sum(dim=0).double()
-            next_rows["rank_spread"] = {
-                "kernel": "k_median_spread<raw> (+ k_window_sum)",
-                "bound": "lds (radix select)",
-                "launch_ms": s_ms,
-                "algorithmic_bytes_per_launch": s_bytes,
-                "achieved": s_bytes / (s_ms / 1e3) / 1e9,
-                "peak": PEAK_HBM_GBPS,
-                "unit": "GB/s",
-                "frac": s_bytes / (s_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
-                "spread_share_all_windows": [round(float(v) / float(wsum.sum()), 6) for v in wsum]
-                if float(wsum.sum()) > 0 else None,
-                "bit_exact_first_steps": s_exact,
-            }
-            del sp, wsp, s_views
+                st = []
+                for _ in range(3):
+                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a.record(stream)
+                    for dv, a1, a2 in s_views:
+                        sf.sf_rank_spread(dv, wl.window, a1, a2, stream=stream)
+                    b.record(stream)
+                    st.append((a, b))
+                torch.cuda.synchronize(dev)
+                s_ms = float(np.mean([a.elapsed_time(b) for a, b in st])) / len(bounds)
+                s_bytes = (8 * T * S * R + 8 * T * S + 8 * W * S) / len(bounds)
+                s_exact = None
+                if oracle_out:
+                    import oracle
+                    x = synth.generate(wl, 0, 8)
+                    osp, _ = oracle.rank_spread(x, wl.window)
+                    s_exact = bool(np.array_equal(sp[:8].cpu().numpy(), osp))
+                wsum = wsp.sum(dim=0).double()
+                next_rows["rank_spread"] = {
+                    "kernel": "k_median_spread<raw> (+ k_window_sum)",
+                    "bound": "valu (radix select)",
+                    "launch_ms": s_ms,
+                    "algorithmic_bytes_per_launch": s_bytes,
+                    "achieved": s_bytes / (s_ms / 1e3) / 1e9,
+                    "peak": PEAK_HBM_GBPS,
+                    "unit": "GB/s",
+                    "frac": s_bytes / (s_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                    "spread_share_all_windows": [round(float(v) / float(wsum.sum()), 6) for v in wsum]
+                    if float(wsum.sum()) > 0 else None,
+                    "bit_exact_first_steps": s_exact,
+                }
+                del sp, wsp, s_views
 
         # next row: routing candidate set (tau 4/5) of the path's windows
-        order = torch.empty((W, S), dtype=torch.int32, device=dev)
-        size = torch.empty((W,), dtype=torch.int32, device=dev)
-        rt = []
-        for _ in range(max(3, args.steps // 2)):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            sf.sf_route(ex, 4, 5, order, size, stream=stream)
-            b.record(stream)
-            rt.append((a, b))
-        torch.cuda.synchronize(dev)
-        next_rows["route"] = {
-            "kernel": "k_route",
-            "bound": "launch",
-            "launch_ms": float(np.mean([a.elapsed_time(b) for a, b in rt])),
-            "windows": W,
-            "candidate_sizes": np.bincount(size.cpu().numpy(), minlength=S + 1).tolist(),
-        }
+        if want("route"):
+            order = torch.empty((W, S), dtype=torch.int32, device=dev)
+            size = torch.empty((W,), dtype=torch.int32, device=dev)
+            rt = []
+            for _ in range(max(3, args.steps // 2)):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                sf.sf_route(ex, 4, 5, order, size, stream=stream)
+                b.record(stream)
+                rt.append((a, b))
+            torch.cuda.synchronize(dev)
+            next_rows["route"] = {
+                "kernel": "k_route",
+                "bound": "launch",
+                "launch_ms": float(np.mean([a.elapsed_time(b) for a, b in rt])),
+                "windows": W,
+                "candidate_sizes": np.bincount(size.cpu().numpy(), minlength=S + 1).tolist(),
+            }
 
     samples = T * S * R
     value = samples / (ms_per_step / 1e3)
