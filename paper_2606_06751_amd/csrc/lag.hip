@@ -44,7 +44,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
     __shared__ u64 red_max[2][NW], red_min[2][NW];
     // two histograms used alternately: while wave 0 scans one, the other
     // waves clear the other for the next pass
-    __shared__ uint32_t hist[2][kLagWords];
+    __shared__ __attribute__((aligned(16))) uint32_t hist[2][kLagWords];
     __shared__ u64 sel[3];     // chosen digit, rank within it, its count
     __shared__ u64 found_u;    // the one remaining value, when a digit isolates it
     __shared__ u64 list[LCAP > 0 ? LCAP : 1];  // candidates, once few enough
@@ -126,6 +126,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
             int lo = sel_first_lo(range), hi = lo + 8;
             u64 prefix = 0;
             uint32_t kk = target;
+            bool first = true;     // every value is a candidate
             bool in_list = false;
             uint32_t n = 0;  // list length, once in_list
             for (;;) {
@@ -133,23 +134,22 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
                 uint32_t* h = hist[cur];
                 if (LCAP > 0 && in_list) {
                     for (uint32_t i = tid; i < n; i += WG) sel_hist_add(h, sel_bin(list[i], lo, hi, prefix));
+                } else if (first) {
+#pragma unroll
+                    for (int k = 0; k < K; ++k) sel_hist_add(h, ok[k / VEC] ? sel_first_bin(P[k], lo) : -1);
                 } else {
 #pragma unroll
                     for (int k = 0; k < K; ++k)
                         sel_hist_add(h, ok[k / VEC] ? sel_bin(P[k], lo, hi, prefix) : -1);
                 }
+                first = false;
                 __syncthreads();
                 if (wave == 0) {
                     // scan of the bins, kSelPerLane per lane; the lane
                     // whose bins hold the target rank names the bin
-                    uint32_t c[kSelPerLane];
-                    const uint32_t* hl = h + lane * (kSelPerLane + 1);  // sel_slot(lane * kSelPerLane)
-                    uint32_t part = 0;
-#pragma unroll
-                    for (int i = 0; i < kSelPerLane; ++i) {
-                        c[i] = hl[i];
-                        part += c[i];
-                    }
+                    const uint4 b4 = sel_lane_bins(h, lane);
+                    const uint32_t c[kSelPerLane] = {b4.x, b4.y, b4.z, b4.w};
+                    const uint32_t part = c[0] + c[1] + c[2] + c[3];
                     const uint32_t incl = wave_scan_incl(part);
                     uint32_t cum = incl - part;
                     if (cum <= kk && kk < incl) {
@@ -188,11 +188,11 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
                     // one value has the chosen digits: its lane publishes it
                     if (LCAP > 0 && in_list) {
                         for (uint32_t i = tid; i < n; i += WG)
-                            if (sel_bin(list[i], lo, hi, prefix) >= 0) found_u = list[i];
+                            if (sel_match(list[i], hi, prefix)) found_u = list[i];
                     } else {
 #pragma unroll
                         for (int k = 0; k < K; ++k)
-                            if (ok[k / VEC] && sel_bin(P[k], lo, hi, prefix) >= 0) found_u = P[k];
+                            if (ok[k / VEC] && sel_match(P[k], hi, prefix)) found_u = P[k];
                     }
                     __syncthreads();
                     prefix = found_u;
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
                     uint32_t cand = 0;  // bit k: P[k] is a candidate
 #pragma unroll
                     for (int k = 0; k < K; ++k)
-                        cand |= (ok[k / VEC] && sel_bin(P[k], lo, hi, prefix) >= 0) ? (1u << k) : 0u;
+                        cand |= (ok[k / VEC] && sel_match(P[k], hi, prefix)) ? (1u << k) : 0u;
                     const uint32_t nc = (uint32_t)__popc(cand);
                     const uint32_t incl = wave_scan_incl(nc);
                     const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);

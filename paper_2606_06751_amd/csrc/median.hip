@@ -48,7 +48,7 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
     constexpr int LIST = 64;         // values left that are compacted
     static_assert(RPW % 2 == 0 && ROWS % RPS == 0 && ROWS >= LIST, "shape");
     __shared__ uint32_t tlo[ROWS * STRIDE], thi[ROWS * STRIDE];
-    __shared__ uint32_t hist[RPW][kSelWords];
+    __shared__ __attribute__((aligned(16))) uint32_t hist[RPW][kSelWords];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -144,28 +144,28 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
             int lo = sel_first_lo(range), hi = lo + 8;
             u64 prefix = 0;
             uint32_t kk = (uint32_t)((q.n - 1) / 2);
+            bool first = true;     // every value is a candidate
             bool compact = false;  // the values left are one per lane in (c1, ok1)
             u64 c1 = 0;
             bool ok1 = false;
             for (;;) {
                 if (compact) {
                     sel_hist_add(h, ok1 ? sel_bin(c1, lo, hi, prefix) : -1);
+                } else if (first) {
+#pragma unroll
+                    for (int k = 0; k < K; ++k) sel_hist_add(h, ok[k] ? sel_first_bin(v[k], lo) : -1);
                 } else {
 #pragma unroll
                     for (int k = 0; k < K; ++k) sel_hist_add(h, ok[k] ? sel_bin(v[k], lo, hi, prefix) : -1);
                 }
+                first = false;
                 wave_lds_fence();
                 // scan of the bins, kSelPerLane per lane; the lane whose bins
                 // hold the target rank names the bin, and every lane clears
                 // its bins
-                uint32_t cnt[kSelPerLane];
-                uint32_t* hl = h + lane * (kSelPerLane + 1);  // sel_slot(lane * kSelPerLane)
-                uint32_t part = 0;
-#pragma unroll
-                for (int i = 0; i < kSelPerLane; ++i) {
-                    cnt[i] = hl[i];
-                    part += cnt[i];
-                }
+                const uint4 b4 = sel_lane_bins(h, lane);
+                const uint32_t cnt[kSelPerLane] = {b4.x, b4.y, b4.z, b4.w};
+                const uint32_t part = cnt[0] + cnt[1] + cnt[2] + cnt[3];
                 const uint32_t incl = wave_scan_incl(part);
                 uint32_t cum = incl - part;
                 int fd = -1;
@@ -181,8 +181,7 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
                         cum += cnt[i];
                     }
                 }
-#pragma unroll
-                for (int i = 0; i <= kSelPerLane; ++i) hl[i] = 0;
+                sel_clear_lane_bins(h, lane);
                 wave_lds_fence();
                 // the candidates hold the target rank, so exactly one lane found it
                 const u64 fm = __ballot(fd >= 0);
@@ -199,12 +198,12 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
                     u64 x = 0;
                     bool has = false;
                     if (compact) {
-                        has = ok1 && sel_bin(c1, lo, hi, prefix) >= 0;
+                        has = ok1 && sel_match(c1, hi, prefix);
                         x = c1;
                     } else {
 #pragma unroll
                         for (int k = 0; k < K; ++k) {
-                            if (ok[k] && sel_bin(v[k], lo, hi, prefix) >= 0) {
+                            if (ok[k] && sel_match(v[k], hi, prefix)) {
                                 x = v[k];
                                 has = true;
                             }
@@ -220,7 +219,7 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
                     uint32_t cand = 0;  // bit k: v[k] is left
 #pragma unroll
                     for (int k = 0; k < K; ++k)
-                        cand |= (ok[k] && sel_bin(v[k], lo, hi, prefix) >= 0) ? (1u << k) : 0u;
+                        cand |= (ok[k] && sel_match(v[k], hi, prefix)) ? (1u << k) : 0u;
                     const uint32_t nc = (uint32_t)__popc(cand);
                     uint32_t pos = wave_scan_incl(nc) - nc;
 #pragma unroll

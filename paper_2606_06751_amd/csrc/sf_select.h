@@ -1,6 +1,6 @@
 // sf_select.h -- building blocks of the exact radix selects (the lag, the
-// raw rank spread and the per-rank window median): 256-bin LDS histograms
-// with padded bins, the digit of a candidate, and a DPP wave scan.
+// raw rank spread and the per-rank window median): 256-bin LDS histograms,
+// the digit of a candidate, and a DPP wave scan.
 #pragma once
 
 #include "sf_device.h"
@@ -8,13 +8,19 @@
 namespace sfk {
 
 constexpr int kSelBins = 256;                // bins per histogram (8-bit digits)
-constexpr int kSelPerLane = kSelBins / 64;   // bins one lane scans
-// bin b lives at word b + b / kSelPerLane: the bins a lane scans start
-// kSelPerLane + 1 (odd) words after the previous lane's, so the scan reads
-// hit distinct banks
-constexpr int kSelWords = kSelBins + kSelBins / kSelPerLane;
+constexpr int kSelPerLane = kSelBins / 64;   // bins one lane scans, with one 16-byte read
+constexpr int kSelWords = kSelBins;          // words per histogram (16-byte aligned)
 
-__device__ __forceinline__ int sel_slot(int b) { return b + b / kSelPerLane; }
+// the kSelPerLane bins of lane `lane`, read at once
+__device__ __forceinline__ uint4 sel_lane_bins(const uint32_t* h, int lane)
+{
+    return *reinterpret_cast<const uint4*>(h + lane * kSelPerLane);
+}
+
+__device__ __forceinline__ void sel_clear_lane_bins(uint32_t* h, int lane)
+{
+    *reinterpret_cast<uint4*>(h + lane * kSelPerLane) = make_uint4(0u, 0u, 0u, 0u);
+}
 
 // DPP lane move of a 32-bit value in which lanes outside the row/bank masks,
 // and lanes whose source lies outside their row, read 0
@@ -56,20 +62,28 @@ __device__ __forceinline__ void sel_hist_add(uint32_t* h, int bin)
     if (__ballot(bin != first) == 0) {
         const u64 active = __ballot(1);
         if (first >= 0 && (int)(threadIdx.x & 63) == __builtin_ctzll(active))
-            atomicAdd(&h[sel_slot(first)], (uint32_t)__popcll(active));
+            atomicAdd(&h[first], (uint32_t)__popcll(active));
     } else if (bin >= 0) {
-        atomicAdd(&h[sel_slot(bin)], 1u);
+        atomicAdd(&h[bin], 1u);
     }
 }
 
 // Selection state: the candidates are the values u with u >> hi == prefix,
-// and a pass histograms their bits [lo, hi) (hi - lo <= 8).  Returns the
-// digit, or -1 for a value that is not a candidate.
+// and a pass histograms their bits [lo, hi) (hi - lo <= 8).
+__device__ __forceinline__ bool sel_match(u64 u, int hi, u64 prefix)
+{
+    return hi >= 64 || (u >> hi) == prefix;
+}
+
+// the digit of a candidate, or -1 for a value that is not one
 __device__ __forceinline__ int sel_bin(u64 u, int lo, int hi, u64 prefix)
 {
-    const bool match = hi >= 64 || (u >> hi) == prefix;
-    return match ? (int)((u >> lo) & ((1u << (hi - lo)) - 1u)) : -1;
+    return sel_match(u, hi, prefix) ? (int)((u >> lo) & ((1u << (hi - lo)) - 1u)) : -1;
 }
+
+// the digit in the first pass, where every value u <= range is a candidate
+// and 2^(lo + 8) > range (sel_first_lo)
+__device__ __forceinline__ int sel_first_bin(u64 u, int lo) { return (int)(uint32_t)(u >> lo); }
 
 // the first pass: 256 bins of width 2^lo cover [0, range] (range > 0)
 __device__ __forceinline__ int sel_first_lo(u64 range)
