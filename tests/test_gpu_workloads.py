@@ -186,3 +186,24 @@ def test_workload_window_median(sf, name):
             om = oracle.window_median(np.ascontiguousarray(x[:, :, r0:r1]), wl.window)
             np.testing.assert_array_equal(m[:, :, r0:r1], om)
         log("window median ok: %s window %d (%d steps, ranks %s)" % (name, w, t1 - t0, slices))
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workload_gain(sf, name):
+    """The direct-exposure gain of Eq. (4) on sampled step ranges of every
+    workload, with the recipe's no-stall stage medians as the baseline."""
+    wl = synth.WORKLOADS[name]
+    S, R = wl.S, wl.R
+    n = min(wl.T, 600 if R <= 1024 else 60)
+    base = np.array([b * synth.MS for b in wl.base_ms], dtype=np.int64)
+    for t0 in sorted({0, wl.T // 2, wl.T - n}):
+        x = synth.generate(wl, t0, t0 + n)
+        W = -(-n // wl.window)
+        bt = np.broadcast_to(base.reshape(1, S, 1), (W, S, R)).copy()
+        out = sf.sf_exposure_gain(torch.from_numpy(x).to("cuda:0"), torch.from_numpy(bt).to("cuda:0"),
+                                  wl.window)
+        torch.cuda.synchronize()
+        o = oracle.exposure_gain(x, bt, wl.window)
+        for k in ("gain", "makespan", "window_gain", "window_makespan"):
+            np.testing.assert_array_equal(out[k].cpu().numpy(), o[k], err_msg=k)
+    log("gain ok: %s (%d steps x 3 ranges)" % (name, n))
