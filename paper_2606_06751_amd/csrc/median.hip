@@ -288,9 +288,12 @@ SF_API int sf_window_median(const int64_t* durations, int64_t T, int32_t R, int3
     const MedianVariant v = vec2 ? pick_median<2>(n_max) : pick_median<1>(n_max);
     const int nchunk = (R + v.RPW - 1) / v.RPW;
     int64_t ntiles = W * S * (int64_t)nchunk;
-    // persistent workgroups: as many as are resident at once
-    int dev = 0, cus = 0, per_cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
+    // persistent workgroups: as many as are resident at once on the
+    // stream's device
+    hipDevice_t dev = 0;
+    int cus = 0, per_cu = 0;
+    const hipError_t de = stream ? hipStreamGetDevice((hipStream_t)stream, &dev) : hipGetDevice(&dev);
+    if (de != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, v.fn, v.WG, 0) != hipSuccess)
         return SF_EHIP;

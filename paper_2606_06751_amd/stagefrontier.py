@@ -89,13 +89,17 @@ def _stream_handle(stream, device) -> int:
     return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def _check(t: torch.Tensor, name: str, dtype, shape):
+def _check(t: torch.Tensor, name: str, dtype, shape, like: torch.Tensor | None = None):
+    """Type, device, layout and shape of one argument; ``like``: the call's
+    first array, whose device every other array must share."""
     if not isinstance(t, torch.Tensor):
         raise TypeError("%s must be a torch.Tensor" % name)
     if t.dtype != dtype:
         raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
     if t.device.type != "cuda":
         raise ValueError("%s must be a GPU tensor" % name)
+    if like is not None and t.device != like.device:
+        raise ValueError("%s is on %s, the call's other arrays on %s" % (name, t.device, like.device))
     if not t.is_contiguous():
         raise ValueError("%s must be contiguous" % name)
     if tuple(t.shape) != tuple(shape):
@@ -120,8 +124,8 @@ def sf_frontier(durations: torch.Tensor, out_increment: torch.Tensor | None = No
         out_increment = torch.empty((T, S), dtype=torch.int64, device=dev)
     if out_leader is None:
         out_leader = torch.empty((T, S), dtype=torch.int32, device=dev)
-    _check(out_increment, "out_increment", torch.int64, (T, S))
-    _check(out_leader, "out_leader", torch.int32, (T, S))
+    _check(out_increment, "out_increment", torch.int64, (T, S), like=durations)
+    _check(out_leader, "out_leader", torch.int32, (T, S), like=durations)
     rc = _lib.sf_frontier(durations.data_ptr(), T, R, S, out_increment.data_ptr(),
                           out_leader.data_ptr(), _stream_handle(stream, dev))
     if rc != SF_OK:
@@ -153,9 +157,9 @@ def sf_frontier_checked(durations: torch.Tensor, out_increment: torch.Tensor | N
         out_leader = torch.empty((T, S), dtype=torch.int32, device=dev)
     if status is None:
         status = torch.zeros((1,), dtype=torch.int32, device=dev)
-    _check(out_increment, "out_increment", torch.int64, (T, S))
-    _check(out_leader, "out_leader", torch.int32, (T, S))
-    _check(status, "status", torch.int32, (1,))
+    _check(out_increment, "out_increment", torch.int64, (T, S), like=durations)
+    _check(out_leader, "out_leader", torch.int32, (T, S), like=durations)
+    _check(status, "status", torch.int32, (1,), like=durations)
     rc = _lib.sf_frontier_checked(durations.data_ptr(), T, R, S, out_increment.data_ptr(),
                                   out_leader.data_ptr(), status.data_ptr(),
                                   _stream_handle(stream, dev))
@@ -181,7 +185,7 @@ def sf_frontier_evidence(durations: torch.Tensor, out: dict | None = None, strea
         dt = torch.int32 if k in ("leader", "ties") else torch.int64
         if k not in out:
             out[k] = torch.empty((T, S), dtype=dt, device=durations.device)
-        _check(out[k], k, dt, (T, S))
+        _check(out[k], k, dt, (T, S), like=durations)
     rc = _lib.sf_frontier_evidence(durations.data_ptr(), T, R, S,
                                    *(out[k].data_ptr() for k in EVIDENCE_FIELDS),
                                    _stream_handle(stream, durations.device))
@@ -203,7 +207,7 @@ def sf_window_summary(increment: torch.Tensor, leader: torch.Tensor, R: int, win
         raise ValueError("increment must be [T, S]")
     T, S = increment.shape
     _check(increment, "increment", torch.int64, (T, S))
-    _check(leader, "leader", torch.int32, (T, S))
+    _check(leader, "leader", torch.int32, (T, S), like=increment)
     W = sf_num_windows(T, window)
     if W < 0:
         raise StageFrontierError(SF_EINVAL, "sf_window_summary")
@@ -214,9 +218,9 @@ def sf_window_summary(increment: torch.Tensor, leader: torch.Tensor, R: int, win
         out_lead_counts = torch.empty((W, S, R), dtype=torch.int32, device=dev)
     if out_top2 is None:
         out_top2 = torch.empty((W, 2, 2), dtype=torch.int32, device=dev)
-    _check(out_stage_exposed, "out_stage_exposed", torch.int64, (W, S))
-    _check(out_lead_counts, "out_lead_counts", torch.int32, (W, S, R))
-    _check(out_top2, "out_top2", torch.int32, (W, 2, 2))
+    _check(out_stage_exposed, "out_stage_exposed", torch.int64, (W, S), like=increment)
+    _check(out_lead_counts, "out_lead_counts", torch.int32, (W, S, R), like=increment)
+    _check(out_top2, "out_top2", torch.int32, (W, 2, 2), like=increment)
     rc = _lib.sf_window_summary(increment.data_ptr(), leader.data_ptr(), T, R, S, window,
                                 out_stage_exposed.data_ptr(), out_lead_counts.data_ptr(),
                                 out_top2.data_ptr(), _stream_handle(stream, dev))
@@ -237,14 +241,14 @@ def sf_ingest(stages: torch.Tensor, wall: torch.Tensor, out_durations: torch.Ten
         raise ValueError("stages must be [R, T, K]")
     R, T, K = stages.shape
     _check(stages, "stages", torch.int64, (R, T, K))
-    _check(wall, "wall", torch.int64, (R, T))
+    _check(wall, "wall", torch.int64, (R, T), like=stages)
     dev = stages.device
     if out_durations is None:
         out_durations = torch.empty((T, K + 1, R), dtype=torch.int64, device=dev)
     if out_overlap is None:
         out_overlap = torch.empty((T, R), dtype=torch.int64, device=dev)
-    _check(out_durations, "out_durations", torch.int64, (T, K + 1, R))
-    _check(out_overlap, "out_overlap", torch.int64, (T, R))
+    _check(out_durations, "out_durations", torch.int64, (T, K + 1, R), like=stages)
+    _check(out_overlap, "out_overlap", torch.int64, (T, R), like=stages)
     rc = _lib.sf_ingest(stages.data_ptr(), wall.data_ptr(), T, R, K, out_durations.data_ptr(),
                         out_overlap.data_ptr(), _stream_handle(stream, dev))
     if rc != SF_OK:
@@ -266,8 +270,8 @@ def sf_route(stage_exposed: torch.Tensor, tau_num: int = 4, tau_den: int = 5,
         out_order = torch.empty((W, S), dtype=torch.int32, device=dev)
     if out_size is None:
         out_size = torch.empty((W,), dtype=torch.int32, device=dev)
-    _check(out_order, "out_order", torch.int32, (W, S))
-    _check(out_size, "out_size", torch.int32, (W,))
+    _check(out_order, "out_order", torch.int32, (W, S), like=stage_exposed)
+    _check(out_size, "out_size", torch.int32, (W,), like=stage_exposed)
     rc = _lib.sf_route(stage_exposed.data_ptr(), W, S, tau_num, tau_den, out_order.data_ptr(),
                        out_size.data_ptr(), _stream_handle(stream, dev))
     if rc != SF_OK:
@@ -294,13 +298,13 @@ def sf_exposure_gain(durations: torch.Tensor, baseline: torch.Tensor, window: in
     if W < 0:
         raise StageFrontierError(SF_EINVAL, "sf_exposure_gain")
     _check(durations, "durations", torch.int64, (T, S, R))
-    _check(baseline, "baseline", torch.int64, (W, S, R))
+    _check(baseline, "baseline", torch.int64, (W, S, R), like=durations)
     shapes = {"gain": (T, S), "makespan": (T,), "window_gain": (W, S), "window_makespan": (W,)}
     out = dict(out or {})
     for k, shp in shapes.items():
         if k not in out:
             out[k] = torch.empty(shp, dtype=torch.int64, device=durations.device)
-        _check(out[k], k, torch.int64, shp)
+        _check(out[k], k, torch.int64, shp, like=durations)
     rc = _lib.sf_exposure_gain(durations.data_ptr(), baseline.data_ptr(), T, R, S, window,
                                *(out[k].data_ptr() for k in GAIN_FIELDS),
                                _stream_handle(stream, durations.device))
@@ -322,8 +326,8 @@ def sf_frontier_lag(durations: torch.Tensor, out_lag: torch.Tensor | None = None
         out_lag = torch.empty((T, S), dtype=torch.int64, device=dev)
     if out_lag_inc is None:
         out_lag_inc = torch.empty((T, S), dtype=torch.int64, device=dev)
-    _check(out_lag, "out_lag", torch.int64, (T, S))
-    _check(out_lag_inc, "out_lag_inc", torch.int64, (T, S))
+    _check(out_lag, "out_lag", torch.int64, (T, S), like=durations)
+    _check(out_lag_inc, "out_lag_inc", torch.int64, (T, S), like=durations)
     rc = _lib.sf_frontier_lag(durations.data_ptr(), T, R, S, out_lag.data_ptr(),
                               out_lag_inc.data_ptr(), _stream_handle(stream, dev))
     if rc != SF_OK:
@@ -348,8 +352,8 @@ def sf_rank_spread(durations: torch.Tensor, window: int, out_spread: torch.Tenso
         out_spread = torch.empty((T, S), dtype=torch.int64, device=dev)
     if out_window_spread is None:
         out_window_spread = torch.empty((W, S), dtype=torch.int64, device=dev)
-    _check(out_spread, "out_spread", torch.int64, (T, S))
-    _check(out_window_spread, "out_window_spread", torch.int64, (W, S))
+    _check(out_spread, "out_spread", torch.int64, (T, S), like=durations)
+    _check(out_window_spread, "out_window_spread", torch.int64, (W, S), like=durations)
     rc = _lib.sf_rank_spread(durations.data_ptr(), T, R, S, window, out_spread.data_ptr(),
                              out_window_spread.data_ptr(), _stream_handle(stream, dev))
     if rc != SF_OK:
@@ -371,7 +375,7 @@ def sf_window_median(durations: torch.Tensor, window: int, out_median: torch.Ten
     dev = durations.device
     if out_median is None:
         out_median = torch.empty((W, S, R), dtype=torch.int64, device=dev)
-    _check(out_median, "out_median", torch.int64, (W, S, R))
+    _check(out_median, "out_median", torch.int64, (W, S, R), like=durations)
     rc = _lib.sf_window_median(durations.data_ptr(), T, R, S, window, out_median.data_ptr(),
                                _stream_handle(stream, dev))
     if rc != SF_OK:

@@ -669,3 +669,39 @@ def test_median_window_longer_than_input(sf):
     d = torch.zeros((1025, 1, 4), dtype=torch.int64, device=DEV)
     with pytest.raises(sf.StageFrontierError):
         sf.sf_window_median(d, 5000)
+
+
+def test_entry_points_on_a_side_stream(sf):
+    """Every entry point enqueues on the stream it is given (a default-
+    priority side stream here) and gives the same results there."""
+    d = synth.random_durations(40, 6, 300, seed=9, hi=10**7)
+    dd = torch.from_numpy(d).to(DEV)
+    oi, ol = oracle.frontier(d)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        inc, lead = sf.sf_frontier(dd, stream=side)
+        cinc, clead, st = sf.sf_frontier_checked(dd, stream=side)
+        ev = sf.sf_frontier_evidence(dd, stream=side)
+        lag, laginc = sf.sf_frontier_lag(dd, stream=side)
+        sp, wsp = sf.sf_rank_spread(dd, 8, stream=side)
+        med = sf.sf_window_median(dd, 8, stream=side)
+        gain = sf.sf_exposure_gain(dd, med, 8, stream=side)
+        ex, cnt, top2 = sf.sf_window_summary(inc, lead, R=300, window=8, stream=side)
+        order, size = sf.sf_route(ex, stream=side)
+    side.synchronize()
+    np.testing.assert_array_equal(inc.cpu().numpy(), oi)
+    np.testing.assert_array_equal(lead.cpu().numpy(), ol)
+    np.testing.assert_array_equal(cinc.cpu().numpy(), oi)
+    assert int(st.cpu()[0]) == 0
+    np.testing.assert_array_equal(ev["gap"].cpu().numpy(), oracle.frontier_evidence(d)["gap"])
+    np.testing.assert_array_equal(lag.cpu().numpy(), oracle.frontier_lag(d)[0])
+    np.testing.assert_array_equal(sp.cpu().numpy(), oracle.rank_spread(d, 8)[0])
+    om = oracle.window_median(d, 8)
+    np.testing.assert_array_equal(med.cpu().numpy(), om)
+    np.testing.assert_array_equal(gain["gain"].cpu().numpy(), oracle.exposure_gain(d, om, 8)["gain"])
+    oe, oc, ot = oracle.window_summary(oi, ol, 300, 8)
+    np.testing.assert_array_equal(ex.cpu().numpy(), oe)
+    np.testing.assert_array_equal(top2.cpu().numpy(), ot)
+    oo, os_ = oracle.route(oe)
+    np.testing.assert_array_equal(order.cpu().numpy(), oo)
