@@ -69,6 +69,20 @@ def measured_traffic(workload: str):
         return None
 
 
+def host_cpu() -> dict:
+    """The host CPU the baseline ran on: model name and logical CPUs."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"model": model, "logical_cpus": os.cpu_count()}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -596,6 +610,7 @@ def main() -> int:
             "kind": "oracle",
             "sample": "sf_frontier oracle (single thread) on steps of the same workload: "
                       "%d of %d steps, %.1f s" % (oracle_steps, T, oracle_time),
+            "host": host_cpu(),
         }
     print(json.dumps(rec), flush=True)
     return 0
