@@ -402,7 +402,7 @@ def test_gain_rank_sweep(sf, R):
         assert_gain_equal(sf, d, bt, window)
 
 
-@pytest.mark.parametrize("S", [1, 2, 7, 8, 9, 16, 17, 32, 33, 64])
+@pytest.mark.parametrize("S", [1, 2, 4, 5, 6, 7, 8, 9, 12, 13, 16, 17, 24, 25, 32, 33, 64])
 def test_gain_stage_sweep(sf, S):
     rng = np.random.Generator(np.random.PCG64(S + 100))
     for R in (8, 200, 1030):
