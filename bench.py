@@ -7,8 +7,9 @@ sf_window_summary over all steps.  The default workload is the largest one
 chunks, windows of 1000 steps).
 
 Prints ONE JSON line with the throughput (rank-stage samples per second),
-the roofline of the dominant kernel (the frontier kernel, HBM bound), and the
-CPU oracle timed on the host on the same bytes.
+the roofline of the dominant kernel (the frontier kernel, HBM bound), the
+plain-read calibration of the same bytes (sf_read_xor), and the CPU oracle
+timed on the host on the same bytes, on one thread and on every core.
 """
 from __future__ import annotations
 
@@ -130,6 +131,14 @@ def main() -> int:
     host_np = host.numpy()
     cpu_budget = args.cpu_seconds
     oracle_steps, oracle_time, oracle_out = 0, 0.0, []
+    # the same oracle on every host core: disjoint step ranges of a piece
+    # through a thread pool (the oracle's C calls run without the GIL)
+    ncores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    mt_steps, mt_time, mt_same = 0, 0.0, True
+    pool = None
+    if cpu_budget > 0 and ncores > 1:
+        from concurrent.futures import ThreadPoolExecutor
+        pool = ThreadPoolExecutor(max_workers=ncores)
     gen_time = h2d_time = 0.0
     for t0 in range(0, T, piece):
         t1 = min(T, t0 + piece)
@@ -150,8 +159,21 @@ def main() -> int:
             oracle_time += time.perf_counter() - tc
             oracle_out.append((t0, oi, ol))
             oracle_steps += n
+            if pool is not None and mt_time < cpu_budget:
+                cuts = [n * k // ncores for k in range(ncores + 1)]
+                tc = time.perf_counter()
+                parts = list(pool.map(lambda ab: oracle.frontier(host_np[ab[0]:ab[1]]),
+                                      [(a, b) for a, b in zip(cuts, cuts[1:]) if b > a]))
+                mt_time += time.perf_counter() - tc
+                mt_steps += n
+                mt_same = mt_same and np.array_equal(np.concatenate([p[0] for p in parts]), oi) \
+                    and np.array_equal(np.concatenate([p[1] for p in parts]), ol)
+    if pool is not None:
+        pool.shutdown()
     log("input: generated in %.1f s, H2D %.2f GB in %.1f s, oracle %d steps in %.1f s"
-        % (gen_time, wl.input_bytes / 1e9, h2d_time, oracle_steps, oracle_time))
+        " (%d threads: %d steps in %.2f s)"
+        % (gen_time, wl.input_bytes / 1e9, h2d_time, oracle_steps, oracle_time, ncores, mt_steps,
+           mt_time))
     del host, host_np
 
     inc = torch.empty((T, S), dtype=torch.int64, device=dev)
@@ -221,6 +243,22 @@ def main() -> int:
     torch.cuda.synchronize(dev)
     read_ms = min(a.elapsed_time(b) for a, b in rd)
     read_ceiling = (t1 - t0) * S * R * 8 / (read_ms / 1e3) / 1e9
+
+    # the plain-read ceiling: sf_read_xor reads the same chunk once and does
+    # nothing else but one XOR word per 64 KB piece (median of 5 launches
+    # after one untimed)
+    xo = torch.empty((sf.sf_read_xor_pieces((t1 - t0) * S * R * 8),), dtype=torch.int64, device=dev)
+    sf.sf_read_xor(d[t0:t1], xo, stream=stream)
+    cal = []
+    for _ in range(5):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        sf.sf_read_xor(d[t0:t1], xo, stream=stream)
+        b.record(stream)
+        cal.append((a, b))
+    torch.cuda.synchronize(dev)
+    cal_ms = float(np.median([a.elapsed_time(b) for a, b in cal]))
+    cal_gbps = (t1 - t0) * S * R * 8 / (cal_ms / 1e3) / 1e9
 
     # next row: the evidence pass (frontier + runner-up gap, tie-set size,
     # per-stage max and sum) over the same chunks, timed the same way
@@ -597,6 +635,14 @@ def main() -> int:
             "algorithmic_bytes_per_launch": launch_bytes,
         },
         "summary_kernels_ms": float(np.mean(summary_ms)),
+        "read_calibration": {
+            "kernel": "k_read_xor",
+            "achieved": cal_gbps,
+            "unit": "GB/s",
+            "launch_ms": cal_ms,
+            "frac_of_peak": cal_gbps / PEAK_HBM_GBPS,
+            "frontier_frac_of_ceiling": achieved / cal_gbps,
+        },
         "torch_sum_read_gbps": read_ceiling,
         "next_rows": next_rows,
         "h2d_gbps_pcie_context": wl.input_bytes / h2d_time / 1e9,
@@ -610,6 +656,17 @@ def main() -> int:
             "kind": "oracle",
             "sample": "sf_frontier oracle (single thread) on steps of the same workload: "
                       "%d of %d steps, %.1f s" % (oracle_steps, T, oracle_time),
+            "host": host_cpu(),
+        }
+    if mt_steps:
+        rec["cpu_baseline_all_cores"] = {
+            "value": mt_steps * S * R / mt_time,
+            "unit": UNIT,
+            "cores": ncores,
+            "kind": "oracle",
+            "sample": "the same sf_frontier oracle on %d threads, each on a disjoint step range of "
+                      "every piece: %d of %d steps, %.2f s, outputs equal to the single-thread "
+                      "run: %s" % (ncores, mt_steps, T, mt_time, mt_same),
             "host": host_cpu(),
         }
     print(json.dumps(rec), flush=True)

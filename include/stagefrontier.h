@@ -333,6 +333,38 @@ int sf_window_summary(const int64_t* increment, const int32_t* leader,
                       int64_t* out_stage_exposed, int32_t* out_lead_counts,
                       int32_t* out_top2, sf_stream_t stream);
 
+/*
+ * sf_read_xor -- plain-read calibration (a measurement aid, not part of the
+ * paper's method): the XOR of the 64-bit words of every SF_XOR_PIECE_BYTES
+ * piece of a device buffer.  It reads each byte exactly once with the
+ * streaming loads of the frontier pass and does nothing else, so its rate
+ * is the device's practical read ceiling, against which the single-pass
+ * kernels (Eq. (1) reads each duration once) are measured.  The words also
+ * serve as a cheap per-piece checksum of a buffer, e.g. after an upload.
+ *
+ *   buf       device buffer, 16-byte aligned, read only.  May be NULL when
+ *             bytes == 0.
+ *   bytes     buffer length, a multiple of 8, >= 0 (0 is a no-op).
+ *   out_xor   device uint64_t[sf_read_xor_pieces(bytes)], 8-byte aligned,
+ *             disjoint from buf.  Word i is the XOR of the little-endian
+ *             64-bit words in bytes [i * SF_XOR_PIECE_BYTES,
+ *             min((i + 1) * SF_XOR_PIECE_BYTES, bytes)) of buf.  The XOR of
+ *             all its words is the XOR of the whole buffer.
+ *   stream    HIP stream.
+ *
+ * Returns SF_OK, SF_EINVAL (alignment, length, NULL, overlap, or more than
+ * 2^31 - 1 pieces) or SF_EHIP.
+ */
+#define SF_XOR_PIECE_BYTES 262144
+int sf_read_xor(const void* buf, int64_t bytes, uint64_t* out_xor, sf_stream_t stream);
+
+/*
+ * sf_read_xor_pieces -- number of words sf_read_xor writes for a buffer of
+ * `bytes` bytes: ceil(bytes / SF_XOR_PIECE_BYTES).  Returns -1 when
+ * bytes < 0.  Host only; no device work.
+ */
+int64_t sf_read_xor_pieces(int64_t bytes);
+
 /* sf_strerror -- static, NUL-terminated description of a status code. */
 const char* sf_strerror(int status);
 

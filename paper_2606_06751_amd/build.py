@@ -12,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 # one translation unit per hot-path row, plus the C-ABI strings
 SOURCES = [os.path.join(CSRC, f) for f in (
     "frontier.hip", "window.hip", "evidence.hip", "lag.hip", "median.hip", "gain.hip",
-    "ingest.hip", "route.hip", "abi.hip")]
+    "ingest.hip", "route.hip", "calib.hip", "abi.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libstagefrontier.so")
 ARCH = "gfx950"

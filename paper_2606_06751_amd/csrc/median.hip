@@ -302,11 +302,8 @@ SF_API int sf_window_median(const int64_t* durations, int64_t T, int32_t R, int3
     int64_t ntiles = W * S * (int64_t)nchunk;
     // persistent workgroups: as many as are resident at once on the
     // stream's device
-    hipDevice_t dev = 0;
     int cus = 0, per_cu = 0;
-    const hipError_t de = stream ? hipStreamGetDevice((hipStream_t)stream, &dev) : hipGetDevice(&dev);
-    if (de != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+    if (device_cus(stream, &cus) != SF_OK ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, v.fn, v.WG, 0) != hipSuccess)
         return SF_EHIP;
     int64_t grid = (int64_t)(cus > 0 ? cus : 1) * (per_cu > 0 ? per_cu : 1);

@@ -46,6 +46,18 @@ static inline size_t lds_request(size_t need, int per_cu)
     return need > cap ? need : cap;
 }
 
+// Compute units of the device that `stream` belongs to (the current device
+// for the NULL stream).
+static inline int device_cus(sf_stream_t stream, int* cus)
+{
+    hipDevice_t dev = 0;
+    const hipError_t de = stream ? hipStreamGetDevice((hipStream_t)stream, &dev) : hipGetDevice(&dev);
+    if (de != hipSuccess ||
+        hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return SF_EHIP;
+    return SF_OK;
+}
+
 // Window sums of the columns of a [T][C] int64 array into [W][C]
 // (window.hip).
 int launch_window_sum(const int64_t* x, int64_t T, int C, int64_t window, int64_t W,

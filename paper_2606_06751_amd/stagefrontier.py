@@ -22,6 +22,7 @@ SF_MAX_S_GAIN = 64
 SF_MAX_R_LAG = 16384
 SF_MAX_WINDOW_MEDIAN = 1024
 SF_MAX_PREFIX_NS = 1 << 47
+SF_XOR_PIECE_BYTES = 262144
 
 LIB_PATH = _build.LIB
 
@@ -57,6 +58,10 @@ def _load() -> ctypes.CDLL:
     lib.sf_rank_spread.restype = ctypes.c_int
     lib.sf_window_median.argtypes = [vp, i64, i32, i32, i64, vp, vp]
     lib.sf_window_median.restype = ctypes.c_int
+    lib.sf_read_xor.argtypes = [vp, i64, vp, vp]
+    lib.sf_read_xor.restype = ctypes.c_int
+    lib.sf_read_xor_pieces.argtypes = [i64]
+    lib.sf_read_xor_pieces.restype = i64
     lib.sf_num_windows.argtypes = [i64, i64]
     lib.sf_num_windows.restype = i64
     lib.sf_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp]
@@ -381,6 +386,42 @@ def sf_window_median(durations: torch.Tensor, window: int, out_median: torch.Ten
     if rc != SF_OK:
         raise StageFrontierError(rc, "sf_window_median")
     return out_median
+
+
+def sf_read_xor_pieces(nbytes: int) -> int:
+    """Words ``sf_read_xor`` writes for a buffer of ``nbytes`` bytes."""
+    return int(_lib.sf_read_xor_pieces(nbytes))
+
+
+def sf_read_xor(buf: torch.Tensor, out_xor: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Plain-read calibration (``sf_read_xor``): the XOR of the 64-bit words
+    of every ``SF_XOR_PIECE_BYTES`` piece of a contiguous GPU tensor whose
+    size in bytes is a multiple of 8.
+
+    ``out_xor`` is an int64 tensor of ``sf_read_xor_pieces(nbytes)``
+    elements on the same device (the bits of the C ABI's uint64 words); a
+    new one is made when none is given.  Returns ``out_xor``.
+    """
+    if not isinstance(buf, torch.Tensor):
+        raise TypeError("buf must be a torch.Tensor")
+    if buf.device.type != "cuda":
+        raise ValueError("buf must be a GPU tensor")
+    if not buf.is_contiguous():
+        raise ValueError("buf must be contiguous")
+    dev = buf.device
+    nbytes = buf.numel() * buf.element_size()
+    if nbytes % 8:
+        raise StageFrontierError(SF_EINVAL, "sf_read_xor")
+    pieces = sf_read_xor_pieces(nbytes)
+    if out_xor is None:
+        out_xor = torch.empty((pieces,), dtype=torch.int64, device=dev)
+    _check(out_xor, "out_xor", torch.int64, (pieces,), like=buf)
+    if nbytes == 0:
+        return out_xor
+    rc = _lib.sf_read_xor(buf.data_ptr(), nbytes, out_xor.data_ptr(), _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_read_xor")
+    return out_xor
 
 
 def raw_library() -> ctypes.CDLL:

@@ -29,7 +29,8 @@ def test_header_declares_the_boundary():
     assert declared_functions() == ["sf_exposure_gain", "sf_frontier", "sf_frontier_checked",
                                     "sf_frontier_evidence",
                                     "sf_frontier_lag", "sf_ingest", "sf_num_windows",
-                                    "sf_rank_spread", "sf_route", "sf_strerror", "sf_version",
+                                    "sf_rank_spread", "sf_read_xor", "sf_read_xor_pieces", "sf_route",
+                                    "sf_strerror", "sf_version",
                                     "sf_window_median", "sf_window_summary"]
 
 
@@ -48,6 +49,7 @@ def test_constants_match_header(sf):
     assert "#define SF_MAX_S_GAIN %d" % sf.SF_MAX_S_GAIN in text
     assert "#define SF_MAX_R_LAG %d" % sf.SF_MAX_R_LAG in text
     assert "#define SF_MAX_WINDOW_MEDIAN %d" % sf.SF_MAX_WINDOW_MEDIAN in text
+    assert "#define SF_XOR_PIECE_BYTES %d" % sf.SF_XOR_PIECE_BYTES in text
     for name in ("SF_OK", "SF_EINVAL", "SF_ERANGE", "SF_EHIP"):
         assert re.search(r"%s = %d" % (name, getattr(sf, name)), text), name
 
@@ -240,6 +242,31 @@ def test_window_median_argument_checks(sf):
     assert call(m=A + 8) == sf.SF_EINVAL                    # output overlaps input
 
 
+def test_read_xor_argument_checks(sf):
+    lib = sf.raw_library()
+    P = sf.SF_XOR_PIECE_BYTES
+
+    def call(**kw):
+        a = dict(dict(buf=A, n=3 * P + 8, out=B), **kw)
+        return lib.sf_read_xor(a["buf"], a["n"], a["out"], None)
+
+    assert call(n=0, buf=None, out=None) == sf.SF_OK       # empty: nothing to do
+    assert call(n=-8) == sf.SF_EINVAL
+    assert call(n=4100) == sf.SF_EINVAL                    # not a multiple of 8
+    assert call(out=None) == sf.SF_EINVAL
+    assert call(out=B + 4) == sf.SF_EINVAL                 # misaligned result words
+    assert call(buf=A + 8) == sf.SF_EINVAL                 # buffer not 16-byte aligned
+    assert call(buf=None) == sf.SF_EINVAL
+    assert call(out=A + 1024) == sf.SF_EINVAL              # result words inside the buffer
+    assert call(out=A - 16) == sf.SF_EINVAL                # 4 result words run into the buffer
+    assert call(n=(1 << 31) * P) == sf.SF_EINVAL           # more than 2^31 - 1 pieces
+    assert sf.sf_read_xor_pieces(0) == 0
+    assert sf.sf_read_xor_pieces(8) == 1
+    assert sf.sf_read_xor_pieces(P) == 1
+    assert sf.sf_read_xor_pieces(P + 8) == 2
+    assert sf.sf_read_xor_pieces(-8) == -1
+
+
 def test_summary_argument_checks(sf):
     lib = sf.raw_library()
     D = 4 << 40
@@ -290,4 +317,5 @@ def test_ctypes_argtypes_cover_header(sf):
     assert len(lib.sf_window_median.argtypes) == 7
     assert len(lib.sf_route.argtypes) == 8
     assert len(lib.sf_window_summary.argtypes) == 10
+    assert len(lib.sf_read_xor.argtypes) == 4
     assert lib.sf_num_windows.restype is ctypes.c_int64
