@@ -58,7 +58,8 @@ __global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, 
     const int j = tid / G;
     const int slot = tid / SUB;
     const bool writer = (tid % SUB) == SUB - 1;
-    const int64_t t = (int64_t)blockIdx.x * SPW + j;
+    const int64_t lb = xcd_block();  // XCD-contiguous step runs
+    const int64_t t = lb * SPW + j;
     uint32_t dhi = 0, khi = 0;  // CHECK: OR of the durations' and the keys' high words
 
     if (t < T) {  // uniform over the step group
@@ -119,7 +120,7 @@ __global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, 
     __syncthreads();
 
     // decode F and the leader per (step, stage); rows of out are contiguous
-    const int64_t tb = (int64_t)blockIdx.x * SPW;
+    const int64_t tb = lb * SPW;
     for (int i = tid; i < SPW * S; i += WG) {
         const int jj = i / S;
         const int s = i - jj * S;

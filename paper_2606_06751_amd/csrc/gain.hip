@@ -36,7 +36,7 @@ __global__ __launch_bounds__(WG) void k_exposure_gain(
     const int gl = tid % G;
     const int slot = tid / SUB;
     const bool writer = (tid % SUB) == SUB - 1;
-    const int64_t tb = (int64_t)blockIdx.x * SPW;
+    const int64_t tb = xcd_block() * SPW;
     const int64_t t = tb + tid / G;
 
     if (t < T) {

@@ -53,7 +53,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int64_t t = blockIdx.x;
+    const int64_t t = xcd_block();
     if (t >= T) return;  // uniform over the workgroup (the grid is T)
     const int64_t* dt = d + t * (int64_t)S * R;
 

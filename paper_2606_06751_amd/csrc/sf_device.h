@@ -16,6 +16,20 @@ constexpr u64 kRankMask = 0xFFFFull;
 
 __device__ __forceinline__ u64 umax64(u64 a, u64 b) { return a > b ? a : b; }
 
+// Workgroups are dispatched round-robin over the 8 XCDs of the chip, each
+// with its own L2.  xcd_block() renumbers them so that each XCD takes one
+// contiguous run of block indices: output rows of neighbouring steps, which
+// share cache lines, are then written from one L2 instead of two (measured
+// on MI355X: 1-3% faster frontier passes at 128-4096 ranks).  A bijection
+// on [0, gridDim.x) for any grid size.
+__device__ __forceinline__ int64_t xcd_block()
+{
+    const int64_t n = gridDim.x, b = blockIdx.x;
+    const int64_t x = b & 7, i = b >> 3;
+    const int64_t per = n >> 3, extra = n & 7;
+    return x * per + (x < extra ? x : extra) + i;
+}
+
 // One DPP lane move of a 64-bit value.  Lanes outside ROW_MASK, and lanes
 // whose source is out of range, keep their own value, which is neutral for
 // a max.
