@@ -652,6 +652,7 @@ def main() -> int:
         rec["cpu_baseline"] = {
             "value": oracle_steps * S * R / oracle_time,
             "unit": UNIT,
+            "gbps": oracle_steps * S * R * 8 / oracle_time / 1e9,
             "cores": 1,
             "kind": "oracle",
             "sample": "sf_frontier oracle (single thread) on steps of the same workload: "
@@ -662,6 +663,7 @@ def main() -> int:
         rec["cpu_baseline_all_cores"] = {
             "value": mt_steps * S * R / mt_time,
             "unit": UNIT,
+            "gbps": mt_steps * S * R * 8 / mt_time / 1e9,
             "cores": ncores,
             "kind": "oracle",
             "sample": "the same sf_frontier oracle on %d threads, each on a disjoint step range of "
