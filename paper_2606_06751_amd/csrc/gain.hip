@@ -164,8 +164,8 @@ GainVariant pick_gain_g(int R)
 {
     if (R <= 16 * K) return gain_variant<VEC, K, 16, 64, SMAX>();
     if (R <= 64 * K) return gain_variant<VEC, K, 64, 256, SMAX>();
-    // four or more tiles per step: running maxima (measured: 7% faster at
-    // 4096 ranks, slower at one or two tiles, where they only cost registers)
+    // four or more tiles per step: running maxima (measured: 1-2% faster at
+    // 4096 and 16384 ranks; at one or two tiles they only cost registers)
     if (SMAX <= 16 && R > 3 * 256 * K) return gain_variant<VEC, K, 256, 256, SMAX, (SMAX <= 16)>();
     return gain_variant<VEC, K, 256, 256, SMAX>();
 }
