@@ -30,7 +30,20 @@ __device__ __forceinline__ u64 lane0(u64 v) { return lane_value(v, 0); }
 // out_inc is not written).  LCAP: capacity of the candidate list (0: every
 // pass reads the registers).  At least 4 waves per SIMD, so at most 128
 // VGPRs: without the cap the raw spread's allocation lands above it.
-template <bool PREFIX, int VEC, int K, int WG, int LCAP>
+//
+// How a pass's histogram is resolved (SCAN_ALL): wave 0 scans it and
+// publishes the digit through LDS, which takes a second barrier per pass,
+// while the other waves clear the other of two histograms; or every wave
+// scans it itself, with three histograms in rotation (pass p adds into
+// hist[p % 3] and clears hist[(p + 1) % 3], last read in pass p - 2's
+// scans), one barrier per pass.  Measured on MI355X: the per-wave scans free
+// the registers that the raw spread otherwise spills at 4-16 waves per step
+// (8-18% faster there), and cost the lag and the one-wave steps 1-7%.
+// PUBU: wave 0 takes the chosen bin into wave-uniform registers before lane
+// 0 publishes it, instead of the finding lane publishing it; the same work,
+// compiled differently (7% faster for the lag with 16 prefixes per lane on
+// 1-4 waves, up to 8% slower elsewhere).
+template <bool PREFIX, int VEC, int K, int WG, int LCAP, bool PUBU>
 __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_median_spread(const int64_t* __restrict__ d, int64_t T,
                                                       int R, int S, int64_t* __restrict__ out,
                                                       int64_t* __restrict__ out_inc)
@@ -38,17 +51,17 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
     static_assert(K % VEC == 0 && WG % 64 == 0 && WG / 64 <= 16, "shape");
     constexpr int NW = WG / 64;
     constexpr int NLD = K / VEC;
+    constexpr bool SCAN_ALL = !PREFIX && NW > 1;
+    constexpr int NH = SCAN_ALL ? 3 : 2;  // histograms
     // per-wave max/min partials, double-buffered by stage parity: a wave
     // may write stage s+1's while another still reads stage s's (when a
     // boundary needs no radix pass there is no barrier between)
     __shared__ u64 red_max[2][NW], red_min[2][NW];
-    // two histograms used alternately: while wave 0 scans one, the other
-    // waves clear the other for the next pass
-    __shared__ __attribute__((aligned(16))) uint32_t hist[2][kLagWords];
-    __shared__ u64 sel[3];     // chosen digit, rank within it, its count
-    __shared__ u64 found_u;    // the one remaining value, when a digit isolates it
+    __shared__ __attribute__((aligned(16))) uint32_t hist[NH][kLagWords];
+    __shared__ uint32_t sel[3];  // wave 0's scan: chosen digit, rank within it, its count
     __shared__ u64 list[LCAP > 0 ? LCAP : 1];  // candidates, once few enough
     __shared__ uint32_t list_n;                // fill position of the list
+    __shared__ int64_t lag_sh[2];              // L of the last two stages, by parity
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -85,10 +98,13 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
     u64 P[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) P[k] = 0;
-    for (int i = tid; i < 2 * kLagWords; i += WG) (&hist[0][0])[i] = 0;
-    if (tid == 0) list_n = 0;
-    int cur = 0;  // the histogram that is clear at the start of a pass
-    int64_t L_prev = 0;
+    for (int i = tid; i < NH * kLagWords; i += WG) (&hist[0][0])[i] = 0;
+    if (tid == 0) {
+        list_n = 0;
+        lag_sh[0] = 0;
+        lag_sh[1] = 0;
+    }
+    int cur = 0;  // the histogram of the next pass (clear)
     const uint32_t target = (uint32_t)((R - 1) / 2);
 
     for (int s = 0; s < S; ++s) {
@@ -121,7 +137,8 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
         const u64 range = F - Pmin;
 #pragma unroll
         for (int k = 0; k < K; ++k) P[k] -= Pmin;
-        u64 um = 0;  // u of the median (0 when every u is 0)
+        u64 um = 0;            // u of the median (0 when every u is 0)
+        bool written = false;  // the lane holding the median wrote the outputs
         if (range != 0) {
             int lo = sel_first_lo(range), hi = lo + 8;
             u64 prefix = 0;
@@ -132,6 +149,10 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
             for (;;) {
                 // histogram of the next digit of the candidates
                 uint32_t* h = hist[cur];
+                if (SCAN_ALL) {
+                    cur = cur == NH - 1 ? 0 : cur + 1;
+                    for (int i = tid; i < kLagWords; i += WG) hist[cur][i] = 0;
+                }
                 if (LCAP > 0 && in_list) {
                     for (uint32_t i = tid; i < n; i += WG) sel_hist_add(h, sel_bin(list[i], lo, hi, prefix));
                 } else if (first) {
@@ -147,58 +168,85 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
                 }
                 first = false;
                 __syncthreads();
-                if (wave == 0) {
-                    // scan of the bins, kSelPerLane per lane; the lane
-                    // whose bins hold the target rank names the bin
-                    const uint4 b4 = sel_lane_bins(h, lane);
-                    const uint32_t c[kSelPerLane] = {b4.x, b4.y, b4.z, b4.w};
-                    const uint32_t part = c[0] + c[1] + c[2] + c[3];
-                    const uint32_t incl = wave_scan_incl(part);
-                    uint32_t cum = incl - part;
-                    if (cum <= kk && kk < incl) {
-                        bool found = false;
-#pragma unroll
-                        for (int i = 0; i < kSelPerLane; ++i) {
-                            if (!found && kk < cum + c[i]) {
-                                found = true;
-                                sel[0] = (u64)(lane * kSelPerLane + i);
-                                sel[1] = (u64)(kk - cum);
-                                sel[2] = (u64)c[i];
-                            }
-                            cum += c[i];
-                        }
-                    }
+                uint32_t digit, count;
+                if (SCAN_ALL) {
+                    sel_scan_wave(h, lane, kk, digit, count);
                 } else {
-                    uint32_t* other = hist[cur ^ 1];
-                    for (int i = tid - 64; i < kLagWords; i += WG - 64) other[i] = 0;
+                    if (wave == 0 && PUBU) {
+                        uint32_t dg, cn;
+                        sel_scan_wave(h, lane, kk, dg, cn);
+                        if (lane == 0) {
+                            sel[0] = dg;
+                            sel[1] = kk;
+                            sel[2] = cn;
+                        }
+                    } else if (wave == 0) {
+                        const uint4 b4 = sel_lane_bins(h, lane);
+                        const uint32_t c[kSelPerLane] = {b4.x, b4.y, b4.z, b4.w};
+                        const uint32_t part = c[0] + c[1] + c[2] + c[3];
+                        const uint32_t incl = wave_scan_incl(part);
+                        uint32_t cum = incl - part;
+                        if (cum <= kk && kk < incl) {
+                            bool found = false;
+#pragma unroll
+                            for (int i = 0; i < kSelPerLane; ++i) {
+                                if (!found && kk < cum + c[i]) {
+                                    found = true;
+                                    sel[0] = (uint32_t)(lane * kSelPerLane + i);
+                                    sel[1] = kk - cum;
+                                    sel[2] = c[i];
+                                }
+                                cum += c[i];
+                            }
+                        }
+                    } else {
+                        uint32_t* other = hist[cur ^ 1];
+                        for (int i = tid - 64; i < kLagWords; i += WG - 64) other[i] = 0;
+                    }
+                    if (NW == 1) {
+                        uint32_t* other = hist[cur ^ 1];
+                        for (int i = tid; i < kLagWords; i += WG) other[i] = 0;
+                    }
+                    __syncthreads();
+                    // h is cleared during the scan of the next pass (or stage)
+                    cur ^= 1;
+                    digit = sel[0];
+                    kk = sel[1];
+                    count = sel[2];
                 }
-                if (NW == 1) {
-                    uint32_t* other = hist[cur ^ 1];
-                    for (int i = tid; i < kLagWords; i += WG) other[i] = 0;
-                }
-                __syncthreads();
-                // h is cleared during the scan of the next pass (or stage)
-                cur ^= 1;
-                // the candidates hold the target rank, so a bin always has it
-                const uint32_t count = (uint32_t)sel[2];
-                prefix = (prefix << (hi - lo)) | sel[0];
-                kk = (uint32_t)sel[1];
+                prefix = (prefix << (hi - lo)) | (u64)digit;
                 hi = lo;
                 if (hi == 0) break;  // every bit chosen: u == prefix
                 lo = lo > 8 ? lo - 8 : 0;
                 // the candidates left are the values with u >> hi == prefix
                 if (count == 1) {
-                    // one value has the chosen digits: its lane publishes it
+                    // one value has the chosen digits: its lane writes the
+                    // outputs (the previous stage's L is in lag_sh)
+                    u64 u = 0;
+                    bool holder = false;
                     if (LCAP > 0 && in_list) {
-                        for (uint32_t i = tid; i < n; i += WG)
-                            if (sel_match(list[i], hi, prefix)) found_u = list[i];
+                        for (uint32_t i = tid; i < n; i += WG) {
+                            if (sel_match(list[i], hi, prefix)) {
+                                u = list[i];
+                                holder = true;
+                            }
+                        }
                     } else {
 #pragma unroll
-                        for (int k = 0; k < K; ++k)
-                            if (ok[k / VEC] && sel_match(P[k], hi, prefix)) found_u = P[k];
+                        for (int k = 0; k < K; ++k) {
+                            if (ok[k / VEC] && sel_match(P[k], hi, prefix)) {
+                                u = P[k];
+                                holder = true;
+                            }
+                        }
                     }
-                    __syncthreads();
-                    prefix = found_u;
+                    if (holder) {
+                        const int64_t L = (int64_t)(range - u);
+                        out[t * S + s] = L;
+                        if (PREFIX) out_inc[t * S + s] = L - lag_sh[(s + 1) & 1];
+                        lag_sh[s & 1] = L;
+                    }
+                    written = true;
                     break;
                 }
                 if (LCAP > 0 && !in_list && count <= (uint32_t)LCAP) {
@@ -209,11 +257,11 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
                     for (int k = 0; k < K; ++k)
                         cand |= (ok[k / VEC] && sel_match(P[k], hi, prefix)) ? (1u << k) : 0u;
                     const uint32_t nc = (uint32_t)__popc(cand);
-                    const uint32_t incl = wave_scan_incl(nc);
-                    const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+                    const uint32_t incl2 = wave_scan_incl(nc);
+                    const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl2, 63);
                     uint32_t wbase = 0;
                     if (lane == 63 && total != 0) wbase = atomicAdd(&list_n, total);
-                    uint32_t pos = (uint32_t)__builtin_amdgcn_readlane((int)wbase, 63) + incl - nc;
+                    uint32_t pos = (uint32_t)__builtin_amdgcn_readlane((int)wbase, 63) + incl2 - nc;
 #pragma unroll
                     for (int k = 0; k < K; ++k) {
                         if ((cand >> k) & 1u) {
@@ -230,16 +278,17 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
                 }
             }
             um = prefix;
-            // sel, found_u and the list are next written after the next
-            // stage's reduction barrier, which every thread passes only
-            // after reading them here
+            // sel and the list are next written after the next stage's
+            // reduction barrier, which every thread passes only after
+            // reading them here
         }
-        const int64_t L = (int64_t)(range - um);
-        if (tid == 0) {
+        if (!written && tid == 0) {
+            const int64_t L = (int64_t)(range - um);
             out[t * S + s] = L;
-            if (PREFIX) out_inc[t * S + s] = L - L_prev;
+            if (PREFIX) out_inc[t * S + s] = L - lag_sh[(s + 1) & 1];
+            lag_sh[s & 1] = L;
         }
-        L_prev = L;
+        // lag_sh[s & 1] is read at stage s + 1, after its reduction barrier
     }
 }
 
@@ -254,7 +303,9 @@ LagVariant lag_variant()
     // candidate list: a quarter of the slots, at most 32 KB; none when a
     // lane holds so few values that the registers are as cheap to re-read
     constexpr int LCAP = K <= 2 ? 0 : (K * WG / 4 < 4096 ? K * WG / 4 : 4096);
-    return LagVariant{reinterpret_cast<const void*>(&k_median_spread<PREFIX, VEC, K, WG, LCAP>), WG};
+    constexpr bool PUBU = PREFIX && K == 16 && WG <= 256;
+    return LagVariant{reinterpret_cast<const void*>(&k_median_spread<PREFIX, VEC, K, WG, LCAP, PUBU>),
+                      WG};
 }
 
 // One step per workgroup with all R prefixes in registers, as few waves as

@@ -164,36 +164,12 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
                 }
                 first = false;
                 wave_lds_fence();
-                // scan of the bins, kSelPerLane per lane; the lane whose bins
-                // hold the target rank names the bin, and every lane clears
-                // its bins
-                const uint4 b4 = sel_lane_bins(h, lane);
-                const uint32_t cnt[kSelPerLane] = {b4.x, b4.y, b4.z, b4.w};
-                const uint32_t part = cnt[0] + cnt[1] + cnt[2] + cnt[3];
-                const uint32_t incl = wave_scan_incl(part);
-                uint32_t cum = incl - part;
-                int fd = -1;
-                uint32_t fk = 0, fc = 0;
-                if (cum <= kk && kk < incl) {
-#pragma unroll
-                    for (int i = 0; i < kSelPerLane; ++i) {
-                        if (fd < 0 && kk < cum + cnt[i]) {
-                            fd = lane * kSelPerLane + i;
-                            fk = kk - cum;
-                            fc = cnt[i];
-                        }
-                        cum += cnt[i];
-                    }
-                }
+                // scan of the bins, then every lane clears its bins
+                uint32_t digit, count;
+                sel_scan_wave(h, lane, kk, digit, count);
                 sel_clear_lane_bins(h, lane);
                 wave_lds_fence();
-                // the candidates hold the target rank, so exactly one lane found it
-                const u64 fm = __ballot(fd >= 0);
-                const int src = fm ? __builtin_ctzll(fm) : 0;
-                const int digit = __builtin_amdgcn_readlane(fd, src);
-                kk = (uint32_t)__builtin_amdgcn_readlane((int)fk, src);
-                const uint32_t count = (uint32_t)__builtin_amdgcn_readlane((int)fc, src);
-                prefix = (prefix << (hi - lo)) | (u64)(uint32_t)digit;
+                prefix = (prefix << (hi - lo)) | (u64)digit;
                 hi = lo;
                 if (hi == 0) break;  // every bit chosen: u == prefix
                 lo = lo > 8 ? lo - 8 : 0;

@@ -53,6 +53,38 @@ __device__ __forceinline__ u64 lane_value(u64 v, int L)
     return ((u64)hi << 32) | lo;
 }
 
+// Scan of a 256-bin histogram by one wave, kSelPerLane bins per lane: the
+// bin that holds the candidate of rank kk (from 0), kk's rank within that
+// bin, and the bin's count, in every lane.  The candidates hold rank kk, so
+// exactly one lane finds it.
+__device__ __forceinline__ void sel_scan_wave(const uint32_t* h, int lane, uint32_t& kk,
+                                              uint32_t& digit, uint32_t& count)
+{
+    const uint4 b4 = sel_lane_bins(h, lane);
+    const uint32_t c[kSelPerLane] = {b4.x, b4.y, b4.z, b4.w};
+    const uint32_t part = c[0] + c[1] + c[2] + c[3];
+    const uint32_t incl = wave_scan_incl(part);
+    uint32_t cum = incl - part;
+    int fd = -1;
+    uint32_t fk = 0, fc = 0;
+    if (cum <= kk && kk < incl) {
+#pragma unroll
+        for (int i = 0; i < kSelPerLane; ++i) {
+            if (fd < 0 && kk < cum + c[i]) {
+                fd = lane * kSelPerLane + i;
+                fk = kk - cum;
+                fc = c[i];
+            }
+            cum += c[i];
+        }
+    }
+    const u64 fm = __ballot(fd >= 0);
+    const int src = fm ? __builtin_ctzll(fm) : 0;
+    digit = (uint32_t)__builtin_amdgcn_readlane(fd, src);
+    kk = (uint32_t)__builtin_amdgcn_readlane((int)fk, src);
+    count = (uint32_t)__builtin_amdgcn_readlane((int)fc, src);
+}
+
 // Add the active lanes' bins (-1: none) to the histogram.  When every active
 // lane has the same bin one lane adds them all, so they do not serialise on
 // one word.
