@@ -34,6 +34,23 @@ def test_header_declares_the_boundary():
                                     "sf_window_median", "sf_window_summary"]
 
 
+def test_header_is_plain_c(tmp_path):
+    """The boundary is usable from C: the header alone compiles as strict C99."""
+    import shutil
+    import subprocess
+
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use.c"
+    src.write_text('#include "stagefrontier.h"\n'
+                   "int use(void) { return SF_OK + (int)sizeof(sf_stream_t); }\n")
+    proc = subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror",
+                           "-I", os.path.join(ROOT, "include"), "-c", str(src),
+                           "-o", str(tmp_path / "use.o")], capture_output=True, text=True)
+    assert proc.returncode == 0, proc.stderr
+
+
 def test_every_declared_symbol_is_exported(sf):
     lib = sf.raw_library()
     for name in declared_functions():
