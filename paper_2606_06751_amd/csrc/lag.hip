@@ -11,7 +11,8 @@
 // first pass histograms 256 equal bins fitted to the top bits of F - Pmin;
 // later passes take the next 8 bits of the values left, which once few
 // enough are compacted into an LDS list so that later passes read only
-// them.  A digit that isolates a single value ends the selection.
+// them.  A digit that isolates a single value ends the selection, and the
+// lane holding that value writes the boundary's outputs.
 
 #include "sf_device.h"
 #include "sf_host.h"
