@@ -106,7 +106,8 @@ def main() -> int:
         return rows is None or row in rows
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path; "
+              "steps shard across GPUs with no exchange, but that is not implemented "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         return 2
 
