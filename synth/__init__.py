@@ -127,7 +127,7 @@ class Workload:
     straggler_pct: int = 0          # persistent straggler: + pct % on all stages
     role_groups: int = 0            # rank role groups with additive offsets
     role_off_ms: tuple = (0, 0)     # offset range per (group, stage), ms
-    stall_frac: float = 0.0         # C1-style data stall propagated as bwd wait
+    stall_frac: float = 0.0         # steps with a data stall on one rank, seen as bwd wait elsewhere
     stall_ms: int = 0
     fault_frac: float = 0.0         # single (stage, rank) delays
     fault_ms: tuple = (0, 0)
