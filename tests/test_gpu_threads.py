@@ -1,0 +1,77 @@
+"""Several host threads drive the library at once, each on a stream of its
+own: the entry points keep no mutable global state, so concurrent calls must
+give each thread exactly its own results (the ctypes calls run without the
+GIL, so the calls really overlap on the host)."""
+import threading
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module")
+def sf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_06751_amd import stagefrontier
+    return stagefrontier
+
+
+def test_concurrent_host_threads(sf):
+    shapes = [(30, 6, 300, 7), (12, 12, 5000, 5), (50, 3, 64, 10), (20, 8, 1025, 4)]
+    jobs = []
+    for i, (T, S, R, window) in enumerate(shapes):
+        d = synth.random_durations(T, S, R, seed=40 + i, hi=[3, 10**6][i % 2])
+        dd = torch.from_numpy(d).to(DEV)
+        W = sf.sf_num_windows(T, window)
+        out = {
+            "inc": torch.empty((T, S), dtype=torch.int64, device=DEV),
+            "lead": torch.empty((T, S), dtype=torch.int32, device=DEV),
+            "ex": torch.empty((W, S), dtype=torch.int64, device=DEV),
+            "cnt": torch.empty((W, S, R), dtype=torch.int32, device=DEV),
+            "top2": torch.empty((W, 2, 2), dtype=torch.int32, device=DEV),
+            "lag": torch.empty((T, S), dtype=torch.int64, device=DEV),
+            "laginc": torch.empty((T, S), dtype=torch.int64, device=DEV),
+        }
+        jobs.append((d, dd, R, window, out, torch.cuda.Stream(DEV)))
+    torch.cuda.synchronize()
+    errors = []
+
+    def work(job):
+        d, dd, R, window, out, st = job
+        try:
+            for _ in range(20):
+                sf.sf_frontier(dd, out["inc"], out["lead"], stream=st)
+                sf.sf_window_summary(out["inc"], out["lead"], R, window, out["ex"], out["cnt"],
+                                     out["top2"], stream=st)
+                sf.sf_frontier_lag(dd, out["lag"], out["laginc"], stream=st)
+        except Exception as e:  # noqa: BLE001  (reported below)
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=work, args=(job,)) for job in jobs]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join(timeout=120)
+    assert not any(th.is_alive() for th in threads), "a host thread did not finish"
+    for job in jobs:
+        job[5].synchronize()
+    assert not errors, errors
+    for d, dd, R, window, out, st in jobs:
+        oi, ol = oracle.frontier(d)
+        oe, oc, ot = oracle.window_summary(oi, ol, R, window)
+        olag, olaginc = oracle.frontier_lag(d)
+        np.testing.assert_array_equal(out["inc"].cpu().numpy(), oi)
+        np.testing.assert_array_equal(out["lead"].cpu().numpy(), ol)
+        np.testing.assert_array_equal(out["ex"].cpu().numpy(), oe)
+        np.testing.assert_array_equal(out["cnt"].cpu().numpy(), oc)
+        np.testing.assert_array_equal(out["top2"].cpu().numpy(), ot)
+        np.testing.assert_array_equal(out["lag"].cpu().numpy(), olag)
+        np.testing.assert_array_equal(out["laginc"].cpu().numpy(), olaginc)
