@@ -84,6 +84,12 @@ def host_cpu() -> dict:
     return {"model": model, "logical_cpus": os.cpu_count()}
 
 
+def row_cpu(samples: int, secs: float, what: str) -> dict:
+    """The oracle's rate on a next row's check sample (one thread)."""
+    return {"value": samples / secs, "unit": UNIT, "cores": 1, "kind": "oracle",
+            "sample": "%s (%d samples, %.2f s)" % (what, samples, secs)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -283,14 +289,17 @@ def main() -> int:
             torch.cuda.synchronize(dev)
             ev_ms = float(np.mean([a.elapsed_time(b) for a, b in evs])) / len(bounds)
             ev_bytes = (8 * T * S * R + 40 * T * S) / len(bounds)
-            ev_exact = None
+            ev_exact = ev_cpu = None
             if oracle_out:
                 import oracle
                 t0c = oracle_out[0][0]
-                n_chk = min(len(oracle_out[0][1]), 64)
+                n_chk = min(len(oracle_out[0][1]), 256)
                 # the first sampled steps, regenerated from the seed for the oracle
                 x = synth.generate(wl, t0c, t0c + n_chk)
+                tc = time.perf_counter()
                 o = oracle.frontier_evidence(x)
+                ev_cpu = row_cpu(x.size, time.perf_counter() - tc,
+                                 "oracle frontier_evidence on %d steps of the workload" % n_chk)
                 ev_exact = all(np.array_equal(ev_out[k][t0c:t0c + n_chk].cpu().numpy(), o[ok])
                                for k, ok in (("increment", "inc"), ("leader", "lead"), ("gap", "gap"),
                                              ("ties", "ties"), ("stage_max", "stage_max"),
@@ -305,6 +314,8 @@ def main() -> int:
                 "unit": "GB/s",
                 "frac": ev_bytes / (ev_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
                 "bit_exact_first_steps": ev_exact,
+                "samples_per_s": T * S * R / len(bounds) / (ev_ms / 1e3),
+                "cpu_baseline": ev_cpu,
             }
             del ev_out, ev_views
 
@@ -328,6 +339,15 @@ def main() -> int:
             torch.cuda.synchronize(dev)
             ck_ms = float(np.mean([a.elapsed_time(b) for a, b in cks])) / len(bounds)
             ck_bytes = (8 * T * S * R + 12 * T * S) / len(bounds)
+            ck_cpu = None
+            if oracle_out:
+                import oracle
+                x = synth.generate(wl, 0, min(T, 256))
+                tc = time.perf_counter()
+                oracle.frontier(x)
+                ck_status_o = oracle.range_status(x)
+                ck_cpu = row_cpu(x.size, time.perf_counter() - tc,
+                                 "oracle frontier + range_status on %d steps (status %d)" % (len(x), ck_status_o))
             next_rows["frontier_checked"] = {
                 "kernel": "k_frontier<..., check>",
                 "bound": "hbm",
@@ -339,6 +359,8 @@ def main() -> int:
                 "frac": ck_bytes / (ck_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
                 "status": int(ck_status.cpu()[0]),
                 "outputs_equal_path": bool(torch.equal(ck_inc, inc) and torch.equal(ck_lead, lead)),
+                "samples_per_s": T * S * R / len(bounds) / (ck_ms / 1e3),
+                "cpu_baseline": ck_cpu,
             }
             del ck_inc, ck_lead, ck_status, ck_views
 
@@ -366,6 +388,17 @@ def main() -> int:
             torch.cuda.synchronize(dev)
             ig_ms = float(np.mean([a.elapsed_time(b) for a, b in ig]))
             ig_bytes = 8 * R * n * (S - 1) + 8 * R * n + 8 * n * S * R + 8 * n * R
+            ig_cpu = None
+            if oracle_out:
+                import oracle
+                # the per-rank buffers of the first steps
+                ni = min(n, 32)
+                xh = xs[:, :ni, :].contiguous().cpu().numpy()
+                wh = wall[:, :ni].contiguous().cpu().numpy()
+                tc = time.perf_counter()
+                oracle.ingest(xh, wh)
+                ig_cpu = row_cpu(ni * S * R, time.perf_counter() - tc,
+                                 "oracle ingest of the first %d steps of every rank" % ni)
             next_rows["ingest"] = {
                 "kernel": "k_ingest",
                 "bound": "hbm",
@@ -377,6 +410,8 @@ def main() -> int:
                 "frac": ig_bytes / (ig_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
                 "shape": {"ranks": R, "steps": n, "explicit_stages": S - 1},
                 "roundtrip_exact": roundtrip,
+                "samples_per_s": n * S * R / (ig_ms / 1e3),
+                "cpu_baseline": ig_cpu,
             }
             del xs, wall, ing_d, ing_o
 
@@ -403,13 +438,17 @@ def main() -> int:
                 torch.cuda.synchronize(dev)
                 m_ms = float(np.mean([a.elapsed_time(b) for a, b in mt])) / len(bounds)
                 m_bytes = (8 * T * S * R + 8 * W * S * R) / len(bounds)
-                m_exact = None
+                m_exact = m_cpu = None
                 if oracle_out:
                     import oracle
                     # window 0, ranks [0, 256): ranks are independent
                     x = synth.generate(wl, 0, min(T, wl.window))
                     rs = min(R, 256)
-                    om = oracle.window_median(np.ascontiguousarray(x[:, :, :rs]), wl.window)
+                    xs = np.ascontiguousarray(x[:, :, :rs])
+                    tc = time.perf_counter()
+                    om = oracle.window_median(xs, wl.window)
+                    m_cpu = row_cpu(xs.size, time.perf_counter() - tc,
+                                    "oracle window_median on window 0, ranks [0, %d)" % rs)
                     m_exact = bool(np.array_equal(btilde[:1, :, :rs].cpu().numpy(), om))
                 next_rows["window_median"] = {
                     "kernel": "k_window_median",
@@ -421,6 +460,8 @@ def main() -> int:
                     "unit": "GB/s",
                     "frac": m_bytes / (m_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
                     "bit_exact_window0_ranks": m_exact,
+                    "samples_per_s": T * S * R / len(bounds) / (m_ms / 1e3),
+                    "cpu_baseline": m_cpu,
                 }
                 del m_views
 
@@ -458,7 +499,7 @@ def main() -> int:
             g_ms = float(np.mean([a.elapsed_time(b) for a, b in gt])) / len(bounds)
             n_per = T / len(bounds)
             g_bytes = (8 * T * S * R + 8 * W * S * R + 8 * T * S + 8 * T + 8 * W * S + 8 * W) / len(bounds)
-            g_exact = None
+            g_exact = g_cpu = None
             if oracle_out:
                 import oracle
                 # the chain window median -> gain on the first 16 steps as one
@@ -473,7 +514,10 @@ def main() -> int:
                     gb, ob = btilde[:1].contiguous(), btilde[:1].cpu().numpy()
                 go = sf.sf_exposure_gain(xd, gb, n_chk, stream=stream)
                 torch.cuda.synchronize(dev)
+                tc = time.perf_counter()
                 o = oracle.exposure_gain(x, ob, n_chk)
+                g_cpu = row_cpu(x.size, time.perf_counter() - tc,
+                                "oracle exposure_gain on %d steps of the workload" % n_chk)
                 g_exact = bool(all(np.array_equal(go[k].cpu().numpy(), o[k]) for k in sf.GAIN_FIELDS))
                 del xd, gb, go
             wg = g_out["window_gain"].sum(dim=0).double()
@@ -491,6 +535,8 @@ def main() -> int:
                 "baseline": g_baseline,
                 "G_s_all_windows": [round(float(v) / wm, 6) for v in wg],
                 "bit_exact_first_steps": g_exact,
+                "samples_per_s": T * S * R / len(bounds) / (g_ms / 1e3),
+                "cpu_baseline": g_cpu,
             }
             del btilde, g_out, g_views
 
@@ -513,13 +559,17 @@ def main() -> int:
                 torch.cuda.synchronize(dev)
                 l_ms = float(np.mean([a.elapsed_time(b) for a, b in lt])) / len(bounds)
                 l_bytes = (8 * T * S * R + 16 * T * S) / len(bounds)
-                l_exact = None
+                l_exact = l_cpu = None
                 if oracle_out:
                     import oracle
-                    x = synth.generate(wl, 0, 8)
+                    nl = min(T, 32)
+                    x = synth.generate(wl, 0, nl)
+                    tc = time.perf_counter()
                     ol, oi = oracle.frontier_lag(x)
-                    l_exact = bool(np.array_equal(lg[:8].cpu().numpy(), ol) and
-                                   np.array_equal(lgi[:8].cpu().numpy(), oi))
+                    l_cpu = row_cpu(x.size, time.perf_counter() - tc,
+                                    "oracle frontier_lag on %d steps of the workload" % nl)
+                    l_exact = bool(np.array_equal(lg[:nl].cpu().numpy(), ol) and
+                                   np.array_equal(lgi[:nl].cpu().numpy(), oi))
                 next_rows["lag"] = {
                     "kernel": "k_median_spread<prefix>",
                     "bound": "valu (radix select)",
@@ -530,6 +580,8 @@ def main() -> int:
                     "unit": "GB/s",
                     "frac": l_bytes / (l_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
                     "bit_exact_first_steps": l_exact,
+                    "samples_per_s": T * S * R / len(bounds) / (l_ms / 1e3),
+                    "cpu_baseline": l_cpu,
                 }
                 del lg, lgi, l_views
 
@@ -556,12 +608,16 @@ def main() -> int:
                 torch.cuda.synchronize(dev)
                 s_ms = float(np.mean([a.elapsed_time(b) for a, b in st])) / len(bounds)
                 s_bytes = (8 * T * S * R + 8 * T * S + 8 * W * S) / len(bounds)
-                s_exact = None
+                s_exact = s_cpu = None
                 if oracle_out:
                     import oracle
-                    x = synth.generate(wl, 0, 8)
+                    ns = min(T, 32)
+                    x = synth.generate(wl, 0, ns)
+                    tc = time.perf_counter()
                     osp, _ = oracle.rank_spread(x, wl.window)
-                    s_exact = bool(np.array_equal(sp[:8].cpu().numpy(), osp))
+                    s_cpu = row_cpu(x.size, time.perf_counter() - tc,
+                                    "oracle rank_spread on %d steps of the workload" % ns)
+                    s_exact = bool(np.array_equal(sp[:ns].cpu().numpy(), osp))
                 wsum = wsp.sum(dim=0).double()
                 next_rows["rank_spread"] = {
                     "kernel": "k_median_spread<raw> (+ k_window_sum)",
@@ -575,6 +631,8 @@ def main() -> int:
                     "spread_share_all_windows": [round(float(v) / float(wsum.sum()), 6) for v in wsum]
                     if float(wsum.sum()) > 0 else None,
                     "bit_exact_first_steps": s_exact,
+                    "samples_per_s": T * S * R / len(bounds) / (s_ms / 1e3),
+                    "cpu_baseline": s_cpu,
                 }
                 del sp, wsp, s_views
 
