@@ -743,6 +743,7 @@ def main() -> int:
             "frac": achieved / PEAK_HBM_GBPS,
             "traffic": traffic,
             "launch_ms": frontier_launch_ms,
+            "launch_ms_median": float(np.median(frontier_ms)) / launches,
             "algorithmic_bytes_per_launch": launch_bytes,
         },
         "summary_kernels_ms": float(np.mean(summary_ms)),
