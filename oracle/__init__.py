@@ -50,6 +50,8 @@ class COracle:
         lib.sfo_frontier.restype = ctypes.c_int
         lib.sfo_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp]
         lib.sfo_window_summary.restype = None
+        lib.sfo_window_lead_exposed.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp]
+        lib.sfo_window_lead_exposed.restype = None
         lib.sfo_frontier_evidence.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp]
         lib.sfo_frontier_evidence.restype = ctypes.c_int
         lib.sfo_ingest.argtypes = [vp, vp, i64, i32, i32, vp, vp]
@@ -230,6 +232,25 @@ class COracle:
                 exposed.ctypes.data, counts.ctypes.data, top2.ctypes.data)
         return exposed, counts, top2
 
+    def window_lead_exposed(self, inc: np.ndarray, lead: np.ndarray, R: int, window: int):
+        """Exposed time each rank led, per window and stage: the sum of the
+        window's advances of the stage whose leader is that rank.
+
+        Returns ``(lead_exposed [W,S,R] int64, top2 [W,2,2] int32)``: the
+        top-2 stages of the window summary, each with the rank that led the
+        most exposed time of it (lowest rank on ties, -1 if none led any).
+        """
+        inc = np.ascontiguousarray(inc, dtype=np.int64)
+        lead = np.ascontiguousarray(lead, dtype=np.int32)
+        T, S = inc.shape
+        W = num_windows(T, window)
+        out = np.empty((W, S, R), dtype=np.int64)
+        top2 = np.empty((W, 2, 2), dtype=np.int32)
+        if W:
+            self.lib.sfo_window_lead_exposed(inc.ctypes.data, lead.ctypes.data, T, R, S, window,
+                                             out.ctypes.data, top2.ctypes.data)
+        return out, top2
+
 
 def num_windows(T: int, window: int) -> int:
     return (T + window - 1) // window
@@ -249,6 +270,10 @@ def _get() -> COracle:
 
 def frontier(d: np.ndarray):
     return _get().frontier(d)
+
+
+def window_lead_exposed(inc: np.ndarray, lead: np.ndarray, R: int, window: int):
+    return _get().window_lead_exposed(inc, lead, R, window)
 
 
 def window_summary(inc: np.ndarray, lead: np.ndarray, R: int, window: int):

@@ -56,6 +56,34 @@ def window_summary(inc, lead, R, window):
     return exposed, counts, top2
 
 
+def window_lead_exposed(inc, lead, R, window):
+    """Returns ``(lead_exposed[w][s][r], top2[w][k][2])``: per window and
+    stage, the advances whose leader is rank r, summed (leaders outside
+    [0, R) not counted); the top-2 stages by window total, each with the rank
+    that led the most exposed time (lowest on ties, -1 if none led any)."""
+    T = len(inc)
+    S = len(inc[0]) if T else 0
+    W = (T + window - 1) // window
+    out, top2 = [], []
+    for w in range(W):
+        steps = range(w * window, min((w + 1) * window, T))
+        le_w = [[sum(inc[t][s] for t in steps if lead[t][s] == r) for r in range(R)]
+                for s in range(S)]
+        totals = [sum(inc[t][s] for t in steps) for s in range(S)]
+        order = sorted(range(S), key=lambda s: (-totals[s], s))
+        picks = order[:2] + [-1] * (2 - len(order[:2]))
+        t2 = []
+        for sk in picks:
+            if sk < 0:
+                t2.append([-1, -1])
+                continue
+            m = max(le_w[sk])
+            t2.append([sk, le_w[sk].index(m) if m > 0 else -1])
+        out.append(le_w)
+        top2.append(t2)
+    return out, top2
+
+
 def frontier_evidence(d):
     """``d[t][s][r]`` -> dict of [t][s] lists: inc, lead, gap, ties,
     stage_max, stage_sum (same readings as the C oracle)."""

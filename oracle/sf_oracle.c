@@ -38,13 +38,19 @@
  *   steps of a window.
  *   Sec. 4, Eq. (4), per-rank window median: a candidate baseline btilde,
  *   the median over the steps of a window of d[t,r,s], per stage and rank.
+ *   Sec. 3 and Sec. 4, rank attribution: every advance a[t,s] is
+ *   attributed to the rank attaining the frontier (the leader); per window,
+ *   stage and rank, the exposed time that rank led is the sum of the
+ *   window's advances of that stage whose leader is that rank; the top-2
+ *   suspects weighted this way pair the two stages of the window summary
+ *   with the rank that led the most exposed time of each.
  *   Sec. 3, the data contract: durations are nonnegative; with the
  *   library's packed keys every prefix must also stay below 2^47 ns.  The
  *   range status is 2 (SF_ERANGE) when some d < 0 or some prefix of
  *   nonnegative durations reaches 2^47, else 0.
  *
- * Readings where the paper leaves a choice open (each is listed with its
- * reason in the design notes of the repository):
+ * Readings where the paper leaves a choice open (each is a reading of the
+ * paper, not a statement it makes):
  *   - leader = lowest rank index attaining F (the paper reports a tie set);
  *   - the leader is emitted and counted at every boundary, also where a = 0;
  *   - top-2 orders stages by the exposed window total (equivalently by the
@@ -74,8 +80,8 @@
  *     tau_den * (their exposed sum) >= tau_num * (window total).
  *
  * Layout: d is [T][S][R] (rank fastest), increments and leaders [T][S],
- * exposed [W][S], counts [W][S][R], top2 [W][2][2], route order [W][S] and
- * route size [W].
+ * exposed [W][S], counts and exposed time led [W][S][R], top2 [W][2][2],
+ * route order [W][S] and route size [W].
  *
  * Parity status: every function here is pinned by the CPU test suite
  * (printed worked examples, closed forms, brute force); see tests/.
@@ -161,6 +167,65 @@ void sfo_window_summary(const int64_t* inc, const int32_t* lead,
                 for (int32_t r = 0; r < R; ++r) {
                     if (c[r] > best) {
                         best = c[r];
+                        rk = r;
+                    }
+                }
+            }
+            top2[w * 4 + 2 * k + 0] = sk;
+            top2[w * 4 + 2 * k + 1] = rk;
+        }
+    }
+}
+
+/* Exposed time led per (window, stage, rank): the sum of a window's
+ * advances of stage s whose leader is rank r.  Leaders outside [0, R) are
+ * not counted.  lead_exposed is [W][S][R].  top2 is [W][2][2]: the same two
+ * stages as sfo_window_summary (largest window total of the advances, lower
+ * stage first on ties), each paired with the rank that led the most exposed
+ * time of that stage (lowest rank on ties; -1 if no rank led any). */
+void sfo_window_lead_exposed(const int64_t* inc, const int32_t* lead, int64_t T, int32_t R,
+                             int32_t S, int64_t window, int64_t* lead_exposed, int32_t* top2)
+{
+    int64_t W = (T + window - 1) / window;
+    for (int64_t w = 0; w < W; ++w) {
+        int64_t t0 = w * window;
+        int64_t t1 = t0 + window < T ? t0 + window : T;
+        for (int32_t s = 0; s < S; ++s) {
+            int64_t* e = lead_exposed + (w * S + s) * (int64_t)R;
+            for (int32_t r = 0; r < R; ++r) e[r] = 0;
+            for (int64_t t = t0; t < t1; ++t) {
+                int32_t r = lead[t * S + s];
+                if (r >= 0 && r < R) e[r] += inc[t * S + s];
+            }
+        }
+
+        /* the stage totals, recomputed from the advances */
+        int32_t s1 = -1, s2 = -1;
+        int64_t e1 = 0, e2 = 0;
+        for (int32_t s = 0; s < S; ++s) {
+            int64_t tot = 0;
+            for (int64_t t = t0; t < t1; ++t) tot += inc[t * S + s];
+            if (s1 < 0 || tot > e1) {
+                s2 = s1;
+                e2 = e1;
+                s1 = s;
+                e1 = tot;
+            } else if (s2 < 0 || tot > e2) {
+                s2 = s;
+                e2 = tot;
+            }
+        }
+
+        int32_t pick[2] = {s1, s2};
+        for (int k = 0; k < 2; ++k) {
+            int32_t sk = pick[k];
+            int32_t rk = -1;
+            if (sk >= 0) {
+                const int64_t* e = lead_exposed + (w * S + sk) * (int64_t)R;
+                int64_t best = 0;
+                for (int32_t r = 0; r < R; ++r) {
+                    if (e[r] > best) {
+                        best = e[r];
                         rk = r;
                     }
                 }

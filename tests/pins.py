@@ -418,6 +418,184 @@ SUMMARY_PINS = [pin_summary_mass, pin_summary_top2, pin_summary_bruteforce]
 
 
 # ----------------------------------------------------------------------------
+# exposed time led per (window, stage, rank): every advance goes to the rank
+# that attains the frontier (the leader)
+
+
+def pin_lead_golden(f, le):
+    """The printed worked examples: the whole advance of each boundary goes
+    to its leader, in one window."""
+    for name in GOLDEN_FILES:
+        g = load_golden(name)
+        d = g["d"]
+        inc, lead = f(d)
+        T, S, R = d.shape
+        out, _ = le(inc, lead, R, T)
+        want = np.zeros((1, S, R), dtype=np.int64)
+        for s, (a, r) in enumerate(zip(g["inc"], g["lead"])):
+            want[0, s, r] = a
+        assert np.array_equal(out, want), name
+
+
+def pin_lead_stall(f, le):
+    """The Sec. 2 stall on half of ten steps: the data stage's exposed time
+    goes to the stalled rank for the stalled steps (50 ms each) and to rank 0
+    for the clean four-way ties (20 ms each); backward never goes to the
+    waiting ranks.  By count the data stage is a 5-5 tie that goes to rank
+    0; by exposed time led it goes to the stalled rank."""
+    d = np.repeat(stall_case(), 10, axis=0)
+    d[5:, 0, 2] -= 30 * MS
+    d[5:, 2, [0, 1, 3]] -= 30 * MS
+    inc, lead = f(d)
+    out, top2 = le(inc, lead, 4, 10)
+    assert out[0, 0].tolist() == [5 * 20 * MS, 0, 5 * 50 * MS, 0]
+    assert out[0, 2].tolist() == [10 * 120 * MS, 0, 0, 0]
+    # stage totals: bwd 1200 ms, fwd 600 ms, data 350 ms
+    assert top2[0].tolist() == [[2, 0], [1, 0]]
+    # with the step time of the model stages cut, data becomes the top stage
+    d2 = d.copy()
+    d2[:, 1:3] //= 10
+    inc2, lead2 = f(d2)
+    _, top2 = le(inc2, lead2, 4, 10)
+    assert top2[0, 0].tolist() == [0, 2]
+
+
+def pin_lead_single_rank(f, le):
+    """R = 1: every advance is the rank's own duration (Sec. 3), so the
+    single rank holds the window sums of its durations."""
+    d = random_cases(13)[0][:, :, :1].copy()
+    T, S, _ = d.shape
+    inc, lead = f(d)
+    for window in (1, 4, T):
+        out, top2 = le(inc, lead, 1, window)
+        for w in range(-(-T // window)):
+            t0, t1 = w * window, min((w + 1) * window, T)
+            assert np.array_equal(out[w, :, 0], d[t0:t1, :, 0].sum(axis=0))
+            for k in range(2):
+                assert top2[w, k, 1] == (0 if out[w, top2[w, k, 0], 0] > 0 else -1)
+
+
+def pin_lead_mass_and_support(f, le):
+    """Per window and stage the ranks' shares add up to the stage's exposed
+    total, and by Theorem 1 over all stages to the window's exposed
+    makespan; shares are nonnegative, and only ranks that led the stage at
+    some step of the window hold any.  Windows add up."""
+    for d in random_cases(14):
+        T, S, R = d.shape
+        inc, lead = f(d)
+        for window in (1, 5, T, T + 2):
+            out, _ = le(inc, lead, R, window)
+            assert out.shape == (-(-T // window), S, R)
+            assert (out >= 0).all()
+            for w in range(out.shape[0]):
+                t0, t1 = w * window, min((w + 1) * window, T)
+                assert np.array_equal(out[w].sum(axis=1), inc[t0:t1].sum(axis=0))
+                assert int(out[w].sum()) == int(rank_totals(d[t0:t1]).max(axis=1).sum())
+                for s in range(S):
+                    led = set(lead[t0:t1, s].tolist())
+                    assert all(r in led for r in np.nonzero(out[w, s])[0].tolist())
+        if T >= 4:
+            whole, _ = le(inc, lead, R, T)
+            halves, _ = le(inc, lead, R, -(-T // 2))
+            assert np.array_equal(halves.sum(axis=0), whole[0])
+
+
+def pin_lead_relabel(f, le):
+    """Relabelling the ranks (tie-free data) relabels the shares and the
+    suspect ranks."""
+    rng = np.random.Generator(np.random.PCG64(15))
+    d = rng.integers(0, 10**9, size=(12, 5, 7), dtype=np.int64)
+    perm = rng.permutation(7)
+    inc, lead = f(d)
+    inc2, lead2 = f(d[:, :, perm])
+    a, ta = le(inc, lead, 7, 4)
+    b, tb = le(inc2, lead2, 7, 4)
+    # new rank j is old rank perm[j]
+    assert np.array_equal(b, a[:, :, perm])
+    assert np.array_equal(tb[:, :, 0], ta[:, :, 0])
+    assert np.array_equal(perm[tb[:, :, 1]], ta[:, :, 1])
+
+
+def pin_lead_counts_and_bincount(f, le):
+    """Against the leader counts and numpy: with every advance of a stage
+    equal to c the share is c times the rank's count, and in general it is
+    numpy's weighted bincount of the leaders; leaders outside [0, R) count
+    nowhere.  The suspects are the two stages of largest window total
+    (numpy lexsort, lower stage first on ties), each with numpy's first
+    argmax of its shares (-1 when every share is 0).  Brute force over
+    every leader pattern of a tiny window set."""
+    R, S, T = 3, 2, 4
+    inc = np.arange(T * S, dtype=np.int64).reshape(T, S) * 5 + 2
+    for flat in itertools.product(range(-1, R + 1), repeat=T * S // 2):
+        lead = np.array(flat + flat, dtype=np.int32).reshape(T, S)
+        for window in (1, 3, 4):
+            out, top2 = le(inc, lead, R, window)
+            for w in range(-(-T // window)):
+                t0, t1 = w * window, min((w + 1) * window, T)
+                for s in range(S):
+                    v = lead[t0:t1, s]
+                    keep = (v >= 0) & (v < R)
+                    want = np.bincount(v[keep], weights=inc[t0:t1, s][keep], minlength=R)[:R]
+                    assert np.array_equal(out[w, s], want.astype(np.int64))
+                e = inc[t0:t1].sum(axis=0)
+                order = np.lexsort((np.arange(S), -e))
+                for k in range(2):
+                    sk = int(order[k])
+                    rk = int(np.argmax(out[w, sk])) if out[w, sk].max() > 0 else -1
+                    assert top2[w, k].tolist() == [sk, rk]
+    c = np.full((T, S), 7, dtype=np.int64)
+    lead = np.array([[0, 2], [2, 2], [0, 1], [0, 0]], dtype=np.int32)
+    assert np.array_equal(le(c, lead, R, T)[0][0], 7 * _expected_counts(lead, R, 0, T))
+
+
+def pin_lead_top2_cases(f, le, g):
+    """Constructed windows: the count-modal rank and the rank that led the
+    most exposed time differ when few long advances outweigh many short
+    ones; with equal advances they agree with the window summary's top-2
+    (every stage and rank, ties included); S = 1 pads; zero totals give
+    rank -1."""
+    R = 4
+    # stage 0: rank 1 leads 4 steps of 1, rank 3 leads 2 steps of 10
+    # (total 24); stage 1: ranks 2 and 0 each lead 3 steps of 5 (total 30)
+    inc = np.array([[1, 5], [1, 5], [10, 5], [1, 5], [10, 5], [1, 5]], dtype=np.int64)
+    lead = np.array([[1, 2], [1, 0], [3, 2], [1, 0], [3, 2], [1, 0]], dtype=np.int32)
+    out, top2 = le(inc, lead, R, 6)
+    assert out[0].tolist() == [[0, 4, 0, 20], [15, 0, 15, 0]]
+    assert top2.tolist() == [[[1, 0], [0, 3]]]
+    _, _, t_count = g(inc, lead, R, 6)
+    assert t_count.tolist() == [[[1, 0], [0, 1]]]
+    # equal advances per stage: same picks as the count-based top-2
+    for d in random_cases(17):
+        T, S, R = d.shape
+        _, lead = f(d)
+        cinc = np.tile(np.arange(S, dtype=np.int64)[::-1] % 3 + 1, (T, 1))
+        for window in (3, T):
+            _, tw = le(cinc, lead, R, window)
+            _, _, tc = g(cinc, lead, R, window)
+            assert np.array_equal(tw, tc)
+    # S = 1 pads the second pair; zero advances lead to no rank
+    _, top2 = le(np.array([[0], [0]], dtype=np.int64), np.array([[1], [1]], dtype=np.int32), 2, 2)
+    assert top2.tolist() == [[[0, -1], [-1, -1]]]
+    _, top2 = le(np.array([[3], [4]], dtype=np.int64), np.array([[2], [2]], dtype=np.int32), 3, 5)
+    assert top2.tolist() == [[[0, 2], [-1, -1]]]
+
+
+def pin_lead_twin(f, le, pyref):
+    for d in random_cases(16):
+        small = d[:9]
+        T, S, R = small.shape
+        inc, lead = f(small)
+        for window in (2, 4, 9):
+            out, top2 = le(inc, lead, R, window)
+            po, pt = pyref.window_lead_exposed(inc.tolist(), lead.tolist(), R, window)
+            assert out.tolist() == po and top2.tolist() == pt
+
+
+LEAD_PINS = [pin_lead_golden, pin_lead_stall, pin_lead_single_rank, pin_lead_mass_and_support,
+             pin_lead_relabel, pin_lead_counts_and_bincount]
+
+
+# ----------------------------------------------------------------------------
 # localization evidence and per-stage baselines (Sec. 4; Props. 1-2)
 #
 # Each pin takes ``e(d) -> dict`` with [T, S] arrays inc, lead, gap, ties,

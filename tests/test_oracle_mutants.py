@@ -47,6 +47,21 @@ MUTANTS = {
     "top2_ascending": ("sfo_window_summary",
                        "if (s2 < 0 || exposed[w * S + s] > exposed[w * S + s2]) s2 = s;",
                        "if (s2 < 0 || exposed[w * S + s] < exposed[w * S + s2]) s2 = s;"),
+    # exposed time led per (window, stage, rank) and its top-2
+    "le_weight_is_count": ("sfo_window_lead_exposed", "if (r >= 0 && r < R) e[r] += inc[t * S + s];",
+                           "if (r >= 0 && r < R) e[r] += 1;"),
+    "le_rank0_not_counted": ("sfo_window_lead_exposed", "if (r >= 0 && r < R) e[r] += inc[t * S + s];",
+                             "if (r > 0 && r < R) e[r] += inc[t * S + s];"),
+    "le_drops_last_step": ("sfo_window_lead_exposed", "int64_t t1 = t0 + window < T ? t0 + window : T;",
+                           "int64_t t1 = t0 + window < T ? t0 + window - 1 : T;"),
+    "le_wrong_stage_weight": ("sfo_window_lead_exposed", "if (r >= 0 && r < R) e[r] += inc[t * S + s];",
+                              "if (r >= 0 && r < R) e[r] += inc[t * S + (S - 1 - s)];"),
+    "le_first_stage_tie_to_higher": ("sfo_window_lead_exposed", "if (s1 < 0 || tot > e1) {",
+                                     "if (s1 < 0 || tot >= e1) {"),
+    "le_second_not_demoted": ("sfo_window_lead_exposed", "s2 = s1;\n                e2 = e1;\n", ""),
+    "le_rank_tie_to_higher": ("sfo_window_lead_exposed", "if (e[r] > best) {",
+                              "if (e[r] >= best && e[r] > 0) {"),
+    "le_rank_first_nonzero": ("sfo_window_lead_exposed", "best = e[r];", "best = INT64_MAX;"),
     # localization evidence and baselines
     "ev_tie_to_highest_rank": ("sfo_frontier_evidence", "if (P[r] > F) {", "if (P[r] >= F) {"),
     "ev_no_prefix_reset": ("sfo_frontier_evidence", "for (int32_t r = 0; r < R; ++r) P[r] = 0;", ""),
@@ -150,6 +165,15 @@ def _run_all(o):
             pin(o.frontier, o.window_summary)
         except AssertionError:
             failed.append(pin.__name__)
+    for pin in pins.LEAD_PINS:
+        try:
+            pin(o.frontier, o.window_lead_exposed)
+        except AssertionError:
+            failed.append(pin.__name__)
+    try:
+        pins.pin_lead_top2_cases(o.frontier, o.window_lead_exposed, o.window_summary)
+    except AssertionError:
+        failed.append("pin_lead_top2_cases")
     for pin in pins.EVIDENCE_PINS:
         try:
             pin(o.frontier_evidence)

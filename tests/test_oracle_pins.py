@@ -16,6 +16,19 @@ def test_summary_pin(pin):
     pin(oracle.frontier, oracle.window_summary)
 
 
+@pytest.mark.parametrize("pin", pins.LEAD_PINS, ids=lambda p: p.__name__)
+def test_lead_exposed_pin(pin):
+    pin(oracle.frontier, oracle.window_lead_exposed)
+
+
+def test_lead_exposed_top2_cases():
+    pins.pin_lead_top2_cases(oracle.frontier, oracle.window_lead_exposed, oracle.window_summary)
+
+
+def test_twin_lead_exposed():
+    pins.pin_lead_twin(oracle.frontier, oracle.window_lead_exposed, oracle.pyref)
+
+
 @pytest.mark.parametrize("pin", pins.EVIDENCE_PINS, ids=lambda p: p.__name__)
 def test_evidence_pin(pin):
     pin(oracle.frontier_evidence)
@@ -47,6 +60,8 @@ def test_empty_and_degenerate():
     assert inc.shape == (0, 3) and lead.shape == (0, 3)
     ex, cnt, top2 = oracle.window_summary(inc, lead, 4, 10)
     assert ex.shape == (0, 3) and cnt.shape == (0, 3, 4) and top2.shape == (0, 2, 2)
+    le, top2 = oracle.window_lead_exposed(inc, lead, 4, 10)
+    assert le.shape == (0, 3, 4) and top2.shape == (0, 2, 2)
     # all-zero durations: zero advances, every boundary a full tie -> rank 0
     inc, lead = oracle.frontier(np.zeros((2, 3, 5), dtype=np.int64))
     assert (inc == 0).all() and (lead == 0).all()
