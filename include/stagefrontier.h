@@ -334,6 +334,37 @@ int sf_window_summary(const int64_t* increment, const int32_t* leader,
                       int32_t* out_top2, sf_stream_t stream);
 
 /*
+ * sf_window_lead_exposed -- the exposed time each rank led, per window and
+ * stage.  Every advance a[t][s] is attributed to the rank attaining the
+ * frontier (Sec. 3), so summing a window's advances of stage s by leader
+ * splits the stage's exposed total (the Eq. (2) numerator) over ranks:
+ * the rank-level counterpart of the stage shares, and the exposed-time
+ * weighting of the top-2 rank localization of Sec. 4.
+ *
+ *   increment, leader, T, R, S, window: as for sf_window_summary.
+ *   out_lead_exposed   [W][S][R] int64: sum of a[t][s] over the steps t of
+ *                      window w whose leader at stage s is rank r (zeros
+ *                      included).  Leaders outside [0, R) count nowhere,
+ *                      so a row sums to out_stage_exposed[w][s] whenever
+ *                      every leader of the window lies in [0, R).
+ *   out_top2           [W][2][2] int32: {{s1, r1}, {s2, r2}}.  s1, s2 are
+ *                      the stages of sf_window_summary's top-2 (largest
+ *                      window total of a[t][s], the lower stage on ties);
+ *                      rk is the rank that led the most exposed time of
+ *                      stage sk (the lower rank on ties; -1 if no entry of
+ *                      that row is positive).  When S == 1 the second pair
+ *                      is {-1, -1}.
+ *   stream             HIP stream.
+ *
+ * Exactness as for sf_window_summary.  Pointers aligned to their element
+ * size; outputs must not overlap inputs or each other.  Returns SF_OK,
+ * SF_EINVAL or SF_EHIP.
+ */
+int sf_window_lead_exposed(const int64_t* increment, const int32_t* leader, int64_t T,
+                           int32_t R, int32_t S, int64_t window, int64_t* out_lead_exposed,
+                           int32_t* out_top2, sf_stream_t stream);
+
+/*
  * sf_read_xor -- plain-read calibration (a measurement aid, not part of the
  * paper's method): the XOR of the 64-bit words of every SF_XOR_PIECE_BYTES
  * piece of a device buffer.  It reads each byte exactly once with the

@@ -1,6 +1,8 @@
 // window.hip -- sf_window_summary and sf_num_windows: window sums of the
 // advances (Eq. (2) numerators), leader counts and top-2 routing (Sec. 4);
-// and the generic window sum used by sf_exposure_gain.
+// sf_window_lead_exposed: the exposed time each rank led (every advance
+// attributed to its leader, Sec. 3) and the top-2 weighted by it; and the
+// generic window sum used by sf_exposure_gain.
 //
 // Window kernels.  One workgroup per (window, stage, rank chunk) builds the
 // leader histogram of the window in LDS with LDS atomics and sums the
@@ -147,6 +149,99 @@ __global__ __launch_bounds__(kTopWG) void k_window_top2(const int64_t* __restric
     }
 }
 
+// Exposed time led: the same segmented histogram as k_window_counts, with
+// every leader weighted by its advance.  One workgroup per (window, stage,
+// rank chunk); 64-bit LDS atomics (two's-complement adds, so any int64
+// advance sums exactly as in int64).
+constexpr int kLeadChunk = 8192;  // ranks per weighted-histogram workgroup (64 KB LDS)
+
+__global__ __launch_bounds__(kSumWG) void k_window_lead_exposed(
+    const int64_t* __restrict__ inc, const int32_t* __restrict__ lead, int64_t T, int R, int S,
+    int64_t window, int64_t W, int nchunk, int64_t* __restrict__ lead_exposed)
+{
+    extern __shared__ u64 whist[];  // [min(R, kLeadChunk)]
+    const int tid = threadIdx.x;
+    const int64_t total = W * S * nchunk;
+    for (int64_t id = blockIdx.x; id < total; id += gridDim.x) {
+        const int c = (int)(id % nchunk);
+        const int64_t ws = id / nchunk;
+        const int s = (int)(ws % S);
+        const int64_t w = ws / S;
+        const int lo = c * kLeadChunk;
+        const int n = min(kLeadChunk, R - lo);
+        const int64_t t0 = w * window;
+        const int64_t t1 = min(t0 + window, T);
+
+        for (int i = tid; i < n; i += kSumWG) whist[i] = 0;
+        __syncthreads();
+        for (int64_t t = t0 + tid; t < t1; t += kSumWG) {
+            const int64_t r = (int64_t)lead[t * S + s] - lo;
+            if (r >= 0 && r < n) atomicAdd(&whist[r], (u64)inc[t * S + s]);
+        }
+        __syncthreads();
+        int64_t* out = lead_exposed + (w * S + s) * (int64_t)R + lo;
+        for (int i = tid; i < n; i += kSumWG) out[i] = (int64_t)whist[i];
+        __syncthreads();  // whist is reused by the next id
+    }
+}
+
+// One workgroup per (window, pick k in {0, 1}); grid-stride.  The stage
+// totals of the window are summed here from the advances (one wave per
+// stage at a time), both workgroups of a window choose the same two stages,
+// and each then finds the rank that led the most exposed time of its own
+// stage: the largest positive entry of the row, the lowest rank on ties.
+__global__ __launch_bounds__(kTopWG) void k_window_lead_top2(
+    const int64_t* __restrict__ inc, const int64_t* __restrict__ lead_exposed, int64_t T, int R,
+    int S, int64_t window, int64_t W, int32_t* __restrict__ top2)
+{
+    __shared__ int64_t tot[SF_MAX_S];
+    __shared__ u64 sh[kTopWG / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int64_t id = blockIdx.x; id < 2 * W; id += gridDim.x) {
+        const int64_t w = id >> 1;
+        const int k = (int)(id & 1);
+        const int64_t t0 = w * window;
+        const int64_t t1 = min(t0 + window, T);
+        for (int s = wave; s < S; s += kTopWG / 64) {
+            int64_t sum = 0;
+            for (int64_t t = t0 + lane; t < t1; t += 64) sum += inc[t * S + s];
+            sum = wave_sum64(sum);
+            if (lane == 0) tot[s] = sum;
+        }
+        __syncthreads();
+        // larger total first, then lower stage index (every thread alike)
+        int s1 = 0;
+        for (int s = 1; s < S; ++s)
+            if (tot[s] > tot[s1]) s1 = s;
+        int s2 = -1;
+        for (int s = 0; s < S; ++s)
+            if (s != s1 && (s2 < 0 || tot[s] > tot[s2])) s2 = s;
+        const int pick = k == 0 ? s1 : s2;
+
+        int rank = -1;
+        if (pick >= 0) {
+            const int64_t* row = lead_exposed + (w * S + pick) * (int64_t)R;
+            int64_t best = 0;
+            int br = -1;
+            for (int r = tid; r < R; r += kTopWG) {
+                const int64_t v = row[r];
+                if (v > best) { best = v; br = r; }
+            }
+            // the largest positive value (0 when none), then the lowest rank
+            // holding it; threads without a positive value cannot win
+            const u64 vmax = block_max64((u64)best, sh);
+            const u64 rkey = (br >= 0 && (u64)best == vmax) ? (u64)(0xFFFFFFFFu - (uint32_t)br) + 1ull : 0ull;
+            const u64 rmax = block_max64(rkey, sh);
+            rank = rmax ? (int)(0xFFFFFFFFu - (uint32_t)(rmax - 1ull)) : -1;
+        }
+        if (tid == 0) {
+            top2[w * 4 + 2 * k] = pick;
+            top2[w * 4 + 2 * k + 1] = rank;
+        }
+        __syncthreads();  // tot is rewritten by the next id
+    }
+}
+
 // Segmented sums over windows of the columns of a [T][C] int64 array: one
 // workgroup per (window, column); grid-stride.
 __global__ __launch_bounds__(kSumWG) void k_window_sum(const int64_t* __restrict__ x, int64_t T,
@@ -229,5 +324,43 @@ SF_API int sf_window_summary(const int64_t* increment, const int32_t* leader, in
     void* a2[] = {(void*)&out_stage_exposed, (void*)&out_lead_counts, (void*)&Ri, (void*)&Si,
                   (void*)&Wl, (void*)&out_top2};
     return launch(reinterpret_cast<const void*>(&k_window_top2), dim3(g2), dim3(kTopWG), a2, 0,
+                  stream);
+}
+
+SF_API int sf_window_lead_exposed(const int64_t* increment, const int32_t* leader, int64_t T,
+                                  int32_t R, int32_t S, int64_t window, int64_t* out_lead_exposed,
+                                  int32_t* out_top2, sf_stream_t stream)
+{
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S || window < 1) return SF_EINVAL;
+    if (!fits(T, S, 1, 8)) return SF_EINVAL;
+    if (T == 0) return SF_OK;
+    const int64_t W = sf_num_windows(T, window);
+    if (!fits(W, S, R, 8)) return SF_EINVAL;
+    if (!increment || !leader || !out_lead_exposed || !out_top2) return SF_EINVAL;
+    if (!aligned(increment, 8) || !aligned(leader, 4) || !aligned(out_lead_exposed, 8) ||
+        !aligned(out_top2, 4))
+        return SF_EINVAL;
+    const void* bufs[4] = {increment, leader, out_lead_exposed, out_top2};
+    const int64_t sizes[4] = {T * S * 8, T * S * 4, W * S * (int64_t)R * 8, W * 16};
+    for (int a = 0; a < 4; ++a)
+        for (int b = (a < 2 ? 2 : a + 1); b < 4; ++b)
+            if (!disjoint(bufs[a], sizes[a], bufs[b], sizes[b])) return SF_EINVAL;
+
+    const int nchunk = (R + kLeadChunk - 1) / kLeadChunk;
+    const int64_t items = W * S * nchunk;
+    const unsigned g1 = (unsigned)(items < 1048576 ? items : 1048576);
+    const size_t lds = (size_t)(R < kLeadChunk ? R : kLeadChunk) * sizeof(u64);
+    int Ri = R, Si = S;
+    int64_t Wl = W;
+    void* a1[] = {(void*)&increment, (void*)&leader, (void*)&T, (void*)&Ri, (void*)&Si,
+                  (void*)&window, (void*)&Wl, (void*)&nchunk, (void*)&out_lead_exposed};
+    int rc = launch(reinterpret_cast<const void*>(&k_window_lead_exposed), dim3(g1), dim3(kSumWG),
+                    a1, lds, stream);
+    if (rc != SF_OK) return rc;
+    const unsigned g2 = (unsigned)(2 * W < 65536 ? 2 * W : 65536);
+    const int64_t* le = out_lead_exposed;
+    void* a2[] = {(void*)&increment, (void*)&le, (void*)&T, (void*)&Ri, (void*)&Si,
+                  (void*)&window, (void*)&Wl, (void*)&out_top2};
+    return launch(reinterpret_cast<const void*>(&k_window_lead_top2), dim3(g2), dim3(kTopWG), a2, 0,
                   stream);
 }

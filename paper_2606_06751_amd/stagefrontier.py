@@ -66,6 +66,8 @@ def _load() -> ctypes.CDLL:
     lib.sf_num_windows.restype = i64
     lib.sf_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp]
     lib.sf_window_summary.restype = ctypes.c_int
+    lib.sf_window_lead_exposed.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp]
+    lib.sf_window_lead_exposed.restype = ctypes.c_int
     lib.sf_strerror.argtypes = [ctypes.c_int]
     lib.sf_strerror.restype = ctypes.c_char_p
     lib.sf_version.argtypes = []
@@ -232,6 +234,37 @@ def sf_window_summary(increment: torch.Tensor, leader: torch.Tensor, R: int, win
     if rc != SF_OK:
         raise StageFrontierError(rc, "sf_window_summary")
     return out_stage_exposed, out_lead_counts, out_top2
+
+
+def sf_window_lead_exposed(increment: torch.Tensor, leader: torch.Tensor, R: int, window: int,
+                           out_lead_exposed: torch.Tensor | None = None,
+                           out_top2: torch.Tensor | None = None, stream=None):
+    """Exposed time each rank led, per window and stage, and the top-2
+    weighted by it (``sf_window_lead_exposed``).
+
+    Returns ``(out_lead_exposed [W, S, R] int64, out_top2 [W, 2, 2] int32)``.
+    """
+    if increment.dim() != 2:
+        raise ValueError("increment must be [T, S]")
+    T, S = increment.shape
+    _check(increment, "increment", torch.int64, (T, S))
+    _check(leader, "leader", torch.int32, (T, S), like=increment)
+    W = sf_num_windows(T, window)
+    if W < 0:
+        raise StageFrontierError(SF_EINVAL, "sf_window_lead_exposed")
+    dev = increment.device
+    if out_lead_exposed is None:
+        out_lead_exposed = torch.empty((W, S, R), dtype=torch.int64, device=dev)
+    if out_top2 is None:
+        out_top2 = torch.empty((W, 2, 2), dtype=torch.int32, device=dev)
+    _check(out_lead_exposed, "out_lead_exposed", torch.int64, (W, S, R), like=increment)
+    _check(out_top2, "out_top2", torch.int32, (W, 2, 2), like=increment)
+    rc = _lib.sf_window_lead_exposed(increment.data_ptr(), leader.data_ptr(), T, R, S, window,
+                                     out_lead_exposed.data_ptr(), out_top2.data_ptr(),
+                                     _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_window_lead_exposed")
+    return out_lead_exposed, out_top2
 
 
 def sf_ingest(stages: torch.Tensor, wall: torch.Tensor, out_durations: torch.Tensor | None = None,

@@ -31,7 +31,8 @@ def test_header_declares_the_boundary():
                                     "sf_frontier_lag", "sf_ingest", "sf_num_windows",
                                     "sf_rank_spread", "sf_read_xor", "sf_read_xor_pieces", "sf_route",
                                     "sf_strerror", "sf_version",
-                                    "sf_window_median", "sf_window_summary"]
+                                    "sf_window_lead_exposed", "sf_window_median",
+                                    "sf_window_summary"]
 
 
 def test_header_is_plain_c(tmp_path):
@@ -306,6 +307,31 @@ def test_summary_argument_checks(sf):
     assert call(top=D + 4) == sf.SF_EINVAL        # outputs overlap
 
 
+def test_lead_exposed_argument_checks(sf):
+    lib = sf.raw_library()
+    D = 4 << 40
+    ok_args = dict(inc=A, lead=B, T=100, R=8, S=6, window=10, le=C, top=D)
+
+    def call(**kw):
+        a = dict(ok_args, **kw)
+        return lib.sf_window_lead_exposed(a["inc"], a["lead"], a["T"], a["R"], a["S"],
+                                          a["window"], a["le"], a["top"], None)
+
+    assert call(T=0, inc=None, lead=None, le=None, top=None) == sf.SF_OK
+    assert call(window=0) == sf.SF_EINVAL
+    assert call(T=-5) == sf.SF_EINVAL
+    assert call(R=0) == sf.SF_EINVAL
+    assert call(R=sf.SF_MAX_R + 1) == sf.SF_EINVAL
+    assert call(S=sf.SF_MAX_S + 1) == sf.SF_EINVAL
+    assert call(le=None) == sf.SF_EINVAL
+    assert call(top=None) == sf.SF_EINVAL
+    assert call(le=C + 4) == sf.SF_EINVAL         # misaligned int64 output
+    assert call(top=D + 2) == sf.SF_EINVAL
+    assert call(le=B + 8) == sf.SF_EINVAL         # output overlaps input
+    assert call(top=C + 8) == sf.SF_EINVAL        # outputs overlap
+    assert call(T=1 << 40, R=65536, S=512, window=1) == sf.SF_EINVAL  # W*S*R*8 overflows
+
+
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     """The binding has no CPU fallback: a missing library is an ImportError."""
     import importlib
@@ -334,5 +360,6 @@ def test_ctypes_argtypes_cover_header(sf):
     assert len(lib.sf_window_median.argtypes) == 7
     assert len(lib.sf_route.argtypes) == 8
     assert len(lib.sf_window_summary.argtypes) == 10
+    assert len(lib.sf_window_lead_exposed.argtypes) == 9
     assert len(lib.sf_read_xor.argtypes) == 4
     assert lib.sf_num_windows.restype is ctypes.c_int64

@@ -203,6 +203,75 @@ def test_summary_ties_and_out_of_range_leaders(sf):
         assert_summary_equal(sf, inc, lead, R, window)
 
 
+def assert_lead_exposed_equal(sf, inc, lead, R, window):
+    ti = torch.from_numpy(np.ascontiguousarray(inc)).to(DEV)
+    tl = torch.from_numpy(np.ascontiguousarray(lead)).to(DEV)
+    le, top2 = sf.sf_window_lead_exposed(ti, tl, R, window)
+    torch.cuda.synchronize()
+    ole, ot = oracle.window_lead_exposed(inc, lead, R, window)
+    np.testing.assert_array_equal(le.cpu().numpy(), ole)
+    np.testing.assert_array_equal(top2.cpu().numpy(), ot)
+
+
+@pytest.mark.parametrize("R,S,T,window", [
+    (8, 6, 1000, 100), (8, 6, 1001, 100), (3, 1, 17, 4), (128, 6, 3000, 1000),
+    (1024, 8, 1200, 500), (5, 13, 40, 1), (4096, 12, 600, 250), (8192, 4, 90, 30),
+    (8193, 4, 90, 31), (16384, 12, 80, 7), (20000, 3, 50, 50), (65536, 2, 10, 3),
+    (7, 512, 70, 9)])
+def test_lead_exposed_from_oracle_steps(sf, R, S, T, window):
+    """Exposed time led and its top-2 on seeded per-step arrays: leaders
+    concentrated on a few ranks, every rank-chunk boundary of the weighted
+    histogram (8192 ranks), the largest stage count."""
+    rng = np.random.Generator(np.random.PCG64(R * 7 + S + T))
+    inc = rng.integers(0, 10**9, size=(T, S), dtype=np.int64)
+    hot = rng.integers(0, R, size=4)
+    lead = np.where(rng.random((T, S)) < 0.7, hot[rng.integers(0, 4, size=(T, S))],
+                    rng.integers(0, R, size=(T, S))).astype(np.int32)
+    print("case R=%d S=%d T=%d window=%d" % (R, S, T, window), flush=True)
+    assert_lead_exposed_equal(sf, inc, lead, R, window)
+
+
+def test_lead_exposed_ties_signs_and_out_of_range_leaders(sf):
+    """Stage-total ties, rank ties on exposed time, zero rows (rank -1),
+    negative advances (never a suspect) and leaders outside [0, R)."""
+    T, S, R = 60, 6, 9
+    inc = np.zeros((T, S), dtype=np.int64)
+    inc[:, 1] = 5
+    inc[:, 3] = 5                       # stages 1 and 3 tie on the total
+    inc[:, 5] = -3                      # negative advances
+    lead = np.tile(np.array([0, 4, 2, 7, 1, 3], dtype=np.int32), (T, 1))
+    lead[::2, 1] = 6                    # ranks 4 and 6 tie on exposed time
+    lead[::3, 0] = -1                   # not counted
+    lead[::5, 2] = 9                    # == R: not counted
+    lead[1::7, 4] = np.iinfo(np.int32).min
+    for window in (1, 6, 7, 60, 61):
+        assert_lead_exposed_equal(sf, inc, lead, R, window)
+    # every advance negative or zero: no rank is a suspect
+    assert_lead_exposed_equal(sf, -np.abs(inc), lead, R, 10)
+    # large magnitudes of both signs (exact two's-complement sums)
+    rng = np.random.Generator(np.random.PCG64(5))
+    big = rng.integers(-(1 << 52), 1 << 52, size=(64, 3), dtype=np.int64)
+    lead = rng.integers(0, 2, size=(64, 3), dtype=np.int32)
+    assert_lead_exposed_equal(sf, big, lead, 2, 16)
+
+
+def test_lead_exposed_after_frontier(sf):
+    """sf_frontier then sf_window_lead_exposed on the 8-rank workload and
+    on the stall pattern; the rows add up to the summary's stage totals."""
+    wl = synth.WORKLOADS["r8_s6_t1k"]
+    d = synth.generate(wl)
+    oi, ol = oracle.frontier(d)
+    dd = torch.from_numpy(d).to(DEV)
+    inc, lead = sf.sf_frontier(dd)
+    le, top2 = sf.sf_window_lead_exposed(inc, lead, wl.R, wl.window)
+    ex, _, _ = sf.sf_window_summary(inc, lead, wl.R, wl.window)
+    torch.cuda.synchronize()
+    ole, ot = oracle.window_lead_exposed(oi, ol, wl.R, wl.window)
+    np.testing.assert_array_equal(le.cpu().numpy(), ole)
+    np.testing.assert_array_equal(top2.cpu().numpy(), ot)
+    np.testing.assert_array_equal(le.sum(dim=2).cpu().numpy(), ex.cpu().numpy())
+
+
 def test_end_to_end_small_workload(sf):
     """sf_frontier then sf_window_summary, as the benchmark chains them."""
     wl = synth.WORKLOADS["r8_s6_t1k"]
@@ -688,6 +757,7 @@ def test_entry_points_on_a_side_stream(sf):
         med = sf.sf_window_median(dd, 8, stream=side)
         gain = sf.sf_exposure_gain(dd, med, 8, stream=side)
         ex, cnt, top2 = sf.sf_window_summary(inc, lead, R=300, window=8, stream=side)
+        le, letop2 = sf.sf_window_lead_exposed(inc, lead, R=300, window=8, stream=side)
         order, size = sf.sf_route(ex, stream=side)
     side.synchronize()
     np.testing.assert_array_equal(inc.cpu().numpy(), oi)
@@ -703,5 +773,8 @@ def test_entry_points_on_a_side_stream(sf):
     oe, oc, ot = oracle.window_summary(oi, ol, 300, 8)
     np.testing.assert_array_equal(ex.cpu().numpy(), oe)
     np.testing.assert_array_equal(top2.cpu().numpy(), ot)
+    ole, olt = oracle.window_lead_exposed(oi, ol, 300, 8)
+    np.testing.assert_array_equal(le.cpu().numpy(), ole)
+    np.testing.assert_array_equal(letop2.cpu().numpy(), olt)
     oo, os_ = oracle.route(oe)
     np.testing.assert_array_equal(order.cpu().numpy(), oo)

@@ -52,6 +52,7 @@ def test_workload_full_parity(sf, name):
     for t0, t1 in bounds:
         sf.sf_frontier(d[t0:t1], inc[t0:t1], lead[t0:t1])
     ex, cnt, top2 = sf.sf_window_summary(inc, lead, R, wl.window)
+    le, letop2 = sf.sf_window_lead_exposed(inc, lead, R, wl.window)
     torch.cuda.synchronize()
     log("gpu done")
     np.testing.assert_array_equal(inc.cpu().numpy(), oi)
@@ -59,6 +60,9 @@ def test_workload_full_parity(sf, name):
     np.testing.assert_array_equal(ex.cpu().numpy(), oe)
     np.testing.assert_array_equal(cnt.cpu().numpy(), oc)
     np.testing.assert_array_equal(top2.cpu().numpy(), ot)
+    ole, olt = oracle.window_lead_exposed(oi, ol, R, wl.window)
+    np.testing.assert_array_equal(le.cpu().numpy(), ole)
+    np.testing.assert_array_equal(letop2.cpu().numpy(), olt)
     # the workloads exercise what they are meant to: ties at the frontier
     # in the tie workload, leaders spread over ranks in the others
     if wl.tie_frac:
@@ -71,7 +75,7 @@ def test_workload_full_parity(sf, name):
                 P_ties += 1
         assert P_ties > 10
     log("parity ok: %s" % name)
-    del d, inc, lead, ex, cnt, top2
+    del d, inc, lead, ex, cnt, top2, le, letop2
     torch.cuda.empty_cache()
 
 
