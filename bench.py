@@ -640,6 +640,7 @@ def main() -> int:
         if want("route"):
             order = torch.empty((W, S), dtype=torch.int32, device=dev)
             size = torch.empty((W,), dtype=torch.int32, device=dev)
+            sf.sf_route(ex, 4, 5, order, size, stream=stream)  # untimed first launch
             rt = []
             for _ in range(max(3, args.steps // 2)):
                 a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -651,10 +652,62 @@ def main() -> int:
             next_rows["route"] = {
                 "kernel": "k_route",
                 "bound": "launch",
-                "launch_ms": float(np.mean([a.elapsed_time(b) for a, b in rt])),
+                "launch_ms": float(np.median([a.elapsed_time(b) for a, b in rt])),
                 "windows": W,
                 "candidate_sizes": np.bincount(size.cpu().numpy(), minlength=S + 1).tolist(),
             }
+
+        # next row: exposed time led per (window, stage, rank) and the top-2
+        # weighted by it, over the path's per-step outputs
+        if want("lead_exposed"):
+            le = torch.empty((W, S, R), dtype=torch.int64, device=dev)
+            le_top2 = torch.empty((W, 2, 2), dtype=torch.int32, device=dev)
+            sf.sf_window_lead_exposed(inc, lead, R, wl.window, le, le_top2, stream=stream)
+            lt = []
+            for _ in range(max(3, args.steps // 2)):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                sf.sf_window_lead_exposed(inc, lead, R, wl.window, le, le_top2, stream=stream)
+                b.record(stream)
+                lt.append((a, b))
+            torch.cuda.synchronize(dev)
+            le_ms = float(np.median([a.elapsed_time(b) for a, b in lt]))
+            # reads the advances twice and the leaders once, the two picked
+            # rows back; writes the table and the pairs
+            le_bytes = 20 * T * S + W * 2 * R * 8 + W * S * R * 8 + 16 * W
+            le_exact = le_cpu = None
+            if oracle_out and bit_exact:
+                import oracle
+                t0c, oi, ol = oracle_out[0]
+                n_chk = len(oi)
+                # the oracle's own advances and leaders of its first sampled
+                # steps (equal to the path's there) against the kernels run
+                # on those steps of the path's output
+                tc = time.perf_counter()
+                ole, olt = oracle.window_lead_exposed(oi, ol, R, wl.window)
+                secs = time.perf_counter() - tc
+                le_cpu = {"value": n_chk * S / secs, "unit": "step·stage advances/s", "cores": 1,
+                          "kind": "oracle",
+                          "sample": "oracle window_lead_exposed over the %d x %d advances of the "
+                                    "first %d steps (%.4f s)" % (n_chk, S, n_chk, secs)}
+                gle, glt = sf.sf_window_lead_exposed(inc[t0c:t0c + n_chk], lead[t0c:t0c + n_chk], R,
+                                                     wl.window, stream=stream)
+                torch.cuda.synchronize(dev)
+                le_exact = bool(np.array_equal(gle.cpu().numpy(), ole)
+                                and np.array_equal(glt.cpu().numpy(), olt))
+            next_rows["lead_exposed"] = {
+                "kernel": "k_window_lead_exposed + k_window_lead_top2",
+                "bound": "launch",
+                "launch_ms": le_ms,
+                "advances_per_s": T * S / (le_ms / 1e3),
+                "bytes_per_launch": le_bytes,
+                "gbps": le_bytes / (le_ms / 1e3) / 1e9,
+                "windows": W,
+                "top2_differs_from_count_top2": int((le_top2.cpu() != top2.cpu()).any(dim=2).sum()),
+                "bit_exact_first_steps": le_exact,
+                "cpu_baseline": le_cpu,
+            }
+            del le, le_top2
 
     # context: the launch-bound 8-rank workload (1000 steps), one step per
     # sf_frontier + sf_window_summary, issued eagerly and as replays of a
