@@ -33,6 +33,8 @@ def test_captured_path_replays(sf):
         "ex": torch.empty((W, S), dtype=torch.int64, device=DEV),
         "cnt": torch.empty((W, S, R), dtype=torch.int32, device=DEV),
         "top2": torch.empty((W, 2, 2), dtype=torch.int32, device=DEV),
+        "le": torch.empty((W, S, R), dtype=torch.int64, device=DEV),
+        "letop2": torch.empty((W, 2, 2), dtype=torch.int32, device=DEV),
         "lag": torch.empty((T, S), dtype=torch.int64, device=DEV),
         "laginc": torch.empty((T, S), dtype=torch.int64, device=DEV),
         "med": torch.empty((W, S, R), dtype=torch.int64, device=DEV),
@@ -46,6 +48,8 @@ def test_captured_path_replays(sf):
         sf.sf_frontier(d_in, out["inc"], out["lead"], stream=stream)
         sf.sf_window_summary(out["inc"], out["lead"], R, window, out["ex"], out["cnt"], out["top2"],
                              stream=stream)
+        sf.sf_window_lead_exposed(out["inc"], out["lead"], R, window, out["le"], out["letop2"],
+                                  stream=stream)
         sf.sf_frontier_lag(d_in, out["lag"], out["laginc"], stream=stream)
         sf.sf_window_median(d_in, window, out["med"], stream=stream)
         sf.sf_exposure_gain(d_in, out["med"], window,
@@ -84,6 +88,9 @@ def test_captured_path_replays(sf):
         np.testing.assert_array_equal(out["ex"].cpu().numpy(), oe)
         np.testing.assert_array_equal(out["cnt"].cpu().numpy(), oc)
         np.testing.assert_array_equal(out["top2"].cpu().numpy(), ot)
+        ole, olt = oracle.window_lead_exposed(oi, ol, R, window)
+        np.testing.assert_array_equal(out["le"].cpu().numpy(), ole)
+        np.testing.assert_array_equal(out["letop2"].cpu().numpy(), olt)
         np.testing.assert_array_equal(out["lag"].cpu().numpy(), olag)
         np.testing.assert_array_equal(out["laginc"].cpu().numpy(), olaginc)
         np.testing.assert_array_equal(out["med"].cpu().numpy(), om)

@@ -56,6 +56,7 @@ def test_random_shape(sf, seed):
         if t1 > t0:
             sf.sf_frontier(dd[t0:t1], inc[t0:t1], lead[t0:t1])
     ex, cnt, top2 = sf.sf_window_summary(inc, lead, R, window)
+    le, letop2 = sf.sf_window_lead_exposed(inc, lead, R, window)
     cinc, clead, st = sf.sf_frontier_checked(dd)
     ev = sf.sf_frontier_evidence(dd)
     torch.cuda.synchronize()
@@ -68,6 +69,9 @@ def test_random_shape(sf, seed):
     np.testing.assert_array_equal(ex.cpu().numpy(), oe)
     np.testing.assert_array_equal(cnt.cpu().numpy(), oc)
     np.testing.assert_array_equal(top2.cpu().numpy(), ot)
+    ole, olt = oracle.window_lead_exposed(oi, ol, R, window)
+    np.testing.assert_array_equal(le.cpu().numpy(), ole)
+    np.testing.assert_array_equal(letop2.cpu().numpy(), olt)
     oev = oracle.frontier_evidence(d)
     for k, ok in (("gap", "gap"), ("ties", "ties"), ("stage_max", "stage_max"),
                   ("stage_sum", "stage_sum")):
