@@ -52,6 +52,8 @@ class COracle:
         lib.sfo_window_summary.restype = None
         lib.sfo_window_lead_exposed.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp]
         lib.sfo_window_lead_exposed.restype = None
+        lib.sfo_window_leader_switches.argtypes = [vp, vp, vp, i64, i32, i64, i64, vp, vp]
+        lib.sfo_window_leader_switches.restype = None
         lib.sfo_frontier_evidence.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp]
         lib.sfo_frontier_evidence.restype = ctypes.c_int
         lib.sfo_ingest.argtypes = [vp, vp, i64, i32, i32, vp, vp]
@@ -110,6 +112,27 @@ class COracle:
             if rc != 0:
                 raise MemoryError("oracle prefix scratch allocation failed")
         return out
+
+    def window_leader_switches(self, lead: np.ndarray, gap: np.ndarray, ties: np.ndarray,
+                               window: int, min_gap: int = 0):
+        """Leader switches between confident unique leaders per window and
+        stage (Sec. 4 localization evidence).  ``lead``, ``ties`` int32 and
+        ``gap`` int64, all [T, S] (as from ``frontier_evidence``).
+
+        Returns ``(switches [W,S] int32, eligible [W,S] int32)``.
+        """
+        lead = np.ascontiguousarray(lead, dtype=np.int32)
+        gap = np.ascontiguousarray(gap, dtype=np.int64)
+        ties = np.ascontiguousarray(ties, dtype=np.int32)
+        T, S = lead.shape
+        assert gap.shape == (T, S) and ties.shape == (T, S)
+        W = num_windows(T, window)
+        sw = np.empty((W, S), dtype=np.int32)
+        el = np.empty((W, S), dtype=np.int32)
+        if W:
+            self.lib.sfo_window_leader_switches(lead.ctypes.data, gap.ctypes.data, ties.ctypes.data,
+                                                T, S, window, min_gap, sw.ctypes.data, el.ctypes.data)
+        return sw, el
 
     def ingest(self, x: np.ndarray, w: np.ndarray):
         """Appendix A closure and the transpose to [T][S][R].
@@ -270,6 +293,10 @@ def _get() -> COracle:
 
 def frontier(d: np.ndarray):
     return _get().frontier(d)
+
+
+def window_leader_switches(lead, gap, ties, window: int, min_gap: int = 0):
+    return _get().window_leader_switches(lead, gap, ties, window, min_gap)
 
 
 def window_lead_exposed(inc: np.ndarray, lead: np.ndarray, R: int, window: int):

@@ -84,6 +84,27 @@ def window_lead_exposed(inc, lead, R, window):
     return out, top2
 
 
+def window_leader_switches(lead, gap, ties, window, min_gap=0):
+    """Returns ``(switches[w][s], eligible[w][s])``: per window and stage,
+    the qualifying boundaries (a single rank at the frontier, ahead by at
+    least min_gap, or with no runner-up) and how often their leader changes
+    from one qualifying boundary to the next."""
+    T = len(lead)
+    S = len(lead[0]) if T else 0
+    W = (T + window - 1) // window
+    switches, eligible = [], []
+    for w in range(W):
+        sw_w, el_w = [], []
+        for s in range(S):
+            seq = [lead[t][s] for t in range(w * window, min((w + 1) * window, T))
+                   if ties[t][s] == 1 and (gap[t][s] >= min_gap or gap[t][s] < 0)]
+            el_w.append(len(seq))
+            sw_w.append(sum(1 for a, b in zip(seq, seq[1:]) if a != b))
+        switches.append(sw_w)
+        eligible.append(el_w)
+    return switches, eligible
+
+
 def frontier_evidence(d):
     """``d[t][s][r]`` -> dict of [t][s] lists: inc, lead, gap, ties,
     stage_max, stage_sum (same readings as the C oracle)."""

@@ -44,6 +44,11 @@
  *   window's advances of that stage whose leader is that rank; the top-2
  *   suspects weighted this way pair the two stages of the window summary
  *   with the rank that led the most exposed time of each.
+ *   Sec. 4 and App. C, leader switches: per window and stage, the number
+ *   of times the leader changes between consecutive confident unique
+ *   leaders (boundaries whose frontier is attained by one rank only, ahead
+ *   of the runner-up by at least a caller-given gap), and how many
+ *   boundaries qualify.
  *   Sec. 3, the data contract: durations are nonnegative; with the
  *   library's packed keys every prefix must also stay below 2^47 ns.  The
  *   range status is 2 (SF_ERANGE) when some d < 0 or some prefix of
@@ -77,9 +82,16 @@
  *     (over ranks, and over the n steps of a window: rank floor((n-1)/2));
  *   - the routing set orders stages like top-2 (exposed total descending,
  *     lower stage first) and compares shares exactly: k stages suffice when
- *     tau_den * (their exposed sum) >= tau_num * (window total).
+ *     tau_den * (their exposed sum) >= tau_num * (window total);
+ *   - a boundary's leader is confident and unique when its tie-set size is
+ *     1 and its gap is at least min_gap (a gap of -1, R = 1, has no
+ *     runner-up and qualifies); switches are counted between consecutive
+ *     qualifying boundaries of the same stage inside one window (each
+ *     window starts afresh), and the paper's switch-rate gates, whose
+ *     values it does not state, are left to the caller.
  *
- * Layout: d is [T][S][R] (rank fastest), increments and leaders [T][S],
+ * Layout: d is [T][S][R] (rank fastest), increments, leaders, gaps and tie
+ * counts [T][S], switch and eligible counts [W][S],
  * exposed [W][S], counts and exposed time led [W][S][R], top2 [W][2][2],
  * route order [W][S] and route size [W].
  *
@@ -232,6 +244,38 @@ void sfo_window_lead_exposed(const int64_t* inc, const int32_t* lead, int64_t T,
             }
             top2[w * 4 + 2 * k + 0] = sk;
             top2[w * 4 + 2 * k + 1] = rk;
+        }
+    }
+}
+
+/* Leader switches between confident unique leaders, per window and stage.
+ * A boundary (t, s) qualifies when ties[t][s] == 1 and (gap[t][s] >= min_gap
+ * or gap[t][s] < 0).  eligible[w][s] counts the qualifying boundaries of
+ * window w; switches[w][s] counts those whose leader differs from the
+ * leader of the previous qualifying boundary of the same stage and window. */
+void sfo_window_leader_switches(const int32_t* lead, const int64_t* gap, const int32_t* ties,
+                                int64_t T, int32_t S, int64_t window, int64_t min_gap,
+                                int32_t* switches, int32_t* eligible)
+{
+    int64_t W = (T + window - 1) / window;
+    for (int64_t w = 0; w < W; ++w) {
+        int64_t t0 = w * window;
+        int64_t t1 = t0 + window < T ? t0 + window : T;
+        for (int32_t s = 0; s < S; ++s) {
+            int32_t n_sw = 0, n_el = 0;
+            int32_t prev = 0;
+            int have_prev = 0;
+            for (int64_t t = t0; t < t1; ++t) {
+                const int64_t i = t * S + s;
+                const int confident = ties[i] == 1 && (gap[i] >= min_gap || gap[i] < 0);
+                if (!confident) continue;
+                n_el += 1;
+                if (have_prev && lead[i] != prev) n_sw += 1;
+                prev = lead[i];
+                have_prev = 1;
+            }
+            switches[w * S + s] = n_sw;
+            eligible[w * S + s] = n_el;
         }
     }
 }

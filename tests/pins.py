@@ -596,6 +596,150 @@ LEAD_PINS = [pin_lead_golden, pin_lead_stall, pin_lead_single_rank, pin_lead_mas
 
 
 # ----------------------------------------------------------------------------
+# leader switches between confident unique leaders (Sec. 4 localization
+# evidence)
+
+
+def _switches_by_runs(lead, gap, ties, window, min_gap):
+    """The definition restated through runs: in each window the qualifying
+    leaders of a stage, in step order, form maximal runs of equal ranks; the
+    switches are the runs minus one (0 when nothing qualifies)."""
+    T, S = lead.shape
+    W = -(-T // window)
+    sw = np.zeros((W, S), dtype=np.int64)
+    el = np.zeros((W, S), dtype=np.int64)
+    for w in range(W):
+        for s in range(S):
+            seq = [int(lead[t, s]) for t in range(w * window, min((w + 1) * window, T))
+                   if ties[t, s] == 1 and (gap[t, s] >= min_gap or gap[t, s] < 0)]
+            runs = len([k for k, _ in itertools.groupby(seq)])
+            el[w, s] = len(seq)
+            sw[w, s] = max(runs - 1, 0)
+    return sw, el
+
+
+def pin_switch_stall(e, sw):
+    """The Sec. 2 stall on every other step of ten: the stalled steps have a
+    unique data leader 30 ms ahead of the other three ranks, the clean steps
+    are four-way ties and never qualify.  One stalled rank: no switch; the
+    stall alternating between ranks 1 and 2: a switch at every qualifying
+    step after the first; a gap threshold above 30 ms: nothing qualifies."""
+    d = np.repeat(stall_case(), 10, axis=0)
+    d[1::2, 0, 2] -= 30 * MS           # clean on odd steps
+    d[1::2, 2, [0, 1, 3]] -= 30 * MS
+    ev = e(d)
+    n, el = sw(ev["lead"], ev["gap"], ev["ties"], 10, 0)
+    assert el[0, 0] == 5 and n[0, 0] == 0
+    # backward: a four-way tie at every step (also where the wait absorbs
+    # the stall), so nothing qualifies
+    assert el[0, 2] == 0 and n[0, 2] == 0
+    d2 = d.copy()
+    for t in (2, 6):                   # the stall moves to rank 1 there
+        d2[t, 0, 2] -= 30 * MS
+        d2[t, 0, 1] += 30 * MS
+        d2[t, 2, 2] += 30 * MS
+        d2[t, 2, 1] -= 30 * MS
+    ev2 = e(d2)
+    n2, el2 = sw(ev2["lead"], ev2["gap"], ev2["ties"], 10, 0)
+    assert ev2["lead"][::2, 0].tolist() == [2, 1, 2, 1, 2]
+    assert el2[0, 0] == 5 and n2[0, 0] == 4
+    # two windows of five steps: the seam between them drops one switch
+    n5, el5 = sw(ev2["lead"], ev2["gap"], ev2["ties"], 5, 0)
+    assert el5[:, 0].tolist() == [3, 2] and n5[:, 0].tolist() == [2, 1]
+    n3, el3 = sw(ev2["lead"], ev2["gap"], ev2["ties"], 10, 30 * MS + 1)
+    assert el3[0, 0] == 0 and n3[0, 0] == 0
+    n4, el4 = sw(ev2["lead"], ev2["gap"], ev2["ties"], 10, 30 * MS)
+    assert el4[0, 0] == 5 and n4[0, 0] == 4
+
+
+def pin_switch_runs(e, sw):
+    """Against the run-count restatement on random evidence arrays (ties and
+    gaps drawn so that about half the boundaries qualify), several windows
+    and thresholds, and against numpy's diff on the qualifying leaders."""
+    rng = np.random.Generator(np.random.PCG64(18))
+    for (T, S) in [(1, 1), (7, 3), (50, 6), (129, 2), (300, 12)]:
+        lead = rng.integers(0, 4, size=(T, S), dtype=np.int32)
+        ties = rng.choice(np.array([1, 1, 1, 2, 3], dtype=np.int32), size=(T, S))
+        gap = np.where(ties == 1, rng.integers(-1, 100, size=(T, S)), 0).astype(np.int64)
+        for window in (1, 4, 7, T, T + 5):
+            for min_gap in (0, 1, 50, 99, 100):
+                n, el = sw(lead, gap, ties, window, min_gap)
+                rn, rel = _switches_by_runs(lead, gap, ties, window, min_gap)
+                assert np.array_equal(n, rn) and np.array_equal(el, rel)
+                for w in range(n.shape[0]):
+                    t0, t1 = w * window, min((w + 1) * window, T)
+                    for s in range(S):
+                        m = (ties[t0:t1, s] == 1) & ((gap[t0:t1, s] >= min_gap) | (gap[t0:t1, s] < 0))
+                        q = lead[t0:t1, s][m]
+                        assert n[w, s] == np.count_nonzero(np.diff(q))
+                        assert el[w, s] == m.sum()
+
+
+def pin_switch_bruteforce(e, sw):
+    """Every leader pattern in {0,1,2}^6 with every qualifying mask of one
+    stage: the switches are the boundaries where the qualifying leader
+    changes, counted by hand."""
+    T = 6
+    for flat in itertools.product(range(3), repeat=T):
+        lead = np.array(flat, dtype=np.int32).reshape(T, 1)
+        for mask in range(1 << T):
+            q = np.array([(mask >> t) & 1 for t in range(T)], dtype=bool).reshape(T, 1)
+            ties = np.where(q, 1, 2).astype(np.int32)
+            gap = np.where(q, 5, 0).astype(np.int64)
+            n, el = sw(lead, gap, ties, 3, 1)
+            for w in range(2):
+                chosen = [flat[t] for t in range(3 * w, 3 * w + 3) if q[t, 0]]
+                want = sum(1 for i in range(1, len(chosen)) if chosen[i] != chosen[i - 1])
+                assert n[w, 0] == want and el[w, 0] == len(chosen)
+
+
+def pin_switch_invariants(e, sw):
+    """R = 1 qualifies every boundary (no runner-up) and never switches;
+    switches < eligible whenever something qualifies; relabelling the
+    leaders changes nothing; a larger threshold never adds qualifying
+    boundaries; at threshold 0 every unique leader qualifies; windows add up
+    in the eligible counts, and joining windows adds at most one switch per
+    seam."""
+    for d in random_cases(19):
+        T, S, R = d.shape
+        ev = e(d)
+        lead, gap, ties = ev["lead"], ev["gap"], ev["ties"]
+        n, el = sw(lead, gap, ties, T, 0)
+        if R == 1:
+            assert (el == T).all() and (n == 0).all()
+        assert np.array_equal(el[0], (ties == 1).sum(axis=0))
+        assert ((n < el) | ((n == 0) & (el == 0))).all()
+        perm = np.random.Generator(np.random.PCG64(R)).permutation(R).astype(np.int32)
+        n2, el2 = sw(perm[lead], gap, ties, T, 0)
+        assert np.array_equal(n, n2) and np.array_equal(el, el2)
+        prev = el
+        for g in (1, 10, 10**6, 10**9):
+            _, elg = sw(lead, gap, ties, T, g)
+            assert (elg <= prev).all()
+            prev = elg
+        if T >= 4:
+            half = -(-T // 2)
+            nh, elh = sw(lead, gap, ties, half, 0)
+            assert np.array_equal(elh.sum(axis=0), el[0])
+            assert (nh.sum(axis=0) <= n[0]).all() and (n[0] <= nh.sum(axis=0) + 1).all()
+
+
+def pin_switch_twin(e, sw, pyref):
+    for d in random_cases(21):
+        small = d[:12]
+        ev = e(small)
+        T, S, _ = small.shape
+        for window, min_gap in ((3, 0), (5, 7), (12, 10**8)):
+            n, el = sw(ev["lead"], ev["gap"], ev["ties"], window, min_gap)
+            pn, pel = pyref.window_leader_switches(ev["lead"].tolist(), ev["gap"].tolist(),
+                                                   ev["ties"].tolist(), window, min_gap)
+            assert n.tolist() == pn and el.tolist() == pel
+
+
+SWITCH_PINS = [pin_switch_stall, pin_switch_runs, pin_switch_bruteforce, pin_switch_invariants]
+
+
+# ----------------------------------------------------------------------------
 # localization evidence and per-stage baselines (Sec. 4; Props. 1-2)
 #
 # Each pin takes ``e(d) -> dict`` with [T, S] arrays inc, lead, gap, ties,

@@ -62,6 +62,19 @@ MUTANTS = {
     "le_rank_tie_to_higher": ("sfo_window_lead_exposed", "if (e[r] > best) {",
                               "if (e[r] >= best && e[r] > 0) {"),
     "le_rank_first_nonzero": ("sfo_window_lead_exposed", "best = e[r];", "best = INT64_MAX;"),
+    # leader switches between confident unique leaders
+    "sw_ties_not_unique": ("sfo_window_leader_switches", "ties[i] == 1 &&", "ties[i] >= 1 &&"),
+    "sw_gap_strict": ("sfo_window_leader_switches", "gap[i] >= min_gap", "gap[i] > min_gap"),
+    "sw_single_rank_not_confident": ("sfo_window_leader_switches", " || gap[i] < 0", ""),
+    "sw_prev_not_updated": ("sfo_window_leader_switches", "prev = lead[i];\n", ""),
+    "sw_prev_from_any_boundary": ("sfo_window_leader_switches", "if (!confident) continue;",
+                                  "if (!confident) { prev = lead[i]; have_prev = 1; continue; }"),
+    "sw_eligible_counts_all": ("sfo_window_leader_switches",
+                               "if (!confident) continue;\n                n_el += 1;",
+                               "n_el += 1;\n                if (!confident) continue;"),
+    "sw_first_compares_rank0": ("sfo_window_leader_switches", "int have_prev = 0;", "int have_prev = 1;"),
+    "sw_short_window": ("sfo_window_leader_switches", "int64_t t1 = t0 + window < T ? t0 + window : T;",
+                        "int64_t t1 = t0 + window < T ? t0 + window - 1 : T;"),
     # localization evidence and baselines
     "ev_tie_to_highest_rank": ("sfo_frontier_evidence", "if (P[r] > F) {", "if (P[r] >= F) {"),
     "ev_no_prefix_reset": ("sfo_frontier_evidence", "for (int32_t r = 0; r < R; ++r) P[r] = 0;", ""),
@@ -174,6 +187,11 @@ def _run_all(o):
         pins.pin_lead_top2_cases(o.frontier, o.window_lead_exposed, o.window_summary)
     except AssertionError:
         failed.append("pin_lead_top2_cases")
+    for pin in pins.SWITCH_PINS:
+        try:
+            pin(o.frontier_evidence, o.window_leader_switches)
+        except AssertionError:
+            failed.append(pin.__name__)
     for pin in pins.EVIDENCE_PINS:
         try:
             pin(o.frontier_evidence)

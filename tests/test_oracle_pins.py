@@ -34,6 +34,15 @@ def test_evidence_pin(pin):
     pin(oracle.frontier_evidence)
 
 
+@pytest.mark.parametrize("pin", pins.SWITCH_PINS, ids=lambda p: p.__name__)
+def test_switch_pin(pin):
+    pin(oracle.frontier_evidence, oracle.window_leader_switches)
+
+
+def test_twin_switches():
+    pins.pin_switch_twin(oracle.frontier_evidence, oracle.window_leader_switches, oracle.pyref)
+
+
 def test_twin_evidence():
     pins.pin_ev_twin(oracle.frontier_evidence, oracle.pyref)
 
