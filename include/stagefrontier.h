@@ -365,6 +365,37 @@ int sf_window_lead_exposed(const int64_t* increment, const int32_t* leader, int6
                            int32_t* out_top2, sf_stream_t stream);
 
 /*
+ * sf_window_leader_switches -- leader-switch evidence of Sec. 4: per window
+ * and stage, how often the frontier's leader changes, counted only between
+ * confident unique leaders.  A boundary (t, s) qualifies when one rank
+ * alone attains F[t][s] (tie-set size 1) and leads the runner-up by at least
+ * min_gap ns (a boundary with no runner-up, R == 1, qualifies).  The paper's
+ * gates on the switch rate and on the qualifying fraction (App. C) state no
+ * values; they are left to the caller, who has both counts.
+ *
+ *   leader         [T][S] int32 (out_leader of sf_frontier_evidence).
+ *   gap            [T][S] int64 (out_gap of sf_frontier_evidence).
+ *   ties           [T][S] int32 (out_ties of sf_frontier_evidence).
+ *   T, S, window   0 <= T, 1 <= S <= SF_MAX_S, 1 <= window, and
+ *                  min(window, T) <= INT32_MAX.  T == 0 is a no-op.
+ *                  Window w covers steps [w*window, min((w+1)*window, T)).
+ *   min_gap        the confidence threshold on the gap, ns.
+ *   out_switches   [W][S] int32: the qualifying boundaries of window w and
+ *                  stage s whose leader differs from the leader of the
+ *                  previous qualifying boundary of the same stage and
+ *                  window (each window starts afresh).
+ *   out_eligible   [W][S] int32: the qualifying boundaries of window w and
+ *                  stage s.  out_switches <= max(out_eligible - 1, 0).
+ *   stream         HIP stream.
+ *
+ * Pointers aligned to their element size; outputs must not overlap inputs
+ * or each other.  Returns SF_OK, SF_EINVAL or SF_EHIP.
+ */
+int sf_window_leader_switches(const int32_t* leader, const int64_t* gap, const int32_t* ties,
+                              int64_t T, int32_t S, int64_t window, int64_t min_gap,
+                              int32_t* out_switches, int32_t* out_eligible, sf_stream_t stream);
+
+/*
  * sf_read_xor -- plain-read calibration (a measurement aid, not part of the
  * paper's method): the XOR of the 64-bit words of every SF_XOR_PIECE_BYTES
  * piece of a device buffer.  It reads each byte exactly once with the

@@ -1,8 +1,10 @@
 // window.hip -- sf_window_summary and sf_num_windows: window sums of the
 // advances (Eq. (2) numerators), leader counts and top-2 routing (Sec. 4);
 // sf_window_lead_exposed: the exposed time each rank led (every advance
-// attributed to its leader, Sec. 3) and the top-2 weighted by it; and the
-// generic window sum used by sf_exposure_gain.
+// attributed to its leader, Sec. 3) and the top-2 weighted by it;
+// sf_window_leader_switches: leader switches between confident unique
+// leaders (Sec. 4 localization evidence); and the generic window sum used
+// by sf_exposure_gain.
 //
 // Window kernels.  One workgroup per (window, stage, rank chunk) builds the
 // leader histogram of the window in LDS with LDS atomics and sums the
@@ -242,6 +244,59 @@ __global__ __launch_bounds__(kTopWG) void k_window_lead_top2(
     }
 }
 
+// Leader switches between confident unique leaders: one wave per (window,
+// stage), walking the window 64 steps at a time.  A ballot marks the
+// qualifying boundaries; each lane takes the leader of the nearest
+// qualifying lane below it (or, for the lowest one, the last qualifying
+// leader of the previous 64 steps) and a second ballot counts the changes.
+// Every count is wave-uniform, so the lanes need no LDS and no barrier.
+constexpr int kSwWG = 256;
+
+__global__ __launch_bounds__(kSwWG) void k_window_switches(
+    const int32_t* __restrict__ lead, const int64_t* __restrict__ gap,
+    const int32_t* __restrict__ ties, int64_t T, int S, int64_t window, int64_t W,
+    int64_t min_gap, int32_t* __restrict__ switches, int32_t* __restrict__ eligible)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t waves = (int64_t)gridDim.x * (kSwWG / 64);
+    for (int64_t id = (int64_t)blockIdx.x * (kSwWG / 64) + (threadIdx.x >> 6); id < W * S;
+         id += waves) {
+        const int64_t w = id / S;
+        const int s = (int)(id - w * S);
+        const int64_t t0 = w * window;
+        const int64_t t1 = min(t0 + window, T);
+        int32_t n_sw = 0, n_el = 0;
+        int32_t carry = 0;  // the last qualifying leader so far
+        bool have = false;  // whether there is one
+        for (int64_t tb = t0; tb < t1; tb += 64) {
+            const int64_t t = tb + lane;
+            bool q = false;
+            int32_t ld = 0;
+            if (t < t1) {
+                const int64_t i = t * S + s;
+                ld = lead[i];
+                const int64_t g = gap[i];
+                q = ties[i] == 1 && (g >= min_gap || g < 0);
+            }
+            const u64 m = __ballot(q);
+            const u64 below = m & ((1ull << lane) - 1ull);
+            const int32_t pv = __shfl(ld, below ? 63 - __clzll((long long)below) : 0, 64);
+            const bool has_prev = below != 0 || have;
+            const int32_t prev = below ? pv : carry;
+            n_sw += __popcll(__ballot(q && has_prev && prev != ld));
+            n_el += __popcll(m);
+            if (m) {
+                carry = __shfl(ld, 63 - __clzll((long long)m), 64);
+                have = true;
+            }
+        }
+        if (lane == 0) {
+            switches[id] = n_sw;
+            eligible[id] = n_el;
+        }
+    }
+}
+
 // Segmented sums over windows of the columns of a [T][C] int64 array: one
 // workgroup per (window, column); grid-stride.
 __global__ __launch_bounds__(kSumWG) void k_window_sum(const int64_t* __restrict__ x, int64_t T,
@@ -362,5 +417,35 @@ SF_API int sf_window_lead_exposed(const int64_t* increment, const int32_t* leade
     void* a2[] = {(void*)&increment, (void*)&le, (void*)&T, (void*)&Ri, (void*)&Si,
                   (void*)&window, (void*)&Wl, (void*)&out_top2};
     return launch(reinterpret_cast<const void*>(&k_window_lead_top2), dim3(g2), dim3(kTopWG), a2, 0,
+                  stream);
+}
+
+SF_API int sf_window_leader_switches(const int32_t* leader, const int64_t* gap,
+                                     const int32_t* ties, int64_t T, int32_t S, int64_t window,
+                                     int64_t min_gap, int32_t* out_switches,
+                                     int32_t* out_eligible, sf_stream_t stream)
+{
+    if (T < 0 || S < 1 || S > SF_MAX_S || window < 1) return SF_EINVAL;
+    if (!fits(T, S, 1, 8)) return SF_EINVAL;
+    if (T == 0) return SF_OK;
+    if ((window < T ? window : T) > INT32_MAX) return SF_EINVAL;  // int32 counts
+    const int64_t W = sf_num_windows(T, window);
+    if (!leader || !gap || !ties || !out_switches || !out_eligible) return SF_EINVAL;
+    if (!aligned(leader, 4) || !aligned(gap, 8) || !aligned(ties, 4) || !aligned(out_switches, 4) ||
+        !aligned(out_eligible, 4))
+        return SF_EINVAL;
+    const void* bufs[5] = {leader, gap, ties, out_switches, out_eligible};
+    const int64_t sizes[5] = {T * S * 4, T * S * 8, T * S * 4, W * S * 4, W * S * 4};
+    for (int a = 0; a < 5; ++a)
+        for (int b = (a < 3 ? 3 : a + 1); b < 5; ++b)
+            if (!disjoint(bufs[a], sizes[a], bufs[b], sizes[b])) return SF_EINVAL;
+
+    const int64_t blocks = (W * S + kSwWG / 64 - 1) / (kSwWG / 64);
+    const unsigned g = (unsigned)(blocks < 65536 ? blocks : 65536);
+    int Si = S;
+    int64_t Wl = W;
+    void* a[] = {(void*)&leader, (void*)&gap, (void*)&ties, (void*)&T, (void*)&Si, (void*)&window,
+                 (void*)&Wl, (void*)&min_gap, (void*)&out_switches, (void*)&out_eligible};
+    return launch(reinterpret_cast<const void*>(&k_window_switches), dim3(g), dim3(kSwWG), a, 0,
                   stream);
 }

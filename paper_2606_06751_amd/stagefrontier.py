@@ -68,6 +68,8 @@ def _load() -> ctypes.CDLL:
     lib.sf_window_summary.restype = ctypes.c_int
     lib.sf_window_lead_exposed.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp]
     lib.sf_window_lead_exposed.restype = ctypes.c_int
+    lib.sf_window_leader_switches.argtypes = [vp, vp, vp, i64, i32, i64, i64, vp, vp, vp]
+    lib.sf_window_leader_switches.restype = ctypes.c_int
     lib.sf_strerror.argtypes = [ctypes.c_int]
     lib.sf_strerror.restype = ctypes.c_char_p
     lib.sf_version.argtypes = []
@@ -265,6 +267,40 @@ def sf_window_lead_exposed(increment: torch.Tensor, leader: torch.Tensor, R: int
     if rc != SF_OK:
         raise StageFrontierError(rc, "sf_window_lead_exposed")
     return out_lead_exposed, out_top2
+
+
+def sf_window_leader_switches(leader: torch.Tensor, gap: torch.Tensor, ties: torch.Tensor,
+                              window: int, min_gap: int = 0,
+                              out_switches: torch.Tensor | None = None,
+                              out_eligible: torch.Tensor | None = None, stream=None):
+    """Leader switches between confident unique leaders, per window and
+    stage (``sf_window_leader_switches``); the inputs are the ``leader``,
+    ``gap`` and ``ties`` outputs of ``sf_frontier_evidence``.
+
+    Returns ``(out_switches [W, S] int32, out_eligible [W, S] int32)``.
+    """
+    if leader.dim() != 2:
+        raise ValueError("leader must be [T, S]")
+    T, S = leader.shape
+    _check(leader, "leader", torch.int32, (T, S))
+    _check(gap, "gap", torch.int64, (T, S), like=leader)
+    _check(ties, "ties", torch.int32, (T, S), like=leader)
+    W = sf_num_windows(T, window)
+    if W < 0:
+        raise StageFrontierError(SF_EINVAL, "sf_window_leader_switches")
+    dev = leader.device
+    if out_switches is None:
+        out_switches = torch.empty((W, S), dtype=torch.int32, device=dev)
+    if out_eligible is None:
+        out_eligible = torch.empty((W, S), dtype=torch.int32, device=dev)
+    _check(out_switches, "out_switches", torch.int32, (W, S), like=leader)
+    _check(out_eligible, "out_eligible", torch.int32, (W, S), like=leader)
+    rc = _lib.sf_window_leader_switches(leader.data_ptr(), gap.data_ptr(), ties.data_ptr(), T, S,
+                                        window, min_gap, out_switches.data_ptr(),
+                                        out_eligible.data_ptr(), _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_window_leader_switches")
+    return out_switches, out_eligible
 
 
 def sf_ingest(stages: torch.Tensor, wall: torch.Tensor, out_durations: torch.Tensor | None = None,

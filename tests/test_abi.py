@@ -31,7 +31,8 @@ def test_header_declares_the_boundary():
                                     "sf_frontier_lag", "sf_ingest", "sf_num_windows",
                                     "sf_rank_spread", "sf_read_xor", "sf_read_xor_pieces", "sf_route",
                                     "sf_strerror", "sf_version",
-                                    "sf_window_lead_exposed", "sf_window_median",
+                                    "sf_window_lead_exposed", "sf_window_leader_switches",
+                                    "sf_window_median",
                                     "sf_window_summary"]
 
 
@@ -332,6 +333,31 @@ def test_lead_exposed_argument_checks(sf):
     assert call(T=1 << 40, R=65536, S=512, window=1) == sf.SF_EINVAL  # W*S*R*8 overflows
 
 
+def test_leader_switches_argument_checks(sf):
+    lib = sf.raw_library()
+    D = 4 << 40
+    E = 5 << 40
+    ok_args = dict(lead=A, gap=B, ties=C, T=100, S=6, window=10, g=0, sw=D, el=E)
+
+    def call(**kw):
+        a = dict(ok_args, **kw)
+        return lib.sf_window_leader_switches(a["lead"], a["gap"], a["ties"], a["T"], a["S"],
+                                             a["window"], a["g"], a["sw"], a["el"], None)
+
+    assert call(T=0, lead=None, gap=None, ties=None, sw=None, el=None) == sf.SF_OK
+    assert call(window=0) == sf.SF_EINVAL
+    assert call(T=-1) == sf.SF_EINVAL
+    assert call(S=0) == sf.SF_EINVAL
+    assert call(S=sf.SF_MAX_S + 1) == sf.SF_EINVAL
+    assert call(ties=None) == sf.SF_EINVAL
+    assert call(el=None) == sf.SF_EINVAL
+    assert call(gap=B + 4) == sf.SF_EINVAL        # misaligned int64 input
+    assert call(sw=D + 2) == sf.SF_EINVAL
+    assert call(sw=C + 8) == sf.SF_EINVAL         # output overlaps an input
+    assert call(el=D + 8) == sf.SF_EINVAL         # outputs overlap
+    assert call(T=1 << 32, S=1, window=1 << 32) == sf.SF_EINVAL  # counts past int32
+
+
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     """The binding has no CPU fallback: a missing library is an ImportError."""
     import importlib
@@ -361,5 +387,6 @@ def test_ctypes_argtypes_cover_header(sf):
     assert len(lib.sf_route.argtypes) == 8
     assert len(lib.sf_window_summary.argtypes) == 10
     assert len(lib.sf_window_lead_exposed.argtypes) == 9
+    assert len(lib.sf_window_leader_switches.argtypes) == 10
     assert len(lib.sf_read_xor.argtypes) == 4
     assert lib.sf_num_windows.restype is ctypes.c_int64

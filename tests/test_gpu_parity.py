@@ -272,6 +272,57 @@ def test_lead_exposed_after_frontier(sf):
     np.testing.assert_array_equal(le.sum(dim=2).cpu().numpy(), ex.cpu().numpy())
 
 
+def assert_switches_equal(sf, lead, gap, ties, window, min_gap):
+    tl, tg, tt = (torch.from_numpy(np.ascontiguousarray(a)).to(DEV) for a in (lead, gap, ties))
+    sw, el = sf.sf_window_leader_switches(tl, tg, tt, window, min_gap)
+    torch.cuda.synchronize()
+    osw, oel = oracle.window_leader_switches(lead, gap, ties, window, min_gap)
+    np.testing.assert_array_equal(sw.cpu().numpy(), osw)
+    np.testing.assert_array_equal(el.cpu().numpy(), oel)
+
+
+@pytest.mark.parametrize("T,S", [(1, 1), (63, 3), (64, 2), (65, 6), (1000, 12), (3001, 5),
+                                 (40, 512)])
+def test_switches_from_random_evidence(sf, T, S):
+    """Leader switches on seeded evidence arrays: 64-step chunk edges of the
+    wave walk, ragged windows, thresholds at and around the gaps, no
+    runner-up (gap -1), ties, leaders of any int32 value."""
+    rng = np.random.Generator(np.random.PCG64(T * 31 + S))
+    lead = rng.integers(0, 5, size=(T, S), dtype=np.int32)
+    lead[::17] = rng.integers(np.iinfo(np.int32).min, np.iinfo(np.int32).max, size=lead[::17].shape,
+                              dtype=np.int32)
+    ties = rng.choice(np.array([1, 1, 1, 2, 7], dtype=np.int32), size=(T, S))
+    gap = np.where(ties == 1, rng.integers(-1, 1000, size=(T, S)), 0).astype(np.int64)
+    print("case T=%d S=%d" % (T, S), flush=True)
+    for window in sorted({1, 5, 63, 64, 65, 128, 1000, T, T + 3}):
+        for min_gap in (0, 500, 1000, -5):
+            assert_switches_equal(sf, lead, gap, ties, window, min_gap)
+
+
+def test_switches_after_evidence(sf):
+    """sf_frontier_evidence then sf_window_leader_switches: the 8-rank
+    workload (stalls on 5% of its steps) and the stall moving between two
+    ranks, against the oracle's own evidence."""
+    wl = synth.WORKLOADS["r8_s6_t1k"]
+    d = synth.generate(wl)
+    ev = sf.sf_frontier_evidence(torch.from_numpy(d).to(DEV))
+    oev = oracle.frontier_evidence(d)
+    for min_gap in (0, 10**6, 25 * 10**6):
+        sw, el = sf.sf_window_leader_switches(ev["leader"], ev["gap"], ev["ties"], wl.window, min_gap)
+        torch.cuda.synchronize()
+        osw, oel = oracle.window_leader_switches(oev["lead"], oev["gap"], oev["ties"], wl.window,
+                                                 min_gap)
+        np.testing.assert_array_equal(sw.cpu().numpy(), osw)
+        np.testing.assert_array_equal(el.cpu().numpy(), oel)
+    # R = 1: every boundary qualifies (no runner-up), no switch
+    d1 = synth.random_durations(70, 4, 1, seed=3, hi=10**6)
+    ev = sf.sf_frontier_evidence(torch.from_numpy(d1).to(DEV))
+    sw, el = sf.sf_window_leader_switches(ev["leader"], ev["gap"], ev["ties"], 32, 10**9)
+    torch.cuda.synchronize()
+    assert el.cpu().numpy().tolist() == [[32] * 4, [32] * 4, [6] * 4]
+    assert (sw.cpu().numpy() == 0).all()
+
+
 def test_end_to_end_small_workload(sf):
     """sf_frontier then sf_window_summary, as the benchmark chains them."""
     wl = synth.WORKLOADS["r8_s6_t1k"]
@@ -758,6 +809,8 @@ def test_entry_points_on_a_side_stream(sf):
         gain = sf.sf_exposure_gain(dd, med, 8, stream=side)
         ex, cnt, top2 = sf.sf_window_summary(inc, lead, R=300, window=8, stream=side)
         le, letop2 = sf.sf_window_lead_exposed(inc, lead, R=300, window=8, stream=side)
+        swc, elc = sf.sf_window_leader_switches(ev["leader"], ev["gap"], ev["ties"], 8, 10**5,
+                                                stream=side)
         order, size = sf.sf_route(ex, stream=side)
     side.synchronize()
     np.testing.assert_array_equal(inc.cpu().numpy(), oi)
@@ -776,5 +829,9 @@ def test_entry_points_on_a_side_stream(sf):
     ole, olt = oracle.window_lead_exposed(oi, ol, 300, 8)
     np.testing.assert_array_equal(le.cpu().numpy(), ole)
     np.testing.assert_array_equal(letop2.cpu().numpy(), olt)
+    oev = oracle.frontier_evidence(d)
+    osw, oel = oracle.window_leader_switches(oev["lead"], oev["gap"], oev["ties"], 8, 10**5)
+    np.testing.assert_array_equal(swc.cpu().numpy(), osw)
+    np.testing.assert_array_equal(elc.cpu().numpy(), oel)
     oo, os_ = oracle.route(oe)
     np.testing.assert_array_equal(order.cpu().numpy(), oo)

@@ -76,6 +76,12 @@ def test_random_shape(sf, seed):
     for k, ok in (("gap", "gap"), ("ties", "ties"), ("stage_max", "stage_max"),
                   ("stage_sum", "stage_sum")):
         np.testing.assert_array_equal(ev[k].cpu().numpy(), oev[ok], err_msg=k)
+    min_gap = [0, 2, 10**6][seed % 3]
+    swc, elc = sf.sf_window_leader_switches(ev["leader"], ev["gap"], ev["ties"], window, min_gap)
+    torch.cuda.synchronize()
+    osw, oel = oracle.window_leader_switches(oev["lead"], oev["gap"], oev["ties"], window, min_gap)
+    np.testing.assert_array_equal(swc.cpu().numpy(), osw)
+    np.testing.assert_array_equal(elc.cpu().numpy(), oel)
 
     # the selects
     lag, laginc = sf.sf_frontier_lag(dd)

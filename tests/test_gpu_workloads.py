@@ -101,7 +101,16 @@ def test_workload_evidence_full_parity(sf, name):
         torch.cuda.synchronize()
         for gk, ok in keys.items():
             np.testing.assert_array_equal(out[gk].cpu().numpy(), o[ok], err_msg=gk)
-        log("evidence chunk [%d, %d) ok" % (t0, t1))
+        # leader switches of the chunk's windows (chunks are window-aligned)
+        for min_gap in (0, 10**6):
+            sw, el = sf.sf_window_leader_switches(out["leader"], out["gap"], out["ties"], wl.window,
+                                                  min_gap)
+            osw, oel = oracle.window_leader_switches(o["lead"], o["gap"], o["ties"], wl.window,
+                                                     min_gap)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(sw.cpu().numpy(), osw)
+            np.testing.assert_array_equal(el.cpu().numpy(), oel)
+        log("evidence and switches chunk [%d, %d) ok" % (t0, t1))
     del d, out
     torch.cuda.empty_cache()
 
