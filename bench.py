@@ -272,7 +272,7 @@ def main() -> int:
     next_rows = {}
     if not args.no_next:
         btilde = None  # the window median, when that row runs
-        if want("frontier_evidence"):
+        if want("frontier_evidence") or want("leader_switches"):
             ev_out = {k: torch.empty((T, S), dtype=torch.int32 if k in ("leader", "ties") else torch.int64,
                                      device=dev) for k in sf.EVIDENCE_FIELDS}
             ev_views = [(d[t0:t1], {k: v[t0:t1] for k, v in ev_out.items()}) for t0, t1 in bounds]
@@ -317,6 +317,47 @@ def main() -> int:
                 "samples_per_s": T * S * R / len(bounds) / (ev_ms / 1e3),
                 "cpu_baseline": ev_cpu,
             }
+            # leader switches between confident unique leaders (gap >= 1 ms)
+            # over the evidence of the whole pass
+            if want("leader_switches"):
+                min_gap = 1_000_000
+                sw = torch.empty((W, S), dtype=torch.int32, device=dev)
+                el = torch.empty((W, S), dtype=torch.int32, device=dev)
+                sw_args = (ev_out["leader"], ev_out["gap"], ev_out["ties"], wl.window, min_gap, sw, el)
+                sf.sf_window_leader_switches(*sw_args, stream=stream)
+                sws = []
+                for _ in range(max(3, args.steps // 2)):
+                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a.record(stream)
+                    sf.sf_window_leader_switches(*sw_args, stream=stream)
+                    b.record(stream)
+                    sws.append((a, b))
+                torch.cuda.synchronize(dev)
+                sw_ms = float(np.median([a.elapsed_time(b) for a, b in sws]))
+                sw_exact = None
+                if oracle_out:
+                    # the oracle's evidence of the first sampled steps
+                    # against the kernel run on the same steps of the pass
+                    gsw, gel = sf.sf_window_leader_switches(
+                        ev_out["leader"][t0c:t0c + n_chk], ev_out["gap"][t0c:t0c + n_chk],
+                        ev_out["ties"][t0c:t0c + n_chk], wl.window, min_gap, stream=stream)
+                    osw, oel = oracle.window_leader_switches(o["lead"], o["gap"], o["ties"],
+                                                             wl.window, min_gap)
+                    torch.cuda.synchronize(dev)
+                    sw_exact = bool(np.array_equal(gsw.cpu().numpy(), osw)
+                                    and np.array_equal(gel.cpu().numpy(), oel))
+                next_rows["leader_switches"] = {
+                    "kernel": "k_window_switches",
+                    "bound": "launch",
+                    "launch_ms": sw_ms,
+                    "min_gap_ns": min_gap,
+                    "bytes_per_launch": 16 * T * S + 8 * W * S,
+                    "windows": W,
+                    "switches_total": int(sw.sum()),
+                    "eligible_total": int(el.sum()),
+                    "bit_exact_first_steps": sw_exact,
+                }
+                del sw, el
             del ev_out, ev_views
 
         # next row: the checked frontier pass (the data contract verified on
