@@ -8,10 +8,11 @@
 // is being resolved, and is then transposed through LDS, where the low and
 // high words sit in separate planes with a row stride of RPW + 1 words so
 // that a wave reading one rank's column hits distinct banks.  Each wave then
-// takes one rank: its n values (K per lane) go to registers, and an exact
-// radix select (a 256-bin histogram of the first digit fitted to the range's
-// top bits, then 8 bits at a time of the values left) finds the lower
-// median.  Once at most 64 values are left they are compacted, one per lane,
+// takes one rank: its n values (K per lane, the tile's zero rows past n
+// included as values below all others) go to registers, and an exact radix
+// select (a 256-bin histogram of the top 8 bits of the OR of the values,
+// then 8 bits at a time of the values left) finds the lower median.  Once
+// at most 64 values are left they are compacted, one per lane,
 // through the wave's own (already read) tile column, so later passes handle
 // one value per lane.  The histogram is private to the wave and a wave's LDS
 // operations complete in issue order, so the waves need no barrier between
@@ -23,6 +24,20 @@
 
 namespace sfk {
 
+// OR over aligned groups of SUB lanes (the DPP pattern of group_max); the
+// result is valid in the last lane of each group
+template <int SUB>
+__device__ __forceinline__ u64 group_or(u64 v)
+{
+    if (SUB >= 2) v |= dpp_move<0xB1, 0xF>(v);
+    if (SUB >= 4) v |= dpp_move<0x4E, 0xF>(v);
+    if (SUB >= 8) v |= dpp_move<0x141, 0xF>(v);
+    if (SUB >= 16) v |= dpp_move<0x140, 0xF>(v);
+    if (SUB >= 32) v |= dpp_move<0x142, 0xA>(v);
+    if (SUB >= 64) v |= dpp_move<0x143, 0xC>(v);
+    return v;
+}
+
 // orders this wave's LDS accesses before the ones that follow (a wave's LDS
 // operations complete in issue order; this keeps the compiler from moving
 // them across)
@@ -32,8 +47,11 @@ __device__ __forceinline__ void wave_lds_fence()
     __builtin_amdgcn_wave_barrier();
 }
 
+// At most 64 VGPRs (8 waves per SIMD) for the shapes of windows up to 256
+// steps, whose tiles leave LDS for two workgroups per CU: without the cap
+// the 256-step shape takes 72 and one workgroup per CU (24% slower).
 template <int VEC, int K, int RPW>
-__global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __restrict__ d,
+__global__ __launch_bounds__(64 * RPW) __attribute__((amdgpu_waves_per_eu(K <= 4 ? 8 : 4))) void k_window_median(const int64_t* __restrict__ d,
                                                             int64_t T, int R, int S,
                                                             int64_t window, int nchunk,
                                                             int64_t ntiles,
@@ -112,13 +130,15 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
             thi[i * STRIDE + c + 1] = (uint32_t)((u64)x1[j] >> 32);
         }
         __syncthreads();
-        // this wave's rank: its column to registers
+        // this wave's rank: its column to registers.  Rows n.. of the tile
+        // hold zeros (the loads leave them 0); durations are >= 0, so the
+        // zeros sort at or below every value and the lower median of the n
+        // values is the slot of rank (n - 1) / 2 + (ROWS - n) among all
+        // ROWS slots: no slot needs a validity test.
         u64 v[K];
-        bool ok[K];
 #pragma unroll
         for (int k = 0; k < K; ++k) {
             const int i = k * 64 + lane;
-            ok[k] = i < q.n;
             v[k] = ((u64)thi[i * STRIDE + wave] << 32) | tlo[i * STRIDE + wave];
         }
         // the next tile's loads fly while this one is resolved
@@ -126,24 +146,17 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
         const int r = q.r0 + wave;
         if (r >= R) continue;  // the barriers are at the top of the loop
 
-        u64 vmax = 0, vmin = ~0ull;
+        // the first digit: the top 8 bits of the OR of the values, which
+        // bounds every value
+        u64 vor = 0;
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-            if (ok[k]) {
-                vmax = umax64(vmax, v[k]);
-                vmin = umin64(vmin, v[k]);
-            }
-        }
-        vmax = lane_value(group_max<64>(vmax), 63);
-        vmin = ~lane_value(group_max<64>(~vmin), 63);
-        const u64 range = vmax - vmin;
-        u64 um = 0;  // the median minus vmin
-        if (range != 0) {
-#pragma unroll
-            for (int k = 0; k < K; ++k) v[k] -= vmin;
-            int lo = sel_first_lo(range), hi = lo + 8;
+        for (int k = 0; k < K; ++k) vor |= v[k];
+        vor = lane_value(group_or<64>(vor), 63);
+        u64 um = 0;  // the median (0 when every value is 0)
+        if (vor != 0) {
+            int lo = sel_first_lo(vor), hi = lo + 8;
             u64 prefix = 0;
-            uint32_t kk = (uint32_t)((q.n - 1) / 2);
+            uint32_t kk = (uint32_t)((q.n - 1) / 2 + (ROWS - q.n));
             bool first = true;     // every value is a candidate
             bool compact = false;  // the values left are one per lane in (c1, ok1)
             u64 c1 = 0;
@@ -156,11 +169,10 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
                     // neighbouring bins are rare: one plain atomic per value
                     // (2-4% faster than adding runs of equal bins at once)
 #pragma unroll
-                    for (int k = 0; k < K; ++k)
-                        if (ok[k]) atomicAdd(&h[sel_first_bin(v[k], lo)], 1u);
+                    for (int k = 0; k < K; ++k) atomicAdd(&h[sel_first_bin(v[k], lo)], 1u);
                 } else {
 #pragma unroll
-                    for (int k = 0; k < K; ++k) sel_hist_add(h, ok[k] ? sel_bin(v[k], lo, hi, prefix) : -1);
+                    for (int k = 0; k < K; ++k) sel_hist_add(h, sel_bin(v[k], lo, hi, prefix));
                 }
                 first = false;
                 wave_lds_fence();
@@ -171,10 +183,14 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
                 wave_lds_fence();
                 prefix = (prefix << (hi - lo)) | (u64)digit;
                 hi = lo;
-                if (hi == 0) break;  // every bit chosen: u == prefix
+                if (hi == 0) break;  // every bit chosen: the median == prefix
                 lo = lo > 8 ? lo - 8 : 0;
                 if (count == 1) {
-                    // one value has the chosen digits: its lane hands it over
+                    // one value has the chosen digits: its lane hands it over.
+                    // The search skips the zero rows (a mask here keeps the
+                    // compiler from holding every slot's match in registers):
+                    // when the one value is such a zero, no lane holds it and
+                    // lane 0's x = 0 is the answer.
                     u64 x = 0;
                     bool has = false;
                     if (compact) {
@@ -183,7 +199,7 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
                     } else {
 #pragma unroll
                         for (int k = 0; k < K; ++k) {
-                            if (ok[k] && sel_match(v[k], hi, prefix)) {
+                            if (k * 64 + lane < q.n && sel_match(v[k], hi, prefix)) {
                                 x = v[k];
                                 has = true;
                             }
@@ -198,8 +214,7 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
                     // of this wave's tile column (read already)
                     uint32_t cand = 0;  // bit k: v[k] is left
 #pragma unroll
-                    for (int k = 0; k < K; ++k)
-                        cand |= (ok[k] && sel_match(v[k], hi, prefix)) ? (1u << k) : 0u;
+                    for (int k = 0; k < K; ++k) cand |= sel_match(v[k], hi, prefix) ? (1u << k) : 0u;
                     const uint32_t nc = (uint32_t)__popc(cand);
                     uint32_t pos = wave_scan_incl(nc) - nc;
 #pragma unroll
@@ -220,7 +235,7 @@ __global__ __launch_bounds__(64 * RPW) void k_window_median(const int64_t* __res
             }
             um = prefix;
         }
-        if (lane == 0) med[(q.w * S + q.s) * (int64_t)R + r] = (int64_t)(vmin + um);
+        if (lane == 0) med[(q.w * S + q.s) * (int64_t)R + r] = (int64_t)um;
     }
 }
 
