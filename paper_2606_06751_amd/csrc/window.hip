@@ -188,27 +188,47 @@ __global__ __launch_bounds__(kSumWG) void k_window_lead_exposed(
 }
 
 // One workgroup per (window, pick k in {0, 1}); grid-stride.  The stage
-// totals of the window are summed here from the advances (one wave per
-// stage at a time), both workgroups of a window choose the same two stages,
-// and each then finds the rank that led the most exposed time of its own
-// stage: the largest positive entry of the row, the lowest rank on ties.
+// totals of the window are summed here from the advances, both workgroups
+// of a window choose the same two stages, and each then finds the rank that
+// led the most exposed time of its own stage: the largest positive entry of
+// the row, the lowest rank on ties.  The sums read the window's [steps][S]
+// block in order: with S < WG, thread j takes stage j % S at every P-th
+// step from step j / S (P = WG / S phases), and the phases are added in LDS
+// (int64 sums wrap alike in any order).
 __global__ __launch_bounds__(kTopWG) void k_window_lead_top2(
     const int64_t* __restrict__ inc, const int64_t* __restrict__ lead_exposed, int64_t T, int R,
     int S, int64_t window, int64_t W, int32_t* __restrict__ top2)
 {
     __shared__ int64_t tot[SF_MAX_S];
+    __shared__ int64_t part[kTopWG];
     __shared__ u64 sh[kTopWG / 64];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x;
+    const int P = S < kTopWG ? kTopWG / S : 1;  // phases per stage
     for (int64_t id = blockIdx.x; id < 2 * W; id += gridDim.x) {
         const int64_t w = id >> 1;
         const int k = (int)(id & 1);
         const int64_t t0 = w * window;
         const int64_t t1 = min(t0 + window, T);
-        for (int s = wave; s < S; s += kTopWG / 64) {
+        if (P > 1) {
             int64_t sum = 0;
-            for (int64_t t = t0 + lane; t < t1; t += 64) sum += inc[t * S + s];
-            sum = wave_sum64(sum);
-            if (lane == 0) tot[s] = sum;
+            if (tid < P * S) {
+                const int s = tid % S, p = tid / S;
+#pragma unroll 8
+                for (int64_t t = t0 + p; t < t1; t += P) sum += inc[t * S + s];
+            }
+            part[tid] = sum;
+            __syncthreads();
+            for (int s = tid; s < S; s += kTopWG) {
+                int64_t acc = 0;
+                for (int p = 0; p < P; ++p) acc += part[p * S + s];
+                tot[s] = acc;
+            }
+        } else {
+            for (int s = tid; s < S; s += kTopWG) {
+                int64_t acc = 0;
+                for (int64_t t = t0; t < t1; ++t) acc += inc[t * S + s];
+                tot[s] = acc;
+            }
         }
         __syncthreads();
         // larger total first, then lower stage index (every thread alike)
@@ -225,6 +245,9 @@ __global__ __launch_bounds__(kTopWG) void k_window_lead_top2(
             const int64_t* row = lead_exposed + (w * S + pick) * (int64_t)R;
             int64_t best = 0;
             int br = -1;
+            // unrolled so that several loads are in flight at once: the
+            // loop is bound by load latency, not bandwidth
+#pragma unroll 8
             for (int r = tid; r < R; r += kTopWG) {
                 const int64_t v = row[r];
                 if (v > best) { best = v; br = r; }
@@ -240,7 +263,7 @@ __global__ __launch_bounds__(kTopWG) void k_window_lead_top2(
             top2[w * 4 + 2 * k] = pick;
             top2[w * 4 + 2 * k + 1] = rank;
         }
-        __syncthreads();  // tot is rewritten by the next id
+        __syncthreads();  // tot and part are rewritten by the next id
     }
 }
 
