@@ -76,17 +76,39 @@ __global__ __launch_bounds__(64 * RPW) __attribute__((amdgpu_waves_per_eu(K <= 4
     for (int i = lane; i < kSelWords; i += 64) h[i] = 0;  // cleared again by every scan
 
     // tile b -> (window, stage, rank chunk), the chunk fastest so that
-    // neighbouring workgroups read neighbouring pieces of the same rows
+    // neighbouring workgroups read neighbouring pieces of the same rows.  A
+    // workgroup's tiles advance by gridDim.x: the position is a mixed-radix
+    // counter (w, s, chunk) advanced with carries, so that the loop does no
+    // 64-bit division (which costs some 300 scalar instructions per tile in
+    // every wave).
     struct Tile {
         int64_t w, t0;
         int s, n, r0;
     };
-    auto tile = [&](int64_t b) {
-        Tile x;
+    struct Pos {
+        int64_t w;
+        int s, c;
+    };
+    auto split = [&](int64_t b) {
         const int64_t wsi = b / nchunk;
-        x.r0 = (int)(b - wsi * nchunk) * RPW;
-        x.s = (int)(wsi % S);
-        x.w = wsi / S;
+        return Pos{wsi / S, (int)(wsi % S), (int)(b - wsi * nchunk)};
+    };
+    const Pos step = split(gridDim.x);
+    auto advance = [&](Pos p) {
+        p.c += step.c;
+        const int cc = p.c >= nchunk;
+        p.c -= cc ? nchunk : 0;
+        p.s += step.s + cc;
+        const int cs = p.s >= S;
+        p.s -= cs ? S : 0;
+        p.w += step.w + cs;
+        return p;
+    };
+    auto tile = [&](const Pos& p) {
+        Tile x;
+        x.r0 = p.c * RPW;
+        x.s = p.s;
+        x.w = p.w;
         x.t0 = x.w * window;
         x.n = (int)((x.t0 + window < T ? x.t0 + window : T) - x.t0);  // 1 <= n <= ROWS
         return x;
@@ -117,9 +139,11 @@ __global__ __launch_bounds__(64 * RPW) __attribute__((amdgpu_waves_per_eu(K <= 4
     };
 
     int64_t b = blockIdx.x;  // the grid is at most ntiles
-    load(tile(b));
+    Pos pos = split(b);
+    load(tile(pos));
     for (; b < ntiles; b += gridDim.x) {
-        const Tile q = tile(b);
+        const Tile q = tile(pos);
+        pos = advance(pos);
         __syncthreads();  // every wave is done with the previous tile's columns
 #pragma unroll
         for (int j = 0; j < NSW; ++j) {
@@ -142,7 +166,7 @@ __global__ __launch_bounds__(64 * RPW) __attribute__((amdgpu_waves_per_eu(K <= 4
             v[k] = ((u64)thi[i * STRIDE + wave] << 32) | tlo[i * STRIDE + wave];
         }
         // the next tile's loads fly while this one is resolved
-        if (b + gridDim.x < ntiles) load(tile(b + gridDim.x));
+        if (b + gridDim.x < ntiles) load(tile(pos));
         const int r = q.r0 + wave;
         if (r >= R) continue;  // the barriers are at the top of the loop
 
