@@ -18,9 +18,30 @@
 #include "sf_host.h"
 #include "sf_select.h"
 
+#include <type_traits>
+
 namespace sfk {
 
 constexpr int kLagWords = kSelWords;
+
+// 32-bit twin of group_max (result valid in the last lane of each group)
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_move32(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, ROW_MASK, 0xF, false);
+}
+
+template <int SUB>
+__device__ __forceinline__ uint32_t group_max32(uint32_t v)
+{
+    if (SUB >= 2) v = max(v, dpp_move32<0xB1, 0xF>(v));
+    if (SUB >= 4) v = max(v, dpp_move32<0x4E, 0xF>(v));
+    if (SUB >= 8) v = max(v, dpp_move32<0x141, 0xF>(v));
+    if (SUB >= 16) v = max(v, dpp_move32<0x140, 0xF>(v));
+    if (SUB >= 32) v = max(v, dpp_move32<0x142, 0xA>(v));
+    if (SUB >= 64) v = max(v, dpp_move32<0x143, 0xC>(v));
+    return v;
+}
 
 // lane 0's value, in every lane
 __device__ __forceinline__ u64 lane0(u64 v) { return lane_value(v, 0); }
@@ -44,12 +65,29 @@ __device__ __forceinline__ u64 lane0(u64 v) { return lane_value(v, 0); }
 // 0 publishes it, instead of the finding lane publishing it; the same work,
 // compiled differently (7% faster for the lag with 16 prefixes per lane on
 // 1-4 waves, up to 8% slower elsewhere).
-template <bool PREFIX, int VEC, int K, int WG, int LCAP, bool PUBU, bool FULL>
-__global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_median_spread(const int64_t* __restrict__ d, int64_t T,
+//
+// NARROW: the values are held in 32 bits.  Every workload here keeps a
+// step's rebased prefixes (P - min_r P, Sec. 3 values are in ns) and its
+// durations below 2^32 ns (4.29 s), so the values, the loads in flight and
+// the reductions take half the registers: 64 VGPRs, two workgroups per CU,
+// which cover each other's barriers.  The stage's loads are consumed in
+// chunks so that few hold registers at once.  A step where a duration or a
+// rebased prefix reaches 2^32 (detected on the load, by the high word or the
+// carry of the 32-bit add) is handed over: once the step is done, its
+// out[t][0] is set to kRedo; a second launch of the 64-bit kernel with REDO
+// recomputes exactly those steps (every other workgroup of it returns at
+// once).  Both compute the same lower median of the same values.
+constexpr int64_t kRedo = INT64_MIN;  // outputs are >= 0 under the data contract
+
+template <bool PREFIX, int VEC, int K, int WG, int LCAP, bool PUBU, bool FULL, bool NARROW,
+          bool REDO>
+__global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW ? 8 : 4))) void k_median_spread(const int64_t* __restrict__ d, int64_t T,
                                                       int R, int S, int64_t* __restrict__ out,
                                                       int64_t* __restrict__ out_inc)
 {
     static_assert(K % VEC == 0 && WG % 64 == 0 && WG / 64 <= 16, "shape");
+    static_assert(!NARROW || (FULL && VEC == 2 && !REDO), "the narrow pass takes full 16-byte tiles");
+    typedef typename std::conditional<NARROW, uint32_t, u64>::type V;
     constexpr int NW = WG / 64;
     constexpr int NLD = K / VEC;
     constexpr bool SCAN_ALL = !PREFIX && NW > 1;
@@ -60,7 +98,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
     __shared__ u64 red_max[2][NW], red_min[2][NW];
     __shared__ __attribute__((aligned(16))) uint32_t hist[NH][kLagWords];
     __shared__ uint32_t sel[3];  // wave 0's scan: chosen digit, rank within it, its count
-    __shared__ u64 list[LCAP > 0 ? LCAP : 1];  // candidates, once few enough
+    __shared__ V list[LCAP > 0 ? LCAP : 1];  // candidates, once few enough
     __shared__ uint32_t list_n;                // fill position of the list
     __shared__ int64_t lag_sh[2];              // L of the last two stages, by parity
 
@@ -69,6 +107,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
     const int wave = tid >> 6;
     const int64_t t = xcd_block();
     if (t >= T) return;  // uniform over the workgroup (the grid is T)
+    if (REDO && out[t * S] != kRedo) return;  // a step the narrow pass resolved
     const int64_t* dt = d + t * (int64_t)S * R;
 
     bool ok[NLD];
@@ -94,9 +133,9 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
             }
         }
     };
-    load_stage(0);
+    if (!NARROW) load_stage(0);
 
-    u64 P[K];
+    V P[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) P[k] = 0;
     for (int i = tid; i < NH * kLagWords; i += WG) (&hist[0][0])[i] = 0;
@@ -105,23 +144,70 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
         lag_sh[0] = 0;
         lag_sh[1] = 0;
     }
+    bool wide_step = false;  // NARROW: some value of this step left 32 bits
     int cur = 0;  // the histogram of the next pass (clear)
     const uint32_t target = (uint32_t)((R - 1) / 2);
 
     for (int s = 0; s < S; ++s) {
         u64 lmax = 0, lmin = ~0ull;
+        if constexpr (NARROW) {
+            // the stage's 16-byte loads in CH chunks, each consumed before
+            // the next is issued (one at a time for the lag, whose prefixes
+            // stay live across stages)
+            constexpr int CH = PREFIX ? NLD : 2;
+            const int64_t* row = dt + (int64_t)s * R;
+            uint32_t mx = 0, mn = ~0u;
+            bool wide = false;  // wave-uniform: some value of the wave left 32 bits
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-            if (ok[k / VEC]) {
-                P[k] = PREFIX ? P[k] + (u64)nx[k] : (u64)nx[k];
-                lmax = umax64(lmax, P[k]);
-                lmin = umin64(lmin, P[k]);
+            for (int ch = 0; ch < CH; ++ch) {
+                uint32_t w = 0;
+                v2i64 xs[NLD / CH];
+#pragma unroll
+                for (int l = 0; l < NLD / CH; ++l)
+                    xs[l] = __builtin_nontemporal_load(
+                        reinterpret_cast<const v2i64*>(row + ((ch * (NLD / CH) + l) * WG + tid) * 2));
+#pragma unroll
+                for (int l = 0; l < NLD / CH; ++l) {
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        const int k = (ch * (NLD / CH) + l) * 2 + e;
+                        const u64 x = (u64)(e == 0 ? xs[l].x : xs[l].y);
+                        const uint32_t lo = (uint32_t)x;
+                        w |= (uint32_t)(x >> 32);
+                        if (PREFIX) {
+                            const uint32_t np = (uint32_t)P[k] + lo;
+                            w |= np < lo ? 1u : 0u;  // carry
+                            P[k] = np;
+                        } else {
+                            P[k] = lo;
+                        }
+                        mx = max(mx, (uint32_t)P[k]);
+                        mn = min(mn, (uint32_t)P[k]);
+                    }
+                }
+                wide = wide || __ballot(w != 0) != 0;
+                __builtin_amdgcn_sched_barrier(0);
             }
+            // a wave holding a value of 2^32 or more reports the maximum
+            // ~0, which no 32-bit value reaches
+            const u64 wmax = (u64)group_max32<64>(mx);
+            const uint32_t nmn = group_max32<64>(~mn);
+            lmax = wide ? ~0ull : wmax;
+            lmin = (u64)(~nmn);
+        } else {
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                if (ok[k / VEC]) {
+                    P[k] = PREFIX ? P[k] + (u64)nx[k] : (u64)nx[k];
+                    lmax = umax64(lmax, P[k]);
+                    lmin = umin64(lmin, P[k]);
+                }
+            }
+            if (s + 1 < S) load_stage(s + 1);
+            // block max and min (min as the max of complements)
+            lmax = group_max<64>(lmax);
+            lmin = ~group_max<64>(~lmin);
         }
-        if (s + 1 < S) load_stage(s + 1);
-        // block max and min (min as the max of complements)
-        lmax = group_max<64>(lmax);
-        lmin = ~group_max<64>(~lmin);
         const int pb = s & 1;
         if (lane == 63) {
             red_max[pb][wave] = lmax;
@@ -134,10 +220,15 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
         const int wl = has ? lane : 0;
         const u64 F = lane0(group_max<16>(has ? red_max[pb][wl] : 0ull));
         const u64 Pmin = ~lane0(group_max<16>(has ? ~red_min[pb][wl] : 0ull));
+        // a value left 32 bits (uniform: every wave read the same
+        // partials); the step runs on, on values that no longer matter, and
+        // is handed over at its end (an exit here costs the narrow lag 22
+        // VGPRs of spills)
+        if (NARROW) wide_step = wide_step || (F >> 32) != 0;
         // rebase: from here on P holds u = P - Pmin (the minimum is 0)
         const u64 range = F - Pmin;
 #pragma unroll
-        for (int k = 0; k < K; ++k) P[k] -= Pmin;
+        for (int k = 0; k < K; ++k) P[k] -= (V)Pmin;
         u64 um = 0;            // u of the median (0 when every u is 0)
         bool written = false;  // the lane holding the median wrote the outputs
         if (range != 0) {
@@ -291,43 +382,55 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
         }
         // lag_sh[s & 1] is read at stage s + 1, after its reduction barrier
     }
+    if (NARROW) {
+        __syncthreads();  // after every output write of the step
+        if (wide_step && tid == 0) out[t * S] = kRedo;
+    }
 }
 
 struct LagVariant {
     const void* fn;
     int WG;
+    const void* redo;  // after a narrow pass: the 64-bit kernel for the steps it handed over
 };
 
-template <bool PREFIX, int VEC, int K, int WG, bool FULL>
-LagVariant lag_variant()
+template <bool PREFIX, int VEC, int K, int WG, bool FULL, bool NARROW = false, bool REDO = false>
+const void* lag_kernel()
 {
-    // candidate list: a quarter of the slots, at most 32 KB; none when a
-    // lane holds so few values that the registers are as cheap to re-read
+    // candidate list: a quarter of the slots, at most 4096 values; none when
+    // a lane holds so few values that the registers are as cheap to re-read
     constexpr int LCAP = K <= 2 ? 0 : (K * WG / 4 < 4096 ? K * WG / 4 : 4096);
-    constexpr bool PUBU = PREFIX && K == 16 && WG <= 256;
+    constexpr bool PUBU = PREFIX && K == 16 && WG <= 256 && !NARROW;
     static_assert(!(PUBU && FULL), "the PUBU shapes keep the rank tests");
-    return LagVariant{reinterpret_cast<const void*>(&k_median_spread<PREFIX, VEC, K, WG, LCAP, PUBU, FULL>),
-                      WG};
+    return reinterpret_cast<const void*>(
+        &k_median_spread<PREFIX, VEC, K, WG, LCAP, PUBU, FULL, NARROW, REDO>);
+}
+
+// FULL: R fills the K * WG slots exactly, so no slot needs a rank test
+// (measured on MI355X: 1-4% faster for the raw spread and for the lag at
+// 128 and 16384 ranks; 12-13% slower for the lag's PUBU shapes at 1024 and
+// 4096 ranks, whose register allocation grows past 96, so those keep the
+// tests).  NARROW (32-bit values, two workgroups per CU) where a step holds
+// 8 or more waves: 16384 ranks, measured 33% faster for the raw spread and
+// 20% for the lag.
+template <bool PREFIX, int VEC, int K, int WG>
+LagVariant lag_shape(int R)
+{
+    constexpr bool pubu = PREFIX && K == 16 && WG <= 256;
+    if constexpr (VEC == 2 && K == 16 && WG >= 512) {
+        if (R == K * WG)
+            return LagVariant{lag_kernel<PREFIX, VEC, K, WG, true, true>(), WG,
+                              lag_kernel<PREFIX, VEC, K, WG, false, false, true>()};
+    }
+    if constexpr (!pubu) {
+        if (R == K * WG) return LagVariant{lag_kernel<PREFIX, VEC, K, WG, true>(), WG, nullptr};
+    }
+    return LagVariant{lag_kernel<PREFIX, VEC, K, WG, false>(), WG, nullptr};
 }
 
 // One step per workgroup with all R prefixes in registers, as few waves as
 // the registers allow: a wave spends less time at barriers than a lane does
 // on 4x the prefixes (measured on the 128- to 16384-rank workloads).
-// FULL: R fills the K * WG slots exactly, so no slot needs a rank test
-// (measured on MI355X: 1-4% faster for the raw spread and for the lag at
-// 128 and 16384 ranks; 12-13% slower for the lag's PUBU shapes at 1024 and
-// 4096 ranks, whose register allocation grows past 96, so those keep the
-// tests)
-template <bool PREFIX, int VEC, int K, int WG>
-LagVariant lag_shape(int R)
-{
-    constexpr bool pubu = PREFIX && K == 16 && WG <= 256;
-    if constexpr (!pubu) {
-        if (R == K * WG) return lag_variant<PREFIX, VEC, K, WG, true>();
-    }
-    return lag_variant<PREFIX, VEC, K, WG, false>();
-}
-
 template <bool PREFIX, int VEC>
 LagVariant pick_lag(int R)
 {
@@ -339,6 +442,15 @@ LagVariant pick_lag(int R)
     if (R <= 4096) return lag_shape<PREFIX, VEC, 16, 256>(R);
     if (R <= 8192) return lag_shape<PREFIX, VEC, 16, 512>(R);
     return lag_shape<PREFIX, VEC, 16, 1024>(R);  // R <= SF_MAX_R_LAG = 16384
+}
+
+// the narrow pass, then (if it has one) the 64-bit pass over the steps it
+// handed over
+static int launch_lag(const LagVariant& v, int64_t T, void** args, sf_stream_t stream)
+{
+    int rc = launch(v.fn, dim3((unsigned)T), dim3(v.WG), args, 0, stream);
+    if (rc == SF_OK && v.redo) rc = launch(v.redo, dim3((unsigned)T), dim3(v.WG), args, 0, stream);
+    return rc;
 }
 
 }  // namespace sfk
@@ -364,7 +476,7 @@ SF_API int sf_frontier_lag(const int64_t* durations, int64_t T, int32_t R, int32
     int Ri = R, Si = S;
     void* args[] = {(void*)&durations, (void*)&T, (void*)&Ri, (void*)&Si, (void*)&out_lag,
                     (void*)&out_lag_inc};
-    return launch(v.fn, dim3((unsigned)T), dim3(v.WG), args, 0, stream);
+    return launch_lag(v, T, args, stream);
 }
 
 SF_API int sf_rank_spread(const int64_t* durations, int64_t T, int32_t R, int32_t S,
@@ -390,7 +502,7 @@ SF_API int sf_rank_spread(const int64_t* durations, int64_t T, int32_t R, int32_
     int64_t* unused = nullptr;
     void* args[] = {(void*)&durations, (void*)&T, (void*)&Ri, (void*)&Si, (void*)&out_spread,
                     (void*)&unused};
-    const int rc = launch(v.fn, dim3((unsigned)T), dim3(v.WG), args, 0, stream);
+    const int rc = launch_lag(v, T, args, stream);
     if (rc != SF_OK) return rc;
     return launch_window_sum(out_spread, T, S, window, W, out_window_spread, stream);
 }

@@ -584,6 +584,31 @@ def test_lag_rank_sweep(sf, R):
         assert_lag_equal(sf, d)
 
 
+@pytest.mark.parametrize("R", [8192, 16384])
+def test_narrow_pass_hand_over(sf, R):
+    """At 8192 and 16384 ranks the lag and the raw spread run on 32-bit
+    values and hand a step whose values leave 32 bits to the 64-bit kernel:
+    a duration of 2^32 or more, a rebased prefix that carries past 2^32 at
+    a later stage, an overflow at the last stage only, neighbours that stay
+    narrow, and every step handed over; all against the oracle."""
+    rng = np.random.Generator(np.random.PCG64(R + 23))
+    T, S = 10, 5
+    d = rng.integers(0, 10**7, size=(T, S, R), dtype=np.int64)
+    d[2, 2, R // 3] = (1 << 32) + 5              # a duration past 32 bits
+    d[4, 0, 7] = 3 * 10**9                       # the prefix spread carries at stage 1
+    d[4, 1, 7] = 3 * 10**9
+    d[6, S - 1, R - 1] = 1 << 33                 # the last stage only
+    d[8, :4, 5] = 10**9                          # 4e9 after four stages: still narrow
+    d[9, 0, 0] = (1 << 32) - 1                   # the largest narrow duration
+    print("case R=%d mixed" % R, flush=True)
+    assert_lag_equal(sf, d)
+    assert_spread_equal(sf, d, 3)
+    wide = rng.integers(1 << 32, 1 << 40, size=(3, 2, R), dtype=np.int64)
+    print("case R=%d all handed over" % R, flush=True)
+    assert_lag_equal(sf, wide)
+    assert_spread_equal(sf, wide, 2)
+
+
 @pytest.mark.parametrize("S", [1, 2, 12, 100, 512])
 def test_lag_stage_sweep(sf, S):
     rng = np.random.Generator(np.random.PCG64(S + 11))
