@@ -410,14 +410,16 @@ const void* lag_kernel()
 // (measured on MI355X: 1-4% faster for the raw spread and for the lag at
 // 128 and 16384 ranks; 12-13% slower for the lag's PUBU shapes at 1024 and
 // 4096 ranks, whose register allocation grows past 96, so those keep the
-// tests).  NARROW (32-bit values, two workgroups per CU) where a step holds
-// 8 or more waves: 16384 ranks, measured 33% faster for the raw spread and
-// 20% for the lag.
+// tests).  NARROW (32-bit values, two workgroups per CU) for the raw spread
+// at 16 values per lane and for the lag where a step holds 8 or more waves
+// (measured at 16384 ranks: 32% faster for the raw spread, 18% for the lag;
+// at 1024 and 4096 ranks the raw spread 9% and 4% faster, the lag 6% slower,
+// so the lag keeps its 64-bit shapes there).
 template <bool PREFIX, int VEC, int K, int WG>
 LagVariant lag_shape(int R)
 {
     constexpr bool pubu = PREFIX && K == 16 && WG <= 256;
-    if constexpr (VEC == 2 && K == 16 && WG >= 512) {
+    if constexpr (VEC == 2 && K == 16 && (WG >= 512 || !PREFIX)) {
         if (R == K * WG)
             return LagVariant{lag_kernel<PREFIX, VEC, K, WG, true, true>(), WG,
                               lag_kernel<PREFIX, VEC, K, WG, false, false, true>()};

@@ -584,10 +584,11 @@ def test_lag_rank_sweep(sf, R):
         assert_lag_equal(sf, d)
 
 
-@pytest.mark.parametrize("R", [8192, 16384])
+@pytest.mark.parametrize("R", [1024, 2048, 4096, 8192, 16384])
 def test_narrow_pass_hand_over(sf, R):
-    """At 8192 and 16384 ranks the lag and the raw spread run on 32-bit
-    values and hand a step whose values leave 32 bits to the 64-bit kernel:
+    """At 1024 to 16384 ranks the raw spread, and at 8192 and 16384 the lag,
+    run on 32-bit values and hand a step whose values leave 32 bits to the
+    64-bit kernel:
     a duration of 2^32 or more, a rebased prefix that carries past 2^32 at
     a later stage, an overflow at the last stage only, neighbours that stay
     narrow, and every step handed over; all against the oracle."""
