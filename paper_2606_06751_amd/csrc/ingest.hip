@@ -92,7 +92,11 @@ __global__ __launch_bounds__(kIngestWG) void k_ingest(const int64_t* __restrict_
             ovl[i] = e < 0 ? -e : 0;
         }
         __syncthreads();
-        // write: each wave writes ROWS_PER_WAVE [t][s] rows of RB ranks at once
+        // write: each wave writes ROWS_PER_WAVE [t][s] rows of RB ranks at
+        // once, with non-temporal stores (the output is written once and not
+        // read again here: measured 2-6% faster than plain stores on the
+        // four large workloads; non-temporal loads of the input, read
+        // through L2 in 512-byte pieces, measured 8-29% slower)
         const int sub = lane / RB;
         const int j = lane & (RB - 1);
         const int nrows = tn * S;
@@ -114,12 +118,12 @@ __global__ __launch_bounds__(kIngestWG) void k_ingest(const int64_t* __restrict_
             }
 #pragma unroll
             for (int u = 0; u < UW; ++u)
-                if (dst[u]) *dst[u] = v[u];
+                if (dst[u]) __builtin_nontemporal_store(v[u], dst[u]);
         }
         for (int i = tid; i < tn * RB; i += kIngestWG) {
             const int tl = i / RB;
             const int jj = i & (RB - 1);
-            if (jj < rn) o[(t0 + tl) * (int64_t)R + r0 + jj] = ovl[i];
+            if (jj < rn) __builtin_nontemporal_store(ovl[i], &o[(t0 + tl) * (int64_t)R + r0 + jj]);
         }
         __syncthreads();  // the tile is reused by the next block
     }
