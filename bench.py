@@ -590,7 +590,7 @@ def main() -> int:
                 for dv, a1, a2 in l_views:
                     sf.sf_frontier_lag(dv, a1, a2, stream=stream)
                 lt = []
-                for _ in range(3):
+                for _ in range(max(3, args.steps // 2)):
                     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                     a.record(stream)
                     for dv, a1, a2 in l_views:
@@ -598,7 +598,7 @@ def main() -> int:
                     b.record(stream)
                     lt.append((a, b))
                 torch.cuda.synchronize(dev)
-                l_ms = float(np.mean([a.elapsed_time(b) for a, b in lt])) / len(bounds)
+                l_ms = float(np.median([a.elapsed_time(b) for a, b in lt])) / len(bounds)
                 l_bytes = (8 * T * S * R + 16 * T * S) / len(bounds)
                 l_exact = l_cpu = None
                 if oracle_out:
@@ -639,7 +639,7 @@ def main() -> int:
                 for dv, a1, a2 in s_views:
                     sf.sf_rank_spread(dv, wl.window, a1, a2, stream=stream)
                 st = []
-                for _ in range(3):
+                for _ in range(max(3, args.steps // 2)):
                     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                     a.record(stream)
                     for dv, a1, a2 in s_views:
@@ -647,7 +647,7 @@ def main() -> int:
                     b.record(stream)
                     st.append((a, b))
                 torch.cuda.synchronize(dev)
-                s_ms = float(np.mean([a.elapsed_time(b) for a, b in st])) / len(bounds)
+                s_ms = float(np.median([a.elapsed_time(b) for a, b in st])) / len(bounds)
                 s_bytes = (8 * T * S * R + 8 * T * S + 8 * W * S) / len(bounds)
                 s_exact = s_cpu = None
                 if oracle_out:

@@ -96,3 +96,54 @@ def test_captured_path_replays(sf):
         np.testing.assert_array_equal(out["med"].cpu().numpy(), om)
         np.testing.assert_array_equal(out["gain"].cpu().numpy(), og["gain"])
         np.testing.assert_array_equal(out["wgain"].cpu().numpy(), og["window_gain"])
+
+
+def test_captured_narrow_pass_replays(sf):
+    """The lag and the raw spread at 16384 ranks (the 32-bit pass plus the
+    64-bit pass over the steps it hands over, two launches) captured once
+    and replayed on inputs that hand over no step, some steps, then none
+    again: the hand-over goes through the output itself, so every replay
+    must stand alone."""
+    T, S, R, window = 5, 3, 16384, 2
+    W = sf.sf_num_windows(T, window)
+    d_in = torch.empty((T, S, R), dtype=torch.int64, device=DEV)
+    lag = torch.empty((T, S), dtype=torch.int64, device=DEV)
+    laginc = torch.empty((T, S), dtype=torch.int64, device=DEV)
+    sp = torch.empty((T, S), dtype=torch.int64, device=DEV)
+    wsp = torch.empty((W, S), dtype=torch.int64, device=DEV)
+
+    def path(stream):
+        sf.sf_frontier_lag(d_in, lag, laginc, stream=stream)
+        sf.sf_rank_spread(d_in, window, sp, wsp, stream=stream)
+
+    def data(seed, wide_steps):
+        d = synth.random_durations(T, S, R, seed=seed, hi=10**7)
+        for t in wide_steps:
+            d[t, 1, 100 + t] = (1 << 32) + t       # a duration past 32 bits
+        return d
+
+    d_in.copy_(torch.from_numpy(data(90, [])))
+    side = torch.cuda.Stream(DEV)
+    side.wait_stream(torch.cuda.current_stream(DEV))
+    with torch.cuda.stream(side):
+        path(side)
+    torch.cuda.current_stream(DEV).wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        path(torch.cuda.current_stream(DEV))
+    torch.cuda.synchronize()
+
+    for rep, wide_steps in enumerate([[], [1, 4], [], [0, 1, 2, 3, 4], []]):
+        d = data(91 + rep, wide_steps)
+        d_in.copy_(torch.from_numpy(d))            # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        print("replay %d handed over %s" % (rep, wide_steps), flush=True)
+        olag, olaginc = oracle.frontier_lag(d)
+        osp, owsp = oracle.rank_spread(d, window)
+        np.testing.assert_array_equal(lag.cpu().numpy(), olag)
+        np.testing.assert_array_equal(laginc.cpu().numpy(), olaginc)
+        np.testing.assert_array_equal(sp.cpu().numpy(), osp)
+        np.testing.assert_array_equal(wsp.cpu().numpy(), owsp)
