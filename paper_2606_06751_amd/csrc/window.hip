@@ -40,12 +40,14 @@ __global__ __launch_bounds__(kSumWG) void k_window_counts(
 
         for (int i = tid; i < n; i += kSumWG) hist[i] = 0;
         __syncthreads();
+#pragma unroll 4
         for (int64_t t = t0 + tid; t < t1; t += kSumWG) {
             const int64_t r = (int64_t)lead[t * S + s] - lo;
             if (r >= 0 && r < n) atomicAdd(&hist[r], 1);
         }
         if (c == 0) {
             int64_t sum = 0;
+#pragma unroll 4
             for (int64_t t = t0 + tid; t < t1; t += kSumWG) sum += inc[t * S + s];
             sum = wave_sum64(sum);
             if ((tid & 63) == 0) part[tid >> 6] = sum;
@@ -91,6 +93,9 @@ __device__ __forceinline__ u64 row_modal_key(const int32_t* __restrict__ c, int 
     if ((R & 3) == 0 && (((uintptr_t)c) & 15) == 0) {
         const int4* c4 = reinterpret_cast<const int4*>(c);
         const int n4 = R >> 2;
+        // unrolled so that several loads are in flight at once (the loop is
+        // bound by load latency)
+#pragma unroll 8
         for (int i = tid; i < n4; i += kTopWG) {
             const int4 x = c4[i];
             const int r = i << 2;
