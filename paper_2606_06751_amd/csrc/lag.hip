@@ -66,11 +66,11 @@ __device__ __forceinline__ u64 lane0(u64 v) { return lane_value(v, 0); }
 // compiled differently (7% faster for the lag with 16 prefixes per lane on
 // 1-4 waves, up to 8% slower elsewhere).
 //
-// NARROW: the values are held in 32 bits.  Every workload here keeps a
-// step's rebased prefixes (P - min_r P, Sec. 3 values are in ns) and its
-// durations below 2^32 ns (4.29 s), so the values, the loads in flight and
-// the reductions take half the registers: 64 VGPRs, two workgroups per CU,
-// which cover each other's barriers.  The stage's loads are consumed in
+// NARROW: the values are held in 32 bits.  Steps whose rebased prefixes
+// (P - min_r P, rebased at every boundary) and durations stay below 2^32 ns
+// (4.29 s; every workload here) need no more, so the values, the loads in
+// flight and the reductions take half the registers: at most 64 VGPRs,
+// twice the workgroups per CU, which cover each other's barriers.  The stage's loads are consumed in
 // chunks so that few hold registers at once.  A step where a duration or a
 // rebased prefix reaches 2^32 (detected on the load, by the high word or the
 // carry of the 32-bit add) is handed over: once the step is done, its
