@@ -610,6 +610,30 @@ def test_narrow_pass_hand_over(sf, R):
     assert_spread_equal(sf, wide, 2)
 
 
+@pytest.mark.parametrize("R", [4096, 16384])
+def test_lag_spread_misaligned_large(sf, R):
+    """A base 8 bytes past 16-byte alignment takes the 8-byte-load shapes
+    (64-bit, full tiles) at the rank counts whose aligned calls take the
+    32-bit pass; wide and narrow values alike."""
+    rng = np.random.Generator(np.random.PCG64(R + 29))
+    T, S = 6, 3
+    d = rng.integers(0, 10**7, size=(T, S, R), dtype=np.int64)
+    d[2, 1, 5] = 1 << 35
+    flat = torch.zeros(T * S * R + 1, dtype=torch.int64, device=DEV)
+    flat[1:] = torch.from_numpy(d.reshape(-1)).to(DEV)
+    dd = flat[1:].view(T, S, R)
+    print("case R=%d misaligned" % R, flush=True)
+    lag, inc = sf.sf_frontier_lag(dd)
+    sp, wsp = sf.sf_rank_spread(dd, 4)
+    torch.cuda.synchronize()
+    ol, oi = oracle.frontier_lag(d)
+    osp, owsp = oracle.rank_spread(d, 4)
+    np.testing.assert_array_equal(lag.cpu().numpy(), ol)
+    np.testing.assert_array_equal(inc.cpu().numpy(), oi)
+    np.testing.assert_array_equal(sp.cpu().numpy(), osp)
+    np.testing.assert_array_equal(wsp.cpu().numpy(), owsp)
+
+
 @pytest.mark.parametrize("S", [1, 2, 12, 100, 512])
 def test_lag_stage_sweep(sf, S):
     rng = np.random.Generator(np.random.PCG64(S + 11))
