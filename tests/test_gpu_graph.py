@@ -35,6 +35,10 @@ def test_captured_path_replays(sf):
         "top2": torch.empty((W, 2, 2), dtype=torch.int32, device=DEV),
         "le": torch.empty((W, S, R), dtype=torch.int64, device=DEV),
         "letop2": torch.empty((W, 2, 2), dtype=torch.int32, device=DEV),
+        "ev": {k: torch.empty((T, S), dtype=torch.int32 if k in ("leader", "ties") else torch.int64,
+                              device=DEV) for k in sf.EVIDENCE_FIELDS},
+        "sw": torch.empty((W, S), dtype=torch.int32, device=DEV),
+        "el": torch.empty((W, S), dtype=torch.int32, device=DEV),
         "lag": torch.empty((T, S), dtype=torch.int64, device=DEV),
         "laginc": torch.empty((T, S), dtype=torch.int64, device=DEV),
         "med": torch.empty((W, S, R), dtype=torch.int64, device=DEV),
@@ -50,6 +54,9 @@ def test_captured_path_replays(sf):
                              stream=stream)
         sf.sf_window_lead_exposed(out["inc"], out["lead"], R, window, out["le"], out["letop2"],
                                   stream=stream)
+        sf.sf_frontier_evidence(d_in, out["ev"], stream=stream)
+        sf.sf_window_leader_switches(out["ev"]["leader"], out["ev"]["gap"], out["ev"]["ties"], window,
+                                     1000, out["sw"], out["el"], stream=stream)
         sf.sf_frontier_lag(d_in, out["lag"], out["laginc"], stream=stream)
         sf.sf_window_median(d_in, window, out["med"], stream=stream)
         sf.sf_exposure_gain(d_in, out["med"], window,
@@ -91,6 +98,11 @@ def test_captured_path_replays(sf):
         ole, olt = oracle.window_lead_exposed(oi, ol, R, window)
         np.testing.assert_array_equal(out["le"].cpu().numpy(), ole)
         np.testing.assert_array_equal(out["letop2"].cpu().numpy(), olt)
+        oev = oracle.frontier_evidence(d)
+        np.testing.assert_array_equal(out["ev"]["gap"].cpu().numpy(), oev["gap"])
+        osw, oel = oracle.window_leader_switches(oev["lead"], oev["gap"], oev["ties"], window, 1000)
+        np.testing.assert_array_equal(out["sw"].cpu().numpy(), osw)
+        np.testing.assert_array_equal(out["el"].cpu().numpy(), oel)
         np.testing.assert_array_equal(out["lag"].cpu().numpy(), olag)
         np.testing.assert_array_equal(out["laginc"].cpu().numpy(), olaginc)
         np.testing.assert_array_equal(out["med"].cpu().numpy(), om)
