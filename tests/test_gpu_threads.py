@@ -25,10 +25,15 @@ def sf():
 
 
 def test_concurrent_host_threads(sf):
-    shapes = [(30, 6, 300, 7), (12, 12, 5000, 5), (50, 3, 64, 10), (20, 8, 1025, 4)]
+    # the last two take the 32-bit lag pass (16384 ranks); one of them hands
+    # a step over to the 64-bit launch
+    shapes = [(30, 6, 300, 7), (12, 12, 5000, 5), (50, 3, 64, 10), (20, 8, 1025, 4),
+              (6, 4, 16384, 3), (6, 4, 16384, 2)]
     jobs = []
     for i, (T, S, R, window) in enumerate(shapes):
         d = synth.random_durations(T, S, R, seed=40 + i, hi=[3, 10**6][i % 2])
+        if i == 5:
+            d[3, 1, 77] = 1 << 33
         dd = torch.from_numpy(d).to(DEV)
         W = sf.sf_num_windows(T, window)
         out = {
