@@ -92,10 +92,29 @@ def sf_num_windows(T: int, window: int) -> int:
     return int(_lib.sf_num_windows(T, window))
 
 
-def _stream_handle(stream, device) -> int:
+def _stream(stream, device):
+    """The torch stream a call runs on: ``stream`` (a torch stream or a raw
+    hipStream_t handle), else the current stream of ``device``."""
     if stream is None:
-        stream = torch.cuda.current_stream(device)
-    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+        return torch.cuda.current_stream(device)
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream), device=device)
+
+
+def _stream_handle(stream, device) -> int:
+    return int(_stream(stream, device).cuda_stream)
+
+
+def _new(shape, dtype, device, stream, zero: bool = False) -> torch.Tensor:
+    """An output the binding allocates for a call on ``stream``.  It is
+    allocated (and, with ``zero``, cleared) on that stream, so the clear is
+    ordered before the call's kernels and the caching allocator does not hand
+    the block to other work while they may still use it."""
+    with torch.cuda.stream(_stream(stream, device)):
+        if zero:
+            return torch.zeros(shape, dtype=dtype, device=device)
+        return torch.empty(shape, dtype=dtype, device=device)
 
 
 def _check(t: torch.Tensor, name: str, dtype, shape, like: torch.Tensor | None = None):
@@ -130,9 +149,9 @@ def sf_frontier(durations: torch.Tensor, out_increment: torch.Tensor | None = No
     _check(durations, "durations", torch.int64, (T, S, R))
     dev = durations.device
     if out_increment is None:
-        out_increment = torch.empty((T, S), dtype=torch.int64, device=dev)
+        out_increment = _new((T, S), torch.int64, dev, stream)
     if out_leader is None:
-        out_leader = torch.empty((T, S), dtype=torch.int32, device=dev)
+        out_leader = _new((T, S), torch.int32, dev, stream)
     _check(out_increment, "out_increment", torch.int64, (T, S), like=durations)
     _check(out_leader, "out_leader", torch.int32, (T, S), like=durations)
     rc = _lib.sf_frontier(durations.data_ptr(), T, R, S, out_increment.data_ptr(),
@@ -161,11 +180,11 @@ def sf_frontier_checked(durations: torch.Tensor, out_increment: torch.Tensor | N
     _check(durations, "durations", torch.int64, (T, S, R))
     dev = durations.device
     if out_increment is None:
-        out_increment = torch.empty((T, S), dtype=torch.int64, device=dev)
+        out_increment = _new((T, S), torch.int64, dev, stream)
     if out_leader is None:
-        out_leader = torch.empty((T, S), dtype=torch.int32, device=dev)
+        out_leader = _new((T, S), torch.int32, dev, stream)
     if status is None:
-        status = torch.zeros((1,), dtype=torch.int32, device=dev)
+        status = _new((1,), torch.int32, dev, stream, zero=True)
     _check(out_increment, "out_increment", torch.int64, (T, S), like=durations)
     _check(out_leader, "out_leader", torch.int32, (T, S), like=durations)
     _check(status, "status", torch.int32, (1,), like=durations)
@@ -193,7 +212,7 @@ def sf_frontier_evidence(durations: torch.Tensor, out: dict | None = None, strea
     for k in EVIDENCE_FIELDS:
         dt = torch.int32 if k in ("leader", "ties") else torch.int64
         if k not in out:
-            out[k] = torch.empty((T, S), dtype=dt, device=durations.device)
+            out[k] = _new((T, S), dt, durations.device, stream)
         _check(out[k], k, dt, (T, S), like=durations)
     rc = _lib.sf_frontier_evidence(durations.data_ptr(), T, R, S,
                                    *(out[k].data_ptr() for k in EVIDENCE_FIELDS),
@@ -222,11 +241,11 @@ def sf_window_summary(increment: torch.Tensor, leader: torch.Tensor, R: int, win
         raise StageFrontierError(SF_EINVAL, "sf_window_summary")
     dev = increment.device
     if out_stage_exposed is None:
-        out_stage_exposed = torch.empty((W, S), dtype=torch.int64, device=dev)
+        out_stage_exposed = _new((W, S), torch.int64, dev, stream)
     if out_lead_counts is None:
-        out_lead_counts = torch.empty((W, S, R), dtype=torch.int32, device=dev)
+        out_lead_counts = _new((W, S, R), torch.int32, dev, stream)
     if out_top2 is None:
-        out_top2 = torch.empty((W, 2, 2), dtype=torch.int32, device=dev)
+        out_top2 = _new((W, 2, 2), torch.int32, dev, stream)
     _check(out_stage_exposed, "out_stage_exposed", torch.int64, (W, S), like=increment)
     _check(out_lead_counts, "out_lead_counts", torch.int32, (W, S, R), like=increment)
     _check(out_top2, "out_top2", torch.int32, (W, 2, 2), like=increment)
@@ -256,9 +275,9 @@ def sf_window_lead_exposed(increment: torch.Tensor, leader: torch.Tensor, R: int
         raise StageFrontierError(SF_EINVAL, "sf_window_lead_exposed")
     dev = increment.device
     if out_lead_exposed is None:
-        out_lead_exposed = torch.empty((W, S, R), dtype=torch.int64, device=dev)
+        out_lead_exposed = _new((W, S, R), torch.int64, dev, stream)
     if out_top2 is None:
-        out_top2 = torch.empty((W, 2, 2), dtype=torch.int32, device=dev)
+        out_top2 = _new((W, 2, 2), torch.int32, dev, stream)
     _check(out_lead_exposed, "out_lead_exposed", torch.int64, (W, S, R), like=increment)
     _check(out_top2, "out_top2", torch.int32, (W, 2, 2), like=increment)
     rc = _lib.sf_window_lead_exposed(increment.data_ptr(), leader.data_ptr(), T, R, S, window,
@@ -290,9 +309,9 @@ def sf_window_leader_switches(leader: torch.Tensor, gap: torch.Tensor, ties: tor
         raise StageFrontierError(SF_EINVAL, "sf_window_leader_switches")
     dev = leader.device
     if out_switches is None:
-        out_switches = torch.empty((W, S), dtype=torch.int32, device=dev)
+        out_switches = _new((W, S), torch.int32, dev, stream)
     if out_eligible is None:
-        out_eligible = torch.empty((W, S), dtype=torch.int32, device=dev)
+        out_eligible = _new((W, S), torch.int32, dev, stream)
     _check(out_switches, "out_switches", torch.int32, (W, S), like=leader)
     _check(out_eligible, "out_eligible", torch.int32, (W, S), like=leader)
     rc = _lib.sf_window_leader_switches(leader.data_ptr(), gap.data_ptr(), ties.data_ptr(), T, S,
@@ -318,9 +337,9 @@ def sf_ingest(stages: torch.Tensor, wall: torch.Tensor, out_durations: torch.Ten
     _check(wall, "wall", torch.int64, (R, T), like=stages)
     dev = stages.device
     if out_durations is None:
-        out_durations = torch.empty((T, K + 1, R), dtype=torch.int64, device=dev)
+        out_durations = _new((T, K + 1, R), torch.int64, dev, stream)
     if out_overlap is None:
-        out_overlap = torch.empty((T, R), dtype=torch.int64, device=dev)
+        out_overlap = _new((T, R), torch.int64, dev, stream)
     _check(out_durations, "out_durations", torch.int64, (T, K + 1, R), like=stages)
     _check(out_overlap, "out_overlap", torch.int64, (T, R), like=stages)
     rc = _lib.sf_ingest(stages.data_ptr(), wall.data_ptr(), T, R, K, out_durations.data_ptr(),
@@ -341,9 +360,9 @@ def sf_route(stage_exposed: torch.Tensor, tau_num: int = 4, tau_den: int = 5,
     _check(stage_exposed, "stage_exposed", torch.int64, (W, S))
     dev = stage_exposed.device
     if out_order is None:
-        out_order = torch.empty((W, S), dtype=torch.int32, device=dev)
+        out_order = _new((W, S), torch.int32, dev, stream)
     if out_size is None:
-        out_size = torch.empty((W,), dtype=torch.int32, device=dev)
+        out_size = _new((W,), torch.int32, dev, stream)
     _check(out_order, "out_order", torch.int32, (W, S), like=stage_exposed)
     _check(out_size, "out_size", torch.int32, (W,), like=stage_exposed)
     rc = _lib.sf_route(stage_exposed.data_ptr(), W, S, tau_num, tau_den, out_order.data_ptr(),
@@ -377,7 +396,7 @@ def sf_exposure_gain(durations: torch.Tensor, baseline: torch.Tensor, window: in
     out = dict(out or {})
     for k, shp in shapes.items():
         if k not in out:
-            out[k] = torch.empty(shp, dtype=torch.int64, device=durations.device)
+            out[k] = _new(shp, torch.int64, durations.device, stream)
         _check(out[k], k, torch.int64, shp, like=durations)
     rc = _lib.sf_exposure_gain(durations.data_ptr(), baseline.data_ptr(), T, R, S, window,
                                *(out[k].data_ptr() for k in GAIN_FIELDS),
@@ -397,9 +416,9 @@ def sf_frontier_lag(durations: torch.Tensor, out_lag: torch.Tensor | None = None
     _check(durations, "durations", torch.int64, (T, S, R))
     dev = durations.device
     if out_lag is None:
-        out_lag = torch.empty((T, S), dtype=torch.int64, device=dev)
+        out_lag = _new((T, S), torch.int64, dev, stream)
     if out_lag_inc is None:
-        out_lag_inc = torch.empty((T, S), dtype=torch.int64, device=dev)
+        out_lag_inc = _new((T, S), torch.int64, dev, stream)
     _check(out_lag, "out_lag", torch.int64, (T, S), like=durations)
     _check(out_lag_inc, "out_lag_inc", torch.int64, (T, S), like=durations)
     rc = _lib.sf_frontier_lag(durations.data_ptr(), T, R, S, out_lag.data_ptr(),
@@ -423,9 +442,9 @@ def sf_rank_spread(durations: torch.Tensor, window: int, out_spread: torch.Tenso
     _check(durations, "durations", torch.int64, (T, S, R))
     dev = durations.device
     if out_spread is None:
-        out_spread = torch.empty((T, S), dtype=torch.int64, device=dev)
+        out_spread = _new((T, S), torch.int64, dev, stream)
     if out_window_spread is None:
-        out_window_spread = torch.empty((W, S), dtype=torch.int64, device=dev)
+        out_window_spread = _new((W, S), torch.int64, dev, stream)
     _check(out_spread, "out_spread", torch.int64, (T, S), like=durations)
     _check(out_window_spread, "out_window_spread", torch.int64, (W, S), like=durations)
     rc = _lib.sf_rank_spread(durations.data_ptr(), T, R, S, window, out_spread.data_ptr(),
@@ -448,7 +467,7 @@ def sf_window_median(durations: torch.Tensor, window: int, out_median: torch.Ten
     _check(durations, "durations", torch.int64, (T, S, R))
     dev = durations.device
     if out_median is None:
-        out_median = torch.empty((W, S, R), dtype=torch.int64, device=dev)
+        out_median = _new((W, S, R), torch.int64, dev, stream)
     _check(out_median, "out_median", torch.int64, (W, S, R), like=durations)
     rc = _lib.sf_window_median(durations.data_ptr(), T, R, S, window, out_median.data_ptr(),
                                _stream_handle(stream, dev))
@@ -483,7 +502,7 @@ def sf_read_xor(buf: torch.Tensor, out_xor: torch.Tensor | None = None, stream=N
         raise StageFrontierError(SF_EINVAL, "sf_read_xor")
     pieces = sf_read_xor_pieces(nbytes)
     if out_xor is None:
-        out_xor = torch.empty((pieces,), dtype=torch.int64, device=dev)
+        out_xor = _new((pieces,), torch.int64, dev, stream)
     _check(out_xor, "out_xor", torch.int64, (pieces,), like=buf)
     if nbytes == 0:
         return out_xor

@@ -885,3 +885,38 @@ def test_entry_points_on_a_side_stream(sf):
     np.testing.assert_array_equal(elc.cpu().numpy(), oel)
     oo, os_ = oracle.route(oe)
     np.testing.assert_array_equal(order.cpu().numpy(), oo)
+
+
+def test_side_stream_outside_stream_context(sf):
+    """Calls given a side stream while torch's current stream is another
+    one: the status word the binding allocates is cleared on the side
+    stream before the checked pass (so a violation is reported, not erased),
+    and outputs the binding allocates belong to that stream."""
+    T, S, R = 64, 5, 777
+    d = synth.random_durations(T, S, R, seed=31, hi=10**8)
+    d[T - 1, S - 1, R - 1] = -5  # outside the data contract
+    dd = torch.from_numpy(d).to(DEV)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    # long work on the current stream first, so an unordered clear there
+    # would land after the side stream's kernel
+    big = torch.ones((1 << 26,), dtype=torch.int64, device=DEV)
+    for _ in range(20):
+        big.mul_(1)
+    _, _, st = sf.sf_frontier_checked(dd, stream=side)
+    inc, lead = sf.sf_frontier(dd, stream=side)
+    side.synchronize()
+    assert int(st.cpu()[0]) == oracle.range_status(d) == sf.SF_ERANGE
+    torch.cuda.synchronize()
+    clean = np.abs(d)
+    dc = torch.from_numpy(clean).to(DEV)
+    torch.cuda.synchronize()
+    for _ in range(20):
+        big.mul_(1)
+    i2, l2, st2 = sf.sf_frontier_checked(dc, stream=side)
+    side.synchronize()
+    assert int(st2.cpu()[0]) == 0
+    oi, ol = oracle.frontier(clean)
+    np.testing.assert_array_equal(i2.cpu().numpy(), oi)
+    np.testing.assert_array_equal(l2.cpu().numpy(), ol)
+    torch.cuda.synchronize()
