@@ -9,24 +9,25 @@ a second, independently written statement.
 from __future__ import annotations
 
 
+def _prefix_matrix(step):
+    """``P[s][r] = sum_{j<=s} step[j][r]`` (Eq. (1)), row by row."""
+    P = []
+    for s, row in enumerate(step):
+        P.append([(P[s - 1][r] if s else 0) + x for r, x in enumerate(row)])
+    return P
+
+
 def frontier(d):
-    """``d[t][s][r]`` nested lists of ints -> ``(inc[t][s], lead[t][s])``."""
+    """``d[t][s][r]`` nested lists of ints -> ``(inc[t][s], lead[t][s])``.
+
+    Eq. (1) per step: the prefix matrix, then the frontier of every boundary
+    with its lowest leader, then the differences of the frontier."""
     inc, lead = [], []
     for step in d:
-        S = len(step)
-        R = len(step[0])
-        P = [0] * R
-        F_prev = 0
-        inc_t, lead_t = [], []
-        for s in range(S):
-            for r in range(R):
-                P[r] = P[r] + step[s][r]
-            F = max(P)
-            inc_t.append(F - F_prev)
-            lead_t.append(P.index(F))  # first (lowest) rank attaining F
-            F_prev = F
-        inc.append(inc_t)
-        lead.append(lead_t)
+        P = _prefix_matrix(step)
+        F = [max(row) for row in P]
+        lead.append([row.index(f) for row, f in zip(P, F)])  # first (lowest) rank attaining F
+        inc.append([f - (F[s - 1] if s else 0) for s, f in enumerate(F)])
     return inc, lead
 
 
@@ -107,28 +108,23 @@ def window_leader_switches(lead, gap, ties, window, min_gap=0):
 
 def frontier_evidence(d):
     """``d[t][s][r]`` -> dict of [t][s] lists: inc, lead, gap, ties,
-    stage_max, stage_sum (same readings as the C oracle)."""
+    stage_max, stage_sum (same readings as the C oracle), in the order of
+    ``frontier``: prefix matrix, per-boundary quantities, differences."""
     out = {k: [] for k in ("inc", "lead", "gap", "ties", "stage_max", "stage_sum")}
     for step in d:
-        S = len(step)
-        R = len(step[0])
-        P = [0] * R
-        F_prev = 0
-        rows = {k: [] for k in out}
-        for s in range(S):
-            P = [P[r] + step[s][r] for r in range(R)]
-            F = max(P)
-            leader = P.index(F)
-            others = sorted(P[:leader] + P[leader + 1:])
-            rows["inc"].append(F - F_prev)
-            rows["lead"].append(leader)
-            rows["gap"].append(F - others[-1] if others else -1)
-            rows["ties"].append(P.count(F))
-            rows["stage_max"].append(max(step[s]))
-            rows["stage_sum"].append(sum(step[s]))
-            F_prev = F
-        for k in out:
-            out[k].append(rows[k])
+        P = _prefix_matrix(step)
+        F = [max(row) for row in P]
+        leaders = [row.index(f) for row, f in zip(P, F)]
+        gaps = []
+        for row, L in zip(P, leaders):
+            others = sorted(row[:L] + row[L + 1:])
+            gaps.append(row[L] - others[-1] if others else -1)
+        out["lead"].append(leaders)
+        out["gap"].append(gaps)
+        out["ties"].append([row.count(f) for row, f in zip(P, F)])
+        out["stage_max"].append([max(x) for x in step])
+        out["stage_sum"].append([sum(x) for x in step])
+        out["inc"].append([f - (F[s - 1] if s else 0) for s, f in enumerate(F)])
     return out
 
 

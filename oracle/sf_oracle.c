@@ -12,9 +12,8 @@
  *   Sec. 3, Eq. (1):  P[t,r,s] = sum_{j<=s} d[t,r,j]
  *                     F[t,s]   = max_r P[t,r,s]
  *                     a[t,s]   = F[t,s] - F[t,s-1],  F[t,0] = 0 (1-based s)
- *   Sec. 3, the accounting core: one pass over steps; for each step the
- *   running prefix of every rank is advanced stage by stage and the
- *   frontier is re-taken at every boundary.
+ *   Each step is independent (Sec. 3 processes steps one at a time); per
+ *   step the oracle forms P, then F and the leaders, then the advances.
  *   Sec. 3, Eq. (2):  the window share numerator sum_{t in window} a[t,s].
  *   Sec. 4: top-2 routing = the two stages with the highest shares.
  *   Sec. 4, localization evidence: the tie set of the frontier and the gap
@@ -102,35 +101,48 @@
 #include <stdlib.h>
 #include <string.h>
 
-/* Frontier advances and leaders, Eq. (1).  Returns 0, or -1 if the prefix
- * scratch cannot be allocated. */
+/* Frontier advances and leaders, Eq. (1), taken in the order the equation
+ * defines them, one step at a time:
+ *   (i)   the rank-local prefix matrix P[s][r] = sum_{j<=s} d[t][j][r], each
+ *         row the previous row plus the stage's durations;
+ *   (ii)  the frontier F[s] = max_r P[s][r], then the leader: the lowest rank
+ *         whose prefix equals F[s];
+ *   (iii) the advances a[s] = F[s] - F[s-1], with F[-1] = 0 (the paper's
+ *         F_{t,0} = 0 in 1-based stages).
+ * Returns 0, or -1 if scratch cannot be allocated. */
 int sfo_frontier(const int64_t* d, int64_t T, int32_t R, int32_t S,
                  int64_t* inc, int32_t* lead)
 {
-    int64_t* P = (int64_t*)malloc(sizeof(int64_t) * (size_t)(R > 0 ? R : 1));
-    if (!P) return -1;
+    int64_t* P = (int64_t*)calloc((size_t)S * (size_t)R, sizeof(int64_t));
+    int64_t* F = (int64_t*)malloc(sizeof(int64_t) * (size_t)S);
+    if (!P || !F) {
+        free(P);
+        free(F);
+        return -1;
+    }
     for (int64_t t = 0; t < T; ++t) {
-        /* rank-local prefixes start at zero for every step */
-        for (int32_t r = 0; r < R; ++r) P[r] = 0;
-        int64_t F_prev = 0; /* F[t,0] = 0 */
+        const int64_t* m = d + t * S * (int64_t)R; /* d[t][s][r] = m[s * R + r] */
+        /* (i) the prefix matrix of the step */
+        for (int32_t s = 0; s < S; ++s)
+            for (int32_t r = 0; r < R; ++r)
+                P[(int64_t)s * R + r] = (s > 0 ? P[(int64_t)(s - 1) * R + r] : 0) + m[(int64_t)s * R + r];
+        /* (ii) the frontier of every boundary and its lowest leader */
         for (int32_t s = 0; s < S; ++s) {
-            const int64_t* row = d + (t * S + s) * (int64_t)R;
-            for (int32_t r = 0; r < R; ++r) P[r] += row[r];
-            /* F[t,s] = max over ranks; strict '>' keeps the lowest rank */
-            int64_t F = P[0];
-            int32_t L = 0;
-            for (int32_t r = 1; r < R; ++r) {
-                if (P[r] > F) {
-                    F = P[r];
-                    L = r;
-                }
-            }
-            inc[t * S + s] = F - F_prev;
+            const int64_t* row = P + (int64_t)s * R;
+            int64_t best = row[0];
+            for (int32_t r = 1; r < R; ++r)
+                if (row[r] > best) best = row[r];
+            F[s] = best;
+            int32_t L = -1;
+            for (int32_t r = 0; r < R && L < 0; ++r)
+                if (row[r] == best) L = r;
             lead[t * S + s] = L;
-            F_prev = F;
         }
+        /* (iii) the advances */
+        for (int32_t s = 0; s < S; ++s) inc[t * S + s] = F[s] - (s > 0 ? F[s - 1] : 0);
     }
     free(P);
+    free(F);
     return 0;
 }
 
@@ -281,57 +293,71 @@ void sfo_window_leader_switches(const int32_t* lead, const int64_t* gap, const i
 }
 
 /* Localization evidence and per-stage baselines of every boundary, with the
- * frontier advances and leaders of sfo_frontier.  Returns 0, or -1 if the
- * prefix scratch cannot be allocated. */
+ * frontier advances and leaders of sfo_frontier, in the same order:
+ *   (i)   the prefix matrix P[s][r] of the step;
+ *   (ii)  per boundary: F[s] = max_r P[s][r]; the leader, the lowest rank
+ *         attaining it; the tie set size #{r : P[s][r] = F[s]}; the runner-up,
+ *         the largest prefix of a rank other than the leader, and the gap
+ *         F[s] minus it (-1 when there is no other rank); the stage's max and
+ *         sum of d over ranks;
+ *   (iii) the advances a[s] = F[s] - F[s-1], F[-1] = 0.
+ * Returns 0, or -1 if scratch cannot be allocated. */
 int sfo_frontier_evidence(const int64_t* d, int64_t T, int32_t R, int32_t S,
                           int64_t* inc, int32_t* lead, int64_t* gap,
                           int32_t* ties, int64_t* stage_max, int64_t* stage_sum)
 {
-    int64_t* P = (int64_t*)malloc(sizeof(int64_t) * (size_t)(R > 0 ? R : 1));
-    if (!P) return -1;
+    int64_t* P = (int64_t*)calloc((size_t)S * (size_t)R, sizeof(int64_t));
+    int64_t* F = (int64_t*)malloc(sizeof(int64_t) * (size_t)S);
+    if (!P || !F) {
+        free(P);
+        free(F);
+        return -1;
+    }
     for (int64_t t = 0; t < T; ++t) {
-        for (int32_t r = 0; r < R; ++r) P[r] = 0;
-        int64_t F_prev = 0;
+        const int64_t* m = d + t * S * (int64_t)R;
+        /* (i) */
+        for (int32_t s = 0; s < S; ++s)
+            for (int32_t r = 0; r < R; ++r)
+                P[(int64_t)s * R + r] = (s > 0 ? P[(int64_t)(s - 1) * R + r] : 0) + m[(int64_t)s * R + r];
+        /* (ii) */
         for (int32_t s = 0; s < S; ++s) {
-            const int64_t* row = d + (t * S + s) * (int64_t)R;
-            int64_t dmax = row[0], dsum = 0;
-            for (int32_t r = 0; r < R; ++r) {
-                P[r] += row[r];
-                if (row[r] > dmax) dmax = row[r];
-                dsum += row[r];
-            }
-            /* frontier and lowest leader */
-            int64_t F = P[0];
-            int32_t L = 0;
-            for (int32_t r = 1; r < R; ++r) {
-                if (P[r] > F) {
-                    F = P[r];
-                    L = r;
-                }
-            }
-            /* tie set size and runner-up: the largest prefix of any rank
-             * other than the leader */
+            const int64_t* row = P + (int64_t)s * R;
+            const int64_t* ds = m + (int64_t)s * R;
+            int64_t best = row[0];
+            for (int32_t r = 1; r < R; ++r)
+                if (row[r] > best) best = row[r];
+            F[s] = best;
+            int32_t L = -1;
+            for (int32_t r = 0; r < R && L < 0; ++r)
+                if (row[r] == best) L = r;
             int32_t n_tie = 0;
+            for (int32_t r = 0; r < R; ++r)
+                if (row[r] == best) n_tie += 1;
             int64_t second = 0;
             int have_second = 0;
             for (int32_t r = 0; r < R; ++r) {
-                if (P[r] == F) n_tie += 1;
-                if (r != L && (!have_second || P[r] > second)) {
-                    second = P[r];
+                if (r != L && (!have_second || row[r] > second)) {
+                    second = row[r];
                     have_second = 1;
                 }
             }
+            int64_t dmax = ds[0], dsum = 0;
+            for (int32_t r = 0; r < R; ++r) {
+                if (ds[r] > dmax) dmax = ds[r];
+                dsum += ds[r];
+            }
             const int64_t i = t * S + s;
-            inc[i] = F - F_prev;
             lead[i] = L;
-            gap[i] = have_second ? F - second : -1;
+            gap[i] = have_second ? best - second : -1;
             ties[i] = n_tie;
             stage_max[i] = dmax;
             stage_sum[i] = dsum;
-            F_prev = F;
         }
+        /* (iii) */
+        for (int32_t s = 0; s < S; ++s) inc[t * S + s] = F[s] - (s > 0 ? F[s - 1] : 0);
     }
     free(P);
+    free(F);
     return 0;
 }
 

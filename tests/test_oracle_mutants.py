@@ -18,18 +18,20 @@ SRC = os.path.join(os.path.dirname(oracle.__file__), "sf_oracle.c")
 # body of that function
 MUTANTS = {
     # frontier
-    "tie_to_highest_rank": ("sfo_frontier", "if (P[r] > F) {", "if (P[r] >= F) {"),
-    "no_prefix_reset": ("sfo_frontier", "for (int32_t r = 0; r < R; ++r) P[r] = 0;", ""),
-    "stage_max_not_prefix": ("sfo_frontier", "for (int32_t r = 0; r < R; ++r) P[r] += row[r];",
-                             "for (int32_t r = 0; r < R; ++r) P[r] = row[r];"),
-    "transposed_layout": ("sfo_frontier", "for (int32_t r = 0; r < R; ++r) P[r] += row[r];",
-                          "for (int32_t r = 0; r < R; ++r) P[r] += d[(t * R + r) * (int64_t)S + s];"),
-    "absolute_not_advance": ("sfo_frontier", "F_prev = F;", ""),
-    "sign_flip": ("sfo_frontier", "inc[t * S + s] = F - F_prev;", "inc[t * S + s] = F_prev - F;"),
-    "rank_relabel": ("sfo_frontier", "L = r;", "L = R - 1 - r;"),
-    "start_leader_minus_one": ("sfo_frontier", "int32_t L = 0;", "int32_t L = -1;"),
-    "skip_first_rank_in_prefix": ("sfo_frontier", "for (int32_t r = 0; r < R; ++r) P[r] += row[r];",
-                                  "for (int32_t r = 1; r < R; ++r) P[r] += row[r];"),
+    "tie_to_highest_rank": ("sfo_frontier", "r < R && L < 0", "r < R"),
+    "no_prefix_reset": ("sfo_frontier", "(s > 0 ? P[(int64_t)(s - 1) * R + r] : 0)",
+                        "(s > 0 ? P[(int64_t)(s - 1) * R + r] : P[(int64_t)(S - 1) * R + r])"),
+    "stage_max_not_prefix": ("sfo_frontier", "(s > 0 ? P[(int64_t)(s - 1) * R + r] : 0) + ", ""),
+    "transposed_layout": ("sfo_frontier", "+ m[(int64_t)s * R + r];", "+ m[(int64_t)r * S + s];"),
+    "exclusive_prefix": ("sfo_frontier", "+ m[(int64_t)s * R + r];",
+                         "+ (s > 0 ? m[(int64_t)(s - 1) * R + r] : 0);"),
+    "absolute_not_advance": ("sfo_frontier", "F[s] - (s > 0 ? F[s - 1] : 0)", "F[s]"),
+    "sign_flip": ("sfo_frontier", "F[s] - (s > 0 ? F[s - 1] : 0)", "(s > 0 ? F[s - 1] : 0) - F[s]"),
+    "rank_relabel": ("sfo_frontier", "lead[t * S + s] = L;", "lead[t * S + s] = R - 1 - L;"),
+    "max_skips_last_rank": ("sfo_frontier", "for (int32_t r = 1; r < R; ++r)\n                if (row[r] > best)",
+                            "for (int32_t r = 1; r < R - 1; ++r)\n                if (row[r] > best)"),
+    "skip_first_rank_in_prefix": ("sfo_frontier", "for (int32_t r = 0; r < R; ++r)\n                P[",
+                                  "for (int32_t r = 1; r < R; ++r)\n                P["),
     # window summary
     "last_window_short": ("sfo_window_summary", "int64_t t1 = t0 + window < T ? t0 + window : T;",
                           "int64_t t1 = t0 + window < T ? t0 + window : T - 1;"),
@@ -76,22 +78,23 @@ MUTANTS = {
     "sw_short_window": ("sfo_window_leader_switches", "int64_t t1 = t0 + window < T ? t0 + window : T;",
                         "int64_t t1 = t0 + window < T ? t0 + window - 1 : T;"),
     # localization evidence and baselines
-    "ev_tie_to_highest_rank": ("sfo_frontier_evidence", "if (P[r] > F) {", "if (P[r] >= F) {"),
-    "ev_no_prefix_reset": ("sfo_frontier_evidence", "for (int32_t r = 0; r < R; ++r) P[r] = 0;", ""),
-    "ev_absolute_not_advance": ("sfo_frontier_evidence", "F_prev = F;", ""),
-    "ev_tie_count_excludes_leader": ("sfo_frontier_evidence", "if (P[r] == F) n_tie += 1;",
-                                     "if (P[r] == F && r != L) n_tie += 1;"),
+    "ev_tie_to_highest_rank": ("sfo_frontier_evidence", "r < R && L < 0", "r < R"),
+    "ev_no_prefix_reset": ("sfo_frontier_evidence", "(s > 0 ? P[(int64_t)(s - 1) * R + r] : 0)",
+                           "(s > 0 ? P[(int64_t)(s - 1) * R + r] : P[(int64_t)(S - 1) * R + r])"),
+    "ev_absolute_not_advance": ("sfo_frontier_evidence", "F[s] - (s > 0 ? F[s - 1] : 0)", "F[s]"),
+    "ev_tie_count_excludes_leader": ("sfo_frontier_evidence", "if (row[r] == best) n_tie += 1;",
+                                     "if (row[r] == best && r != L) n_tie += 1;"),
     "ev_runner_up_may_be_leader": ("sfo_frontier_evidence",
-                                   "if (r != L && (!have_second || P[r] > second)) {",
-                                   "if (!have_second || P[r] > second) {"),
-    "ev_gap_sign": ("sfo_frontier_evidence", "gap[i] = have_second ? F - second : -1;",
-                    "gap[i] = have_second ? second - F : -1;"),
-    "ev_single_rank_gap_zero": ("sfo_frontier_evidence", "gap[i] = have_second ? F - second : -1;",
-                                "gap[i] = have_second ? F - second : 0;"),
-    "ev_stage_max_of_prefix": ("sfo_frontier_evidence", "if (row[r] > dmax) dmax = row[r];",
-                               "if (P[r] > dmax) dmax = P[r];"),
-    "ev_stage_sum_skips_rank0": ("sfo_frontier_evidence", "dsum += row[r];",
-                                 "if (r) dsum += row[r];"),
+                                   "if (r != L && (!have_second || row[r] > second)) {",
+                                   "if (!have_second || row[r] > second) {"),
+    "ev_gap_sign": ("sfo_frontier_evidence", "gap[i] = have_second ? best - second : -1;",
+                    "gap[i] = have_second ? second - best : -1;"),
+    "ev_single_rank_gap_zero": ("sfo_frontier_evidence", "gap[i] = have_second ? best - second : -1;",
+                                "gap[i] = have_second ? best - second : 0;"),
+    "ev_stage_max_of_prefix": ("sfo_frontier_evidence", "if (ds[r] > dmax) dmax = ds[r];",
+                               "if (row[r] > dmax) dmax = row[r];"),
+    "ev_stage_sum_skips_rank0": ("sfo_frontier_evidence", "dsum += ds[r];",
+                                 "if (r) dsum += ds[r];"),
     # ingest
     "ingest_residual_unclamped": ("sfo_ingest", "d[(t * S + K) * R + r] = e > 0 ? e : 0;",
                                   "d[(t * S + K) * R + r] = e;"),
