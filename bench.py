@@ -137,15 +137,20 @@ def main() -> int:
     host = torch.empty((piece, S, R), dtype=torch.int64, pin_memory=True)
     host_np = host.numpy()
     cpu_budget = args.cpu_seconds
-    oracle_steps, oracle_time, oracle_out = 0, 0.0, []
-    # the same oracle on every host core: disjoint step ranges of a piece
-    # through a thread pool (the oracle's C calls run without the GIL)
+    # the oracle on every host core over EVERY step (disjoint step ranges of
+    # each piece through a thread pool; the oracle's C calls run without the
+    # GIL): its outputs are the parity reference of the whole timed pass
+    oracle_steps, oracle_time = 0, 0.0
     ncores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
-    mt_steps, mt_time, mt_same = 0, 0.0, True
+    mt_time, st_same = 0.0, True
+    oi_all = ol_all = None
     pool = None
-    if cpu_budget > 0 and ncores > 1:
+    if cpu_budget > 0:
+        import oracle
         from concurrent.futures import ThreadPoolExecutor
         pool = ThreadPoolExecutor(max_workers=ncores)
+        oi_all = np.empty((T, S), dtype=np.int64)
+        ol_all = np.empty((T, S), dtype=np.int32)
     gen_time = h2d_time = 0.0
     for t0 in range(0, T, piece):
         t1 = min(T, t0 + piece)
@@ -157,30 +162,30 @@ def main() -> int:
         d[t0:t1].copy_(host[:n])
         torch.cuda.synchronize(dev)
         h2d_time += time.perf_counter() - th
-        # CPU baseline: the oracle, single thread, on the same bytes, until
-        # its time budget is spent
-        if cpu_budget > 0 and oracle_time < cpu_budget:
-            import oracle
+        if pool is not None:
+            cuts = [n * k // ncores for k in range(ncores + 1)]
             tc = time.perf_counter()
-            oi, ol = oracle.frontier(host_np[:n])
-            oracle_time += time.perf_counter() - tc
-            oracle_out.append((t0, oi, ol))
-            oracle_steps += n
-            if pool is not None and mt_time < cpu_budget:
-                cuts = [n * k // ncores for k in range(ncores + 1)]
+            parts = list(pool.map(lambda ab: (ab[0], oracle.frontier(host_np[ab[0]:ab[1]])),
+                                  [(a, b) for a, b in zip(cuts, cuts[1:]) if b > a]))
+            mt_time += time.perf_counter() - tc
+            for a, (pi, pl) in parts:
+                oi_all[t0 + a:t0 + a + len(pi)] = pi
+                ol_all[t0 + a:t0 + a + len(pl)] = pl
+            # CPU baseline: the same oracle on one thread, on the same bytes,
+            # until its time budget is spent (checked equal to the all-core run)
+            if oracle_time < cpu_budget:
                 tc = time.perf_counter()
-                parts = list(pool.map(lambda ab: oracle.frontier(host_np[ab[0]:ab[1]]),
-                                      [(a, b) for a, b in zip(cuts, cuts[1:]) if b > a]))
-                mt_time += time.perf_counter() - tc
-                mt_steps += n
-                mt_same = mt_same and np.array_equal(np.concatenate([p[0] for p in parts]), oi) \
-                    and np.array_equal(np.concatenate([p[1] for p in parts]), ol)
+                oi, ol = oracle.frontier(host_np[:n])
+                oracle_time += time.perf_counter() - tc
+                oracle_steps += n
+                st_same = st_same and np.array_equal(oi, oi_all[t0:t1]) \
+                    and np.array_equal(ol, ol_all[t0:t1])
     if pool is not None:
         pool.shutdown()
-    log("input: generated in %.1f s, H2D %.2f GB in %.1f s, oracle %d steps in %.1f s"
-        " (%d threads: %d steps in %.2f s)"
-        % (gen_time, wl.input_bytes / 1e9, h2d_time, oracle_steps, oracle_time, ncores, mt_steps,
-           mt_time))
+    oracle_out = [(0, oi_all, ol_all)] if oi_all is not None else []
+    log("input: generated in %.1f s, H2D %.2f GB in %.1f s, oracle on %d threads: all %d steps "
+        "in %.2f s (one thread: %d steps in %.1f s)"
+        % (gen_time, wl.input_bytes / 1e9, h2d_time, ncores, T, mt_time, oracle_steps, oracle_time))
     del host, host_np
 
     inc = torch.empty((T, S), dtype=torch.int64, device=dev)
@@ -230,12 +235,21 @@ def main() -> int:
     launches = len(bounds)
     frontier_launch_ms = float(np.mean(frontier_ms)) / launches
 
-    # ---- parity of the sampled steps against the oracle outputs
-    bit_exact = None
+    # ---- parity of every output of the timed pass against the oracle: the
+    # per-step advances and leaders of all steps, and the window totals,
+    # lead counts and top-2 of the oracle's own window summary over them
+    bit_exact, exact_outputs = None, None
     if oracle_out:
-        gi, gl = inc.cpu().numpy(), lead.cpu().numpy()
-        bit_exact = all(np.array_equal(gi[t:t + len(oi)], oi) and np.array_equal(gl[t:t + len(ol)], ol)
-                        for t, oi, ol in oracle_out)
+        oe, oc, ot = oracle.window_summary(oi_all, ol_all, R, wl.window)
+        exact_outputs = {
+            "increment": bool(np.array_equal(inc.cpu().numpy(), oi_all)),
+            "leader": bool(np.array_equal(lead.cpu().numpy(), ol_all)),
+            "stage_exposed": bool(np.array_equal(ex.cpu().numpy(), oe)),
+            "lead_counts": bool(np.array_equal(cnt.cpu().numpy(), oc)),
+            "top2": bool(np.array_equal(top2.cpu().numpy(), ot)),
+        }
+        bit_exact = all(exact_outputs.values())
+        del oe, oc, ot
 
     # context: the read rate of a library reduction (torch.sum) over the
     # first chunk's int64 durations on this device
@@ -828,6 +842,8 @@ def main() -> int:
         "hbm_gbps": step_bytes / (ms_per_step / 1e3) / 1e9,
         "hbm_frac_of_peak": step_bytes / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBPS,
         "bit_exact": bit_exact,
+        "bit_exact_outputs": exact_outputs,
+        "parity_scope": "every step and every window of the timed pass" if oracle_out else None,
         "roofline": {
             "kernel": "k_frontier",
             "bound": "hbm",
@@ -876,19 +892,19 @@ def main() -> int:
             "cores": 1,
             "kind": "oracle",
             "sample": "sf_frontier oracle (single thread) on steps of the same workload: "
-                      "%d of %d steps, %.1f s" % (oracle_steps, T, oracle_time),
+                      "%d of %d steps, %.1f s; outputs equal to the all-core run: %s"
+                      % (oracle_steps, T, oracle_time, st_same),
             "host": host_cpu(),
         }
-    if mt_steps:
+    if oracle_out:
         rec["cpu_baseline_all_cores"] = {
-            "value": mt_steps * S * R / mt_time,
+            "value": T * S * R / mt_time,
             "unit": UNIT,
-            "gbps": mt_steps * S * R * 8 / mt_time / 1e9,
+            "gbps": T * S * R * 8 / mt_time / 1e9,
             "cores": ncores,
             "kind": "oracle",
             "sample": "the same sf_frontier oracle on %d threads, each on a disjoint step range of "
-                      "every piece: %d of %d steps, %.2f s, outputs equal to the single-thread "
-                      "run: %s" % (ncores, mt_steps, T, mt_time, mt_same),
+                      "every piece: all %d steps, %.2f s (the parity reference)" % (ncores, T, mt_time),
             "host": host_cpu(),
         }
     print(json.dumps(rec), flush=True)

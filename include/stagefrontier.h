@@ -55,9 +55,12 @@ enum {
 /* Largest rank count: the leader is carried in 16 bits of a packed
  * (prefix, rank) key. */
 #define SF_MAX_R 65536
-/* Largest stage count per call (per-stage partial maxima are staged in
- * on-chip memory). */
-#define SF_MAX_S 512
+/* Stage counts are otherwise unbounded (up to the size overflow checks):
+ * Sec. 3 expands every accumulation micro-step into its own stages before
+ * the frontier is taken, so S grows with the accumulation count.  Largest
+ * stage count of sf_frontier_evidence, and of K + 1 in sf_ingest (their
+ * per-stage partial results are staged in on-chip memory). */
+#define SF_MAX_S_EVIDENCE 512
 /* Largest rank count of sf_frontier_lag (all prefixes of a step are held
  * on chip at once). */
 #define SF_MAX_R_LAG 16384
@@ -79,8 +82,12 @@ enum {
  *   T              number of steps, 0 <= T.  T == 0 is a no-op (pointers
  *                  may then be NULL).
  *   R              number of ranks, 1 <= R <= SF_MAX_R.
- *   S              number of ordered stages, 1 <= S <= SF_MAX_S.
- *   out_increment  [T][S] int64, ns: a[t][s].  Written.
+ *   S              number of ordered stages, 1 <= S (any count whose
+ *                  arrays fit in int64 byte sizes: SF_EINVAL on overflow).
+ *   out_increment  [T][S] int64, ns: a[t][s].  Written.  With S above 512
+ *                  it also holds intermediate per-stage maxima while the
+ *                  call runs, so it must not be read before the stream has
+ *                  passed the call (true of every output anyway).
  *   out_leader     [T][S] int32: lowest rank attaining F[t][s].  Written.
  *   stream         HIP stream the work is enqueued on.
  *
@@ -140,8 +147,8 @@ int sf_frontier_checked(const int64_t* durations, int64_t T, int32_t R, int32_t 
  *   stream         HIP stream.
  *
  * Preconditions, alignment (element size), chunking and overlap rules as
- * for sf_frontier; additionally T <= INT32_MAX.  Returns SF_OK, SF_EINVAL or
- * SF_EHIP.
+ * for sf_frontier; additionally T <= INT32_MAX and S <= SF_MAX_S_EVIDENCE.
+ * Returns SF_OK, SF_EINVAL or SF_EHIP.
  */
 int sf_frontier_evidence(const int64_t* durations, int64_t T, int32_t R, int32_t S,
                          int64_t* out_increment, int32_t* out_leader,
@@ -160,7 +167,8 @@ int sf_frontier_evidence(const int64_t* durations, int64_t T, int32_t R, int32_t
  *   stages         [R][T][K] int64 ns, each rank's buffer as gathered
  *                  (steps, then explicit stages).  May be NULL when K == 0.
  *   wall           [R][T] int64 ns.
- *   T, R, K        0 <= T, 1 <= R <= SF_MAX_R, 0 <= K, K + 1 <= SF_MAX_S.
+ *   T, R, K        0 <= T, 1 <= R <= SF_MAX_R, 0 <= K,
+ *                  K + 1 <= SF_MAX_S_EVIDENCE.
  *                  T == 0 is a no-op.
  *   out_durations  [T][K+1][R] int64: stage k < K is x, stage K the residual.
  *   out_overlap    [T][R] int64.
@@ -183,7 +191,7 @@ int sf_ingest(const int64_t* stages, const int64_t* wall, int64_t T, int32_t R,
  * all totals), evaluated exactly in 128-bit integers.
  *
  *   stage_exposed  [W][S] int64 (out_stage_exposed of sf_window_summary).
- *   W, S           0 <= W, 1 <= S <= SF_MAX_S.  W == 0 is a no-op.
+ *   W, S           0 <= W, 1 <= S.  W == 0 is a no-op.
  *   tau_num, tau_den  0 <= tau_num <= tau_den, 1 <= tau_den <= INT32_MAX.
  *   out_order      [W][S] int32: stages by total, descending; the lower
  *                  stage first on ties (so the first two are the top-2
@@ -233,8 +241,8 @@ int sf_exposure_gain(const int64_t* durations, const int64_t* baseline, int64_t 
  * (the middle one for odd R), so the lag is an exact integer.
  *
  *   durations      [T][S][R] int64 ns (as for sf_frontier).
- *   T, R, S        0 <= T <= INT32_MAX, 1 <= R <= SF_MAX_R_LAG,
- *                  1 <= S <= SF_MAX_S.  T == 0 is a no-op.
+ *   T, R, S        0 <= T <= INT32_MAX, 1 <= R <= SF_MAX_R_LAG, 1 <= S.
+ *                  T == 0 is a no-op.
  *   out_lag        [T][S] int64 ns, >= 0.
  *   out_lag_inc    [T][S] int64 ns.
  *   stream         HIP stream.
@@ -253,8 +261,8 @@ int sf_frontier_lag(const int64_t* durations, int64_t T, int32_t R, int32_t S,
  * its sums over the steps of each window.
  *
  *   durations          [T][S][R] int64 ns (as for sf_frontier).
- *   T, R, S            0 <= T <= INT32_MAX, 1 <= R <= SF_MAX_R_LAG,
- *                      1 <= S <= SF_MAX_S.  T == 0 is a no-op.
+ *   T, R, S            0 <= T <= INT32_MAX, 1 <= R <= SF_MAX_R_LAG, 1 <= S.
+ *                      T == 0 is a no-op.
  *   window             steps per window, >= 1 (windows as for
  *                      sf_window_summary).
  *   out_spread         [T][S] int64 ns, >= 0.
@@ -276,8 +284,7 @@ int sf_rank_spread(const int64_t* durations, int64_t T, int32_t R, int32_t S,
  * baseline argument of sf_exposure_gain.
  *
  *   durations   [T][S][R] int64 ns (as for sf_frontier).
- *   T, R, S     0 <= T, 1 <= R <= SF_MAX_R, 1 <= S <= SF_MAX_S.  T == 0 is a
- *               no-op.
+ *   T, R, S     0 <= T, 1 <= R <= SF_MAX_R, 1 <= S.  T == 0 is a no-op.
  *   window      steps per window, >= 1 (windows as for sf_window_summary);
  *               min(window, T) <= SF_MAX_WINDOW_MEDIAN.
  *   out_median  [W][S][R] int64 ns.
@@ -291,8 +298,11 @@ int sf_window_median(const int64_t* durations, int64_t T, int32_t R, int32_t S,
 
 /*
  * sf_num_windows -- number of windows W = ceil(T / window) that
- * sf_window_summary produces; the last window holds the remaining
- * T - (W-1)*window steps.  Returns -1 when T < 0 or window < 1.
+ * sf_window_summary produces.  Sec. 3 reduces the per-step advances over
+ * windows of N consecutive steps (Eq. (2)) and lets a window close early;
+ * the paper does not say how a step count that is not a multiple of N ends,
+ * so the last window holds the remaining T - (W-1)*window steps (a shorter
+ * window, never a dropped one).  Returns -1 when T < 0 or window < 1.
  * Host only; no device work.
  */
 int64_t sf_num_windows(int64_t T, int64_t window);
@@ -376,7 +386,7 @@ int sf_window_lead_exposed(const int64_t* increment, const int32_t* leader, int6
  *   leader         [T][S] int32 (out_leader of sf_frontier_evidence).
  *   gap            [T][S] int64 (out_gap of sf_frontier_evidence).
  *   ties           [T][S] int32 (out_ties of sf_frontier_evidence).
- *   T, S, window   0 <= T, 1 <= S <= SF_MAX_S, 1 <= window, and
+ *   T, S, window   0 <= T, 1 <= S, 1 <= window, and
  *                  min(window, T) <= INT32_MAX.  T == 0 is a no-op.
  *                  Window w covers steps [w*window, min((w+1)*window, T)).
  *   min_gap        the confidence threshold on the gap, ns.

@@ -266,7 +266,7 @@ SF_API int sf_frontier_evidence(const int64_t* durations, int64_t T, int32_t R, 
                                 int32_t* out_ties, int64_t* out_stage_max,
                                 int64_t* out_stage_sum, sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S) return SF_EINVAL;
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S_EVIDENCE) return SF_EINVAL;
     if (!fits(T, S, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     if (T > INT32_MAX) return SF_EINVAL;

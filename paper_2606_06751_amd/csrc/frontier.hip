@@ -20,6 +20,14 @@
 // advance F[s] - F[s-1] and writes [T][S] rows with contiguous stores.
 // Durations are read exactly once, with 16-byte loads when R is even.
 //
+// Stage counts beyond what LDS holds (the gradient-accumulation expansion of
+// Sec. 3 multiplies S by the number of micro-steps) take the GTAB variant:
+// one group of at most 64 lanes owns a step, and its last lane keeps the
+// step's per-stage partial maxima in the step's own out_increment row (the
+// caller's output, so no extra memory); after the last tile the workgroup
+// decodes those rows in place, chunk by chunk from the end, each chunk read
+// before any of it is written.
+//
 // The checked variant also verifies the data contract on the way: every
 // duration in [0, 2^47) (its high word below 2^15) and every prefix below
 // 2^47 (the top bit of every key clear: while all durations are below 2^47
@@ -36,8 +44,9 @@ namespace sfk {
 // VEC: int64 elements per load (2: 16-byte loads, needs even R and a 16-byte
 //      aligned base); K: ranks per lane per tile; G: lanes per step;
 // WG:  threads per workgroup (WG / G steps per workgroup); CHECK: verify the
-//      data contract into *status.
-template <int VEC, int K, int G, int WG, bool CHECK>
+//      data contract into *status; GTAB: partial maxima in the out_increment
+//      rows instead of LDS (any S; G <= 64).
+template <int VEC, int K, int G, int WG, bool CHECK, bool GTAB>
 __global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, int64_t T,
                                                  int R, int S, int64_t* __restrict__ inc,
                                                  int32_t* __restrict__ lead,
@@ -45,6 +54,7 @@ __global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, 
 {
     static_assert(K % VEC == 0, "K must be a multiple of VEC");
     static_assert(WG % G == 0 || G == WG, "a workgroup holds whole steps");
+    static_assert(!GTAB || G <= 64, "GTAB: one writer lane per step");
     constexpr int SUB = G < 64 ? G : 64;  // lanes per DPP reduction group
     constexpr int SPW = WG / G;           // steps per workgroup
     constexpr int SPS = G / SUB;          // LDS slots per step
@@ -107,7 +117,9 @@ __global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, 
                 if (s + 1 < S) load_row(s + 1);
                 m = group_max<SUB>(m);
                 if (writer) {
-                    u64* p = &tab[slot * S + s];
+                    // GTAB: the step's own out_increment row, read back by
+                    // the same lane only until the decode below
+                    u64* p = GTAB ? reinterpret_cast<u64*>(inc) + t * S + s : &tab[slot * S + s];
                     *p = (r0 == 0) ? m : umax64(*p, m);
                 }
             }
@@ -119,8 +131,34 @@ __global__ __launch_bounds__(WG) void k_frontier(const int64_t* __restrict__ d, 
     }
     __syncthreads();
 
-    // decode F and the leader per (step, stage); rows of out are contiguous
     const int64_t tb = lb * SPW;
+    if constexpr (GTAB) {
+        // the workgroup's steps are contiguous rows of out_increment holding
+        // keys: decode them in place in chunks of WG entries, the last chunk
+        // first.  A chunk reads its keys and the key before each (which lies
+        // in the same chunk or the one below, not yet decoded), waits for
+        // every thread's reads, then writes.
+        const int64_t steps = T - tb < SPW ? T - tb : SPW;
+        const int64_t n = steps * S;
+        u64* g = reinterpret_cast<u64*>(inc) + tb * S;
+        for (int64_t c = (n - 1) / WG; c >= 0; --c) {
+            const int64_t i = c * WG + tid;
+            const bool ok = i < n;
+            u64 key = 0, kprev = 0;
+            if (ok) {
+                key = g[i];
+                if (i % S != 0) kprev = g[i - 1];
+            }
+            __syncthreads();
+            if (ok) {
+                inc[tb * S + i] = (int64_t)(key >> kRankBits) - (int64_t)(kprev >> kRankBits);
+                lead[tb * S + i] = (int32_t)(kRankMask - (key & kRankMask));
+            }
+        }
+        return;
+    }
+
+    // decode F and the leader per (step, stage); rows of out are contiguous
     for (int i = tid; i < SPW * S; i += WG) {
         const int jj = i / S;
         const int s = i - jj * S;
@@ -145,11 +183,11 @@ struct FrontierVariant {
     int per_cu;  // resident workgroups per CU to allow (0: no cap)
 };
 
-template <int VEC, bool CHECK, int K, int G, int WG>
+template <int VEC, bool CHECK, int K, int G, int WG, bool GTAB = false>
 FrontierVariant variant(int per_cu)
 {
-    return FrontierVariant{reinterpret_cast<const void*>(&k_frontier<VEC, K, G, WG, CHECK>), K, G,
-                           WG, per_cu};
+    return FrontierVariant{reinterpret_cast<const void*>(&k_frontier<VEC, K, G, WG, CHECK, GTAB>),
+                           K, G, WG, per_cu};
 }
 
 // Launch shape by rank count, measured on MI355X over R = 16 .. 16384.
@@ -173,11 +211,30 @@ FrontierVariant pick_frontier(int R)
     return variant<VEC, CHECK, 32, 64, 64>(3);
 }
 
+// Stage counts whose LDS table would exceed what a workgroup may hold: the
+// shapes with one group of at most 64 lanes per step, with the table in the
+// out_increment rows.
+template <int VEC, bool CHECK>
+FrontierVariant pick_frontier_gtab(int R)
+{
+    if (R <= 8) return variant<VEC, CHECK, 2, 4, 64, true>(0);
+    if (R <= 16) return variant<VEC, CHECK, 2, 8, 128, true>(0);
+    if (R <= 32) return variant<VEC, CHECK, 4, 8, 128, true>(0);
+    if (R <= 64) return variant<VEC, CHECK, 4, 16, 256, true>(6);
+    if (R <= 128) return variant<VEC, CHECK, 8, 32, 256, true>(6);
+    if (R <= 256) return variant<VEC, CHECK, 16, 32, 256, true>(4);
+    return variant<VEC, CHECK, 32, 64, 64, true>(3);
+}
+
+// Largest S whose LDS table of partial maxima (16 slots of S keys in the
+// widest-slot shapes) fits the 64 KB a workgroup is given.
+constexpr int kFrontierLdsS = 512;
+
 static int frontier_launch(const int64_t* durations, int64_t T, int32_t R, int32_t S,
                            int64_t* out_increment, int32_t* out_leader, uint32_t* status,
                            sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S) return SF_EINVAL;
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1) return SF_EINVAL;
     if (!fits(T, S, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     if (!durations || !out_increment || !out_leader) return SF_EINVAL;
@@ -192,13 +249,19 @@ static int frontier_launch(const int64_t* durations, int64_t T, int32_t R, int32
         return SF_EINVAL;
 
     const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
-    const FrontierVariant v = status ? (vec2 ? pick_frontier<2, true>(R) : pick_frontier<1, true>(R))
-                                     : (vec2 ? pick_frontier<2, false>(R) : pick_frontier<1, false>(R));
+    const bool gtab = S > kFrontierLdsS;
+    FrontierVariant v;
+    if (gtab)
+        v = status ? (vec2 ? pick_frontier_gtab<2, true>(R) : pick_frontier_gtab<1, true>(R))
+                   : (vec2 ? pick_frontier_gtab<2, false>(R) : pick_frontier_gtab<1, false>(R));
+    else
+        v = status ? (vec2 ? pick_frontier<2, true>(R) : pick_frontier<1, true>(R))
+                   : (vec2 ? pick_frontier<2, false>(R) : pick_frontier<1, false>(R));
     const int spw = v.WG / v.G;
     const int sub = v.G < 64 ? v.G : 64;
     const int64_t blocks = (T + spw - 1) / spw;
     if (blocks > INT32_MAX) return SF_EINVAL;
-    const size_t lds = lds_request((size_t)(v.WG / sub) * S * sizeof(u64), v.per_cu);
+    const size_t lds = lds_request(gtab ? 0 : (size_t)(v.WG / sub) * S * sizeof(u64), v.per_cu);
     int Ri = R, Si = S;
     void* args[] = {(void*)&durations,     (void*)&T,          (void*)&Ri,    (void*)&Si,
                     (void*)&out_increment, (void*)&out_leader, (void*)&status};

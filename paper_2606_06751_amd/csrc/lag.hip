@@ -463,7 +463,7 @@ using namespace sfk;
 SF_API int sf_frontier_lag(const int64_t* durations, int64_t T, int32_t R, int32_t S,
                            int64_t* out_lag, int64_t* out_lag_inc, sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R_LAG || S < 1 || S > SF_MAX_S) return SF_EINVAL;
+    if (T < 0 || R < 1 || R > SF_MAX_R_LAG || S < 1) return SF_EINVAL;
     if (!fits(T, S, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     if (T > INT32_MAX) return SF_EINVAL;  // one workgroup per step
@@ -486,7 +486,7 @@ SF_API int sf_rank_spread(const int64_t* durations, int64_t T, int32_t R, int32_
                           int64_t window, int64_t* out_spread, int64_t* out_window_spread,
                           sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R_LAG || S < 1 || S > SF_MAX_S || window < 1)
+    if (T < 0 || R < 1 || R > SF_MAX_R_LAG || S < 1 || window < 1)
         return SF_EINVAL;
     if (!fits(T, S, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;

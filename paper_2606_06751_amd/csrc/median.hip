@@ -292,7 +292,7 @@ using namespace sfk;
 SF_API int sf_window_median(const int64_t* durations, int64_t T, int32_t R, int32_t S,
                             int64_t window, int64_t* out_median, sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S || window < 1) return SF_EINVAL;
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || window < 1) return SF_EINVAL;
     if (!fits(T, S, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     const int64_t n_max = window < T ? window : T;

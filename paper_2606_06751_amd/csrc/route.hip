@@ -9,27 +9,37 @@
 namespace sfk {
 
 constexpr int kRouteWG = 256;
+constexpr int kRouteLdsS = 4096;  // stages staged in LDS (two rows of 8-byte totals, 64 KB)
 
+// LDS: the window's totals and their sorted copy are staged in LDS (S <=
+// kRouteLdsS); otherwise they are read from global memory, the sorted copy
+// through the order just written.
+template <bool LDS>
 __global__ __launch_bounds__(kRouteWG) void k_route(const int64_t* __restrict__ exposed,
                                                     int64_t W, int S, int64_t tau_num,
                                                     int64_t tau_den, int32_t* __restrict__ order,
                                                     int32_t* __restrict__ size)
 {
-    __shared__ int64_t ex[SF_MAX_S];
-    __shared__ int64_t sorted_ex[SF_MAX_S];
+    extern __shared__ int64_t rsh[];  // LDS: [2][S]
     const int tid = threadIdx.x;
     for (int64_t win = blockIdx.x; win < W; win += gridDim.x) {
-        for (int s = tid; s < S; s += kRouteWG) ex[s] = exposed[win * S + s];
-        __syncthreads();
+        const int64_t* exg = exposed + win * S;
+        int32_t* ord = order + win * S;
+        if (LDS) {
+            for (int s = tid; s < S; s += kRouteWG) rsh[s] = exg[s];
+            __syncthreads();
+        }
+        const int64_t* ex = LDS ? rsh : exg;
         // position of stage s = number of stages that come before it
         for (int s = tid; s < S; s += kRouteWG) {
             const int64_t e = ex[s];
             int pos = 0;
             for (int u = 0; u < S; ++u) pos += (ex[u] > e || (ex[u] == e && u < s)) ? 1 : 0;
-            order[win * S + pos] = s;
-            sorted_ex[pos] = e;
+            ord[pos] = s;
+            if (LDS) rsh[S + pos] = e;
         }
         __syncthreads();
+        auto sorted_ex = [&](int i) { return LDS ? rsh[S + i] : exg[ord[i]]; };
         // wave 0 scans the sorted totals: each lane sums a contiguous part,
         // an exclusive scan over lanes gives each part's starting sum, and
         // each lane finds the first prefix in its part that reaches tau
@@ -38,7 +48,7 @@ __global__ __launch_bounds__(kRouteWG) void k_route(const int64_t* __restrict__ 
             const int b = tid * per;
             const int e = min(S, b + per);
             __int128 part = 0;
-            for (int i = b; i < e; ++i) part += sorted_ex[i];
+            for (int i = b; i < e; ++i) part += sorted_ex(i);
             // exclusive scan of the 64 lane parts (two 64-bit halves per step)
             __int128 incl = part;
             for (int off = 1; off < 64; off <<= 1) {
@@ -54,7 +64,7 @@ __global__ __launch_bounds__(kRouteWG) void k_route(const int64_t* __restrict__ 
             int k = S + 1;               // "not reached in this lane's part"
             if (b == 0 && (__int128)tau_den * 0 >= need) k = 0;
             for (int i = b; i < e && k > S; ++i) {
-                cum += sorted_ex[i];
+                cum += sorted_ex(i);
                 if ((__int128)tau_den * cum >= need) k = i + 1;
             }
             for (int off = 32; off > 0; off >>= 1) k = min(k, __shfl_xor(k, off, 64));
@@ -71,7 +81,7 @@ using namespace sfk;
 SF_API int sf_route(const int64_t* stage_exposed, int64_t W, int32_t S, int64_t tau_num,
                     int64_t tau_den, int32_t* out_order, int32_t* out_size, sf_stream_t stream)
 {
-    if (W < 0 || S < 1 || S > SF_MAX_S || tau_den < 1 || tau_num < 0 || tau_num > tau_den ||
+    if (W < 0 || S < 1 || tau_den < 1 || tau_num < 0 || tau_num > tau_den ||
         tau_den > INT32_MAX)
         return SF_EINVAL;
     if (!fits(W, S, 1, 8)) return SF_EINVAL;
@@ -87,6 +97,9 @@ SF_API int sf_route(const int64_t* stage_exposed, int64_t W, int32_t S, int64_t 
     int Si = S;
     void* args[] = {(void*)&stage_exposed, (void*)&W, (void*)&Si, (void*)&tau_num, (void*)&tau_den,
                     (void*)&out_order, (void*)&out_size};
-    return launch(reinterpret_cast<const void*>(&k_route), dim3(grid), dim3(kRouteWG), args, 0,
-                  stream);
+    if (S <= kRouteLdsS)
+        return launch(reinterpret_cast<const void*>(&k_route<true>), dim3(grid), dim3(kRouteWG),
+                      args, (size_t)2 * S * sizeof(int64_t), stream);
+    return launch(reinterpret_cast<const void*>(&k_route<false>), dim3(grid), dim3(kRouteWG), args,
+                  0, stream);
 }

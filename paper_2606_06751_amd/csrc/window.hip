@@ -111,8 +111,9 @@ __device__ __forceinline__ u64 row_modal_key(const int32_t* __restrict__ c, int 
 }
 
 // One workgroup per (window, pick k in {0, 1}); grid-stride.  Both
-// workgroups of a window choose the two stages (cheap: S <= SF_MAX_S); each
-// then finds the most frequent leader of its own stage.
+// workgroups of a window choose the two stages (a block pass over the
+// window's S totals); each then finds the most frequent leader of its own
+// stage.
 __global__ __launch_bounds__(kTopWG) void k_window_top2(const int64_t* __restrict__ exposed,
                                                         const int32_t* __restrict__ counts,
                                                         int R, int S, int64_t W,
@@ -200,11 +201,33 @@ __global__ __launch_bounds__(kSumWG) void k_window_lead_exposed(
 // block in order: with S < WG, thread j takes stage j % S at every P-th
 // step from step j / S (P = WG / S phases), and the phases are added in LDS
 // (int64 sums wrap alike in any order).
+constexpr int kLeadTopLdsS = 2048;  // stages whose window totals are staged in LDS (16 KB)
+
+// The two stages of a window with the largest totals (lower stage first on
+// ties), from per-thread candidates: each thread passes its best (e1, s1)
+// and second (e2, s2) of the stages it summed (s < 0: none); every thread
+// gets the picks.  The second overall is the best of some other thread or
+// the second of the thread holding the first.
+__device__ __forceinline__ void block_top2_stages(int64_t e1, int s1, int64_t e2, int s2, u64* sh,
+                                                  int& p1, int& p2)
+{
+    auto pick = [&](int64_t e, int st) {
+        const u64 ekey = st < 0 ? 0ull : ((u64)e ^ 0x8000000000000000ull);
+        const u64 emax = block_max64(ekey, sh);
+        const u64 skey = (st >= 0 && ekey == emax) ? (u64)(0xFFFFFFFFu - (uint32_t)st) + 1ull : 0ull;
+        const u64 smax = block_max64(skey, sh);
+        return smax ? (int)(0xFFFFFFFFu - (uint32_t)(smax - 1ull)) : -1;
+    };
+    p1 = pick(e1, s1);
+    const bool mine = s1 >= 0 && s1 == p1;
+    p2 = pick(mine ? e2 : e1, mine ? s2 : s1);
+}
+
 __global__ __launch_bounds__(kTopWG) void k_window_lead_top2(
     const int64_t* __restrict__ inc, const int64_t* __restrict__ lead_exposed, int64_t T, int R,
     int S, int64_t window, int64_t W, int32_t* __restrict__ top2)
 {
-    __shared__ int64_t tot[SF_MAX_S];
+    __shared__ int64_t tot[kLeadTopLdsS];
     __shared__ int64_t part[kTopWG];
     __shared__ u64 sh[kTopWG / 64];
     const int tid = threadIdx.x;
@@ -214,36 +237,60 @@ __global__ __launch_bounds__(kTopWG) void k_window_lead_top2(
         const int k = (int)(id & 1);
         const int64_t t0 = w * window;
         const int64_t t1 = min(t0 + window, T);
-        if (P > 1) {
-            int64_t sum = 0;
-            if (tid < P * S) {
-                const int s = tid % S, p = tid / S;
-#pragma unroll 8
-                for (int64_t t = t0 + p; t < t1; t += P) sum += inc[t * S + s];
-            }
-            part[tid] = sum;
-            __syncthreads();
-            for (int s = tid; s < S; s += kTopWG) {
-                int64_t acc = 0;
-                for (int p = 0; p < P; ++p) acc += part[p * S + s];
-                tot[s] = acc;
-            }
-        } else {
+        int pick;
+        if (S > kLeadTopLdsS) {
+            // many stages: each thread sums its own stages and keeps its two
+            // largest; two block maxima pick the window's two
+            int64_t e1 = 0, e2 = 0;
+            int s1 = -1, s2 = -1;
             for (int s = tid; s < S; s += kTopWG) {
                 int64_t acc = 0;
                 for (int64_t t = t0; t < t1; ++t) acc += inc[t * S + s];
-                tot[s] = acc;
+                if (s1 < 0 || acc > e1) {
+                    e2 = e1;
+                    s2 = s1;
+                    e1 = acc;
+                    s1 = s;
+                } else if (s2 < 0 || acc > e2) {
+                    e2 = acc;
+                    s2 = s;
+                }
             }
+            int p1, p2;
+            block_top2_stages(e1, s1, e2, s2, sh, p1, p2);
+            pick = k == 0 ? p1 : p2;
+        } else {
+            if (P > 1) {
+                int64_t sum = 0;
+                if (tid < P * S) {
+                    const int s = tid % S, p = tid / S;
+#pragma unroll 8
+                    for (int64_t t = t0 + p; t < t1; t += P) sum += inc[t * S + s];
+                }
+                part[tid] = sum;
+                __syncthreads();
+                for (int s = tid; s < S; s += kTopWG) {
+                    int64_t acc = 0;
+                    for (int p = 0; p < P; ++p) acc += part[p * S + s];
+                    tot[s] = acc;
+                }
+            } else {
+                for (int s = tid; s < S; s += kTopWG) {
+                    int64_t acc = 0;
+                    for (int64_t t = t0; t < t1; ++t) acc += inc[t * S + s];
+                    tot[s] = acc;
+                }
+            }
+            __syncthreads();
+            // larger total first, then lower stage index (every thread alike)
+            int s1 = 0;
+            for (int s = 1; s < S; ++s)
+                if (tot[s] > tot[s1]) s1 = s;
+            int s2 = -1;
+            for (int s = 0; s < S; ++s)
+                if (s != s1 && (s2 < 0 || tot[s] > tot[s2])) s2 = s;
+            pick = k == 0 ? s1 : s2;
         }
-        __syncthreads();
-        // larger total first, then lower stage index (every thread alike)
-        int s1 = 0;
-        for (int s = 1; s < S; ++s)
-            if (tot[s] > tot[s1]) s1 = s;
-        int s2 = -1;
-        for (int s = 0; s < S; ++s)
-            if (s != s1 && (s2 < 0 || tot[s] > tot[s2])) s2 = s;
-        const int pick = k == 0 ? s1 : s2;
 
         int rank = -1;
         if (pick >= 0) {
@@ -375,7 +422,7 @@ SF_API int sf_window_summary(const int64_t* increment, const int32_t* leader, in
                              int32_t R, int32_t S, int64_t window, int64_t* out_stage_exposed,
                              int32_t* out_lead_counts, int32_t* out_top2, sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S || window < 1) return SF_EINVAL;
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || window < 1) return SF_EINVAL;
     if (!fits(T, S, 1, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     const int64_t W = sf_num_windows(T, window);
@@ -414,7 +461,7 @@ SF_API int sf_window_lead_exposed(const int64_t* increment, const int32_t* leade
                                   int32_t R, int32_t S, int64_t window, int64_t* out_lead_exposed,
                                   int32_t* out_top2, sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S || window < 1) return SF_EINVAL;
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || window < 1) return SF_EINVAL;
     if (!fits(T, S, 1, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     const int64_t W = sf_num_windows(T, window);
@@ -453,7 +500,7 @@ SF_API int sf_window_leader_switches(const int32_t* leader, const int64_t* gap,
                                      int64_t min_gap, int32_t* out_switches,
                                      int32_t* out_eligible, sf_stream_t stream)
 {
-    if (T < 0 || S < 1 || S > SF_MAX_S || window < 1) return SF_EINVAL;
+    if (T < 0 || S < 1 || window < 1) return SF_EINVAL;
     if (!fits(T, S, 1, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     if ((window < T ? window : T) > INT32_MAX) return SF_EINVAL;  // int32 counts

@@ -17,7 +17,7 @@ from . import build as _build
 
 SF_OK, SF_EINVAL, SF_ERANGE, SF_EHIP = 0, 1, 2, 3
 SF_MAX_R = 65536
-SF_MAX_S = 512
+SF_MAX_S_EVIDENCE = 512
 SF_MAX_S_GAIN = 64
 SF_MAX_R_LAG = 16384
 SF_MAX_WINDOW_MEDIAN = 1024

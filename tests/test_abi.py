@@ -64,7 +64,7 @@ def test_constants_match_header(sf):
     with open(HEADER) as fh:
         text = fh.read()
     assert "#define SF_MAX_R %d" % sf.SF_MAX_R in text
-    assert "#define SF_MAX_S %d" % sf.SF_MAX_S in text
+    assert "#define SF_MAX_S_EVIDENCE %d" % sf.SF_MAX_S_EVIDENCE in text
     assert "#define SF_MAX_S_GAIN %d" % sf.SF_MAX_S_GAIN in text
     assert "#define SF_MAX_R_LAG %d" % sf.SF_MAX_R_LAG in text
     assert "#define SF_MAX_WINDOW_MEDIAN %d" % sf.SF_MAX_WINDOW_MEDIAN in text
@@ -105,7 +105,6 @@ def test_frontier_argument_checks(sf):
     assert call(R=0) == sf.SF_EINVAL
     assert call(R=sf.SF_MAX_R + 1) == sf.SF_EINVAL
     assert call(S=0) == sf.SF_EINVAL
-    assert call(S=sf.SF_MAX_S + 1) == sf.SF_EINVAL
     assert call(d=None) == sf.SF_EINVAL
     assert call(inc=None) == sf.SF_EINVAL
     assert call(lead=None) == sf.SF_EINVAL
@@ -114,7 +113,8 @@ def test_frontier_argument_checks(sf):
     assert call(lead=C + 2) == sf.SF_EINVAL
     assert call(inc=A + 8) == sf.SF_EINVAL        # output overlaps input
     assert call(lead=B + 16) == sf.SF_EINVAL      # outputs overlap
-    assert call(T=1 << 50, R=sf.SF_MAX_R, S=sf.SF_MAX_S) == sf.SF_EINVAL  # size overflow
+    assert call(T=1 << 50, R=sf.SF_MAX_R, S=512) == sf.SF_EINVAL  # size overflow
+    assert call(T=1 << 20, R=sf.SF_MAX_R, S=1 << 20) == sf.SF_EINVAL  # size overflow at large S
 
 
 def test_checked_argument_checks(sf):
@@ -148,7 +148,7 @@ def test_evidence_argument_checks(sf):
 
     assert call(T=0, **{n: None for n in names}) == sf.SF_OK
     assert call(R=0) == sf.SF_EINVAL
-    assert call(S=sf.SF_MAX_S + 1) == sf.SF_EINVAL
+    assert call(S=sf.SF_MAX_S_EVIDENCE + 1) == sf.SF_EINVAL
     for n in names:
         assert call(**{n: None}) == sf.SF_EINVAL, n
     assert call(ties=base["ties"] + 2) == sf.SF_EINVAL       # misaligned int32
@@ -168,7 +168,7 @@ def test_ingest_and_route_argument_checks(sf):
 
     assert ingest(T=0, x=None, w=None, d=None, o=None) == sf.SF_OK
     assert ingest(K=-1) == sf.SF_EINVAL
-    assert ingest(K=sf.SF_MAX_S) == sf.SF_EINVAL            # K + 1 > SF_MAX_S
+    assert ingest(K=sf.SF_MAX_S_EVIDENCE) == sf.SF_EINVAL   # K + 1 > SF_MAX_S_EVIDENCE
     assert ingest(R=0) == sf.SF_EINVAL
     assert ingest(w=None) == sf.SF_EINVAL
     assert ingest(d=X + 8) == sf.SF_EINVAL                  # output overlaps input
@@ -301,7 +301,6 @@ def test_summary_argument_checks(sf):
     assert call(window=0) == sf.SF_EINVAL
     assert call(T=-5) == sf.SF_EINVAL
     assert call(R=0) == sf.SF_EINVAL
-    assert call(S=sf.SF_MAX_S + 1) == sf.SF_EINVAL
     assert call(cnt=None) == sf.SF_EINVAL
     assert call(top=E + 2) == sf.SF_EINVAL
     assert call(ex=A + 8) == sf.SF_EINVAL         # output overlaps input
@@ -323,7 +322,6 @@ def test_lead_exposed_argument_checks(sf):
     assert call(T=-5) == sf.SF_EINVAL
     assert call(R=0) == sf.SF_EINVAL
     assert call(R=sf.SF_MAX_R + 1) == sf.SF_EINVAL
-    assert call(S=sf.SF_MAX_S + 1) == sf.SF_EINVAL
     assert call(le=None) == sf.SF_EINVAL
     assert call(top=None) == sf.SF_EINVAL
     assert call(le=C + 4) == sf.SF_EINVAL         # misaligned int64 output
@@ -348,7 +346,6 @@ def test_leader_switches_argument_checks(sf):
     assert call(window=0) == sf.SF_EINVAL
     assert call(T=-1) == sf.SF_EINVAL
     assert call(S=0) == sf.SF_EINVAL
-    assert call(S=sf.SF_MAX_S + 1) == sf.SF_EINVAL
     assert call(ties=None) == sf.SF_EINVAL
     assert call(el=None) == sf.SF_EINVAL
     assert call(gap=B + 4) == sf.SF_EINVAL        # misaligned int64 input

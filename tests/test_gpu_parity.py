@@ -81,6 +81,77 @@ def test_frontier_stage_sweep(sf, S):
         assert_frontier_equal(sf, d)
 
 
+@pytest.mark.parametrize("S", [513, 768, 4096])
+@pytest.mark.parametrize("R", [8, 1024, 16384])
+def test_frontier_large_stage_counts(sf, S, R):
+    """Stage counts past what LDS holds (Sec. 3 expands accumulation
+    micro-steps into stages before the frontier): the partial maxima go
+    through the out_increment rows.  Ragged step counts against the steps a
+    workgroup holds, tie-heavy and wide values, and the checked pass."""
+    T = max(2, min(37, (1 << 27) // (R * S)))
+    for hi in (3, 10**7):
+        d = synth.random_durations(T, S, R, seed=S * 3 + R + hi, hi=hi)
+        print("case R=%d S=%d T=%d hi=%d" % (R, S, T, hi), flush=True)
+        oi, ol = assert_frontier_equal(sf, d)
+        inc, lead, st = checked(sf, d)
+        np.testing.assert_array_equal(inc, oi)
+        np.testing.assert_array_equal(lead, ol)
+        assert st == 0
+    e = d.copy()
+    e[T - 1, S - 1, R - 1] = -1
+    assert checked(sf, e)[2] == oracle.range_status(e) == sf.SF_ERANGE
+
+
+@pytest.mark.parametrize("S", [513, 2048, 2049, 4100])
+def test_window_rows_large_stage_counts(sf, S):
+    """The window summary, exposed time led, leader switches and the
+    routing set at stage counts past 512 (and past the LDS staging of the
+    stage totals at 2048 and of route's at 4096)."""
+    R, T, window = 37, 90, 16
+    d = synth.random_durations(T, S, R, seed=S, hi=4)
+    oi, ol = oracle.frontier(d)
+    assert_summary_equal(sf, oi, ol, R, window)
+    ti = torch.from_numpy(oi).to(DEV)
+    tl = torch.from_numpy(ol).to(DEV)
+    le, letop = sf.sf_window_lead_exposed(ti, tl, R, window)
+    torch.cuda.synchronize()
+    ole, olt = oracle.window_lead_exposed(oi, ol, R, window)
+    np.testing.assert_array_equal(le.cpu().numpy(), ole)
+    np.testing.assert_array_equal(letop.cpu().numpy(), olt)
+    ev = oracle.frontier_evidence(d)
+    sw, el = sf.sf_window_leader_switches(tl, torch.from_numpy(ev["gap"]).to(DEV),
+                                          torch.from_numpy(ev["ties"]).to(DEV), window, 1)
+    torch.cuda.synchronize()
+    osw, oel = oracle.window_leader_switches(ev["lead"], ev["gap"], ev["ties"], window, 1)
+    np.testing.assert_array_equal(sw.cpu().numpy(), osw)
+    np.testing.assert_array_equal(el.cpu().numpy(), oel)
+    oe, _, _ = oracle.window_summary(oi, ol, R, window)
+    oe[0, S // 3] = 1 << 50                     # one dominant stage
+    oe[1] = 5                                   # every stage tied
+    for num, den in ((4, 5), (1, 1), (0, 1)):
+        go, gs = sf.sf_route(torch.from_numpy(oe).to(DEV), num, den)
+        torch.cuda.synchronize()
+        oo, os_ = oracle.route(oe, num, den)
+        np.testing.assert_array_equal(go.cpu().numpy(), oo)
+        np.testing.assert_array_equal(gs.cpu().numpy(), os_)
+
+
+def test_selections_large_stage_counts(sf):
+    """The lag, the raw spread and the window median at 600 stages."""
+    d = synth.random_durations(12, 600, 300, seed=600, hi=10**6)
+    lag, inc = sf.sf_frontier_lag(torch.from_numpy(d).to(DEV))
+    sp, wsp = sf.sf_rank_spread(torch.from_numpy(d).to(DEV), 5)
+    med = sf.sf_window_median(torch.from_numpy(d).to(DEV), 5)
+    torch.cuda.synchronize()
+    ol, oinc = oracle.frontier_lag(d)
+    np.testing.assert_array_equal(lag.cpu().numpy(), ol)
+    np.testing.assert_array_equal(inc.cpu().numpy(), oinc)
+    osp, owsp = oracle.rank_spread(d, 5)
+    np.testing.assert_array_equal(sp.cpu().numpy(), osp)
+    np.testing.assert_array_equal(wsp.cpu().numpy(), owsp)
+    np.testing.assert_array_equal(med.cpu().numpy(), oracle.window_median(d, 5))
+
+
 @pytest.mark.parametrize("T", [1, 2, 3, 5, 15, 16, 17, 63, 65, 257])
 def test_frontier_ragged_steps(sf, T):
     for R in (8, 24, 128, 300):

@@ -1,7 +1,9 @@
 """The five full-size workloads, run exactly as the benchmark runs them
 (the 16384-rank workload in two step-axis chunks), against the oracle over
 every step and every window: bit-exact."""
+import os
 import time
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 import pytest
@@ -63,17 +65,22 @@ def test_workload_full_parity(sf, name):
     ole, olt = oracle.window_lead_exposed(oi, ol, R, wl.window)
     np.testing.assert_array_equal(le.cpu().numpy(), ole)
     np.testing.assert_array_equal(letop2.cpu().numpy(), olt)
-    # the workloads exercise what they are meant to: ties at the frontier
-    # in the tie workload, leaders spread over ranks in the others
+    # the tie workload exercises what it is meant to: every injected tie
+    # that lands on the frontier (both ranks at the step's largest prefix;
+    # the others were overtaken by a third rank or a later injection) is led
+    # by the lower of its two ranks, and nearly all of them do land
     if wl.tie_frac:
         P_ties = 0
-        for t, kind, (s, r1, r2, _) in synth.injections(wl)[:50]:
+        injected = [e for e in synth.injections(wl) if e[1] == "tie"]
+        assert len(injected) == round(wl.tie_frac * T * S)
+        for t, kind, (s, r1, r2, _) in injected:
             x = synth.generate(wl, t, t + 1)[0]
             P = x[: s + 1].sum(axis=0)
             if P[r1] == P[r2] == P.max():
-                assert ol[t, s] == min(r1, r2)
+                assert ol[t, s] == min(r1, r2) == np.flatnonzero(P == P.max())[0], (t, s, r1, r2)
                 P_ties += 1
-        assert P_ties > 10
+        log("%d of %d injected ties are frontier ties" % (P_ties, len(injected)))
+        assert P_ties >= 2300
     log("parity ok: %s" % name)
     del d, inc, lead, ex, cnt, top2, le, letop2
     torch.cuda.empty_cache()
@@ -148,61 +155,110 @@ def test_workload_ingest_and_route(sf, name):
     log("route ok: %s, %d windows, sizes %s" % (name, len(ex), np.bincount(os2).tolist()))
 
 
-@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
-def test_workload_lag(sf, name):
-    """The lag over the median rank on sampled step ranges of every
-    workload (the oracle sorts R prefixes per boundary)."""
-    wl = synth.WORKLOADS[name]
-    n = min(wl.T, 600 if wl.R <= 1024 else 60)
-    for t0 in sorted({0, wl.T // 2, wl.T - n}):
-        x = synth.generate(wl, t0, t0 + n)
-        lag, inc = sf.sf_frontier_lag(torch.from_numpy(x).to("cuda:0"))
-        torch.cuda.synchronize()
-        ol, oi = oracle.frontier_lag(x)
-        np.testing.assert_array_equal(lag.cpu().numpy(), ol)
-        np.testing.assert_array_equal(inc.cpu().numpy(), oi)
-    log("lag ok: %s (%d steps x 3 ranges)" % (name, n))
+def host_threads() -> int:
+    """Oracle worker threads: the CPU share of the box (at most 16)."""
+    n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    return max(1, min(16, n))
+
+
+def whole_input(wl):
+    """The workload's full [T, S, R] input on the host and in HBM."""
+    x = synth.generate(wl)
+    d = torch.from_numpy(x).to("cuda:0")
+    return x, d
+
+
+def window_ranges(wl, per=1):
+    """[t0, t1) of runs of `per` whole windows covering all steps."""
+    step = wl.window * per
+    return [(t0, min(wl.T, t0 + step)) for t0 in range(0, wl.T, step)]
 
 
 @pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
-def test_workload_spread(sf, name):
-    """The raw rank spread on sampled step ranges of every workload."""
-    wl = synth.WORKLOADS[name]
-    n = min(wl.T, 600 if wl.R <= 1024 else 60)
-    for t0 in sorted({0, wl.T // 2, wl.T - n}):
-        x = synth.generate(wl, t0, t0 + n)
-        sp, wsp = sf.sf_rank_spread(torch.from_numpy(x).to("cuda:0"), wl.window)
-        torch.cuda.synchronize()
-        osp, owsp = oracle.rank_spread(x, wl.window)
-        np.testing.assert_array_equal(sp.cpu().numpy(), osp)
-        np.testing.assert_array_equal(wsp.cpu().numpy(), owsp)
-    log("spread ok: %s (%d steps x 3 ranges)" % (name, n))
-
-
-@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
-def test_workload_window_median(sf, name):
-    """The per-rank window median of the first and the last window of every
-    workload, in the launch shape the benchmark uses (one full window);
-    above 1024 ranks the oracle checks slices of 512 ranks at both ends
-    and in the middle (ranks are independent)."""
+def test_workload_lag_spread_full(sf, name):
+    """The lag over the median rank and the raw rank spread over every step
+    of every workload, in the launch configuration the benchmark times (the
+    16384-rank workload as two chunk launches), against the oracle run on
+    disjoint step ranges (lag) and whole windows (spread) over the host's
+    cores: every output bit-exact."""
     wl = synth.WORKLOADS[name]
     T, S, R = wl.T, wl.S, wl.R
+    log("lag/spread %s: T=%d S=%d R=%d" % (name, T, S, R))
+    x, d = whole_input(wl)
+    lag = torch.empty((T, S), dtype=torch.int64, device="cuda:0")
+    linc = torch.empty_like(lag)
+    sp = torch.empty_like(lag)
     W = wl.num_windows
-    for w in sorted({0, W - 1}):
-        t0, t1 = w * wl.window, min(T, (w + 1) * wl.window)
-        x = synth.generate(wl, t0, t1)
-        m = sf.sf_window_median(torch.from_numpy(x).to("cuda:0"), wl.window)
-        torch.cuda.synchronize()
-        m = m.cpu().numpy()
-        slices = [(0, R)] if R <= 1024 else [(0, 512), (R // 2 - 256, R // 2 + 256), (R - 512, R)]
-        for r0, r1 in slices:
-            om = oracle.window_median(np.ascontiguousarray(x[:, :, r0:r1]), wl.window)
-            np.testing.assert_array_equal(m[:, :, r0:r1], om)
-        log("window median ok: %s window %d (%d steps, ranks %s)" % (name, w, t1 - t0, slices))
+    wsp = torch.empty((W, S), dtype=torch.int64, device="cuda:0")
+    for t0, t1 in wl.chunk_bounds():
+        w0, w1 = t0 // wl.window, -(-t1 // wl.window)
+        sf.sf_frontier_lag(d[t0:t1], lag[t0:t1], linc[t0:t1])
+        sf.sf_rank_spread(d[t0:t1], wl.window, sp[t0:t1], wsp[w0:w1])
+    torch.cuda.synchronize()
+    log("gpu done")
+    nth = host_threads()
+    cuts = [T * k // (4 * nth) for k in range(4 * nth + 1)]
+    with ThreadPoolExecutor(max_workers=nth) as pool:
+        lag_parts = list(pool.map(lambda ab: oracle.frontier_lag(x[ab[0]:ab[1]]),
+                                  [(a, b) for a, b in zip(cuts, cuts[1:]) if b > a]))
+        log("oracle lag done")
+        sp_parts = list(pool.map(lambda ab: oracle.rank_spread(x[ab[0]:ab[1]], wl.window),
+                                 window_ranges(wl)))
+        log("oracle spread done")
+    np.testing.assert_array_equal(lag.cpu().numpy(), np.concatenate([p[0] for p in lag_parts]))
+    np.testing.assert_array_equal(linc.cpu().numpy(), np.concatenate([p[1] for p in lag_parts]))
+    np.testing.assert_array_equal(sp.cpu().numpy(), np.concatenate([p[0] for p in sp_parts]))
+    np.testing.assert_array_equal(wsp.cpu().numpy(), np.concatenate([p[1] for p in sp_parts]))
+    log("lag and spread ok: %s, all %d steps" % (name, T))
+    del d, lag, linc, sp, wsp
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
-def test_workload_gain(sf, name):
+def test_workload_median_gain_full(sf, name):
+    """The per-rank window median of every window, stage and rank of every
+    workload, and the direct-exposure gain of Eq. (4) over every step with
+    that median as the baseline (the chain the benchmark times, chunk by
+    chunk), against the oracle run window by window over the host's cores:
+    every output bit-exact."""
+    wl = synth.WORKLOADS[name]
+    T, S, R = wl.T, wl.S, wl.R
+    log("median/gain %s: T=%d S=%d R=%d window=%d" % (name, T, S, R, wl.window))
+    x, d = whole_input(wl)
+    W = wl.num_windows
+    med = torch.empty((W, S, R), dtype=torch.int64, device="cuda:0")
+    shapes = {"gain": (T, S), "makespan": (T,), "window_gain": (W, S), "window_makespan": (W,)}
+    g = {k: torch.empty(v, dtype=torch.int64, device="cuda:0") for k, v in shapes.items()}
+    for t0, t1 in wl.chunk_bounds():
+        w0, w1 = t0 // wl.window, -(-t1 // wl.window)
+        sf.sf_window_median(d[t0:t1], wl.window, med[w0:w1])
+        sf.sf_exposure_gain(d[t0:t1], med[w0:w1], wl.window,
+                            {"gain": g["gain"][t0:t1], "makespan": g["makespan"][t0:t1],
+                             "window_gain": g["window_gain"][w0:w1],
+                             "window_makespan": g["window_makespan"][w0:w1]})
+    torch.cuda.synchronize()
+    log("gpu done")
+
+    def one_window(ab):
+        t0, t1 = ab
+        xs = x[t0:t1]
+        om = oracle.window_median(xs, wl.window)
+        return om, oracle.exposure_gain(xs, om, wl.window)
+
+    with ThreadPoolExecutor(max_workers=host_threads()) as pool:
+        parts = list(pool.map(one_window, window_ranges(wl)))
+    log("oracle done")
+    np.testing.assert_array_equal(med.cpu().numpy(), np.concatenate([p[0] for p in parts]))
+    for k in shapes:
+        np.testing.assert_array_equal(g[k].cpu().numpy(), np.concatenate([p[1][k] for p in parts]),
+                                      err_msg=k)
+    log("window median and gain ok: %s, all %d windows" % (name, W))
+    del d, med, g
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workload_gain_no_stall_baseline(sf, name):
     """The direct-exposure gain of Eq. (4) on sampled step ranges of every
     workload, with the recipe's no-stall stage medians as the baseline."""
     wl = synth.WORKLOADS[name]
