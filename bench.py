@@ -473,52 +473,50 @@ def main() -> int:
         # next row: the per-rank window median (a baseline btilde of Eq. (4)),
         # per chunk (the chunks are whole windows)
         if want("window_median"):
-            btilde = None
-            if min(wl.window, T) <= sf.SF_MAX_WINDOW_MEDIAN:
-                btilde = torch.empty((W, S, R), dtype=torch.int64, device=dev)
-                m_views = []
-                for t0, t1 in bounds:
-                    w0, w1 = t0 // wl.window, -(-t1 // wl.window)
-                    m_views.append((d[t0:t1], btilde[w0:w1]))
+            btilde = torch.empty((W, S, R), dtype=torch.int64, device=dev)
+            m_views = []
+            for t0, t1 in bounds:
+                w0, w1 = t0 // wl.window, -(-t1 // wl.window)
+                m_views.append((d[t0:t1], btilde[w0:w1]))
+            for dv, mv in m_views:
+                sf.sf_window_median(dv, wl.window, mv, stream=stream)
+            mt = []
+            for _ in range(max(3, args.steps // 2)):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
                 for dv, mv in m_views:
                     sf.sf_window_median(dv, wl.window, mv, stream=stream)
-                mt = []
-                for _ in range(max(3, args.steps // 2)):
-                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    a.record(stream)
-                    for dv, mv in m_views:
-                        sf.sf_window_median(dv, wl.window, mv, stream=stream)
-                    b.record(stream)
-                    mt.append((a, b))
-                torch.cuda.synchronize(dev)
-                m_ms = float(np.mean([a.elapsed_time(b) for a, b in mt])) / len(bounds)
-                m_bytes = (8 * T * S * R + 8 * W * S * R) / len(bounds)
-                m_exact = m_cpu = None
-                if oracle_out:
-                    import oracle
-                    # window 0, ranks [0, 256): ranks are independent
-                    x = synth.generate(wl, 0, min(T, wl.window))
-                    rs = min(R, 256)
-                    xs = np.ascontiguousarray(x[:, :, :rs])
-                    tc = time.perf_counter()
-                    om = oracle.window_median(xs, wl.window)
-                    m_cpu = row_cpu(xs.size, time.perf_counter() - tc,
-                                    "oracle window_median on window 0, ranks [0, %d)" % rs)
-                    m_exact = bool(np.array_equal(btilde[:1, :, :rs].cpu().numpy(), om))
-                next_rows["window_median"] = {
-                    "kernel": "k_window_median",
-                    "bound": "hbm",
-                    "launch_ms": m_ms,
-                    "algorithmic_bytes_per_launch": m_bytes,
-                    "achieved": m_bytes / (m_ms / 1e3) / 1e9,
-                    "peak": PEAK_HBM_GBPS,
-                    "unit": "GB/s",
-                    "frac": m_bytes / (m_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
-                    "bit_exact_window0_ranks": m_exact,
-                    "samples_per_s": T * S * R / len(bounds) / (m_ms / 1e3),
-                    "cpu_baseline": m_cpu,
-                }
-                del m_views
+                b.record(stream)
+                mt.append((a, b))
+            torch.cuda.synchronize(dev)
+            m_ms = float(np.mean([a.elapsed_time(b) for a, b in mt])) / len(bounds)
+            m_bytes = (8 * T * S * R + 8 * W * S * R) / len(bounds)
+            m_exact = m_cpu = None
+            if oracle_out:
+                import oracle
+                # window 0, ranks [0, 256): ranks are independent
+                x = synth.generate(wl, 0, min(T, wl.window))
+                rs = min(R, 256)
+                xs = np.ascontiguousarray(x[:, :, :rs])
+                tc = time.perf_counter()
+                om = oracle.window_median(xs, wl.window)
+                m_cpu = row_cpu(xs.size, time.perf_counter() - tc,
+                                "oracle window_median on window 0, ranks [0, %d)" % rs)
+                m_exact = bool(np.array_equal(btilde[:1, :, :rs].cpu().numpy(), om))
+            next_rows["window_median"] = {
+                "kernel": "k_window_median",
+                "bound": "hbm",
+                "launch_ms": m_ms,
+                "algorithmic_bytes_per_launch": m_bytes,
+                "achieved": m_bytes / (m_ms / 1e3) / 1e9,
+                "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s",
+                "frac": m_bytes / (m_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                "bit_exact_window0_ranks": m_exact,
+                "samples_per_s": T * S * R / len(bounds) / (m_ms / 1e3),
+                "cpu_baseline": m_cpu,
+            }
+            del m_views
 
         # next row: direct-exposure gain, Eq. (4), with the per-rank window
         # median as btilde (else the workload recipe's no-stall stage medians)
@@ -562,11 +560,8 @@ def main() -> int:
                 n_chk = min(16, T)
                 x = synth.generate(wl, 0, n_chk)
                 xd = torch.from_numpy(x).to(dev)
-                if n_chk <= sf.SF_MAX_WINDOW_MEDIAN:
-                    gb = sf.sf_window_median(xd, n_chk, stream=stream)
-                    ob = oracle.window_median(x, n_chk)
-                else:
-                    gb, ob = btilde[:1].contiguous(), btilde[:1].cpu().numpy()
+                gb = sf.sf_window_median(xd, n_chk, stream=stream)
+                ob = oracle.window_median(x, n_chk)
                 go = sf.sf_exposure_gain(xd, gb, n_chk, stream=stream)
                 torch.cuda.synchronize(dev)
                 tc = time.perf_counter()

@@ -67,9 +67,6 @@ enum {
 /* Largest stage count of sf_exposure_gain (its per-stage reductions are
  * kept in registers). */
 #define SF_MAX_S_GAIN 64
-/* Longest window of sf_window_median (a window's values for 16 ranks are
- * held on chip at once). */
-#define SF_MAX_WINDOW_MEDIAN 1024
 /* Every rank-local prefix P[t][r][s] must be below this many ns (about
  * 39 hours) so that the packed key fits in 64 bits. */
 #define SF_MAX_PREFIX_NS ((int64_t)1 << 47)
@@ -285,8 +282,10 @@ int sf_rank_spread(const int64_t* durations, int64_t T, int32_t R, int32_t S,
  *
  *   durations   [T][S][R] int64 ns (as for sf_frontier).
  *   T, R, S     0 <= T, 1 <= R <= SF_MAX_R, 1 <= S.  T == 0 is a no-op.
- *   window      steps per window, >= 1 (windows as for sf_window_summary);
- *               min(window, T) <= SF_MAX_WINDOW_MEDIAN.
+ *   window      steps per window, >= 1 (windows as for sf_window_summary).
+ *               Windows of up to 1024 steps are held on chip in tiles of
+ *               ranks; longer ones are selected from global memory, one
+ *               column at a time (slower, same results).
  *   out_median  [W][S][R] int64 ns.
  *   stream      HIP stream.
  *

@@ -2,41 +2,38 @@
 // (Sec. 4): med[w][s][r] = the lower median over the n steps t of window w of
 // d[t][s][r] (the value of rank floor((n-1)/2) in ascending order).
 //
-// A tile is (window, stage, RPW adjacent ranks).  Persistent workgroups walk
-// the tiles; each tile is read once along the rank rows (8 * RPW contiguous
-// bytes per step, in 16-byte loads) into registers, while the previous tile
-// is being resolved, and is then transposed through LDS, where the low and
-// high words sit in separate planes with a row stride of RPW + 1 words so
-// that a wave reading one rank's column hits distinct banks.  Each wave then
-// takes one rank: its n values (K per lane, the tile's zero rows past n
-// included as values below all others) go to registers, and an exact radix
-// select (a 256-bin histogram of the top 8 bits of the OR of the values,
-// then 8 bits at a time of the values left) finds the lower median.  Once
-// at most 64 values are left they are compacted, one per lane,
-// through the wave's own (already read) tile column, so later passes handle
-// one value per lane.  The histogram is private to the wave and a wave's LDS
-// operations complete in issue order, so the waves need no barrier between
-// them during the selection.
+// A tile is (window, stage, RPW adjacent ranks).  Persistent workgroups of
+// 16 waves walk the tiles; each tile is read once along the rank rows
+// (8 * RPW contiguous bytes per step, 256 bytes for windows up to 1024
+// steps, in 16-byte loads) into registers while the previous tile is being
+// resolved.  Durations in every workload are far below 2^32 ns (4.3 s), so
+// the tile is kept in LDS as 32-bit values: its low words, transposed so
+// that rank j's column is a run of words with a stride of RPW + 1 (an odd
+// stride: a wave reading one column hits distinct banks), while the high
+// words are OR-ed together.  Each wave then takes RPW / 16 ranks in turn:
+// a column's n values (K per lane, the tile's zero rows past n included as
+// values below all others) go to registers, and an exact radix select (a
+// 256-bin histogram of the top 8 bits of the OR of the values, then 8 bits
+// at a time of the values left) finds the lower median.  Once at most 64
+// values are left they are compacted, one per lane, into the wave's list
+// (a ballot and a lane count per slot), so later passes handle one value
+// per lane.  The histogram and the list are private to the wave and a
+// wave's LDS operations complete in issue order, so the waves need no
+// barrier between them during the selection.
+//
+// A tile with some value at or above 2^32 (a high word not 0) is resolved
+// in 64 bits instead: each wave re-reads its ranks' columns from global
+// memory (they were just read, so mostly from the caches) pass by pass.
+// Windows longer than the tile rows take the same 64-bit streaming select,
+// one wave per (window, stage, rank).
 
 #include "sf_device.h"
 #include "sf_host.h"
 #include "sf_select.h"
 
-namespace sfk {
+#include <type_traits>
 
-// OR over aligned groups of SUB lanes (the DPP pattern of group_max); the
-// result is valid in the last lane of each group
-template <int SUB>
-__device__ __forceinline__ u64 group_or(u64 v)
-{
-    if (SUB >= 2) v |= dpp_move<0xB1, 0xF>(v);
-    if (SUB >= 4) v |= dpp_move<0x4E, 0xF>(v);
-    if (SUB >= 8) v |= dpp_move<0x141, 0xF>(v);
-    if (SUB >= 16) v |= dpp_move<0x140, 0xF>(v);
-    if (SUB >= 32) v |= dpp_move<0x142, 0xA>(v);
-    if (SUB >= 64) v |= dpp_move<0x143, 0xC>(v);
-    return v;
-}
+namespace sfk {
 
 // orders this wave's LDS accesses before the ones that follow (a wave's LDS
 // operations complete in issue order; this keeps the compiler from moving
@@ -47,44 +44,214 @@ __device__ __forceinline__ void wave_lds_fence()
     __builtin_amdgcn_wave_barrier();
 }
 
-// At most 64 VGPRs (8 waves per SIMD) for the shapes of windows up to 256
-// steps, whose tiles leave LDS for two workgroups per CU: without the cap
-// the 256-step shape takes 72 and one workgroup per CU (24% slower).
-template <int VEC, int K, int RPW>
-__global__ __launch_bounds__(64 * RPW) __attribute__((amdgpu_waves_per_eu(K <= 4 ? 8 : 4))) void k_window_median(const int64_t* __restrict__ d,
-                                                            int64_t T, int R, int S,
-                                                            int64_t window, int nchunk,
-                                                            int64_t ntiles,
-                                                            int64_t* __restrict__ med)
+// OR over the 64 lanes, in every lane
+__device__ __forceinline__ uint32_t wave_or32(uint32_t v)
 {
-    constexpr int WG = 64 * RPW;
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, true);
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, true);
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, true);
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, true);
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, true);
+    v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, true);
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+__device__ __forceinline__ u64 wave_or64(u64 v)
+{
+    return ((u64)wave_or32((uint32_t)(v >> 32)) << 32) | wave_or32((uint32_t)v);
+}
+
+// the position of this lane among the lanes of `mask` below it
+__device__ __forceinline__ uint32_t lane_rank(u64 mask)
+{
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+template <typename V>
+__device__ __forceinline__ bool sel_match_t(V u, int hi, V prefix)
+{
+    return hi >= (int)(8 * sizeof(V)) || (u >> hi) == prefix;
+}
+
+template <typename V>
+__device__ __forceinline__ int sel_first_lo_t(V range)
+{
+    const int nbits = (int)(8 * sizeof(V)) - (sizeof(V) == 8 ? __builtin_clzll((u64)range)
+                                                              : __builtin_clz((uint32_t)range));
+    return nbits > 8 ? nbits - 8 : 0;
+}
+
+// Exact lower-median select over one wave's KV values per lane, read from
+// LDS at every pass (slot k of lane l is col[(k * 64 + l) * STRIDE]; rows
+// n.. are zeros, which sort at or below every duration), so that no value
+// occupies a register between passes.  vor is the OR of all the values, kk
+// the target's rank among all 64 * KV slots, h the wave's 256-bin histogram
+// (zero on entry and on return) and lst the wave's 64-entry list.
+template <int KV, int STRIDE>
+__device__ uint32_t wave_select_col(const uint32_t* col, uint32_t vor, uint32_t kk, int n,
+                                    uint32_t* h, uint32_t* lst, int lane)
+{
+    if (vor == 0) return 0;  // every value is 0
+    auto val = [&](int k) { return col[(k * 64 + lane) * STRIDE]; };
+    // the first digit: the top 8 bits of the OR of the values, which bounds
+    // every value
+    int lo = sel_first_lo_t(vor), hi = lo + 8;
+    uint32_t prefix = 0;
+    bool first = true;     // every value is a candidate
+    bool compact = false;  // the values left are one per lane in (c1, ok1)
+    uint32_t c1 = 0;
+    bool ok1 = false;
+    for (;;) {
+        if (compact) {
+            sel_hist_add(h, ok1 && sel_match_t(c1, hi, prefix) ? (int)((c1 >> lo) & ((1u << (hi - lo)) - 1u)) : -1);
+        } else if (first) {
+            // a lane's values come from unrelated steps, so equal
+            // neighbouring bins are rare: one plain atomic per value
+#pragma unroll 8
+            for (int k = 0; k < KV; ++k) atomicAdd(&h[val(k) >> lo], 1u);
+        } else {
+#pragma unroll 8
+            for (int k = 0; k < KV; ++k) {
+                const uint32_t x = val(k);
+                sel_hist_add(h, sel_match_t(x, hi, prefix) ? (int)((x >> lo) & ((1u << (hi - lo)) - 1u)) : -1);
+            }
+        }
+        first = false;
+        wave_lds_fence();
+        // scan of the bins, then every lane clears its bins
+        uint32_t digit, count;
+        sel_scan_wave(h, lane, kk, digit, count);
+        sel_clear_lane_bins(h, lane);
+        wave_lds_fence();
+        prefix = (prefix << (hi - lo)) | digit;
+        hi = lo;
+        if (hi == 0) return prefix;  // every bit chosen: the median == prefix
+        lo = lo > 8 ? lo - 8 : 0;
+        if (count == 1) {
+            // one value has the chosen digits: its lane hands it over.  The
+            // search skips the zero rows: when the one value is such a zero,
+            // no lane holds it and lane 0's x = 0 is the answer.
+            uint32_t x = 0;
+            bool has = false;
+            if (compact) {
+                has = ok1 && sel_match_t(c1, hi, prefix);
+                x = c1;
+            } else {
+#pragma unroll 8
+                for (int k = 0; k < KV; ++k) {
+                    const uint32_t y = val(k);
+                    if (k * 64 + lane < n && sel_match_t(y, hi, prefix)) {
+                        x = y;
+                        has = true;
+                    }
+                }
+            }
+            const u64 hm = __ballot(has);
+            return (uint32_t)__builtin_amdgcn_readlane((int)x, hm ? __builtin_ctzll(hm) : 0);
+        }
+        if (!compact && count <= 64u) {
+            // the values left into the list, one slot each: a ballot per
+            // register slot and the lane's rank among the matching lanes
+            uint32_t base = 0;
+#pragma unroll 8
+            for (int k = 0; k < KV; ++k) {
+                const uint32_t x = val(k);
+                const bool m = sel_match_t(x, hi, prefix);
+                const u64 bm = __ballot(m);
+                if (m) lst[base + lane_rank(bm)] = x;  // < count <= 64
+                base += (uint32_t)__popcll(bm);
+            }
+            wave_lds_fence();
+            ok1 = (uint32_t)lane < count;
+            c1 = ok1 ? lst[lane] : 0u;
+            compact = true;
+        }
+    }
+}
+
+// Exact lower median of the n 64-bit values get(0..n-1), read pass by pass
+// (any n): the OR, then one histogram pass per digit, then a search for the
+// one value left.  h: the wave's histogram (zero on entry and on return).
+template <typename Get>
+__device__ u64 wave_select_stream(Get get, int64_t n, uint32_t* h, int lane)
+{
+    u64 vor = 0;
+    for (int64_t i = lane; i < n; i += 64) vor |= get(i);
+    vor = wave_or64(vor);
+    if (vor == 0) return 0;
+    int lo = sel_first_lo_t(vor), hi = lo + 8;
+    u64 prefix = 0;
+    uint32_t kk = (uint32_t)((n - 1) / 2);
+    for (;;) {
+        for (int64_t i = lane; i < n; i += 64) {
+            const u64 x = get(i);
+            if (sel_match_t(x, hi, prefix)) atomicAdd(&h[(uint32_t)((x >> lo) & ((1u << (hi - lo)) - 1u))], 1u);
+        }
+        wave_lds_fence();
+        uint32_t digit, count;
+        sel_scan_wave(h, lane, kk, digit, count);
+        sel_clear_lane_bins(h, lane);
+        wave_lds_fence();
+        prefix = (prefix << (hi - lo)) | (u64)digit;
+        hi = lo;
+        if (hi == 0) return prefix;
+        lo = lo > 8 ? lo - 8 : 0;
+        if (count == 1) {
+            u64 x = 0;
+            bool has = false;
+            for (int64_t i = lane; i < n; i += 64) {
+                const u64 y = get(i);
+                if (sel_match_t(y, hi, prefix)) {
+                    x = y;
+                    has = true;
+                }
+            }
+            const u64 hm = __ballot(has);
+            return lane_value(x, hm ? __builtin_ctzll(hm) : 0);
+        }
+    }
+}
+
+constexpr int kMedWaves = 16;            // waves per workgroup
+constexpr int kMedWG = 64 * kMedWaves;
+constexpr int64_t kMedTileRows = 1024;   // longest window of the tiled kernel
+
+// VEC: int64 elements per load (2: 16-byte loads, even R and a 16-byte
+// aligned base); K: values per lane (tile rows 64 * K >= n); RPW: ranks per
+// tile (the tile is 64 * K * (RPW + 1) words, about 130 KB).  One workgroup
+// per CU: 16 waves of at most 128 VGPRs.
+template <int VEC, int K, int RPW>
+__global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) void k_window_median(
+    const int64_t* __restrict__ d, int64_t T, int R, int S, int64_t window, int nchunk,
+    int64_t ntiles, int64_t* __restrict__ med)
+{
     constexpr int ROWS = 64 * K;     // tile rows (steps), >= n
-    constexpr int STRIDE = RPW + 1;  // words per tile row in each plane
+    constexpr int STRIDE = RPW + 1;  // words per tile row
     constexpr int TPR = RPW / 2;     // threads per tile row, two ranks each
-    constexpr int RPS = WG / TPR;    // rows per load sweep
+    constexpr int RPS = kMedWG / TPR;  // rows per load sweep
     constexpr int NSW = ROWS / RPS;  // load sweeps
-    constexpr int LIST = 64;         // values left that are compacted
-    static_assert(RPW % 2 == 0 && ROWS % RPS == 0 && ROWS >= LIST, "shape");
-    __shared__ uint32_t tlo[ROWS * STRIDE], thi[ROWS * STRIDE];
-    __shared__ __attribute__((aligned(16))) uint32_t hist[RPW][kSelWords];
+    constexpr int RPWV = RPW / kMedWaves;  // ranks per wave
+    static_assert(RPW % (2 * kMedWaves) == 0 && ROWS % RPS == 0, "shape");
+    __shared__ uint32_t tile[ROWS * STRIDE];
+    __shared__ __attribute__((aligned(16))) uint32_t hist[kMedWaves][kSelWords];
+    __shared__ uint32_t lists[kMedWaves][64];
+    __shared__ uint32_t wide_flag[2];  // by tile parity: some high word is not 0
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int c = (tid % TPR) * 2;  // this thread's rank pair within a tile row
+    const int i0 = tid / TPR;          // this thread's first tile row
+    const int c = (tid % TPR) * 2;     // its rank pair within a tile row
     uint32_t* h = hist[wave];
     for (int i = lane; i < kSelWords; i += 64) h[i] = 0;  // cleared again by every scan
+    if (tid < 2) wide_flag[tid] = 0;
 
     // tile b -> (window, stage, rank chunk), the chunk fastest so that
     // neighbouring workgroups read neighbouring pieces of the same rows.  A
     // workgroup's tiles advance by gridDim.x: the position is a mixed-radix
     // counter (w, s, chunk) advanced with carries, so that the loop does no
-    // 64-bit division (which costs some 300 scalar instructions per tile in
-    // every wave).
-    struct Tile {
-        int64_t w, t0;
-        int s, n, r0;
-    };
+    // 64-bit division.
     struct Pos {
         int64_t w;
         int s, c;
@@ -104,185 +271,147 @@ __global__ __launch_bounds__(64 * RPW) __attribute__((amdgpu_waves_per_eu(K <= 4
         p.w += step.w + cs;
         return p;
     };
-    auto tile = [&](const Pos& p) {
-        Tile x;
-        x.r0 = p.c * RPW;
-        x.s = p.s;
-        x.w = p.w;
-        x.t0 = x.w * window;
-        x.n = (int)((x.t0 + window < T ? x.t0 + window : T) - x.t0);  // 1 <= n <= ROWS
-        return x;
+    auto rows_of = [&](const Pos& p) {  // 1 <= n <= ROWS
+        const int64_t t0 = p.w * window;
+        return (int)((t0 + window < T ? t0 + window : T) - t0);
     };
-    // the next tile in flight: thread (row i, pair c) holds ranks r0 + c, r0 + c + 1
+    const int64_t rstride = (int64_t)RPS * S * R;  // elements between sweeps
+    // the next tile in flight: thread (row i0 + j * RPS, pair c) holds ranks
+    // r0 + c, r0 + c + 1 of that row
     int64_t x0[NSW], x1[NSW];
-    auto load = [&](const Tile& q) {
-        const int r = q.r0 + c;
+    auto load = [&](const Pos& p) {
+        const int n = rows_of(p);
+        const int r = p.c * RPW + c;
+        const int64_t* q = d + ((p.w * window + i0) * S + p.s) * (int64_t)R + r;
 #pragma unroll
         for (int j = 0; j < NSW; ++j) {
-            const int i = tid / TPR + j * RPS;
             x0[j] = 0;
             x1[j] = 0;
-            if (i < q.n) {
-                const int64_t* p = d + ((q.t0 + i) * S + q.s) * (int64_t)R + r;
+            if (i0 + j * RPS < n) {
                 if (VEC == 2) {
                     if (r < R) {  // R even: r + 1 < R too
-                        const v2i64 v = __builtin_nontemporal_load(reinterpret_cast<const v2i64*>(p));
+                        const v2i64 v = __builtin_nontemporal_load(reinterpret_cast<const v2i64*>(q));
                         x0[j] = v.x;
                         x1[j] = v.y;
                     }
                 } else {
-                    if (r < R) x0[j] = __builtin_nontemporal_load(p);
-                    if (r + 1 < R) x1[j] = __builtin_nontemporal_load(p + 1);
+                    if (r < R) x0[j] = __builtin_nontemporal_load(q);
+                    if (r + 1 < R) x1[j] = __builtin_nontemporal_load(q + 1);
                 }
             }
+            q += rstride;
         }
     };
 
     int64_t b = blockIdx.x;  // the grid is at most ntiles
     Pos pos = split(b);
-    load(tile(pos));
-    for (; b < ntiles; b += gridDim.x) {
-        const Tile q = tile(pos);
+    load(pos);
+    for (int it = 0; b < ntiles; b += gridDim.x, ++it) {
+        const Pos cur = pos;
+        const int n = rows_of(cur);
         pos = advance(pos);
-        __syncthreads();  // every wave is done with the previous tile's columns
+        __syncthreads();  // every wave is done with the previous tile's columns and flag
+        if (tid == 0) wide_flag[(it + 1) & 1] = 0;  // the previous tile's flag, for the next
+        uint32_t hiw = 0;
 #pragma unroll
         for (int j = 0; j < NSW; ++j) {
-            const int i = tid / TPR + j * RPS;
-            tlo[i * STRIDE + c] = (uint32_t)x0[j];
-            thi[i * STRIDE + c] = (uint32_t)((u64)x0[j] >> 32);
-            tlo[i * STRIDE + c + 1] = (uint32_t)x1[j];
-            thi[i * STRIDE + c + 1] = (uint32_t)((u64)x1[j] >> 32);
+            const int i = i0 + j * RPS;
+            tile[i * STRIDE + c] = (uint32_t)x0[j];
+            tile[i * STRIDE + c + 1] = (uint32_t)x1[j];
+            hiw |= (uint32_t)((u64)x0[j] >> 32) | (uint32_t)((u64)x1[j] >> 32);
         }
+        if (__ballot(hiw != 0) != 0 && lane == 0) atomicOr(&wide_flag[it & 1], 1u);
         __syncthreads();
-        // this wave's rank: its column to registers.  Rows n.. of the tile
-        // hold zeros (the loads leave them 0); durations are >= 0, so the
-        // zeros sort at or below every value and the lower median of the n
-        // values is the slot of rank (n - 1) / 2 + (ROWS - n) among all
-        // ROWS slots: no slot needs a validity test.
-        u64 v[K];
+        const bool wide = wide_flag[it & 1] != 0;  // uniform over the workgroup
+        const bool more = b + gridDim.x < ntiles;
+        const int64_t t0 = cur.w * window;
+        int64_t* mrow = med + (cur.w * S + cur.s) * (int64_t)R + cur.c * RPW;
+        if (!wide) {
+            // the next tile's loads fly while this one is resolved
+            if (more) load(pos);
+            const uint32_t kk = (uint32_t)((n - 1) / 2 + (ROWS - n));
+#pragma unroll 1
+            for (int rr = 0; rr < RPWV; ++rr) {
+                const int j = wave + rr * kMedWaves;  // the tile column
+                if (cur.c * RPW + j >= R) break;      // wave-uniform
+                const uint32_t* col = tile + lane * STRIDE + j;
+                uint32_t vor = 0;
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-            const int i = k * 64 + lane;
-            v[k] = ((u64)thi[i * STRIDE + wave] << 32) | tlo[i * STRIDE + wave];
-        }
-        // the next tile's loads fly while this one is resolved
-        if (b + gridDim.x < ntiles) load(tile(pos));
-        const int r = q.r0 + wave;
-        if (r >= R) continue;  // the barriers are at the top of the loop
-
-        // the first digit: the top 8 bits of the OR of the values, which
-        // bounds every value
-        u64 vor = 0;
-#pragma unroll
-        for (int k = 0; k < K; ++k) vor |= v[k];
-        vor = lane_value(group_or<64>(vor), 63);
-        u64 um = 0;  // the median (0 when every value is 0)
-        if (vor != 0) {
-            int lo = sel_first_lo(vor), hi = lo + 8;
-            u64 prefix = 0;
-            uint32_t kk = (uint32_t)((q.n - 1) / 2 + (ROWS - q.n));
-            bool first = true;     // every value is a candidate
-            bool compact = false;  // the values left are one per lane in (c1, ok1)
-            u64 c1 = 0;
-            bool ok1 = false;
-            for (;;) {
-                if (compact) {
-                    sel_hist_add(h, ok1 ? sel_bin(c1, lo, hi, prefix) : -1);
-                } else if (first) {
-                    // a lane's values come from unrelated steps, so equal
-                    // neighbouring bins are rare: one plain atomic per value
-                    // (2-4% faster than adding runs of equal bins at once)
-#pragma unroll
-                    for (int k = 0; k < K; ++k) atomicAdd(&h[sel_first_bin(v[k], lo)], 1u);
-                } else {
-#pragma unroll
-                    for (int k = 0; k < K; ++k) sel_hist_add(h, sel_bin(v[k], lo, hi, prefix));
-                }
-                first = false;
-                wave_lds_fence();
-                // scan of the bins, then every lane clears its bins
-                uint32_t digit, count;
-                sel_scan_wave(h, lane, kk, digit, count);
-                sel_clear_lane_bins(h, lane);
-                wave_lds_fence();
-                prefix = (prefix << (hi - lo)) | (u64)digit;
-                hi = lo;
-                if (hi == 0) break;  // every bit chosen: the median == prefix
-                lo = lo > 8 ? lo - 8 : 0;
-                if (count == 1) {
-                    // one value has the chosen digits: its lane hands it over.
-                    // The search skips the zero rows (a mask here keeps the
-                    // compiler from holding every slot's match in registers):
-                    // when the one value is such a zero, no lane holds it and
-                    // lane 0's x = 0 is the answer.
-                    u64 x = 0;
-                    bool has = false;
-                    if (compact) {
-                        has = ok1 && sel_match(c1, hi, prefix);
-                        x = c1;
-                    } else {
-#pragma unroll
-                        for (int k = 0; k < K; ++k) {
-                            if (k * 64 + lane < q.n && sel_match(v[k], hi, prefix)) {
-                                x = v[k];
-                                has = true;
-                            }
-                        }
-                    }
-                    const u64 hm = __ballot(has);
-                    prefix = lane_value(x, hm ? __builtin_ctzll(hm) : 0);
-                    break;
-                }
-                if (!compact && count <= (uint32_t)LIST) {
-                    // the values left, one per lane, through rows [0, count)
-                    // of this wave's tile column (read already)
-                    uint32_t cand = 0;  // bit k: v[k] is left
-#pragma unroll
-                    for (int k = 0; k < K; ++k) cand |= sel_match(v[k], hi, prefix) ? (1u << k) : 0u;
-                    const uint32_t nc = (uint32_t)__popc(cand);
-                    uint32_t pos = wave_scan_incl(nc) - nc;
-#pragma unroll
-                    for (int k = 0; k < K; ++k) {
-                        if ((cand >> k) & 1u) {
-                            if (pos < (uint32_t)LIST) {  // always, as count <= LIST
-                                tlo[pos * STRIDE + wave] = (uint32_t)v[k];
-                                thi[pos * STRIDE + wave] = (uint32_t)(v[k] >> 32);
-                            }
-                            ++pos;
-                        }
-                    }
-                    wave_lds_fence();
-                    ok1 = (uint32_t)lane < count;
-                    c1 = ok1 ? (((u64)thi[lane * STRIDE + wave] << 32) | tlo[lane * STRIDE + wave]) : 0ull;
-                    compact = true;
-                }
+                for (int k = 0; k < K; ++k) vor |= col[k * 64 * STRIDE];
+                const uint32_t m = wave_select_col<K, STRIDE>(tile + j, wave_or32(vor), kk, n, h,
+                                                              lists[wave], lane);
+                if (lane == 0) mrow[j] = (int64_t)m;
             }
-            um = prefix;
+        } else {
+            // some value of the tile needs 64 bits: each wave streams its
+            // ranks' columns from global memory
+#pragma unroll 1
+            for (int rr = 0; rr < RPWV; ++rr) {
+                const int j = wave + rr * kMedWaves;
+                const int r = cur.c * RPW + j;
+                if (r >= R) break;
+                const int64_t* col = d + (t0 * S + cur.s) * (int64_t)R + r;
+                const int64_t cs = (int64_t)S * R;
+                const u64 m = wave_select_stream([&](int64_t i) { return (u64)col[i * cs]; }, n, h, lane);
+                if (lane == 0) mrow[j] = (int64_t)m;
+            }
+            if (more) load(pos);
         }
-        if (lane == 0) med[(q.w * S + q.s) * (int64_t)R + r] = (int64_t)um;
+    }
+}
+
+// Windows longer than the tile rows: one wave per (window, stage, rank),
+// the 64-bit streaming select over the column in global memory.
+constexpr int kMedLongWG = 256;
+
+__global__ __launch_bounds__(kMedLongWG) void k_window_median_long(const int64_t* __restrict__ d,
+                                                                    int64_t T, int R, int S,
+                                                                    int64_t window, int64_t W,
+                                                                    int64_t* __restrict__ med)
+{
+    __shared__ __attribute__((aligned(16))) uint32_t hist[kMedLongWG / 64][kSelWords];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    uint32_t* h = hist[wave];
+    for (int i = lane; i < kSelWords; i += 64) h[i] = 0;
+    wave_lds_fence();
+    const int64_t total = W * S * (int64_t)R;
+    const int64_t waves = (int64_t)gridDim.x * (kMedLongWG / 64);
+    for (int64_t id = (int64_t)blockIdx.x * (kMedLongWG / 64) + wave; id < total; id += waves) {
+        const int64_t ws = id / R;
+        const int r = (int)(id - ws * R);
+        const int64_t w = ws / S;
+        const int s = (int)(ws - w * S);
+        const int64_t t0 = w * window;
+        const int64_t n = (t0 + window < T ? t0 + window : T) - t0;
+        const int64_t* col = d + (t0 * S + s) * (int64_t)R + r;
+        const int64_t cs = (int64_t)S * R;
+        const u64 m = wave_select_stream([&](int64_t i) { return (u64)col[i * cs]; }, n, h, lane);
+        if (lane == 0) med[id] = (int64_t)m;
     }
 }
 
 struct MedianVariant {
     const void* fn;
-    int WG, RPW;
+    int RPW;
 };
 
 template <int VEC, int K, int RPW>
 MedianVariant median_variant()
 {
-    return MedianVariant{reinterpret_cast<const void*>(&k_window_median<VEC, K, RPW>), 64 * RPW, RPW};
+    return MedianVariant{reinterpret_cast<const void*>(&k_window_median<VEC, K, RPW>), RPW};
 }
 
-// K values per lane for windows up to 64 K steps, 16 ranks per workgroup
-// (128-byte rows; the 1024-step tile fills 156 KB of LDS)
+// K values per lane for windows up to 64 K steps; the rank tile widens as
+// the window shortens, so that every tile holds about 128 KB of 32-bit
+// values (256-byte rows at 1024 steps, 2 KB rows at 128)
 template <int VEC>
 MedianVariant pick_median(int64_t n)
 {
-    if (n <= 128) return median_variant<VEC, 2, 16>();
-    if (n <= 256) return median_variant<VEC, 4, 16>();
-    if (n <= 512) return median_variant<VEC, 8, 16>();
-    return median_variant<VEC, 16, 16>();  // n <= SF_MAX_WINDOW_MEDIAN = 1024
+    if (n <= 128) return median_variant<VEC, 2, 256>();
+    if (n <= 256) return median_variant<VEC, 4, 128>();
+    if (n <= 512) return median_variant<VEC, 8, 64>();
+    return median_variant<VEC, 16, 32>();  // n <= kMedTileRows
 }
 
 }  // namespace sfk
@@ -296,27 +425,35 @@ SF_API int sf_window_median(const int64_t* durations, int64_t T, int32_t R, int3
     if (!fits(T, S, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     const int64_t n_max = window < T ? window : T;
-    if (n_max > SF_MAX_WINDOW_MEDIAN) return SF_EINVAL;
     const int64_t W = sf_num_windows(T, window);
     if (!fits(W, S, R, 8)) return SF_EINVAL;
     if (!durations || !out_median) return SF_EINVAL;
     if (!aligned(durations, 8) || !aligned(out_median, 8)) return SF_EINVAL;
     if (!disjoint(durations, T * S * (int64_t)R * 8, out_median, W * S * (int64_t)R * 8))
         return SF_EINVAL;
+    int cus = 0;
+    if (device_cus(stream, &cus) != SF_OK) return SF_EHIP;
+    if (cus < 1) cus = 1;
+    if (n_max > kMedTileRows) {
+        const int64_t total = W * S * (int64_t)R;
+        const int64_t want = (total + kMedLongWG / 64 - 1) / (kMedLongWG / 64);
+        const int64_t grid = want < (int64_t)cus * 8 ? want : (int64_t)cus * 8;
+        int Ri = R, Si = S;
+        int64_t Wl = W;
+        void* args[] = {(void*)&durations, (void*)&T, (void*)&Ri, (void*)&Si,
+                        (void*)&window, (void*)&Wl, (void*)&out_median};
+        return launch(reinterpret_cast<const void*>(&k_window_median_long), dim3((unsigned)grid),
+                      dim3(kMedLongWG), args, 0, stream);
+    }
     const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
     const MedianVariant v = vec2 ? pick_median<2>(n_max) : pick_median<1>(n_max);
     const int nchunk = (R + v.RPW - 1) / v.RPW;
     int64_t ntiles = W * S * (int64_t)nchunk;
-    // persistent workgroups: as many as are resident at once on the
-    // stream's device
-    int cus = 0, per_cu = 0;
-    if (device_cus(stream, &cus) != SF_OK ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, v.fn, v.WG, 0) != hipSuccess)
-        return SF_EHIP;
-    int64_t grid = (int64_t)(cus > 0 ? cus : 1) * (per_cu > 0 ? per_cu : 1);
+    // persistent workgroups: one per CU (each holds about 150 KB of LDS)
+    int64_t grid = cus;
     if (grid > ntiles) grid = ntiles;
     int Ri = R, Si = S;
     void* args[] = {(void*)&durations, (void*)&T,      (void*)&Ri,     (void*)&Si,
                     (void*)&window,    (void*)&nchunk, (void*)&ntiles, (void*)&out_median};
-    return launch(v.fn, dim3((unsigned)grid), dim3(v.WG), args, 0, stream);
+    return launch(v.fn, dim3((unsigned)grid), dim3(kMedWG), args, 0, stream);
 }

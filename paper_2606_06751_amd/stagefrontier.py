@@ -20,7 +20,6 @@ SF_MAX_R = 65536
 SF_MAX_S_EVIDENCE = 512
 SF_MAX_S_GAIN = 64
 SF_MAX_R_LAG = 16384
-SF_MAX_WINDOW_MEDIAN = 1024
 SF_MAX_PREFIX_NS = 1 << 47
 SF_XOR_PIECE_BYTES = 262144
 

@@ -67,7 +67,7 @@ def test_constants_match_header(sf):
     assert "#define SF_MAX_S_EVIDENCE %d" % sf.SF_MAX_S_EVIDENCE in text
     assert "#define SF_MAX_S_GAIN %d" % sf.SF_MAX_S_GAIN in text
     assert "#define SF_MAX_R_LAG %d" % sf.SF_MAX_R_LAG in text
-    assert "#define SF_MAX_WINDOW_MEDIAN %d" % sf.SF_MAX_WINDOW_MEDIAN in text
+    assert "SF_MAX_WINDOW_MEDIAN" not in text and "#define SF_MAX_S " not in text
     assert "#define SF_XOR_PIECE_BYTES %d" % sf.SF_XOR_PIECE_BYTES in text
     for name in ("SF_OK", "SF_EINVAL", "SF_ERANGE", "SF_EHIP"):
         assert re.search(r"%s = %d" % (name, getattr(sf, name)), text), name
@@ -255,7 +255,6 @@ def test_window_median_argument_checks(sf):
     assert call(R=0) == sf.SF_EINVAL
     assert call(R=sf.SF_MAX_R + 1) == sf.SF_EINVAL
     assert call(window=0) == sf.SF_EINVAL
-    assert call(T=5000, window=sf.SF_MAX_WINDOW_MEDIAN + 1) == sf.SF_EINVAL
     assert call(m=None) == sf.SF_EINVAL
     assert call(m=B + 4) == sf.SF_EINVAL                    # misaligned
     assert call(m=A + 8) == sf.SF_EINVAL                    # output overlaps input

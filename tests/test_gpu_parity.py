@@ -799,7 +799,7 @@ def assert_median_equal(sf, d, window):
 
 
 @pytest.mark.parametrize("window", [1, 2, 3, 64, 100, 127, 128, 129, 250, 256, 257, 500, 512, 513,
-                                    1000, 1024])
+                                    1000, 1024, 1025, 2048])
 def test_median_window_sweep(sf, window):
     rng = np.random.Generator(np.random.PCG64(window + 23))
     T = 2 * window + window // 3 + 1             # a ragged last window
@@ -811,10 +811,29 @@ def test_median_window_sweep(sf, window):
         assert_median_equal(sf, d, window)
 
 
-@pytest.mark.parametrize("R", [1, 2, 15, 16, 17, 31, 1000, 4097])
+@pytest.mark.parametrize("R", [1, 2, 15, 16, 17, 31, 32, 33, 63, 64, 65, 127, 128, 129, 255, 256,
+                               257, 1000, 4097])
 def test_median_rank_sweep(sf, R):
-    d = synth.random_durations(250, 2, R, seed=R, hi=10**7)
-    assert_median_equal(sf, d, 100)
+    """Rank counts at the edges of every tile width (32 ranks for windows
+    of up to 1024 steps, 64 up to 512, 128 up to 256, 256 up to 128), odd
+    counts (8-byte loads) and a partial last tile."""
+    for window, T in ((100, 250), (200, 410), (400, 800), (1000, 1100)):
+        d = synth.random_durations(T, 2, R, seed=R + window, hi=10**7)
+        print("case R=%d window=%d T=%d" % (R, window, T), flush=True)
+        assert_median_equal(sf, d, window)
+
+
+def test_median_wide_and_narrow_tiles_mixed(sf):
+    """Tiles whose values all fit 32 bits next to tiles with one value of
+    2^32 or more (resolved in 64 bits from global memory): per stage, per
+    window and per 32-rank tile, on all four tile widths."""
+    for window, T, R in ((1000, 2000, 96), (500, 1000, 192), (250, 500, 384), (100, 200, 768)):
+        d = synth.random_durations(T, 3, R, seed=window, hi=10**9)
+        d[window + 7, 1, R // 2] = (1 << 32) + 5     # window 1, stage 1, a middle tile
+        d[3, 0, R - 1] = (1 << 32) - 1               # the largest 32-bit value: narrow
+        d[window - 1, 2, 0] = 1 << 45                # window 0, stage 2, tile 0
+        print("case window=%d T=%d R=%d" % (window, T, R), flush=True)
+        assert_median_equal(sf, d, window)
 
 
 def test_median_pins_and_layouts(sf):
@@ -901,15 +920,12 @@ def pins_range_edges_gpu(sf):
 
 
 def test_median_window_longer_than_input(sf):
-    """A window longer than the input is one window of all T steps; the
-    limit applies to min(window, T), so a 5000-step window over 1000 steps
-    is accepted and one over 1025 steps is not."""
-    for T, window, R in ((300, 1024, 20), (1000, 5000, 33), (1, 7, 5), (129, 10**9, 2)):
+    """A window longer than the input is one window of all T steps: on the
+    tiled kernel up to 1024 steps and on the column-streaming one above."""
+    for T, window, R in ((300, 1024, 20), (1000, 5000, 33), (1, 7, 5), (129, 10**9, 2),
+                         (1025, 5000, 4), (3001, 4000, 7)):
         d = synth.random_durations(T, 3, R, seed=T + R, hi=10**8)
         assert_median_equal(sf, d, window)
-    d = torch.zeros((1025, 1, 4), dtype=torch.int64, device=DEV)
-    with pytest.raises(sf.StageFrontierError):
-        sf.sf_window_median(d, 5000)
 
 
 def test_entry_points_on_a_side_stream(sf):
