@@ -82,18 +82,19 @@ __device__ __forceinline__ int sel_first_lo_t(V range)
     return nbits > 8 ? nbits - 8 : 0;
 }
 
-// Exact lower-median select over one wave's KV values per lane, read from
-// LDS at every pass (slot k of lane l is col[(k * 64 + l) * STRIDE]; rows
-// n.. are zeros, which sort at or below every duration), so that no value
-// occupies a register between passes.  vor is the OR of all the values, kk
+// Exact lower-median select over one wave's KV values per lane, v[k] the
+// value of row k * 64 + l of lane l (rows n.. are zeros, which sort at or
+// below every duration); the column is read from LDS once, into registers,
+// and every pass works on them.  vor is the OR of all the values, kk
 // the target's rank among all 64 * KV slots, h the wave's 256-bin histogram
-// (zero on entry and on return) and lst the wave's 64-entry list.
-template <int KV, int STRIDE>
-__device__ uint32_t wave_select_col(const uint32_t* col, uint32_t vor, uint32_t kk, int n,
+// (zero on entry and on return) and lst the wave's list: 64 entries, then
+// one spare word per lane.
+template <int KV>
+__device__ uint32_t wave_select_regs(const uint32_t (&v)[KV], uint32_t vor, uint32_t kk, int n,
                                     uint32_t* h, uint32_t* lst, int lane)
 {
     if (vor == 0) return 0;  // every value is 0
-    auto val = [&](int k) { return col[(k * 64 + lane) * STRIDE]; };
+    auto val = [&](int k) { return v[k]; };
     // the first digit: the top 8 bits of the OR of the values, which bounds
     // every value
     int lo = sel_first_lo_t(vor), hi = lo + 8;
@@ -104,7 +105,10 @@ __device__ uint32_t wave_select_col(const uint32_t* col, uint32_t vor, uint32_t 
     bool ok1 = false;
     for (;;) {
         if (compact) {
-            sel_hist_add(h, ok1 && sel_match_t(c1, hi, prefix) ? (int)((c1 >> lo) & ((1u << (hi - lo)) - 1u)) : -1);
+            // one value per lane: a lane without a candidate adds into its
+            // own spare word of the list instead of branching
+            const bool c = ok1 && sel_match_t(c1, hi, prefix);
+            atomicAdd(c ? &h[(c1 >> lo) & ((1u << (hi - lo)) - 1u)] : &lst[64 + lane], 1u);
         } else if (first) {
             // a lane's values come from unrelated steps, so equal
             // neighbouring bins are rare: one plain atomic per value
@@ -151,16 +155,20 @@ __device__ uint32_t wave_select_col(const uint32_t* col, uint32_t vor, uint32_t 
             return (uint32_t)__builtin_amdgcn_readlane((int)x, hm ? __builtin_ctzll(hm) : 0);
         }
         if (!compact && count <= 64u) {
-            // the values left into the list, one slot each: a ballot per
-            // register slot and the lane's rank among the matching lanes
-            uint32_t base = 0;
+            // the values left into the list: each lane marks its candidate
+            // slots, a wave scan of the per-lane counts gives each lane its
+            // first list position, and every slot is stored, a non-candidate
+            // into the lane's spare word (no branch, no per-slot ballot)
+            uint32_t cand = 0;
 #pragma unroll 8
+            for (int k = 0; k < KV; ++k) cand |= sel_match_t(val(k), hi, prefix) ? (1u << k) : 0u;
+            const uint32_t nc = (uint32_t)__popc(cand);
+            uint32_t pos = wave_scan_incl(nc) - nc;  // < count <= 64 for every candidate
+#pragma unroll 4
             for (int k = 0; k < KV; ++k) {
-                const uint32_t x = val(k);
-                const bool m = sel_match_t(x, hi, prefix);
-                const u64 bm = __ballot(m);
-                if (m) lst[base + lane_rank(bm)] = x;  // < count <= 64
-                base += (uint32_t)__popcll(bm);
+                const bool m = (cand >> k) & 1u;
+                lst[m ? pos : 64 + lane] = val(k);
+                pos += m ? 1u : 0u;
             }
             wave_lds_fence();
             ok1 = (uint32_t)lane < count;
@@ -235,7 +243,7 @@ __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) voi
     static_assert(RPW % (2 * kMedWaves) == 0 && ROWS % RPS == 0, "shape");
     __shared__ uint32_t tile[ROWS * STRIDE];
     __shared__ __attribute__((aligned(16))) uint32_t hist[kMedWaves][kSelWords];
-    __shared__ uint32_t lists[kMedWaves][64];
+    __shared__ uint32_t lists[kMedWaves][128];  // 64 entries, then a spare word per lane
     __shared__ uint32_t wide_flag[2];  // by tile parity: some high word is not 0
 
     const int tid = threadIdx.x;
@@ -335,11 +343,14 @@ __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) voi
                 const int j = wave + rr * kMedWaves;  // the tile column
                 if (cur.c * RPW + j >= R) break;      // wave-uniform
                 const uint32_t* col = tile + lane * STRIDE + j;
+                uint32_t v[K];
                 uint32_t vor = 0;
 #pragma unroll
-                for (int k = 0; k < K; ++k) vor |= col[k * 64 * STRIDE];
-                const uint32_t m = wave_select_col<K, STRIDE>(tile + j, wave_or32(vor), kk, n, h,
-                                                              lists[wave], lane);
+                for (int k = 0; k < K; ++k) {
+                    v[k] = col[k * 64 * STRIDE];
+                    vor |= v[k];
+                }
+                const uint32_t m = wave_select_regs<K>(v, wave_or32(vor), kk, n, h, lists[wave], lane);
                 if (lane == 0) mrow[j] = (int64_t)m;
             }
         } else {
