@@ -592,99 +592,97 @@ def main() -> int:
 
         # next row: lag over the median rank (exact radix select per boundary)
         if want("lag"):
-            if R <= sf.SF_MAX_R_LAG:
-                lg = torch.empty((T, S), dtype=torch.int64, device=dev)
-                lgi = torch.empty((T, S), dtype=torch.int64, device=dev)
-                l_views = [(d[t0:t1], lg[t0:t1], lgi[t0:t1]) for t0, t1 in bounds]
+            lg = torch.empty((T, S), dtype=torch.int64, device=dev)
+            lgi = torch.empty((T, S), dtype=torch.int64, device=dev)
+            l_views = [(d[t0:t1], lg[t0:t1], lgi[t0:t1]) for t0, t1 in bounds]
+            for dv, a1, a2 in l_views:
+                sf.sf_frontier_lag(dv, a1, a2, stream=stream)
+            lt = []
+            for _ in range(max(3, args.steps // 2)):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
                 for dv, a1, a2 in l_views:
                     sf.sf_frontier_lag(dv, a1, a2, stream=stream)
-                lt = []
-                for _ in range(max(3, args.steps // 2)):
-                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    a.record(stream)
-                    for dv, a1, a2 in l_views:
-                        sf.sf_frontier_lag(dv, a1, a2, stream=stream)
-                    b.record(stream)
-                    lt.append((a, b))
-                torch.cuda.synchronize(dev)
-                l_ms = float(np.median([a.elapsed_time(b) for a, b in lt])) / len(bounds)
-                l_bytes = (8 * T * S * R + 16 * T * S) / len(bounds)
-                l_exact = l_cpu = None
-                if oracle_out:
-                    import oracle
-                    nl = min(T, 32)
-                    x = synth.generate(wl, 0, nl)
-                    tc = time.perf_counter()
-                    ol, oi = oracle.frontier_lag(x)
-                    l_cpu = row_cpu(x.size, time.perf_counter() - tc,
-                                    "oracle frontier_lag on %d steps of the workload" % nl)
-                    l_exact = bool(np.array_equal(lg[:nl].cpu().numpy(), ol) and
-                                   np.array_equal(lgi[:nl].cpu().numpy(), oi))
-                next_rows["lag"] = {
-                    "kernel": "k_median_spread<prefix>",
-                    "bound": "valu (radix select)",
-                    "launch_ms": l_ms,
-                    "algorithmic_bytes_per_launch": l_bytes,
-                    "achieved": l_bytes / (l_ms / 1e3) / 1e9,
-                    "peak": PEAK_HBM_GBPS,
-                    "unit": "GB/s",
-                    "frac": l_bytes / (l_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
-                    "bit_exact_first_steps": l_exact,
-                    "samples_per_s": T * S * R / len(bounds) / (l_ms / 1e3),
-                    "cpu_baseline": l_cpu,
-                }
-                del lg, lgi, l_views
+                b.record(stream)
+                lt.append((a, b))
+            torch.cuda.synchronize(dev)
+            l_ms = float(np.median([a.elapsed_time(b) for a, b in lt])) / len(bounds)
+            l_bytes = (8 * T * S * R + 16 * T * S) / len(bounds)
+            l_exact = l_cpu = None
+            if oracle_out:
+                import oracle
+                nl = min(T, 32)
+                x = synth.generate(wl, 0, nl)
+                tc = time.perf_counter()
+                ol, oi = oracle.frontier_lag(x)
+                l_cpu = row_cpu(x.size, time.perf_counter() - tc,
+                                "oracle frontier_lag on %d steps of the workload" % nl)
+                l_exact = bool(np.array_equal(lg[:nl].cpu().numpy(), ol) and
+                               np.array_equal(lgi[:nl].cpu().numpy(), oi))
+            next_rows["lag"] = {
+                "kernel": "k_median_spread<prefix>",
+                "bound": "valu (radix select)",
+                "launch_ms": l_ms,
+                "algorithmic_bytes_per_launch": l_bytes,
+                "achieved": l_bytes / (l_ms / 1e3) / 1e9,
+                "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s",
+                "frac": l_bytes / (l_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                "bit_exact_first_steps": l_exact,
+                "samples_per_s": T * S * R / len(bounds) / (l_ms / 1e3),
+                "cpu_baseline": l_cpu,
+            }
+            del lg, lgi, l_views
 
         # next row: raw rank spread (the dispersion baseline of Sec. 6.2),
         # the lag's selection on each stage's durations
         if want("rank_spread"):
-            if R <= sf.SF_MAX_R_LAG:
-                sp = torch.empty((T, S), dtype=torch.int64, device=dev)
-                wsp = torch.empty((W, S), dtype=torch.int64, device=dev)
-                s_views = []
-                for t0, t1 in bounds:
-                    w0, w1 = t0 // wl.window, -(-t1 // wl.window)
-                    s_views.append((d[t0:t1], sp[t0:t1], wsp[w0:w1]))
+            sp = torch.empty((T, S), dtype=torch.int64, device=dev)
+            wsp = torch.empty((W, S), dtype=torch.int64, device=dev)
+            s_views = []
+            for t0, t1 in bounds:
+                w0, w1 = t0 // wl.window, -(-t1 // wl.window)
+                s_views.append((d[t0:t1], sp[t0:t1], wsp[w0:w1]))
+            for dv, a1, a2 in s_views:
+                sf.sf_rank_spread(dv, wl.window, a1, a2, stream=stream)
+            st = []
+            for _ in range(max(3, args.steps // 2)):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
                 for dv, a1, a2 in s_views:
                     sf.sf_rank_spread(dv, wl.window, a1, a2, stream=stream)
-                st = []
-                for _ in range(max(3, args.steps // 2)):
-                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    a.record(stream)
-                    for dv, a1, a2 in s_views:
-                        sf.sf_rank_spread(dv, wl.window, a1, a2, stream=stream)
-                    b.record(stream)
-                    st.append((a, b))
-                torch.cuda.synchronize(dev)
-                s_ms = float(np.median([a.elapsed_time(b) for a, b in st])) / len(bounds)
-                s_bytes = (8 * T * S * R + 8 * T * S + 8 * W * S) / len(bounds)
-                s_exact = s_cpu = None
-                if oracle_out:
-                    import oracle
-                    ns = min(T, 32)
-                    x = synth.generate(wl, 0, ns)
-                    tc = time.perf_counter()
-                    osp, _ = oracle.rank_spread(x, wl.window)
-                    s_cpu = row_cpu(x.size, time.perf_counter() - tc,
-                                    "oracle rank_spread on %d steps of the workload" % ns)
-                    s_exact = bool(np.array_equal(sp[:ns].cpu().numpy(), osp))
-                wsum = wsp.sum(dim=0).double()
-                next_rows["rank_spread"] = {
-                    "kernel": "k_median_spread<raw> (+ k_window_sum)",
-                    "bound": "valu (radix select)",
-                    "launch_ms": s_ms,
-                    "algorithmic_bytes_per_launch": s_bytes,
-                    "achieved": s_bytes / (s_ms / 1e3) / 1e9,
-                    "peak": PEAK_HBM_GBPS,
-                    "unit": "GB/s",
-                    "frac": s_bytes / (s_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
-                    "spread_share_all_windows": [round(float(v) / float(wsum.sum()), 6) for v in wsum]
-                    if float(wsum.sum()) > 0 else None,
-                    "bit_exact_first_steps": s_exact,
-                    "samples_per_s": T * S * R / len(bounds) / (s_ms / 1e3),
-                    "cpu_baseline": s_cpu,
-                }
-                del sp, wsp, s_views
+                b.record(stream)
+                st.append((a, b))
+            torch.cuda.synchronize(dev)
+            s_ms = float(np.median([a.elapsed_time(b) for a, b in st])) / len(bounds)
+            s_bytes = (8 * T * S * R + 8 * T * S + 8 * W * S) / len(bounds)
+            s_exact = s_cpu = None
+            if oracle_out:
+                import oracle
+                ns = min(T, 32)
+                x = synth.generate(wl, 0, ns)
+                tc = time.perf_counter()
+                osp, _ = oracle.rank_spread(x, wl.window)
+                s_cpu = row_cpu(x.size, time.perf_counter() - tc,
+                                "oracle rank_spread on %d steps of the workload" % ns)
+                s_exact = bool(np.array_equal(sp[:ns].cpu().numpy(), osp))
+            wsum = wsp.sum(dim=0).double()
+            next_rows["rank_spread"] = {
+                "kernel": "k_median_spread<raw> (+ k_window_sum)",
+                "bound": "valu (radix select)",
+                "launch_ms": s_ms,
+                "algorithmic_bytes_per_launch": s_bytes,
+                "achieved": s_bytes / (s_ms / 1e3) / 1e9,
+                "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s",
+                "frac": s_bytes / (s_ms / 1e3) / 1e9 / PEAK_HBM_GBPS,
+                "spread_share_all_windows": [round(float(v) / float(wsum.sum()), 6) for v in wsum]
+                if float(wsum.sum()) > 0 else None,
+                "bit_exact_first_steps": s_exact,
+                "samples_per_s": T * S * R / len(bounds) / (s_ms / 1e3),
+                "cpu_baseline": s_cpu,
+            }
+            del sp, wsp, s_views
 
         # next row: routing candidate set (tau 4/5) of the path's windows
         if want("route"):
@@ -775,6 +773,9 @@ def main() -> int:
               torch.empty((W8, 2, 2), dtype=torch.int32, device=dev)]
 
         def step8(st):
+            sf.sf_frontier_summary(d8, wl8.window, *o8, stream=st)
+
+        def step8_separate(st):
             sf.sf_frontier(d8, o8[0], o8[1], stream=st)
             sf.sf_window_summary(o8[0], o8[1], R8, wl8.window, o8[2], o8[3], o8[4], stream=st)
 
@@ -792,6 +793,12 @@ def main() -> int:
             step8(stream)
         torch.cuda.synchronize(dev)
         eager_us = (time.perf_counter() - t0) * 1e6 / n8
+        t0 = time.perf_counter()
+        for _ in range(n8):
+            step8_separate(stream)
+        torch.cuda.synchronize()
+        sep_us = (time.perf_counter() - t0) * 1e6 / n8
+        same = all(torch.equal(a, b) for a, b in zip(o8, eager_ref))
         g8 = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g8):
             for _ in range(10):
@@ -800,15 +807,22 @@ def main() -> int:
             x.fill_(-1)
         g8.replay()
         torch.cuda.synchronize(dev)
-        same = all(torch.equal(a, b) for a, b in zip(o8, eager_ref))
+        same = same and all(torch.equal(a, b) for a, b in zip(o8, eager_ref))
         t0 = time.perf_counter()
         for _ in range(n8 // 10):
             g8.replay()
         torch.cuda.synchronize(dev)
         graph_us = (time.perf_counter() - t0) * 1e6 / n8
-        graph_replay = {"workload": wl8.name, "eager_us_per_step": eager_us,
+        oi8, ol8 = oracle.frontier(synth.generate(wl8)) if oracle_out else (None, None)
+        exact8 = None
+        if oi8 is not None:
+            want8 = (oi8, ol8) + oracle.window_summary(oi8, ol8, R8, wl8.window)
+            exact8 = all(np.array_equal(a.cpu().numpy(), b) for a, b in zip(o8, want8))
+        graph_replay = {"workload": wl8.name, "call": "sf_frontier_summary (one launch)",
+                        "eager_us_per_step": eager_us,
+                        "eager_us_per_step_separate_calls": sep_us,
                         "graph_us_per_step": graph_us, "steps": n8,
-                        "outputs_equal_eager": same}
+                        "outputs_equal_eager": same, "bit_exact": exact8}
         del g8, d8, o8, eager_ref
 
     samples = T * S * R

@@ -61,12 +61,6 @@ enum {
  * stage count of sf_frontier_evidence, and of K + 1 in sf_ingest (their
  * per-stage partial results are staged in on-chip memory). */
 #define SF_MAX_S_EVIDENCE 512
-/* Largest rank count of sf_frontier_lag (all prefixes of a step are held
- * on chip at once). */
-#define SF_MAX_R_LAG 16384
-/* Largest stage count of sf_exposure_gain (its per-stage reductions are
- * kept in registers). */
-#define SF_MAX_S_GAIN 64
 /* Every rank-local prefix P[t][r][s] must be below this many ns (about
  * 39 hours) so that the packed key fits in 64 bits. */
 #define SF_MAX_PREFIX_NS ((int64_t)1 << 47)
@@ -214,7 +208,11 @@ int sf_route(const int64_t* stage_exposed, int64_t W, int32_t S, int64_t tau_num
  *   baseline             [W][S][R] int64 ns: btilde for the steps of window
  *                        w (a per-rank window median, a cohort median, a
  *                        no-stall reference, ...).
- *   T, R, S, window      as for sf_window_summary; S <= SF_MAX_S_GAIN.
+ *   T, R, S, window      as for sf_window_summary.  Up to 64 stages the
+ *                        per-stage deltas are held in registers and the
+ *                        durations read once; past 64 a two-pass kernel
+ *                        reads each step's durations twice (slower, same
+ *                        results).
  *   out_gain             [T][S] int64: the gain of each step and stage.
  *   out_makespan         [T] int64: F[t][S-1], the step's exposed makespan.
  *   out_window_gain      [W][S] int64: window sums of out_gain.
@@ -238,7 +236,11 @@ int sf_exposure_gain(const int64_t* durations, const int64_t* baseline, int64_t 
  * (the middle one for odd R), so the lag is an exact integer.
  *
  *   durations      [T][S][R] int64 ns (as for sf_frontier).
- *   T, R, S        0 <= T <= INT32_MAX, 1 <= R <= SF_MAX_R_LAG, 1 <= S.
+ *   T, R, S        0 <= T <= INT32_MAX, 1 <= R <= SF_MAX_R, 1 <= S.  A
+ *                  step's values are held on chip up to 16384 ranks (up to
+ *                  32768 for even R with a 16-byte aligned base); beyond
+ *                  that a kernel re-reads them from global memory at every
+ *                  select pass (slower, same results).
  *                  T == 0 is a no-op.
  *   out_lag        [T][S] int64 ns, >= 0.
  *   out_lag_inc    [T][S] int64 ns.
@@ -258,7 +260,8 @@ int sf_frontier_lag(const int64_t* durations, int64_t T, int32_t R, int32_t S,
  * its sums over the steps of each window.
  *
  *   durations          [T][S][R] int64 ns (as for sf_frontier).
- *   T, R, S            0 <= T <= INT32_MAX, 1 <= R <= SF_MAX_R_LAG, 1 <= S.
+ *   T, R, S            0 <= T <= INT32_MAX, 1 <= R <= SF_MAX_R, 1 <= S
+ *                      (above 16384 ranks as for sf_frontier_lag).
  *                      T == 0 is a no-op.
  *   window             steps per window, >= 1 (windows as for
  *                      sf_window_summary).
@@ -341,6 +344,32 @@ int sf_window_summary(const int64_t* increment, const int32_t* leader,
                       int64_t T, int32_t R, int32_t S, int64_t window,
                       int64_t* out_stage_exposed, int32_t* out_lead_counts,
                       int32_t* out_top2, sf_stream_t stream);
+
+/*
+ * sf_frontier_summary -- sf_frontier followed by sf_window_summary over the
+ * same steps, as one call: the per-step accounting of Sec. 3 (Eq. (1)) and
+ * its reduction over windows (Eq. (2) numerators, lead counts, the top-2 of
+ * Sec. 4).  Small inputs (R <= 256, S <= 64, min(window, T) <= 1024 and
+ * T * S * R <= 2^20 samples) run as ONE kernel launch, one workgroup per
+ * window, for callers bound by launch latency (a per-step or per-window
+ * serving loop); larger ones run the two calls' kernels.  Every output is
+ * identical to sf_frontier's and sf_window_summary's.
+ *
+ *   durations          [T][S][R] int64 ns (as for sf_frontier).
+ *   T, R, S, window    as for sf_window_summary (T == 0 is a no-op).
+ *   out_increment      [T][S] int64, out_leader [T][S] int32: as for
+ *                      sf_frontier.
+ *   out_stage_exposed  [W][S] int64, out_lead_counts [W][S][R] int32,
+ *   out_top2           [W][2][2] int32: as for sf_window_summary.
+ *   stream             HIP stream.
+ *
+ * Preconditions as for sf_frontier.  Pointers aligned to their element
+ * size; no two arrays may overlap.  Returns SF_OK, SF_EINVAL or SF_EHIP.
+ */
+int sf_frontier_summary(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                        int64_t window, int64_t* out_increment, int32_t* out_leader,
+                        int64_t* out_stage_exposed, int32_t* out_lead_counts,
+                        int32_t* out_top2, sf_stream_t stream);
 
 /*
  * sf_window_lead_exposed -- the exposed time each rank led, per window and

@@ -143,6 +143,93 @@ __global__ __launch_bounds__(WG) void k_exposure_gain(
     }
 }
 
+// Any number of stages (past what the registers of k_exposure_gain hold):
+// for each rank tile the step group makes two passes over the stages, the
+// rank totals first and then every stage's candidate max (the durations of
+// the tile are read twice).  The group's last lane keeps the maxima over
+// tiles in the step's own out_gain row (the replaced-stage maxima) and
+// out_makespan entry (F), and after a barrier the workgroup turns the rows
+// into gains.  Slots past R re-read rank r0, which cannot change a max.
+template <int VEC, int K, int G, int WG>
+__global__ __launch_bounds__(WG) void k_exposure_gain_wide(
+    const int64_t* __restrict__ d, const int64_t* __restrict__ btilde, int64_t T, int R, int S,
+    int64_t window, int64_t* __restrict__ gain, int64_t* __restrict__ makespan)
+{
+    static_assert(K % VEC == 0 && G <= 64 && WG % G == 0, "one writer lane per step");
+    constexpr int SPW = WG / G;
+    constexpr int NLD = K / VEC;
+    constexpr int RT = G * K;
+    const int tid = threadIdx.x;
+    const int gl = tid % G;
+    const bool writer = gl == G - 1;
+    const int64_t tb = xcd_block() * SPW;
+    const int64_t t = tb + tid / G;
+    if (t < T) {
+        const int64_t* dt = d + t * (int64_t)S * R;
+        const int64_t* bw = btilde + (t / window) * (int64_t)S * R;
+        u64* fr = reinterpret_cast<u64*>(gain) + t * S;  // replaced-stage maxima so far
+        u64* fm = reinterpret_cast<u64*>(makespan) + t;  // F so far
+        for (int r0 = 0; r0 < R; r0 += RT) {
+            int idx[NLD];
+#pragma unroll
+            for (int l = 0; l < NLD; ++l) {
+                const int r = r0 + (l * G + gl) * VEC;
+                idx[l] = r < R ? r : r0;
+            }
+            auto load = [&](const int64_t* row, int l, int64_t* x) {
+                if (VEC == 2) {
+                    const v2i64 a = *reinterpret_cast<const v2i64*>(row + idx[l]);
+                    x[0] = a.x;
+                    x[VEC - 1] = a.y;
+                } else {
+                    x[0] = row[idx[l]];
+                }
+            };
+            int64_t tot[K];
+#pragma unroll
+            for (int k = 0; k < K; ++k) tot[k] = 0;
+            for (int s = 0; s < S; ++s) {
+#pragma unroll
+                for (int l = 0; l < NLD; ++l) {
+                    int64_t x[VEC];
+                    load(dt + (int64_t)s * R, l, x);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) tot[l * VEC + e] += x[e];
+                }
+            }
+            u64 f = 0;
+#pragma unroll
+            for (int k = 0; k < K; ++k) f = umax64(f, (u64)tot[k]);
+            f = group_max<G>(f);
+            if (writer) *fm = r0 == 0 ? f : umax64(*fm, f);
+            for (int s = 0; s < S; ++s) {
+                u64 m = 0;
+#pragma unroll
+                for (int l = 0; l < NLD; ++l) {
+                    int64_t x[VEC], y[VEC];
+                    load(dt + (int64_t)s * R, l, x);
+                    load(bw + (int64_t)s * R, l, y);
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) {
+                        const int64_t red = x[e] - y[e];
+                        m = umax64(m, (u64)(tot[l * VEC + e] - (red > 0 ? red : 0)));
+                    }
+                }
+                m = group_max<G>(m);
+                if (writer) fr[s] = r0 == 0 ? m : umax64(fr[s], m);
+            }
+        }
+    }
+    __syncthreads();  // the writer lanes' maxima are visible to the workgroup
+    for (int i = tid; i < SPW * S; i += WG) {
+        const int jj = i / S;
+        const int64_t tt = tb + jj;
+        if (tt >= T) break;
+        const int64_t idx = tt * S + (i - jj * S);
+        gain[idx] = makespan[tt] - gain[idx];
+    }
+}
+
 struct GainVariant {
     const void* fn;
     int G, WG;
@@ -179,6 +266,8 @@ GainVariant pick_gain_s(int R, bool vec2)
 // SMAX close above S: every unrolled stage past S still issues its two loads
 // and holds its deltas, so 12 stages under SMAX = 16 ran 14-18% slower than
 // under SMAX = 12 (and 6 under 8, 9% slower) on MI355X.
+constexpr int kGainRegS = 64;  // stages whose deltas k_exposure_gain keeps in registers
+
 GainVariant pick_gain(int R, int S, bool vec2)
 {
     if (S <= 4) return pick_gain_s<4>(R, vec2);
@@ -188,7 +277,7 @@ GainVariant pick_gain(int R, int S, bool vec2)
     if (S <= 16) return pick_gain_s<16>(R, vec2);
     if (S <= 24) return pick_gain_s<24>(R, vec2);
     if (S <= 32) return pick_gain_s<32>(R, vec2);
-    return pick_gain_g<1, 1, 64>(R);
+    return pick_gain_g<1, 1, 64>(R);  // S <= kGainRegS
 }
 
 }  // namespace sfk
@@ -200,8 +289,7 @@ SF_API int sf_exposure_gain(const int64_t* durations, const int64_t* baseline, i
                             int64_t* out_makespan, int64_t* out_window_gain,
                             int64_t* out_window_makespan, sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S_GAIN || window < 1)
-        return SF_EINVAL;
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || window < 1) return SF_EINVAL;
     if (!fits(T, S, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     const int64_t W = sf_num_windows(T, window);
@@ -217,7 +305,11 @@ SF_API int sf_exposure_gain(const int64_t* durations, const int64_t* baseline, i
             if (!disjoint(bufs[a], sizes[a], bufs[b], sizes[b])) return SF_EINVAL;
 
     const bool vec2 = (R % 2 == 0) && aligned(durations, 16) && aligned(baseline, 16);
-    const GainVariant v = pick_gain(R, S, vec2);
+    const GainVariant v =
+        S <= kGainRegS ? pick_gain(R, S, vec2)
+                       : GainVariant{vec2 ? reinterpret_cast<const void*>(&k_exposure_gain_wide<2, 2, 64, 256>)
+                                          : reinterpret_cast<const void*>(&k_exposure_gain_wide<1, 2, 64, 256>),
+                                     64, 256};
     const int spw = v.WG / v.G;
     const int64_t blocks = (T + spw - 1) / spw;
     if (blocks > INT32_MAX) return SF_EINVAL;

@@ -81,12 +81,12 @@ constexpr int64_t kRedo = INT64_MIN;  // outputs are >= 0 under the data contrac
 
 template <bool PREFIX, int VEC, int K, int WG, int LCAP, bool PUBU, bool FULL, bool NARROW,
           bool REDO>
-__global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW ? 8 : 4))) void k_median_spread(const int64_t* __restrict__ d, int64_t T,
+__global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K <= 16 ? 8 : 4))) void k_median_spread(const int64_t* __restrict__ d, int64_t T,
                                                       int R, int S, int64_t* __restrict__ out,
                                                       int64_t* __restrict__ out_inc)
 {
     static_assert(K % VEC == 0 && WG % 64 == 0 && WG / 64 <= 16, "shape");
-    static_assert(!NARROW || (FULL && VEC == 2 && !REDO), "the narrow pass takes full 16-byte tiles");
+    static_assert(!NARROW || (VEC == 2 && !REDO), "the narrow pass takes 16-byte loads");
     typedef typename std::conditional<NARROW, uint32_t, u64>::type V;
     constexpr int NW = WG / 64;
     constexpr int NLD = K / VEC;
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW ? 8 :
             // the next is issued (two at a time for the lag, whose prefixes
             // stay live across stages: one at a time measured 9% slower,
             // four at a time spilled 32 bytes and 17% slower)
-            constexpr int CH = PREFIX ? NLD / 2 : 2;
+            constexpr int CH = PREFIX ? NLD / 2 : (K <= 32 ? 2 : NLD / 4);
             const int64_t* row = dt + (int64_t)s * R;
             uint32_t mx = 0, mn = ~0u;
             bool wide = false;  // wave-uniform: some value of the wave left 32 bits
@@ -166,15 +166,18 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW ? 8 :
 #pragma unroll
                 for (int l = 0; l < NLD / CH; ++l)
                     xs[l] = __builtin_nontemporal_load(
-                        reinterpret_cast<const v2i64*>(row + ((ch * (NLD / CH) + l) * WG + tid) * 2));
+                        reinterpret_cast<const v2i64*>(row + idx[ch * (NLD / CH) + l]));
 #pragma unroll
                 for (int l = 0; l < NLD / CH; ++l) {
+                    // a slot pair past R (re-reading the row's first pair)
+                    // keeps 0 and is left out of every reduction and pass
+                    const bool okl = ok[ch * (NLD / CH) + l];
 #pragma unroll
                     for (int e = 0; e < 2; ++e) {
                         const int k = (ch * (NLD / CH) + l) * 2 + e;
                         const u64 x = (u64)(e == 0 ? xs[l].x : xs[l].y);
-                        const uint32_t lo = (uint32_t)x;
-                        w |= (uint32_t)(x >> 32);
+                        const uint32_t lo = okl ? (uint32_t)x : 0u;
+                        w |= okl ? (uint32_t)(x >> 32) : 0u;
                         if (PREFIX) {
                             const uint32_t np = (uint32_t)P[k] + lo;
                             w |= np < lo ? 1u : 0u;  // carry
@@ -182,8 +185,8 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW ? 8 :
                         } else {
                             P[k] = lo;
                         }
-                        mx = max(mx, (uint32_t)P[k]);
-                        mn = min(mn, (uint32_t)P[k]);
+                        mx = max(mx, okl ? (uint32_t)P[k] : 0u);
+                        mn = min(mn, okl ? (uint32_t)P[k] : ~0u);
                     }
                 }
                 wide = wide || __ballot(w != 0) != 0;
@@ -389,6 +392,141 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW ? 8 :
     }
 }
 
+// More ranks than one workgroup holds in registers as 64-bit values: the
+// 64-bit select with the values recomputed from global memory at every pass
+// (a prefix from its stage rows, a duration from its row), one workgroup of
+// kStreamWG threads per step.  Per boundary: a pass for the max and min,
+// then radix passes over u = value - min (256 bins; a digit isolating one
+// value ends it; once at most kStreamList values are left they go to an LDS
+// list and later passes read only it).  It redoes the steps the 32-bit pass
+// hands over (REDO: every other workgroup returns at once); the durations
+// of a step are read several times over, from the caches when the step fits
+// them.
+constexpr int kStreamWG = 1024;
+constexpr int kStreamList = 4096;
+
+template <bool PREFIX, bool REDO>
+__global__ __launch_bounds__(kStreamWG) void k_median_stream(const int64_t* __restrict__ d,
+                                                             int64_t T, int R, int S,
+                                                             int64_t* __restrict__ out,
+                                                             int64_t* __restrict__ out_inc)
+{
+    constexpr int NW = kStreamWG / 64;
+    __shared__ __attribute__((aligned(16))) uint32_t hist[kSelWords];
+    __shared__ u64 red_max[NW], red_min[NW];
+    __shared__ uint32_t sel[3];
+    __shared__ u64 list[kStreamList];
+    __shared__ uint32_t list_n;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int64_t t = blockIdx.x;
+    if (t >= T) return;
+    if (REDO && out[t * S] != kRedo) return;  // a step the narrow pass resolved
+    const int64_t* dt = d + t * (int64_t)S * R;
+    for (int i = tid; i < kSelWords; i += kStreamWG) hist[i] = 0;
+    int64_t L_prev = 0;
+    for (int s = 0; s < S; ++s) {
+        auto val = [&](int r) -> u64 {
+            if (!PREFIX) return (u64)dt[(int64_t)s * R + r];
+            u64 p = 0;
+            for (int j = 0; j <= s; ++j) p += (u64)dt[(int64_t)j * R + r];
+            return p;
+        };
+        u64 mx = 0, mn = ~0ull;
+        for (int r = tid; r < R; r += kStreamWG) {
+            const u64 v = val(r);
+            mx = umax64(mx, v);
+            mn = umin64(mn, v);
+        }
+        mx = group_max<64>(mx);
+        mn = ~group_max<64>(~mn);
+        if (lane == 63) {
+            red_max[wave] = mx;
+            red_min[wave] = mn;
+        }
+        __syncthreads();
+        u64 F = 0, Pmin = ~0ull;
+        for (int i = 0; i < NW; ++i) {
+            F = umax64(F, red_max[i]);
+            Pmin = umin64(Pmin, red_min[i]);
+        }
+        const u64 range = F - Pmin;
+        u64 um = 0;  // u of the median
+        if (range != 0) {
+            int lo = sel_first_lo(range), hi = lo + 8;
+            u64 prefix = 0;
+            uint32_t kk = (uint32_t)((R - 1) / 2);
+            bool in_list = false;
+            uint32_t n = 0;
+            for (;;) {
+                if (in_list) {
+                    for (uint32_t i = tid; i < n; i += kStreamWG) {
+                        const u64 u = list[i];
+                        if (sel_match(u, hi, prefix)) atomicAdd(&hist[sel_bin(u, lo, hi, prefix)], 1u);
+                    }
+                } else {
+                    for (int r = tid; r < R; r += kStreamWG) {
+                        const u64 u = val(r) - Pmin;
+                        if (sel_match(u, hi, prefix)) atomicAdd(&hist[sel_bin(u, lo, hi, prefix)], 1u);
+                    }
+                }
+                __syncthreads();
+                if (wave == 0) {
+                    uint32_t dg, cn, k2 = kk;
+                    sel_scan_wave(hist, lane, k2, dg, cn);
+                    if (lane == 0) {
+                        sel[0] = dg;
+                        sel[1] = k2;
+                        sel[2] = cn;
+                    }
+                }
+                __syncthreads();
+                const uint32_t digit = sel[0], count = sel[2];
+                kk = sel[1];
+                for (int i = tid; i < kSelWords; i += kStreamWG) hist[i] = 0;
+                if (tid == 0) list_n = 0;
+                __syncthreads();  // sel, hist and list_n are rewritten next
+                prefix = (prefix << (hi - lo)) | (u64)digit;
+                hi = lo;
+                if (hi == 0) break;  // every bit chosen
+                lo = lo > 8 ? lo - 8 : 0;
+                if (count == 1 || (!in_list && count <= (uint32_t)kStreamList)) {
+                    // the values left (one, or few enough for the list)
+                    if (in_list) {
+                        for (uint32_t i = tid; i < n; i += kStreamWG)
+                            if (sel_match(list[i], hi, prefix)) red_max[0] = list[i];
+                    } else {
+                        for (int r = tid; r < R; r += kStreamWG) {
+                            const u64 u = val(r) - Pmin;
+                            if (sel_match(u, hi, prefix)) {
+                                if (count == 1) red_max[0] = u;
+                                else list[atomicAdd(&list_n, 1u)] = u;  // < count
+                            }
+                        }
+                    }
+                    __syncthreads();
+                    if (count == 1) {
+                        prefix = red_max[0];
+                        __syncthreads();  // red_max is rewritten by the next stage
+                        break;
+                    }
+                    in_list = true;
+                    n = count;
+                }
+            }
+            um = prefix;
+        }
+        if (tid == 0) {
+            const int64_t L = (int64_t)(range - um);
+            out[t * S + s] = L;
+            if (PREFIX) out_inc[t * S + s] = L - L_prev;
+        }
+        L_prev = (int64_t)(range - um);
+        __syncthreads();  // red_max, red_min and the list are rewritten by the next stage
+    }
+}
+
 struct LagVariant {
     const void* fn;
     int WG;
@@ -416,6 +554,23 @@ const void* lag_kernel()
 // (measured at 16384 ranks: 32% faster for the raw spread, 18% for the lag;
 // at 1024 and 4096 ranks the raw spread 9% and 4% faster, the lag 6% slower,
 // so the lag keeps its 64-bit shapes there).
+// More than 16384 ranks: up to 32768 the 32-bit pass with 32 values per
+// lane (16-byte loads), the streaming 64-bit kernel redoing the steps it
+// hands over; beyond that (64 values per lane spill) and with 8-byte loads
+// (odd R or a misaligned base) the streaming kernel alone.
+template <bool PREFIX, int VEC>
+LagVariant lag_wide(int R)
+{
+    if constexpr (VEC == 2) {
+        const void* redo = reinterpret_cast<const void*>(&k_median_stream<PREFIX, true>);
+        if (R == 32 * 1024) return LagVariant{lag_kernel<PREFIX, 2, 32, 1024, true, true>(), 1024, redo};
+        if (R < 32 * 1024) return LagVariant{lag_kernel<PREFIX, 2, 32, 1024, false, true>(), 1024, redo};
+    }
+    (void)R;
+    return LagVariant{reinterpret_cast<const void*>(&k_median_stream<PREFIX, false>), kStreamWG,
+                      nullptr};
+}
+
 template <bool PREFIX, int VEC, int K, int WG>
 LagVariant lag_shape(int R)
 {
@@ -444,7 +599,8 @@ LagVariant pick_lag(int R)
     if (R <= 2048) return lag_shape<PREFIX, VEC, 16, 128>(R);
     if (R <= 4096) return lag_shape<PREFIX, VEC, 16, 256>(R);
     if (R <= 8192) return lag_shape<PREFIX, VEC, 16, 512>(R);
-    return lag_shape<PREFIX, VEC, 16, 1024>(R);  // R <= SF_MAX_R_LAG = 16384
+    if (R <= 16384) return lag_shape<PREFIX, VEC, 16, 1024>(R);
+    return lag_wide<PREFIX, VEC>(R);  // R <= SF_MAX_R
 }
 
 // the narrow pass, then (if it has one) the 64-bit pass over the steps it
@@ -463,7 +619,7 @@ using namespace sfk;
 SF_API int sf_frontier_lag(const int64_t* durations, int64_t T, int32_t R, int32_t S,
                            int64_t* out_lag, int64_t* out_lag_inc, sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R_LAG || S < 1) return SF_EINVAL;
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1) return SF_EINVAL;
     if (!fits(T, S, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     if (T > INT32_MAX) return SF_EINVAL;  // one workgroup per step
@@ -486,7 +642,7 @@ SF_API int sf_rank_spread(const int64_t* durations, int64_t T, int32_t R, int32_
                           int64_t window, int64_t* out_spread, int64_t* out_window_spread,
                           sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R_LAG || S < 1 || window < 1)
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || window < 1)
         return SF_EINVAL;
     if (!fits(T, S, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;

@@ -13,6 +13,7 @@
 
 #include "sf_device.h"
 #include "sf_host.h"
+#include "sf_select.h"
 
 namespace sfk {
 
@@ -155,6 +156,178 @@ __global__ __launch_bounds__(kTopWG) void k_window_top2(const int64_t* __restric
             top2[w * 4 + 2 * k + 1] = rank;
         }
     }
+}
+
+// Fused frontier pass and window summary for small inputs (few ranks and
+// stages, short windows): one workgroup of 1024 threads per window does the
+// whole path of Sec. 3 for the window's steps.  Groups of G lanes own a step
+// (K ranks per lane, one rank tile, the packed keys and DPP maxima of
+// k_frontier), loading a chunk of stage rows at once; the group's last lane
+// writes each boundary's advance and leader as soon as the stage is reduced
+// and adds them into the window's LDS totals and lead counts; then the
+// workgroup writes the counts and picks the top-2.  One launch instead of
+// three, for callers bound by launch latency.
+constexpr int kFusedMaxR = 256;
+constexpr int kFusedMaxS = 64;
+constexpr int64_t kFusedMaxWindow = 1024;
+constexpr int64_t kFusedMaxSamples = 1 << 20;
+
+constexpr int kFusedWG = 1024;  // threads of the fused kernel: 1024 / G steps per round
+
+// Sum over the 64 lanes, valid in lane 63 (the DPP pattern of group_max,
+// with lanes outside a move's rows or sources reading 0)
+__device__ __forceinline__ u64 wave_sum64_dpp(u64 v)
+{
+#define SF_DPP_ADD(CTRL, ROWS)                                                                        \
+    {                                                                                                 \
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, ROWS, 0xF, true); \
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, ROWS, 0xF, true); \
+        v += ((u64)hi << 32) | lo;                                                                    \
+    }
+    SF_DPP_ADD(0xB1, 0xF)   // quad_perm [1,0,3,2]
+    SF_DPP_ADD(0x4E, 0xF)   // quad_perm [2,3,0,1]
+    SF_DPP_ADD(0x141, 0xF)  // row_half_mirror
+    SF_DPP_ADD(0x140, 0xF)  // row_mirror
+    SF_DPP_ADD(0x142, 0xA)  // row_bcast:15 -> rows 1, 3
+    SF_DPP_ADD(0x143, 0xC)  // row_bcast:31 -> rows 2, 3
+#undef SF_DPP_ADD
+    return v;
+}
+
+template <int VEC, int K, int G>
+__global__ __launch_bounds__(kFusedWG) void k_frontier_summary(
+    const int64_t* __restrict__ d, int64_t T, int R, int S, int64_t window, int64_t W,
+    int64_t* __restrict__ inc, int32_t* __restrict__ lead, int64_t* __restrict__ exposed,
+    int32_t* __restrict__ counts, int32_t* __restrict__ top2)
+{
+    static_assert(K % VEC == 0 && G <= 32, "one DPP group per step");
+    constexpr int SPW = kFusedWG / G;  // steps per round
+    constexpr int NLD = K / VEC;
+    constexpr int CH = K >= 8 ? 1 : 16 / K;  // stage rows loaded at once (up to 16 values per lane)
+    __shared__ u64 ex_sh[kFusedMaxS];
+    __shared__ int32_t cnt_sh[kFusedMaxS * kFusedMaxR];
+    const int tid = threadIdx.x;
+    const int gl = tid % G;
+    const int j = tid / G;
+    const bool writer = gl == G - 1;
+    const int SR = S * R;
+    for (int64_t w = blockIdx.x; w < W; w += gridDim.x) {
+        const int64_t t0 = w * window;
+        const int64_t t1 = min(t0 + window, T);
+        for (int i = tid; i < S; i += kFusedWG) ex_sh[i] = 0;
+        for (int i = tid; i < SR; i += kFusedWG) cnt_sh[i] = 0;
+        __syncthreads();
+        for (int64_t tb = t0; tb < t1; tb += SPW) {
+            // every lane runs the stage loop (the wave sums below need all
+            // lanes); a group past the window re-reads the window's first
+            // step and contributes nothing
+            const bool act = tb + j < t1;
+            const int64_t t = act ? tb + j : t0;
+            const int64_t* dt = d + t * (int64_t)S * R;
+            u64 q[K];
+            int idx[NLD];
+#pragma unroll
+            for (int l = 0; l < NLD; ++l) {
+                const int r = (l * G + gl) * VEC;
+                const bool ok = r < R;
+                // a slot past R re-reads rank 0 with rank field 0: its key
+                // stays strictly below rank 0's own
+                idx[l] = ok ? r : 0;
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) q[l * VEC + e] = ok ? (kRankMask - (u64)(r + e)) : 0ull;
+            }
+            int64_t Fp = 0;
+            for (int s0 = 0; s0 < S; s0 += CH) {
+                // the chunk's rows are loaded before any is reduced, so their
+                // latencies overlap
+                int64_t x[CH][K];
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    const int64_t* row = dt + (int64_t)(s0 + c < S ? s0 + c : s0) * R;
+#pragma unroll
+                    for (int l = 0; l < NLD; ++l) {
+                        if (VEC == 2) {
+                            const v2i64 v = *reinterpret_cast<const v2i64*>(row + idx[l]);
+                            x[c][2 * l] = v.x;
+                            x[c][2 * l + 1] = v.y;
+                        } else {
+                            x[c][l] = row[idx[l]];
+                        }
+                    }
+                }
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    const int s = s0 + c;
+                    if (s >= S) break;
+                    u64 m = 0;
+#pragma unroll
+                    for (int k = 0; k < K; ++k) {
+                        q[k] += (u64)x[c][k] << kRankBits;
+                        m = umax64(m, q[k]);
+                    }
+                    m = group_max<G>(m);
+                    const int64_t F = (int64_t)(m >> kRankBits);
+                    const bool wr = writer && act;
+                    if (wr) {
+                        const int r = (int)(kRankMask - (m & kRankMask));
+                        inc[t * S + s] = F - Fp;
+                        lead[t * S + s] = r;
+                        atomicAdd(&cnt_sh[s * R + r], 1);
+                    }
+                    // the window total: the wave's advances summed first,
+                    // one LDS atomic per wave (wraps as int64 sums do)
+                    const u64 sum = wave_sum64_dpp(wr ? (u64)(F - Fp) : 0ull);
+                    if ((tid & 63) == 63) atomicAdd(&ex_sh[s], sum);
+                    Fp = F;
+                }
+            }
+        }
+        __syncthreads();
+        for (int i = tid; i < S; i += kFusedWG) exposed[w * S + i] = (int64_t)ex_sh[i];
+        for (int i = tid; i < SR; i += kFusedWG) counts[w * (int64_t)SR + i] = cnt_sh[i];
+        if (tid < 64) {
+            // wave 0 alone picks the top-2 with DPP wave maxima (no block
+            // barriers): the stage of the largest total (a second max takes
+            // the lowest stage among the lanes holding it; S <= 64, one stage
+            // per lane), then its most frequent leader (R <= 256, four ranks
+            // per lane, the lowest rank on equal counts)
+            const int lane = tid;
+            int sk = -1;
+            for (int k = 0; k < 2; ++k) {
+                const bool has = lane < S && lane != sk;
+                const u64 ekey = has ? (ex_sh[lane] ^ 0x8000000000000000ull) : 0ull;
+                const u64 emax = lane_value(group_max<64>(ekey), 63);
+                const u64 skey = (has && ekey == emax) ? (u64)(64 - lane) : 0ull;
+                const u64 smax = lane_value(group_max<64>(skey), 63);
+                const int pick = smax ? (int)(64 - smax) : -1;  // -1 only when S == 1 and k == 1
+                u64 best = 0;
+                if (pick >= 0) {
+                    for (int r = lane; r < R; r += 64) {
+                        const u64 key = ((u64)(uint32_t)cnt_sh[pick * R + r] << 32) | (u64)(0xFFFFFFFFu - (uint32_t)r);
+                        best = umax64(best, key);
+                    }
+                }
+                const u64 m = lane_value(group_max<64>(best), 63);
+                if (lane == 0) {
+                    top2[w * 4 + 2 * k] = pick;
+                    top2[w * 4 + 2 * k + 1] = (pick >= 0 && (m >> 32)) ? (int)(0xFFFFFFFFu - (uint32_t)(m & 0xFFFFFFFFull)) : -1;
+                }
+                sk = pick;
+            }
+        }
+        __syncthreads();  // the LDS tables are cleared for the next window
+    }
+}
+
+template <int VEC>
+const void* pick_fused(int R)
+{
+    if (R <= 8) return reinterpret_cast<const void*>(&k_frontier_summary<VEC, 2, 4>);
+    if (R <= 16) return reinterpret_cast<const void*>(&k_frontier_summary<VEC, 2, 8>);
+    if (R <= 32) return reinterpret_cast<const void*>(&k_frontier_summary<VEC, 2, 16>);
+    if (R <= 64) return reinterpret_cast<const void*>(&k_frontier_summary<VEC, 2, 32>);
+    if (R <= 128) return reinterpret_cast<const void*>(&k_frontier_summary<VEC, 4, 32>);
+    return reinterpret_cast<const void*>(&k_frontier_summary<VEC, 8, 32>);  // R <= kFusedMaxR
 }
 
 // Exposed time led: the same segmented histogram as k_window_counts, with
@@ -523,4 +696,43 @@ SF_API int sf_window_leader_switches(const int32_t* leader, const int64_t* gap,
                  (void*)&Wl, (void*)&min_gap, (void*)&out_switches, (void*)&out_eligible};
     return launch(reinterpret_cast<const void*>(&k_window_switches), dim3(g), dim3(kSwWG), a, 0,
                   stream);
+}
+
+SF_API int sf_frontier_summary(const int64_t* durations, int64_t T, int32_t R, int32_t S,
+                               int64_t window, int64_t* out_increment, int32_t* out_leader,
+                               int64_t* out_stage_exposed, int32_t* out_lead_counts,
+                               int32_t* out_top2, sf_stream_t stream)
+{
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || window < 1) return SF_EINVAL;
+    if (!fits(T, S, R, 8)) return SF_EINVAL;
+    if (T == 0) return SF_OK;
+    const int64_t W = sf_num_windows(T, window);
+    if (!fits(W, S, R, 4)) return SF_EINVAL;
+    const void* bufs[6] = {durations, out_increment, out_leader, out_stage_exposed,
+                           out_lead_counts, out_top2};
+    const int64_t sizes[6] = {T * S * (int64_t)R * 8, T * S * 8, T * S * 4, W * S * 8,
+                              W * S * (int64_t)R * 4, W * 16};
+    const uintptr_t align[6] = {8, 8, 4, 8, 4, 4};
+    for (int a = 0; a < 6; ++a)
+        if (!bufs[a] || !aligned(bufs[a], align[a])) return SF_EINVAL;
+    for (int a = 0; a < 6; ++a)
+        for (int b = a + 1; b < 6; ++b)
+            if (!disjoint(bufs[a], sizes[a], bufs[b], sizes[b])) return SF_EINVAL;
+    const int64_t n_max = window < T ? window : T;
+    if (R <= kFusedMaxR && S <= kFusedMaxS && n_max <= kFusedMaxWindow &&
+        T * S * (int64_t)R <= kFusedMaxSamples) {
+        const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
+        const void* fn = vec2 ? pick_fused<2>(R) : pick_fused<1>(R);
+        int Ri = R, Si = S;
+        int64_t Wl = W;
+        void* args[] = {(void*)&durations,         (void*)&T,               (void*)&Ri,
+                        (void*)&Si,                (void*)&window,          (void*)&Wl,
+                        (void*)&out_increment,     (void*)&out_leader,      (void*)&out_stage_exposed,
+                        (void*)&out_lead_counts,   (void*)&out_top2};
+        return launch(fn, dim3((unsigned)(W < 65536 ? W : 65536)), dim3(kFusedWG), args, 0, stream);
+    }
+    const int rc = sf_frontier(durations, T, R, S, out_increment, out_leader, stream);
+    if (rc != SF_OK) return rc;
+    return sf_window_summary(out_increment, out_leader, T, R, S, window, out_stage_exposed,
+                             out_lead_counts, out_top2, stream);
 }

@@ -18,8 +18,6 @@ from . import build as _build
 SF_OK, SF_EINVAL, SF_ERANGE, SF_EHIP = 0, 1, 2, 3
 SF_MAX_R = 65536
 SF_MAX_S_EVIDENCE = 512
-SF_MAX_S_GAIN = 64
-SF_MAX_R_LAG = 16384
 SF_MAX_PREFIX_NS = 1 << 47
 SF_XOR_PIECE_BYTES = 262144
 
@@ -65,6 +63,8 @@ def _load() -> ctypes.CDLL:
     lib.sf_num_windows.restype = i64
     lib.sf_window_summary.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp, vp]
     lib.sf_window_summary.restype = ctypes.c_int
+    lib.sf_frontier_summary.argtypes = [vp, i64, i32, i32, i64, vp, vp, vp, vp, vp, vp]
+    lib.sf_frontier_summary.restype = ctypes.c_int
     lib.sf_window_lead_exposed.argtypes = [vp, vp, i64, i32, i32, i64, vp, vp, vp]
     lib.sf_window_lead_exposed.restype = ctypes.c_int
     lib.sf_window_leader_switches.argtypes = [vp, vp, vp, i64, i32, i64, i64, vp, vp, vp]
@@ -102,6 +102,8 @@ def _stream(stream, device):
 
 
 def _stream_handle(stream, device) -> int:
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
     return int(_stream(stream, device).cuda_stream)
 
 
@@ -118,19 +120,22 @@ def _new(shape, dtype, device, stream, zero: bool = False) -> torch.Tensor:
 
 def _check(t: torch.Tensor, name: str, dtype, shape, like: torch.Tensor | None = None):
     """Type, device, layout and shape of one argument; ``like``: the call's
-    first array, whose device every other array must share."""
-    if not isinstance(t, torch.Tensor):
-        raise TypeError("%s must be a torch.Tensor" % name)
-    if t.dtype != dtype:
-        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
-    if t.device.type != "cuda":
+    first array, whose device every other array must share.  (Kept to a
+    few cheap attribute reads: launch-bound callers pay for it per call.)"""
+    try:
+        same_dtype = t.dtype is dtype
+    except AttributeError:
+        raise TypeError("%s must be a torch.Tensor" % name) from None
+    if not same_dtype or not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a %s torch.Tensor, got %r" % (name, dtype, getattr(t, "dtype", t)))
+    if not t.is_cuda:
         raise ValueError("%s must be a GPU tensor" % name)
-    if like is not None and t.device != like.device:
+    if like is not None and t.get_device() != like.get_device():
         raise ValueError("%s is on %s, the call's other arrays on %s" % (name, t.device, like.device))
+    if t.shape != shape:
+        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
     if not t.is_contiguous():
         raise ValueError("%s must be contiguous" % name)
-    if tuple(t.shape) != tuple(shape):
-        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
 
 
 def sf_frontier(durations: torch.Tensor, out_increment: torch.Tensor | None = None,
@@ -254,6 +259,42 @@ def sf_window_summary(increment: torch.Tensor, leader: torch.Tensor, R: int, win
     if rc != SF_OK:
         raise StageFrontierError(rc, "sf_window_summary")
     return out_stage_exposed, out_lead_counts, out_top2
+
+
+def sf_frontier_summary(durations: torch.Tensor, window: int, out_increment: torch.Tensor | None = None,
+                        out_leader: torch.Tensor | None = None,
+                        out_stage_exposed: torch.Tensor | None = None,
+                        out_lead_counts: torch.Tensor | None = None,
+                        out_top2: torch.Tensor | None = None, stream=None):
+    """``sf_frontier`` and ``sf_window_summary`` in one call
+    (``sf_frontier_summary``; one kernel launch for small inputs).
+
+    Returns ``(out_increment [T, S], out_leader [T, S], out_stage_exposed
+    [W, S], out_lead_counts [W, S, R], out_top2 [W, 2, 2])``.
+    """
+    if durations.dim() != 3:
+        raise ValueError("durations must be [T, S, R]")
+    T, S, R = durations.shape
+    _check(durations, "durations", torch.int64, (T, S, R))
+    W = sf_num_windows(T, window)
+    if W < 0:
+        raise StageFrontierError(SF_EINVAL, "sf_frontier_summary")
+    dev = durations.device
+    outs = [(out_increment, (T, S), torch.int64), (out_leader, (T, S), torch.int32),
+            (out_stage_exposed, (W, S), torch.int64), (out_lead_counts, (W, S, R), torch.int32),
+            (out_top2, (W, 2, 2), torch.int32)]
+    names = ("out_increment", "out_leader", "out_stage_exposed", "out_lead_counts", "out_top2")
+    res = []
+    for (t, shp, dt), nm in zip(outs, names):
+        if t is None:
+            t = _new(shp, dt, dev, stream)
+        _check(t, nm, dt, shp, like=durations)
+        res.append(t)
+    rc = _lib.sf_frontier_summary(durations.data_ptr(), T, R, S, window,
+                                  *(t.data_ptr() for t in res), _stream_handle(stream, dev))
+    if rc != SF_OK:
+        raise StageFrontierError(rc, "sf_frontier_summary")
+    return tuple(res)
 
 
 def sf_window_lead_exposed(increment: torch.Tensor, leader: torch.Tensor, R: int, window: int,

@@ -28,7 +28,8 @@ def sf():
 def test_header_declares_the_boundary():
     assert declared_functions() == ["sf_exposure_gain", "sf_frontier", "sf_frontier_checked",
                                     "sf_frontier_evidence",
-                                    "sf_frontier_lag", "sf_ingest", "sf_num_windows",
+                                    "sf_frontier_lag", "sf_frontier_summary", "sf_ingest",
+                                    "sf_num_windows",
                                     "sf_rank_spread", "sf_read_xor", "sf_read_xor_pieces", "sf_route",
                                     "sf_strerror", "sf_version",
                                     "sf_window_lead_exposed", "sf_window_leader_switches",
@@ -65,9 +66,8 @@ def test_constants_match_header(sf):
         text = fh.read()
     assert "#define SF_MAX_R %d" % sf.SF_MAX_R in text
     assert "#define SF_MAX_S_EVIDENCE %d" % sf.SF_MAX_S_EVIDENCE in text
-    assert "#define SF_MAX_S_GAIN %d" % sf.SF_MAX_S_GAIN in text
-    assert "#define SF_MAX_R_LAG %d" % sf.SF_MAX_R_LAG in text
-    assert "SF_MAX_WINDOW_MEDIAN" not in text and "#define SF_MAX_S " not in text
+    for gone in ("SF_MAX_WINDOW_MEDIAN", "#define SF_MAX_S ", "SF_MAX_S_GAIN", "SF_MAX_R_LAG"):
+        assert gone not in text, gone
     assert "#define SF_XOR_PIECE_BYTES %d" % sf.SF_XOR_PIECE_BYTES in text
     for name in ("SF_OK", "SF_EINVAL", "SF_ERANGE", "SF_EHIP"):
         assert re.search(r"%s = %d" % (name, getattr(sf, name)), text), name
@@ -199,7 +199,6 @@ def test_gain_argument_checks(sf):
                                     *(a[n] for n in names[2:]), None)
 
     assert call(T=0) == sf.SF_OK
-    assert call(S=sf.SF_MAX_S_GAIN + 1) == sf.SF_EINVAL
     assert call(window=0) == sf.SF_EINVAL
     for n in names:
         assert call(**{n: None}) == sf.SF_EINVAL, n
@@ -216,7 +215,7 @@ def test_lag_argument_checks(sf):
         return lib.sf_frontier_lag(a["d"], a["T"], a["R"], a["S"], a["lag"], a["inc"], None)
 
     assert call(T=0, d=None, lag=None, inc=None) == sf.SF_OK
-    assert call(R=sf.SF_MAX_R_LAG + 1) == sf.SF_EINVAL
+    assert call(R=sf.SF_MAX_R + 1) == sf.SF_EINVAL
     assert call(S=0) == sf.SF_EINVAL
     assert call(inc=None) == sf.SF_EINVAL
     assert call(lag=B + 4) == sf.SF_EINVAL
@@ -234,7 +233,7 @@ def test_spread_argument_checks(sf):
                                   None)
 
     assert call(T=0, d=None, sp=None, wsp=None) == sf.SF_OK
-    assert call(R=sf.SF_MAX_R_LAG + 1) == sf.SF_EINVAL
+    assert call(R=sf.SF_MAX_R + 1) == sf.SF_EINVAL
     assert call(S=0) == sf.SF_EINVAL
     assert call(window=0) == sf.SF_EINVAL
     assert call(wsp=None) == sf.SF_EINVAL
@@ -386,3 +385,28 @@ def test_ctypes_argtypes_cover_header(sf):
     assert len(lib.sf_window_leader_switches.argtypes) == 10
     assert len(lib.sf_read_xor.argtypes) == 4
     assert lib.sf_num_windows.restype is ctypes.c_int64
+
+
+def test_frontier_summary_argument_checks(sf):
+    lib = sf.raw_library()
+    names = ["d", "inc", "lead", "ex", "cnt", "top"]
+    base = {n: (i + 1) << 40 for i, n in enumerate(names)}
+
+    def call(**kw):
+        a = dict(dict(base, T=100, R=8, S=6, window=10), **kw)
+        return lib.sf_frontier_summary(a["d"], a["T"], a["R"], a["S"], a["window"],
+                                       *(a[n] for n in names[1:]), None)
+
+    assert call(T=0, **{n: None for n in names}) == sf.SF_OK
+    assert call(T=-1) == sf.SF_EINVAL
+    assert call(R=0) == sf.SF_EINVAL
+    assert call(R=sf.SF_MAX_R + 1) == sf.SF_EINVAL
+    assert call(S=0) == sf.SF_EINVAL
+    assert call(window=0) == sf.SF_EINVAL
+    for n in names:
+        assert call(**{n: None}) == sf.SF_EINVAL, n
+    assert call(inc=base["inc"] + 4) == sf.SF_EINVAL      # misaligned int64
+    assert call(lead=base["lead"] + 2) == sf.SF_EINVAL    # misaligned int32
+    assert call(ex=base["d"] + 8) == sf.SF_EINVAL         # output overlaps input
+    assert call(cnt=base["inc"] + 8) == sf.SF_EINVAL      # outputs overlap
+    assert call(T=1 << 50, R=sf.SF_MAX_R, S=512) == sf.SF_EINVAL  # size overflow

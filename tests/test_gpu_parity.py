@@ -284,6 +284,53 @@ def assert_lead_exposed_equal(sf, inc, lead, R, window):
     np.testing.assert_array_equal(top2.cpu().numpy(), ot)
 
 
+
+@pytest.mark.parametrize("R", [1, 2, 7, 8, 9, 16, 17, 33, 64, 65, 128, 129, 200, 256, 257])
+def test_frontier_summary_fused(sf, R):
+    """sf_frontier_summary against the oracle's frontier and window summary,
+    on both sides of every limit of its one-launch path (ranks, stages,
+    window length, total samples) and on ragged windows."""
+    cases = [(37, 5, 10, 3), (250, 6, 100, 10**6), (33, 64, 7, 2), (20, 65, 6, 5)]
+    if R <= 32:
+        cases += [(1030, 2, 1030, 10**4), (2100, 2, 1025, 4)]
+    cases.append(((1 << 20) // (4 * R) + 3, 4, 64, 10**5))  # just past 2^20 samples
+    for T, S, window, hi in cases:
+        d = synth.random_durations(T, S, R, seed=R * 7 + S + window, hi=hi)
+        print("case R=%d S=%d T=%d window=%d" % (R, S, T, window), flush=True)
+        out = sf.sf_frontier_summary(torch.from_numpy(d).to(DEV), window)
+        torch.cuda.synchronize()
+        oi, ol = oracle.frontier(d)
+        oe, oc, ot = oracle.window_summary(oi, ol, R, window)
+        for got, want in zip(out, (oi, ol, oe, oc, ot)):
+            np.testing.assert_array_equal(got.cpu().numpy(), want)
+
+
+def test_frontier_summary_small_workload_and_stall(sf):
+    """The 8-rank workload and the hand-built data stall through the fused
+    call, against the oracle and the separate calls."""
+    wl = synth.WORKLOADS["r8_s6_t1k"]
+    d = synth.generate(wl)
+    dd = torch.from_numpy(d).to(DEV)
+    out = sf.sf_frontier_summary(dd, wl.window)
+    inc, lead = sf.sf_frontier(dd)
+    sep = (inc, lead) + sf.sf_window_summary(inc, lead, wl.R, wl.window)
+    torch.cuda.synchronize()
+    oi, ol = oracle.frontier(d)
+    want = (oi, ol) + oracle.window_summary(oi, ol, wl.R, wl.window)
+    for got, s_, w in zip(out, sep, want):
+        np.testing.assert_array_equal(got.cpu().numpy(), w)
+        np.testing.assert_array_equal(s_.cpu().numpy(), w)
+    ms = 1_000_000
+    st = np.ascontiguousarray(np.array([[20, 60, 120, 2, 15, 3]] * 4, dtype=np.int64).T[None] * ms)
+    st[0, 0, 2] += 30 * ms
+    st[0, 2, [0, 1, 3]] += 30 * ms
+    out = sf.sf_frontier_summary(torch.from_numpy(st).to(DEV), 1)
+    torch.cuda.synchronize()
+    assert out[0].cpu().numpy().tolist() == [[50 * ms, 60 * ms, 120 * ms, 2 * ms, 15 * ms, 3 * ms]]
+    assert out[1].cpu().numpy().tolist() == [[2, 2, 0, 0, 0, 0]]
+    assert int(out[3].cpu()[0, 0, 2]) == 1
+
+
 @pytest.mark.parametrize("R,S,T,window", [
     (8, 6, 1000, 100), (8, 6, 1001, 100), (3, 1, 17, 4), (128, 6, 3000, 1000),
     (1024, 8, 1200, 500), (5, 13, 40, 1), (4096, 12, 600, 250), (8192, 4, 90, 30),
@@ -593,7 +640,8 @@ def test_gain_rank_sweep(sf, R):
         assert_gain_equal(sf, d, bt, window)
 
 
-@pytest.mark.parametrize("S", [1, 2, 4, 5, 6, 7, 8, 9, 12, 13, 16, 17, 24, 25, 32, 33, 64])
+@pytest.mark.parametrize("S", [1, 2, 4, 5, 6, 7, 8, 9, 12, 13, 16, 17, 24, 25, 32, 33, 64, 65, 128,
+                               200])
 def test_gain_stage_sweep(sf, S):
     rng = np.random.Generator(np.random.PCG64(S + 100))
     for R in (8, 200, 1030):
@@ -602,6 +650,19 @@ def test_gain_stage_sweep(sf, S):
         bt = rng.integers(0, 4, size=(-(-T // 3), S, R), dtype=np.int64)
         print("case R=%d S=%d T=%d" % (R, S, T), flush=True)
         assert_gain_equal(sf, d, bt, 3)
+
+
+def test_gain_many_stages_wide_values(sf):
+    """Past 64 stages (the two-pass kernel): several rank tiles with a
+    ragged last one, odd ranks (8-byte loads), wide values, a window
+    boundary inside a workgroup's steps."""
+    rng = np.random.Generator(np.random.PCG64(128))
+    for T, S, R, window, hi in ((9, 128, 16384, 4, 10**9), (13, 100, 301, 5, 1 << 40),
+                                (6, 65, 129, 2, 3)):
+        d = rng.integers(0, hi, size=(T, S, R), dtype=np.int64)
+        bt = rng.integers(0, hi, size=(-(-T // window), S, R), dtype=np.int64)
+        print("case T=%d S=%d R=%d window=%d" % (T, S, R, window), flush=True)
+        assert_gain_equal(sf, d, bt, window)
 
 
 def test_gain_golden_cases(sf):
@@ -679,6 +740,35 @@ def test_narrow_pass_hand_over(sf, R):
     print("case R=%d all handed over" % R, flush=True)
     assert_lag_equal(sf, wide)
     assert_spread_equal(sf, wide, 2)
+
+
+
+@pytest.mark.parametrize("R", [16385, 16386, 20000, 32767, 32768, 40000, 65536])
+def test_lag_spread_past_16384_ranks(sf, R):
+    """More ranks than a step holds in 64-bit registers: up to 32768 the
+    32-bit pass with 32 values per lane (partial last tile for R below it)
+    and the streaming 64-bit kernel for the steps it hands over; odd R and
+    more than 32768 ranks the streaming kernel alone.  Tie-heavy and wide
+    values, and steps forced past 32 bits (a duration of 2^32 + 5, a prefix
+    spread past 2^32 at a later stage) next to steps that stay narrow."""
+    rng = np.random.Generator(np.random.PCG64(R))
+    T, S = 5, 4
+    for hi in (3, 10**8):
+        d = rng.integers(0, hi, size=(T, S, R), dtype=np.int64)
+        if hi > 3:
+            d[1, 2, R // 3] = (1 << 32) + 5
+            d[3, :, R - 1] = [1 << 30, 1 << 31, 1 << 31, 5]
+        print("case R=%d hi=%d" % (R, hi), flush=True)
+        dd = torch.from_numpy(d).to(DEV)
+        lag, inc = sf.sf_frontier_lag(dd)
+        sp, wsp = sf.sf_rank_spread(dd, 2)
+        torch.cuda.synchronize()
+        ol, oi = oracle.frontier_lag(d)
+        np.testing.assert_array_equal(lag.cpu().numpy(), ol)
+        np.testing.assert_array_equal(inc.cpu().numpy(), oi)
+        osp, owsp = oracle.rank_spread(d, 2)
+        np.testing.assert_array_equal(sp.cpu().numpy(), osp)
+        np.testing.assert_array_equal(wsp.cpu().numpy(), owsp)
 
 
 @pytest.mark.parametrize("R", [4096, 16384])
