@@ -218,9 +218,11 @@ __global__ __launch_bounds__(kFusedWG) void k_frontier_summary(
         for (int i = tid; i < SR; i += kFusedWG) cnt_sh[i] = 0;
         __syncthreads();
         for (int64_t tb = t0; tb < t1; tb += SPW) {
-            // every lane runs the stage loop (the wave sums below need all
-            // lanes); a group past the window re-reads the window's first
-            // step and contributes nothing
+            // a wave whose first step is past the window has nothing to do;
+            // in the others every lane runs the stage loop (the wave sums
+            // below need all lanes), and a group past the window loads
+            // nothing and contributes nothing
+            if (tb + (tid & ~63) / G >= t1) continue;
             const bool act = tb + j < t1;
             const int64_t t = act ? tb + j : t0;
             const int64_t* dt = d + t * (int64_t)S * R;
@@ -243,10 +245,13 @@ __global__ __launch_bounds__(kFusedWG) void k_frontier_summary(
                 int64_t x[CH][K];
 #pragma unroll
                 for (int c = 0; c < CH; ++c) {
-                    const int64_t* row = dt + (int64_t)(s0 + c < S ? s0 + c : s0) * R;
+                    const int64_t* row = dt + (int64_t)(s0 + c) * R;
 #pragma unroll
                     for (int l = 0; l < NLD; ++l) {
-                        if (VEC == 2) {
+                        if (!act || s0 + c >= S) {
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) x[c][l * VEC + e] = 0;
+                        } else if (VEC == 2) {
                             const v2i64 v = *reinterpret_cast<const v2i64*>(row + idx[l]);
                             x[c][2 * l] = v.x;
                             x[c][2 * l + 1] = v.y;

@@ -9,6 +9,7 @@ missing, importing this module raises.
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 
 import torch  # loaded first so that the library binds to torch's HIP runtime
@@ -91,6 +92,12 @@ def sf_num_windows(T: int, window: int) -> int:
     return int(_lib.sf_num_windows(T, window))
 
 
+@functools.lru_cache(maxsize=64)
+def _num_windows(T: int, window: int) -> int:
+    """sf_num_windows, remembered for the (T, window) pairs a caller repeats."""
+    return int(_lib.sf_num_windows(T, window))
+
+
 def _stream(stream, device):
     """The torch stream a call runs on: ``stream`` (a torch stream or a raw
     hipStream_t handle), else the current stream of ``device``."""
@@ -120,22 +127,24 @@ def _new(shape, dtype, device, stream, zero: bool = False) -> torch.Tensor:
 
 def _check(t: torch.Tensor, name: str, dtype, shape, like: torch.Tensor | None = None):
     """Type, device, layout and shape of one argument; ``like``: the call's
-    first array, whose device every other array must share.  (Kept to a
-    few cheap attribute reads: launch-bound callers pay for it per call.)"""
+    first array, whose device every other array must share.  (One chained
+    test of cheap attribute reads on the good path: launch-bound callers pay
+    for it per call; the reason is worked out only on failure.)"""
     try:
-        same_dtype = t.dtype is dtype
+        if (t.dtype is dtype and t.is_cuda and t.shape == shape and t.is_contiguous()
+                and (like is None or t.get_device() == like.get_device())):
+            return
     except AttributeError:
         raise TypeError("%s must be a torch.Tensor" % name) from None
-    if not same_dtype or not isinstance(t, torch.Tensor):
-        raise TypeError("%s must be a %s torch.Tensor, got %r" % (name, dtype, getattr(t, "dtype", t)))
+    if t.dtype is not dtype or not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a %s torch.Tensor, got %r" % (name, dtype, t.dtype))
     if not t.is_cuda:
         raise ValueError("%s must be a GPU tensor" % name)
-    if like is not None and t.get_device() != like.get_device():
-        raise ValueError("%s is on %s, the call's other arrays on %s" % (name, t.device, like.device))
     if t.shape != shape:
         raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
     if not t.is_contiguous():
         raise ValueError("%s must be contiguous" % name)
+    raise ValueError("%s is on %s, the call's other arrays on %s" % (name, t.device, like.device))
 
 
 def sf_frontier(durations: torch.Tensor, out_increment: torch.Tensor | None = None,
@@ -270,31 +279,39 @@ def sf_frontier_summary(durations: torch.Tensor, window: int, out_increment: tor
     (``sf_frontier_summary``; one kernel launch for small inputs).
 
     Returns ``(out_increment [T, S], out_leader [T, S], out_stage_exposed
-    [W, S], out_lead_counts [W, S, R], out_top2 [W, 2, 2])``.
+    [W, S], out_lead_counts [W, S, R], out_top2 [W, 2, 2])``.  Written out
+    argument by argument: callers of this entry point are bound by its
+    per-call cost.
     """
     if durations.dim() != 3:
         raise ValueError("durations must be [T, S, R]")
     T, S, R = durations.shape
     _check(durations, "durations", torch.int64, (T, S, R))
-    W = sf_num_windows(T, window)
+    W = _num_windows(T, window)
     if W < 0:
         raise StageFrontierError(SF_EINVAL, "sf_frontier_summary")
-    dev = durations.device
-    outs = [(out_increment, (T, S), torch.int64), (out_leader, (T, S), torch.int32),
-            (out_stage_exposed, (W, S), torch.int64), (out_lead_counts, (W, S, R), torch.int32),
-            (out_top2, (W, 2, 2), torch.int32)]
-    names = ("out_increment", "out_leader", "out_stage_exposed", "out_lead_counts", "out_top2")
-    res = []
-    for (t, shp, dt), nm in zip(outs, names):
-        if t is None:
-            t = _new(shp, dt, dev, stream)
-        _check(t, nm, dt, shp, like=durations)
-        res.append(t)
-    rc = _lib.sf_frontier_summary(durations.data_ptr(), T, R, S, window,
-                                  *(t.data_ptr() for t in res), _stream_handle(stream, dev))
+    if out_increment is None:
+        out_increment = _new((T, S), torch.int64, durations.device, stream)
+    if out_leader is None:
+        out_leader = _new((T, S), torch.int32, durations.device, stream)
+    if out_stage_exposed is None:
+        out_stage_exposed = _new((W, S), torch.int64, durations.device, stream)
+    if out_lead_counts is None:
+        out_lead_counts = _new((W, S, R), torch.int32, durations.device, stream)
+    if out_top2 is None:
+        out_top2 = _new((W, 2, 2), torch.int32, durations.device, stream)
+    _check(out_increment, "out_increment", torch.int64, (T, S), durations)
+    _check(out_leader, "out_leader", torch.int32, (T, S), durations)
+    _check(out_stage_exposed, "out_stage_exposed", torch.int64, (W, S), durations)
+    _check(out_lead_counts, "out_lead_counts", torch.int32, (W, S, R), durations)
+    _check(out_top2, "out_top2", torch.int32, (W, 2, 2), durations)
+    rc = _lib.sf_frontier_summary(durations.data_ptr(), T, R, S, window, out_increment.data_ptr(),
+                                  out_leader.data_ptr(), out_stage_exposed.data_ptr(),
+                                  out_lead_counts.data_ptr(), out_top2.data_ptr(),
+                                  _stream_handle(stream, durations.device))
     if rc != SF_OK:
         raise StageFrontierError(rc, "sf_frontier_summary")
-    return tuple(res)
+    return out_increment, out_leader, out_stage_exposed, out_lead_counts, out_top2
 
 
 def sf_window_lead_exposed(increment: torch.Tensor, leader: torch.Tensor, R: int, window: int,
