@@ -58,9 +58,9 @@ enum {
 /* Stage counts are otherwise unbounded (up to the size overflow checks):
  * Sec. 3 expands every accumulation micro-step into its own stages before
  * the frontier is taken, so S grows with the accumulation count.  Largest
- * stage count of sf_frontier_evidence, and of K + 1 in sf_ingest (their
- * per-stage partial results are staged in on-chip memory). */
-#define SF_MAX_S_EVIDENCE 512
+ * K + 1 of sf_ingest (a rank's explicit stages of a step are staged in
+ * on-chip memory). */
+#define SF_MAX_S_INGEST 512
 /* Every rank-local prefix P[t][r][s] must be below this many ns (about
  * 39 hours) so that the packed key fits in 64 bits. */
 #define SF_MAX_PREFIX_NS ((int64_t)1 << 47)
@@ -138,7 +138,9 @@ int sf_frontier_checked(const int64_t* durations, int64_t T, int32_t R, int32_t 
  *   stream         HIP stream.
  *
  * Preconditions, alignment (element size), chunking and overlap rules as
- * for sf_frontier; additionally T <= INT32_MAX and S <= SF_MAX_S_EVIDENCE.
+ * for sf_frontier; additionally T <= INT32_MAX.  Any S: past 819 stages the
+ * per-stage partial results of a step are kept in its own output rows
+ * instead of on chip (slower, same results).
  * Returns SF_OK, SF_EINVAL or SF_EHIP.
  */
 int sf_frontier_evidence(const int64_t* durations, int64_t T, int32_t R, int32_t S,
@@ -159,7 +161,7 @@ int sf_frontier_evidence(const int64_t* durations, int64_t T, int32_t R, int32_t
  *                  (steps, then explicit stages).  May be NULL when K == 0.
  *   wall           [R][T] int64 ns.
  *   T, R, K        0 <= T, 1 <= R <= SF_MAX_R, 0 <= K,
- *                  K + 1 <= SF_MAX_S_EVIDENCE.
+ *                  K + 1 <= SF_MAX_S_INGEST.
  *                  T == 0 is a no-op.
  *   out_durations  [T][K+1][R] int64: stage k < K is x, stage K the residual.
  *   out_overlap    [T][R] int64.

@@ -76,13 +76,20 @@ __device__ __forceinline__ void ev_store(int64_t i, const EvAcc& a, u64 kprev, i
 // R ranks of its step, the group's last lane writes each boundary's outputs
 // as soon as the stage is reduced; otherwise partial results go through LDS
 // (5 arrays of [WG / min(G, 64)][S]) and the workgroup writes them at the end.
-template <int VEC, int K, int G, int WG>
+// GTAB (stage counts past what LDS holds; G <= 64): the group's last lane
+// keeps the partial results of its step in the step's own output rows (the
+// largest key in out_increment, the runner-up key in out_gap, the tie count,
+// max and sum in their final rows), and after the last tile the workgroup
+// decodes the increment, leader and gap in place, chunk by chunk from the
+// end, each chunk read before any of it is written.
+template <int VEC, int K, int G, int WG, bool GTAB>
 __global__ __launch_bounds__(WG) void k_frontier_evidence(
     const int64_t* __restrict__ d, int64_t T, int R, int S, int64_t* __restrict__ inc,
     int32_t* __restrict__ lead, int64_t* __restrict__ gap, int32_t* __restrict__ ties,
     int64_t* __restrict__ stage_max, int64_t* __restrict__ stage_sum)
 {
     static_assert(K % VEC == 0 && (WG % G == 0 || G == WG), "shape");
+    static_assert(!GTAB || G <= 64, "GTAB: one writer lane per step");
     constexpr int SUB = G < 64 ? G : 64;
     constexpr int SPW = WG / G;
     constexpr int SPS = G / SUB;
@@ -162,6 +169,24 @@ __global__ __launch_bounds__(WG) void k_frontier_evidence(
                     if (direct) {
                         ev_store(t * S + s, a, kprev, R, inc, lead, gap, ties, stage_max, stage_sum);
                         kprev = a.k1;
+                    } else if (GTAB) {
+                        // the step's own output rows, read back by this lane
+                        // only until the decode below
+                        const int64_t i = t * S + s;
+                        if (r0 > 0) {
+                            EvAcc b;
+                            b.k1 = (u64)inc[i];
+                            b.k2 = (u64)gap[i];
+                            b.c = (uint32_t)ties[i];
+                            b.smax = stage_max[i];
+                            b.ssum = stage_sum[i];
+                            ev_merge(a, b);
+                        }
+                        inc[i] = (int64_t)a.k1;
+                        gap[i] = (int64_t)a.k2;
+                        ties[i] = (int32_t)a.c;
+                        stage_max[i] = a.smax;
+                        stage_sum[i] = a.ssum;
                     } else {
                         const int i = slot * S + s;
                         if (r0 > 0) {
@@ -185,6 +210,34 @@ __global__ __launch_bounds__(WG) void k_frontier_evidence(
     }
     if (direct) return;
     __syncthreads();
+
+    if constexpr (GTAB) {
+        // the workgroup's steps are contiguous rows; a chunk of WG entries
+        // reads its keys and the key before each (in the same chunk or the
+        // one below, not yet decoded), waits for every thread's reads, then
+        // writes.  The tie count, max and sum are final already.
+        const int64_t steps = T - tb < SPW ? T - tb : SPW;
+        const int64_t n = steps * S;
+        const int64_t base = tb * S;
+        for (int64_t c = (n - 1) / WG; c >= 0; --c) {
+            const int64_t i = c * WG + tid;
+            const bool ok = i < n;
+            u64 key = 0, kprev = 0, key2 = 0;
+            if (ok) {
+                key = (u64)inc[base + i];
+                key2 = (u64)gap[base + i];
+                if (i % S != 0) kprev = (u64)inc[base + i - 1];
+            }
+            __syncthreads();
+            if (ok) {
+                const int64_t F = (int64_t)(key >> kRankBits);
+                inc[base + i] = F - (int64_t)(kprev >> kRankBits);
+                lead[base + i] = (int32_t)(kRankMask - (key & kRankMask));
+                gap[base + i] = R > 1 ? F - (int64_t)(key2 >> kRankBits) : -1;
+            }
+        }
+        return;
+    }
 
     for (int i = tid; i < SPW * S; i += WG) {
         const int jj = i / S;
@@ -220,19 +273,20 @@ struct EvidenceVariant {
     int per_cu;  // resident workgroups per CU to allow (0: no cap)
 };
 
-template <int VEC, int K, int G, int WG>
+template <int VEC, int K, int G, int WG, bool GTAB = false>
 EvidenceVariant ev_variant(int per_cu)
 {
-    return EvidenceVariant{reinterpret_cast<const void*>(&k_frontier_evidence<VEC, K, G, WG>), K,
-                           G, WG, per_cu};
+    return EvidenceVariant{reinterpret_cast<const void*>(&k_frontier_evidence<VEC, K, G, WG, GTAB>),
+                           K, G, WG, per_cu};
 }
 
 // LDS bytes a variant needs: none when one group of <= 64 lanes covers the
-// step's ranks, else 5 arrays of [WG / min(G, 64)][S] u64.
-size_t ev_lds_need(const EvidenceVariant& v, int R, int S)
+// step's ranks or the partial results live in the output rows, else 5
+// arrays of [WG / min(G, 64)][S] u64.
+size_t ev_lds_need(const EvidenceVariant& v, int R, int S, bool gtab)
 {
     const int sub = v.G < 64 ? v.G : 64;
-    if (v.G <= 64 && R <= v.G * v.K) return 0;
+    if (gtab || (v.G <= 64 && R <= v.G * v.K)) return 0;
     return (size_t)5 * (v.WG / sub) * S * 8;
 }
 
@@ -253,8 +307,22 @@ EvidenceVariant pick_evidence(int R, int S)
     else if (R <= 1024) v = ev_variant<VEC, 16, 32, 64>(8);
     else if (R <= 4096) v = ev_variant<VEC, 16, 256, 256>(2);
     else v = ev_variant<VEC, 32, 256, 256>(0);
-    if (ev_lds_need(v, R, S) > kLdsMaxPerWg) v = ev_variant<VEC, 16, 128, 128>(0);
+    if (ev_lds_need(v, R, S, false) > kLdsMaxPerWg) v = ev_variant<VEC, 16, 128, 128>(0);
     return v;
+}
+
+// Stage counts whose LDS table would not fit even the two-slot fallback
+// (more than 819 stages): one group of at most 64 lanes per step, the
+// partial results in the output rows.
+template <int VEC>
+EvidenceVariant pick_evidence_gtab(int R)
+{
+    if (R <= 8) return ev_variant<VEC, 2, 4, 64, true>(0);
+    if (R <= 16) return ev_variant<VEC, 2, 8, 64, true>(0);
+    if (R <= 32) return ev_variant<VEC, 4, 8, 64, true>(0);
+    if (R <= 64) return ev_variant<VEC, 4, 16, 64, true>(0);
+    if (R <= 512) return ev_variant<VEC, 16, 32, 64, true>(0);
+    return ev_variant<VEC, 16, 64, 64, true>(0);
 }
 
 }  // namespace sfk
@@ -266,7 +334,7 @@ SF_API int sf_frontier_evidence(const int64_t* durations, int64_t T, int32_t R, 
                                 int32_t* out_ties, int64_t* out_stage_max,
                                 int64_t* out_stage_sum, sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1 || S > SF_MAX_S_EVIDENCE) return SF_EINVAL;
+    if (T < 0 || R < 1 || R > SF_MAX_R || S < 1) return SF_EINVAL;
     if (!fits(T, S, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     if (T > INT32_MAX) return SF_EINVAL;
@@ -282,9 +350,11 @@ SF_API int sf_frontier_evidence(const int64_t* durations, int64_t T, int32_t R, 
             if (!disjoint(bufs[a], sizes[a], bufs[b], sizes[b])) return SF_EINVAL;
 
     const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
-    const EvidenceVariant v = vec2 ? pick_evidence<2>(R, S) : pick_evidence<1>(R, S);
+    EvidenceVariant v = vec2 ? pick_evidence<2>(R, S) : pick_evidence<1>(R, S);
+    const bool gtab = ev_lds_need(v, R, S, false) > kLdsMaxPerWg;
+    if (gtab) v = vec2 ? pick_evidence_gtab<2>(R) : pick_evidence_gtab<1>(R);
     const int spw = v.WG / v.G;
-    const size_t lds = lds_request(ev_lds_need(v, R, S), v.per_cu);
+    const size_t lds = lds_request(ev_lds_need(v, R, S, gtab), v.per_cu);
     const int64_t blocks = (T + spw - 1) / spw;
     int Ri = R, Si = S;
     void* args[] = {(void*)&durations, (void*)&T, (void*)&Ri, (void*)&Si,

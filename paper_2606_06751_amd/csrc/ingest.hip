@@ -165,7 +165,7 @@ SF_API int sf_ingest(const int64_t* stages, const int64_t* wall, int64_t T, int3
                      int32_t K, int64_t* out_durations, int64_t* out_overlap,
                      sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R || K < 0 || K + 1 > SF_MAX_S_EVIDENCE) return SF_EINVAL;
+    if (T < 0 || R < 1 || R > SF_MAX_R || K < 0 || K + 1 > SF_MAX_S_INGEST) return SF_EINVAL;
     if (!fits(T, K + 2, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     const int64_t S = K + 1;

@@ -514,6 +514,22 @@ def test_evidence_stage_sweep(sf, S):
         assert_evidence_equal(sf, d)
 
 
+@pytest.mark.parametrize("S", [513, 819, 820, 1500, 4096])
+@pytest.mark.parametrize("R", [8, 301, 1000, 1025, 16384])
+def test_evidence_large_stage_counts(sf, S, R):
+    """Stage counts past what LDS holds (the accumulation expansion of
+    Sec. 3): from 820 stages the partial results of a step go through its
+    own output rows.  Odd rank counts (8-byte loads), rank tiles with a
+    ragged last one, step counts ragged against the steps a workgroup holds,
+    tie-heavy and wide values."""
+    T = max(2, min(37, (1 << 25) // (R * S)))
+    T += 1 - T % 2  # odd
+    for hi in (2, (1 << 47) // S - 1):  # every prefix stays below 2^47
+        d = synth.random_durations(T, S, R, seed=S * 11 + R + (hi & 0xFF), hi=hi)
+        print("case R=%d S=%d T=%d hi=%d" % (R, S, T, hi), flush=True)
+        assert_evidence_equal(sf, d)
+
+
 def test_evidence_max_ranks_and_odd_base(sf):
     d = synth.random_durations(2, 3, sf.SF_MAX_R, seed=19, hi=1)
     assert_evidence_equal(sf, d)
