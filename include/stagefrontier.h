@@ -55,12 +55,9 @@ enum {
 /* Largest rank count: the leader is carried in 16 bits of a packed
  * (prefix, rank) key. */
 #define SF_MAX_R 65536
-/* Stage counts are otherwise unbounded (up to the size overflow checks):
- * Sec. 3 expands every accumulation micro-step into its own stages before
- * the frontier is taken, so S grows with the accumulation count.  Largest
- * K + 1 of sf_ingest (a rank's explicit stages of a step are staged in
- * on-chip memory). */
-#define SF_MAX_S_INGEST 512
+/* Stage counts are unbounded (up to the size overflow checks): Sec. 3
+ * expands every accumulation micro-step into its own stages before the
+ * frontier is taken, so S grows with the accumulation count. */
 /* Every rank-local prefix P[t][r][s] must be below this many ns (about
  * 39 hours) so that the packed key fits in 64 bits. */
 #define SF_MAX_PREFIX_NS ((int64_t)1 << 47)
@@ -160,8 +157,10 @@ int sf_frontier_evidence(const int64_t* durations, int64_t T, int32_t R, int32_t
  *   stages         [R][T][K] int64 ns, each rank's buffer as gathered
  *                  (steps, then explicit stages).  May be NULL when K == 0.
  *   wall           [R][T] int64 ns.
- *   T, R, K        0 <= T, 1 <= R <= SF_MAX_R, 0 <= K,
- *                  K + 1 <= SF_MAX_S_INGEST.
+ *   T, R, K        0 <= T, 1 <= R <= SF_MAX_R, 0 <= K <= INT32_MAX - 2.
+ *                  Up to 511 explicit stages a rank's segment of a step is
+ *                  staged in LDS; beyond, each thread walks its (step, rank)
+ *                  segment in global memory (slower, same results).
  *                  T == 0 is a no-op.
  *   out_durations  [T][K+1][R] int64: stage k < K is x, stage K the residual.
  *   out_overlap    [T][R] int64.

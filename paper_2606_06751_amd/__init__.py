@@ -11,7 +11,6 @@ _BINDING_NAMES = ("sf_frontier", "sf_frontier_checked", "sf_frontier_evidence", 
                   "sf_window_median", "sf_window_summary", "sf_frontier_summary", "sf_window_lead_exposed", "sf_window_leader_switches", "sf_ingest", "sf_route",
                   "sf_exposure_gain", "sf_read_xor", "sf_read_xor_pieces", "sf_num_windows", "sf_strerror", "sf_version",
                   "StageFrontierError", "SF_OK", "SF_EINVAL", "SF_ERANGE", "SF_EHIP", "SF_MAX_R",
-                  "SF_MAX_S_INGEST",
                   "SF_MAX_PREFIX_NS", "SF_XOR_PIECE_BYTES")
 
 

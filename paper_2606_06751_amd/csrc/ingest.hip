@@ -129,6 +129,41 @@ __global__ __launch_bounds__(kIngestWG) void k_ingest(const int64_t* __restrict_
     }
 }
 
+// More explicit stages than a rank's segment of one step fits in LDS
+// (K + 1 > kIngestTiledS): one thread per (step, rank), walking the rank's
+// K contiguous values of the step, writing each to its [t][s] row (the
+// threads of a wave cover 64 adjacent ranks, so every store is coalesced)
+// and summing them for the closure.  Each lane's reads run along its own
+// row, so the cache lines of a row are fetched once and used for the next
+// values.
+constexpr int kIngestTiledS = 512;
+
+__global__ __launch_bounds__(kIngestWG) void k_ingest_wide(const int64_t* __restrict__ x,
+                                                           const int64_t* __restrict__ w,
+                                                           int64_t T, int R, int K,
+                                                           int64_t* __restrict__ d,
+                                                           int64_t* __restrict__ o)
+{
+    const int64_t nrc = (R + kIngestWG - 1) / kIngestWG;
+    const int64_t S = (int64_t)K + 1;
+    for (int64_t blk = blockIdx.x; blk < nrc * T; blk += gridDim.x) {
+        const int64_t t = blk / nrc;
+        const int r = (int)(blk - t * nrc) * kIngestWG + (int)threadIdx.x;
+        if (r >= R) continue;
+        const int64_t* src = x + ((int64_t)r * T + t) * K;
+        int64_t* dst = d + t * S * R + r;
+        int64_t sum = 0;
+        for (int k = 0; k < K; ++k) {
+            const int64_t v = src[k];
+            __builtin_nontemporal_store(v, dst + (int64_t)k * R);
+            sum += v;
+        }
+        const int64_t e = w[(int64_t)r * T + t] - sum;
+        __builtin_nontemporal_store(e > 0 ? e : (int64_t)0, dst + (int64_t)K * R);
+        __builtin_nontemporal_store(e < 0 ? -e : (int64_t)0, &o[t * R + r]);
+    }
+}
+
 template <int RB, bool BATCH>
 IngestTile ingest_variant(int K, int64_t T)
 {
@@ -165,7 +200,7 @@ SF_API int sf_ingest(const int64_t* stages, const int64_t* wall, int64_t T, int3
                      int32_t K, int64_t* out_durations, int64_t* out_overlap,
                      sf_stream_t stream)
 {
-    if (T < 0 || R < 1 || R > SF_MAX_R || K < 0 || K + 1 > SF_MAX_S_INGEST) return SF_EINVAL;
+    if (T < 0 || R < 1 || R > SF_MAX_R || K < 0 || K > INT32_MAX - 2) return SF_EINVAL;
     if (!fits(T, K + 2, R, 8)) return SF_EINVAL;
     if (T == 0) return SF_OK;
     const int64_t S = K + 1;
@@ -178,6 +213,15 @@ SF_API int sf_ingest(const int64_t* stages, const int64_t* wall, int64_t T, int3
         for (int b = (a < 2 ? 2 : a + 1); b < 4; ++b)
             if (sizes[a] > 0 && sizes[b] > 0 && !disjoint(bufs[a], sizes[a], bufs[b], sizes[b]))
                 return SF_EINVAL;
+    if (S > kIngestTiledS) {
+        const int64_t nblk = ((R + kIngestWG - 1) / kIngestWG) * T;
+        const unsigned grid = (unsigned)(nblk < (1 << 20) ? nblk : (1 << 20));
+        int Ri = R, Ki = K;
+        void* args[] = {(void*)&stages, (void*)&wall,          (void*)&T,          (void*)&Ri,
+                        (void*)&Ki,     (void*)&out_durations, (void*)&out_overlap};
+        return launch(reinterpret_cast<const void*>(&k_ingest_wide), dim3(grid), dim3(kIngestWG),
+                      args, 0, stream);
+    }
     const IngestTile g = pick_ingest(K, T);
     const int64_t nblk = ((R + g.RB - 1) / g.RB) * ((T + g.TB - 1) / g.TB);
     const unsigned grid = (unsigned)(nblk < (1 << 20) ? nblk : (1 << 20));

@@ -18,7 +18,6 @@ from . import build as _build
 
 SF_OK, SF_EINVAL, SF_ERANGE, SF_EHIP = 0, 1, 2, 3
 SF_MAX_R = 65536
-SF_MAX_S_INGEST = 512
 SF_MAX_PREFIX_NS = 1 << 47
 SF_XOR_PIECE_BYTES = 262144
 

@@ -568,7 +568,8 @@ def _ingest_inputs(R, T, K, seed, slack=10**5):
 @pytest.mark.parametrize("R,T,K", [(1, 1, 0), (1, 9, 5), (8, 100, 5), (7, 33, 1), (64, 64, 5),
                                    (65, 17, 11), (130, 50, 7), (1000, 12, 63), (3, 5, 64),
                                    (40, 3, 127), (17, 2, 255), (9, 2, 511), (65536, 2, 3),
-                                   (4099, 19, 11)])
+                                   (4099, 19, 11), (5, 3, 512), (300, 7, 600), (257, 2, 4095),
+                                   (1, 4, 1000)])
 def test_ingest_matches_oracle(sf, R, T, K):
     x, w = _ingest_inputs(R, T, K, seed=R * 7 + T + K)
     print("case R=%d T=%d K=%d" % (R, T, K), flush=True)
