@@ -10,14 +10,22 @@
 // the tile is kept in LDS as 32-bit values: its low words, transposed so
 // that rank j's column is a run of words with a stride of RPW + 1 (an odd
 // stride: a wave reading one column hits distinct banks), while the high
-// words are OR-ed together.  Each wave then takes RPW / 16 ranks in turn:
+// words are OR-ed together.  Each wave then takes RPW / 16 ranks in turn,
 // a column's n values (K per lane, the tile's zero rows past n included as
-// values below all others) go to registers, and an exact radix select (a
-// 256-bin histogram of the top 8 bits of the OR of the values, then 8 bits
-// at a time of the values left) finds the lower median.  Once at most 64
-// values are left they are compacted, one per lane, into the wave's list
-// (a ballot and a lane count per slot), so later passes handle one value
-// per lane.  The histogram and the list are private to the wave and a
+// values below all others) in registers.
+//
+// A workgroup walks the windows of one (stage, rank chunk) in order, so a
+// column usually has a close guess of its median: the same rank's median in
+// the window before (or, in the first window, the median the wave just
+// found for a rank 16 below).  Two ballot counts per value then bracket the
+// target between g - g/2^e and g + g/2^e, the values inside (about a
+// hundred) are listed, and the target is selected among them
+// (wave_select_bracket).  Without a guess, or when the bracket misses the
+// target, an exact radix select over the whole column finds it: a 256-bin
+// histogram of the top 8 bits of the OR of the values, then 8 bits at a time
+// of the values left; once at most 64 are left they are compacted, one per
+// lane, into the wave's list.  The guess changes which values are listed,
+// never the result.  Histograms and lists are private to the wave and a
 // wave's LDS operations complete in issue order, so the waves need no
 // barrier between them during the selection.
 //
@@ -224,15 +232,124 @@ __device__ u64 wave_select_stream(Get get, int64_t n, uint32_t* h, int lane)
 constexpr int kMedWaves = 16;            // waves per workgroup
 constexpr int kMedWG = 64 * kMedWaves;
 constexpr int64_t kMedTileRows = 1024;   // longest window of the tiled kernel
+// bracketed values a wave lists in its histogram words: list positions
+// start at most kMedListCap, so with the 63 lanes of one ballot they stay
+// below kSelWords (past the cap they overwrite each other, and the count,
+// then above the cap, rejects the list)
+constexpr uint32_t kMedListCap = kSelWords - 64;
+
+// Exact select among at most four values per lane (slot i of lane l is list
+// entry l + 64 i; ok: the slot holds a value), every value <= bound (> 0):
+// 8-bit histogram passes over the values left, until a digit isolates one
+// value or every bit is chosen.  kk: the target's rank among the listed
+// values; h: the wave's histogram (zero on entry and on return).
+__device__ uint32_t wave_select_list(const uint32_t (&x)[4], const bool (&ok)[4], uint32_t kk,
+                                     uint32_t bound, uint32_t* h, int lane)
+{
+    int lo = sel_first_lo_t(bound), hi = lo + 8;
+    uint32_t prefix = 0;
+    for (;;) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (ok[i] && sel_match_t(x[i], hi, prefix))
+                atomicAdd(&h[(x[i] >> lo) & ((1u << (hi - lo)) - 1u)], 1u);
+        wave_lds_fence();
+        uint32_t digit, count;
+        sel_scan_wave(h, lane, kk, digit, count);
+        sel_clear_lane_bins(h, lane);
+        wave_lds_fence();
+        prefix = (prefix << (hi - lo)) | digit;
+        hi = lo;
+        if (hi == 0) return prefix;  // every bit chosen
+        lo = lo > 8 ? lo - 8 : 0;
+        if (count == 1) {
+            // one listed value has the chosen digits: its lane hands it over
+            uint32_t y = 0;
+            bool has = false;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if (ok[i] && sel_match_t(x[i], hi, prefix)) {
+                    y = x[i];
+                    has = true;
+                }
+            }
+            const u64 hm = __ballot(has);
+            return (uint32_t)__builtin_amdgcn_readlane((int)y, hm ? __builtin_ctzll(hm) : 0);
+        }
+    }
+}
+
+// The lower median of a column started from a guess g of it, with the
+// column and kk as for wave_select_regs.  Two counts over the column tell
+// whether the target lies in the bracket [g - delta, g + delta), delta =
+// g / 2^e; the values inside it (about 100 when the guess is close) are
+// listed, offset by the bracket's lower end, in the wave's histogram words
+// (every other lane stores into its word of `spare`), and the target is
+// selected among them.  Returns false, with h zero, when the target lies
+// outside the bracket or the bracket holds more than kMedListCap values:
+// the caller then runs the full select.  The guess decides only which
+// values are listed, so any guess gives the same median.
+template <int KV>
+__device__ bool wave_select_bracket(const uint32_t (&v)[KV], uint32_t g, int e, uint32_t kk,
+                                    uint32_t* h, uint32_t* spare, int lane, uint32_t& med)
+{
+    const uint32_t delta = max(g >> e, 1u);
+    // lo >= 1 puts the zero rows below the bracket; lo + 2 delta <= 2^32
+    // keeps every value below lo out of it after the wrapping subtraction
+    if (g <= delta || g > 0xFFFFFFFFu - delta) return false;
+    const uint32_t lo = g - delta, w2 = 2u * delta;
+    const uint32_t nlo = 0u - lo;  // v < lo exactly when v - lo wraps to >= 2^32 - lo
+    uint32_t below = 0, n_in = 0;  // wave-uniform counts
+    uint32_t* const dump = spare + lane;  // where a value outside the bracket is stored
+#pragma unroll
+    for (int k = 0; k < KV; ++k) {
+        const uint32_t x = v[k] - lo;
+        below += (uint32_t)__popcll(__ballot(x >= nlo));
+        const bool in = x < w2;
+        const u64 m = __ballot(in);
+        const uint32_t r = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        uint32_t* const at = h + (n_in < kMedListCap ? n_in : kMedListCap) + r;
+        n_in += (uint32_t)__popcll(m);
+        *(in ? at : dump) = x;  // every lane stores: no branch
+    }
+    wave_lds_fence();
+    const bool hit = below <= kk && kk - below < n_in && n_in <= kMedListCap;
+    uint32_t x[4];
+    bool ok[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t idx = (uint32_t)lane + 64u * (uint32_t)i;
+        ok[i] = idx < n_in;
+        x[i] = h[idx];
+    }
+    wave_lds_fence();
+    sel_clear_lane_bins(h, lane);
+    wave_lds_fence();
+    if (!hit) return false;
+    med = lo + wave_select_list(x, ok, kk - below, w2 - 1u, h, lane);
+    return true;
+}
 
 // VEC: int64 elements per load (2: 16-byte loads, even R and a 16-byte
 // aligned base); K: values per lane (tile rows 64 * K >= n); RPW: ranks per
 // tile (the tile is 64 * K * (RPW + 1) words, about 130 KB).  One workgroup
 // per CU: 16 waves of at most 128 VGPRs.
+//
+// Work units: unit u = q * P + p covers the tile pair p = c * S + s (rank
+// chunk c, stage s) over the windows [q * L, min((q + 1) * L, W)).  A
+// workgroup takes units blockIdx.x, blockIdx.x + gridDim.x, ... and walks
+// each unit's windows in order, so that every median after a unit's first
+// window starts from the same rank's median of the window before
+// (wave_select_bracket; e sets the bracket width).  Pairs are numbered stage
+// fastest, so the units in flight at once spread over every stage row of
+// their steps, which the HBM channels serve faster than neighbouring pieces
+// of one row (measured on MI355X, plain reads of this walk: 82% of 8 TB/s
+// against 76% with the rank chunk fastest).
 template <int VEC, int K, int RPW>
 __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) void k_window_median(
-    const int64_t* __restrict__ d, int64_t T, int R, int S, int64_t window, int nchunk,
-    int64_t ntiles, int64_t* __restrict__ med)
+    const int64_t* __restrict__ d, int64_t T, int R, int S, int64_t window, int nchunk, int64_t P,
+    int64_t W, int64_t L, int64_t U, int e, int64_t* __restrict__ med)
 {
     constexpr int ROWS = 64 * K;     // tile rows (steps), >= n
     constexpr int STRIDE = RPW + 1;  // words per tile row
@@ -240,7 +357,7 @@ __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) voi
     constexpr int RPS = kMedWG / TPR;  // rows per load sweep
     constexpr int NSW = ROWS / RPS;  // load sweeps
     constexpr int RPWV = RPW / kMedWaves;  // ranks per wave
-    static_assert(RPW % (2 * kMedWaves) == 0 && ROWS % RPS == 0, "shape");
+    static_assert(RPW % (2 * kMedWaves) == 0 && ROWS % RPS == 0 && RPWV <= 64, "shape");
     __shared__ uint32_t tile[ROWS * STRIDE];
     __shared__ __attribute__((aligned(16))) uint32_t hist[kMedWaves][kSelWords];
     __shared__ uint32_t lists[kMedWaves][128];  // 64 entries, then a spare word per lane
@@ -248,49 +365,45 @@ __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) voi
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS bases in SGPRs
     const int i0 = tid / TPR;          // this thread's first tile row
     const int c = (tid % TPR) * 2;     // its rank pair within a tile row
     uint32_t* h = hist[wave];
     for (int i = lane; i < kSelWords; i += 64) h[i] = 0;  // cleared again by every scan
     if (tid < 2) wide_flag[tid] = 0;
 
-    // tile b -> (window, stage, rank chunk), the chunk fastest so that
-    // neighbouring workgroups read neighbouring pieces of the same rows.  A
-    // workgroup's tiles advance by gridDim.x: the position is a mixed-radix
-    // counter (w, s, chunk) advanced with carries, so that the loop does no
-    // 64-bit division.
-    struct Pos {
-        int64_t w;
+    struct Cur {
+        int64_t u, w, w0, wend;  // unit, window, the unit's windows [w0, wend)
         int s, c;
     };
-    auto split = [&](int64_t b) {
-        const int64_t wsi = b / nchunk;
-        return Pos{wsi / S, (int)(wsi % S), (int)(b - wsi * nchunk)};
+    auto unit_start = [&](int64_t u) {
+        const int64_t q = u / P;
+        const int64_t p = u - q * P;
+        Cur k;
+        k.u = u;
+        k.w0 = q * L;
+        k.w = k.w0;
+        k.wend = k.w0 + L < W ? k.w0 + L : W;
+        k.c = (int)(p / S);
+        k.s = (int)(p - (int64_t)k.c * S);
+        return k;
     };
-    const Pos step = split(gridDim.x);
-    auto advance = [&](Pos p) {
-        p.c += step.c;
-        const int cc = p.c >= nchunk;
-        p.c -= cc ? nchunk : 0;
-        p.s += step.s + cc;
-        const int cs = p.s >= S;
-        p.s -= cs ? S : 0;
-        p.w += step.w + cs;
-        return p;
+    auto advance = [&](Cur k) {
+        if (++k.w >= k.wend) k = unit_start(k.u + gridDim.x);
+        return k;
     };
-    auto rows_of = [&](const Pos& p) {  // 1 <= n <= ROWS
-        const int64_t t0 = p.w * window;
+    auto rows_of = [&](const Cur& k) {  // 1 <= n <= ROWS
+        const int64_t t0 = k.w * window;
         return (int)((t0 + window < T ? t0 + window : T) - t0);
     };
     const int64_t rstride = (int64_t)RPS * S * R;  // elements between sweeps
     // the next tile in flight: thread (row i0 + j * RPS, pair c) holds ranks
     // r0 + c, r0 + c + 1 of that row
     int64_t x0[NSW], x1[NSW];
-    auto load = [&](const Pos& p) {
-        const int n = rows_of(p);
-        const int r = p.c * RPW + c;
-        const int64_t* q = d + ((p.w * window + i0) * S + p.s) * (int64_t)R + r;
+    auto load = [&](const Cur& k) {
+        const int n = rows_of(k);
+        const int r = k.c * RPW + c;
+        const int64_t* q = d + ((k.w * window + i0) * S + k.s) * (int64_t)R + r;
 #pragma unroll
         for (int j = 0; j < NSW; ++j) {
             x0[j] = 0;
@@ -311,11 +424,13 @@ __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) voi
         }
     };
 
-    int64_t b = blockIdx.x;  // the grid is at most ntiles
-    Pos pos = split(b);
+    // lane rr of `guess` holds the guess for this wave's rank rr (wave + rr
+    // * kMedWaves of the tile): the median just found for it, 0 for none
+    uint32_t guess = 0;
+    Cur pos = unit_start(blockIdx.x);  // the grid is at most U
     load(pos);
-    for (int it = 0; b < ntiles; b += gridDim.x, ++it) {
-        const Pos cur = pos;
+    for (int it = 0; pos.u < U; ++it) {
+        const Cur cur = pos;
         const int n = rows_of(cur);
         pos = advance(pos);
         __syncthreads();  // every wave is done with the previous tile's columns and flag
@@ -331,26 +446,38 @@ __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) voi
         if (__ballot(hiw != 0) != 0 && lane == 0) atomicOr(&wide_flag[it & 1], 1u);
         __syncthreads();
         const bool wide = wide_flag[it & 1] != 0;  // uniform over the workgroup
-        const bool more = b + gridDim.x < ntiles;
+        const bool more = pos.u < U;
+        const bool guessed = cur.w != cur.w0;  // the window before is this unit's
         const int64_t t0 = cur.w * window;
         int64_t* mrow = med + (cur.w * S + cur.s) * (int64_t)R + cur.c * RPW;
         if (!wide) {
             // the next tile's loads fly while this one is resolved
             if (more) load(pos);
             const uint32_t kk = (uint32_t)((n - 1) / 2 + (ROWS - n));
+            uint32_t m_prev = 0;
 #pragma unroll 1
             for (int rr = 0; rr < RPWV; ++rr) {
                 const int j = wave + rr * kMedWaves;  // the tile column
                 if (cur.c * RPW + j >= R) break;      // wave-uniform
                 const uint32_t* col = tile + lane * STRIDE + j;
                 uint32_t v[K];
-                uint32_t vor = 0;
 #pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    v[k] = col[k * 64 * STRIDE];
-                    vor |= v[k];
+                for (int k = 0; k < K; ++k) v[k] = col[k * 64 * STRIDE];
+                // the guess: this rank's median in the window before, else
+                // (a unit's first window) the median this wave just found
+                // for the rank kMedWaves below
+                const uint32_t g = guessed ? (uint32_t)__builtin_amdgcn_readlane((int)guess, rr) : m_prev;
+                uint32_t m = 0;
+                const bool found = (guessed || rr > 0) &&
+                                   wave_select_bracket<K>(v, g, e, kk, h, lists[wave] + 64, lane, m);
+                if (!found) {
+                    uint32_t vor = 0;
+#pragma unroll
+                    for (int k = 0; k < K; ++k) vor |= v[k];
+                    m = wave_select_regs<K>(v, wave_or32(vor), kk, n, h, lists[wave], lane);
                 }
-                const uint32_t m = wave_select_regs<K>(v, wave_or32(vor), kk, n, h, lists[wave], lane);
+                guess = lane == rr ? m : guess;
+                m_prev = m;
                 if (lane == 0) mrow[j] = (int64_t)m;
             }
         } else {
@@ -364,6 +491,7 @@ __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) voi
                 const int64_t* col = d + (t0 * S + cur.s) * (int64_t)R + r;
                 const int64_t cs = (int64_t)S * R;
                 const u64 m = wave_select_stream([&](int64_t i) { return (u64)col[i * cs]; }, n, h, lane);
+                guess = lane == rr ? ((m >> 32) ? 0u : (uint32_t)m) : guess;
                 if (lane == 0) mrow[j] = (int64_t)m;
             }
             if (more) load(pos);
@@ -459,12 +587,38 @@ SF_API int sf_window_median(const int64_t* durations, int64_t T, int32_t R, int3
     const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
     const MedianVariant v = vec2 ? pick_median<2>(n_max) : pick_median<1>(n_max);
     const int nchunk = (R + v.RPW - 1) / v.RPW;
-    int64_t ntiles = W * S * (int64_t)nchunk;
-    // persistent workgroups: one per CU (each holds about 150 KB of LDS)
-    int64_t grid = cus;
-    if (grid > ntiles) grid = ntiles;
+    const int64_t P = (int64_t)nchunk * S;  // tile pairs (rank chunk, stage)
+    // persistent workgroups, at most one per CU (each holds about 150 KB of
+    // LDS), over units of L consecutive windows of one pair: the split Q of
+    // the windows that minimises the units per workgroup times the unit's
+    // cost, counting its first window (no guess, the full select) twice
+    int64_t L = W, U = P;
+    double best = -1.0;
+    const int64_t qmax = W < 4 * (int64_t)cus ? W : 4 * (int64_t)cus;
+    for (int64_t q = 1; q <= qmax; ++q) {
+        const int64_t l = (W + q - 1) / q;
+        if (P > INT64_MAX / ((W + l - 1) / l)) break;
+        const int64_t u = P * ((W + l - 1) / l);  // every range non-empty
+        const int64_t g = u < cus ? u : cus;
+        const double cost = (double)((u + g - 1) / g) * (double)(l + 1);
+        if (best < 0.0 || cost < best) {
+            best = cost;
+            L = l;
+            U = u;
+        }
+    }
+    const int64_t grid = U < cus ? U : cus;
+    // bracket half-width g / 2^e for windows of n_max steps: about 3.7
+    // sqrt(n) values inside for a spread of a tenth of the value, so that a
+    // guess off by the statistical error of a median still brackets it
+    int lg = 0;
+    while (((int64_t)2 << lg) <= n_max) ++lg;  // floor(log2(n_max))
+    int e = (lg + 1) / 2 + 1;
+    if (e < 4) e = 4;
     int Ri = R, Si = S;
-    void* args[] = {(void*)&durations, (void*)&T,      (void*)&Ri,     (void*)&Si,
-                    (void*)&window,    (void*)&nchunk, (void*)&ntiles, (void*)&out_median};
+    int64_t Wl = W;
+    void* args[] = {(void*)&durations, (void*)&T, (void*)&Ri, (void*)&Si, (void*)&window,
+                    (void*)&nchunk,    (void*)&P, (void*)&Wl, (void*)&L,  (void*)&U,
+                    (void*)&e,         (void*)&out_median};
     return launch(v.fn, dim3((unsigned)grid), dim3(kMedWG), args, 0, stream);
 }
