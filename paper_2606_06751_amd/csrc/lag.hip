@@ -12,7 +12,10 @@
 // later passes take the next 8 bits of the values left, which once few
 // enough are compacted into an LDS list so that later passes read only
 // them.  A digit that isolates a single value ends the selection, and the
-// lane holding that value writes the boundary's outputs.
+// lane holding that value writes the boundary's outputs.  The barriers
+// inside a step order LDS accesses only (lds_barrier), so the next stage's
+// loads stay in flight across them (a full barrier waits for every load of
+// the wave: measured 11% slower at 4096 ranks).
 
 #include "sf_device.h"
 #include "sf_host.h"
@@ -153,10 +156,12 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
         if constexpr (NARROW) {
             // the stage's 16-byte loads in CH chunks, each consumed before
             // the next is issued (two at a time for the lag, whose prefixes
-            // stay live across stages: one at a time measured 9% slower,
-            // four at a time spilled 32 bytes and 17% slower)
+            // stay live across stages: one at a time measured 9% slower;
+            // four or eight at a time spill and ran 14-20% slower)
             constexpr int CH = PREFIX ? NLD / 2 : (K <= 32 ? 2 : NLD / 4);
-            const int64_t* row = dt + (int64_t)s * R;
+            // the stage row through a buffer resource: its base in SGPRs, a
+            // lane's offset in one VGPR (FULL: the same for every load)
+            const auto rs = buffer_rsrc(dt + (int64_t)s * R, (uint32_t)R * 8u);
             uint32_t mx = 0, mn = ~0u;
             bool wide = false;  // wave-uniform: some value of the wave left 32 bits
 #pragma unroll
@@ -164,9 +169,12 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
                 uint32_t w = 0;
                 v2i64 xs[NLD / CH];
 #pragma unroll
-                for (int l = 0; l < NLD / CH; ++l)
-                    xs[l] = __builtin_nontemporal_load(
-                        reinterpret_cast<const v2i64*>(row + idx[ch * (NLD / CH) + l]));
+                for (int l = 0; l < NLD / CH; ++l) {
+                    const int ll = ch * (NLD / CH) + l;
+                    xs[l] = FULL ? buffer_load16_nt(rs, (uint32_t)tid * 16u, (uint32_t)(ll * WG * 16))
+                                 : buffer_load16_nt(rs, (uint32_t)idx[ll] * 8u, 0u);
+                }
+                __builtin_amdgcn_sched_barrier(0);  // the chunk's loads all in flight first
 #pragma unroll
                 for (int l = 0; l < NLD / CH; ++l) {
                     // a slot pair past R (re-reading the row's first pair)
@@ -217,7 +225,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
             red_max[pb][wave] = lmax;
             red_min[pb][wave] = lmin;
         }
-        __syncthreads();
+        lds_barrier();
         // every wave combines the partials the same way, lane w taking
         // wave w's (w < NW <= 16: row 0), so the results are uniform
         const bool has = lane < NW;
@@ -263,7 +271,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
                         sel_hist_add(h, ok[k / VEC] ? sel_bin(P[k], lo, hi, prefix) : -1);
                 }
                 first = false;
-                __syncthreads();
+                lds_barrier();
                 uint32_t digit, count;
                 if (SCAN_ALL) {
                     sel_scan_wave(h, lane, kk, digit, count);
@@ -303,7 +311,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
                         uint32_t* other = hist[cur ^ 1];
                         for (int i = tid; i < kLagWords; i += WG) other[i] = 0;
                     }
-                    __syncthreads();
+                    lds_barrier();
                     // h is cleared during the scan of the next pass (or stage)
                     cur ^= 1;
                     digit = sel[0];
@@ -365,7 +373,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
                             ++pos;
                         }
                     }
-                    __syncthreads();
+                    lds_barrier();
                     // every wave has taken its base: reset for the next boundary
                     // (its next use follows at least one more barrier)
                     if (tid == 0) list_n = 0;
@@ -387,7 +395,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
         // lag_sh[s & 1] is read at stage s + 1, after its reduction barrier
     }
     if (NARROW) {
-        __syncthreads();  // after every output write of the step
+        __syncthreads();  // after every output write of the step (global stores)
         if (wide_step && tid == 0) out[t * S] = kRedo;
     }
 }

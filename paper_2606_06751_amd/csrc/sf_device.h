@@ -60,6 +60,32 @@ __device__ __forceinline__ u64 group_max(u64 v)
 
 __device__ __forceinline__ u64 umin64(u64 a, u64 b) { return a < b ? a : b; }
 
+// A workgroup barrier that orders LDS accesses only: waves wait for their
+// own LDS operations, not for their global loads in flight, so a load issued
+// before it (the next stage's rows) keeps flying across it.  __syncthreads()
+// would wait for those loads too.  Not for communication through global
+// memory.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// A raw buffer resource over `bytes` bytes at `base` (gfx950 word 3: raw,
+// 32-bit untyped), so that loads take the base from SGPRs, a lane's byte
+// offset from one VGPR and a wave-uniform byte offset from an SGPR.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+
+// 16 bytes at base + voff + soff, non-temporal (aux bit 1)
+__device__ __forceinline__ v2i64 buffer_load16_nt(__amdgpu_buffer_rsrc_t rs, uint32_t voff, uint32_t soff)
+{
+    return __builtin_bit_cast(v2i64, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)voff, (int)soff, 2));
+}
+
 constexpr int kSumWG = 256;  // threads of the window reduction kernels
 
 __device__ __forceinline__ int64_t wave_sum64(int64_t v)
