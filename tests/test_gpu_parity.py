@@ -930,6 +930,37 @@ def test_median_rank_sweep(sf, R):
         assert_median_equal(sf, d, window)
 
 
+@pytest.mark.parametrize("window", [100, 250, 1000])
+def test_median_warm_start_edges(sf, window):
+    """The warm start of the window median (a column's median bracketed
+    around the same rank's median of the window before, or in a unit's
+    first window around a median already found in the tile) must give the
+    oracle's median whether the guess lands inside its bracket, just past
+    its edge or far off, and when the bracket holds too many values: window
+    scales that drift by 0 to 60% from one window to the next, ranks whose
+    scales differ 50-fold inside one tile, constant columns and columns of
+    mass ties (every value in the bracket), values next to 2^32 (no bracket
+    fits below 2^32), zeros, and a ragged last window."""
+    rng = np.random.Generator(np.random.PCG64(window))
+    R, S = 96, 3
+    shifts = [0.0, 0.004, -0.008, 0.012, 0.02, -0.03, 0.05, 0.5, -0.6, 1e-4]
+    scale = np.cumprod([1.0] + [1.0 + x for x in shifts])   # one per window
+    W = len(scale)
+    T = window * (W - 1) + window // 2 + 1                   # ragged last window
+    w_of_t = np.minimum(np.arange(T) // window, W - 1)
+    noise = 1.0 + 0.1 * rng.standard_normal((T, S, R))
+    d = np.rint(2e7 * scale[w_of_t][:, None, None] * noise).clip(1, None).astype(np.int64)
+    d[:, :, R // 2:] *= 50                                   # a 50-fold scale change inside tile 1
+    d[:, 1, 5] = 5_000_000                                   # a constant column
+    ties = rng.random((T, R)) < 0.5
+    d[:, 1, 40:60] = np.where(ties[:, 40:60], 7_000_000, d[:, 1, 40:60])  # mass ties at the median
+    d[:, 2, R - 1] = (1 << 32) - 1 - rng.integers(0, 1000, size=T)        # next to 2^32
+    d[:, 2, 0] = 0                                           # zeros
+    d[:, 2, 1] = rng.integers(0, 3, size=T)                  # medians of 0, 1 or 2
+    print("case window=%d T=%d R=%d" % (window, T, R), flush=True)
+    assert_median_equal(sf, d, window)
+
+
 def test_median_wide_and_narrow_tiles_mixed(sf):
     """Tiles whose values all fit 32 bits next to tiles with one value of
     2^32 or more (resolved in 64 bits from global memory): per stage, per
