@@ -682,6 +682,32 @@ def test_gain_many_stages_wide_values(sf):
         assert_gain_equal(sf, d, bt, window)
 
 
+@pytest.mark.parametrize("S,R,T,window,hi", [
+    (1, 2048, 40, 7, 10**6), (3, 2050, 30, 8, 10**6), (4, 4096, 700, 1000, 10**6),
+    (5, 2560, 20, 3, 1 << 40), (8, 16384, 150, 100, 10**9), (9, 3000, 16, 5, 4),
+    (13, 2048, 12, 4, 10**6), (16, 2048, 12, 5, 1 << 40)])
+def test_gain_rank_tiles(sf, S, R, T, window, hi):
+    """From 2048 ranks and up to 16 stages (even R, aligned): several
+    512-rank tiles per step with a ragged last one, T below the window, a
+    ragged last window, heavy ties, and values past 2^32."""
+    rng = np.random.Generator(np.random.PCG64(S * 7919 + R))
+    d = rng.integers(0, hi, size=(T, S, R), dtype=np.int64)
+    bt = rng.integers(0, hi, size=(-(-T // window), S, R), dtype=np.int64)
+    print("case S=%d R=%d T=%d window=%d" % (S, R, T, window), flush=True)
+    assert_gain_equal(sf, d, bt, window)
+
+
+def test_gain_large_gain_column(sf):
+    """Stage 2 carries more than 2^32 on every rank, so replacing it puts
+    every candidate more than 2^32 below F (a gain past 4.3 s)."""
+    rng = np.random.Generator(np.random.PCG64(4242))
+    T, S, R, window = 10, 6, 4096, 3
+    d = rng.integers(0, 1000, size=(T, S, R), dtype=np.int64)
+    d[:, 2, :] += (1 << 34) + rng.integers(0, 1 << 20, size=(T, R))
+    bt = rng.integers(0, 10, size=(-(-T // window), S, R), dtype=np.int64)
+    assert_gain_equal(sf, d, bt, window)
+
+
 def test_gain_golden_cases(sf):
     import pins
     pins.pin_gain_sync_wait(lambda d, b, w: {k: v.cpu().numpy() for k, v in sf.sf_exposure_gain(
