@@ -685,11 +685,16 @@ def test_gain_many_stages_wide_values(sf):
 @pytest.mark.parametrize("S,R,T,window,hi", [
     (1, 2048, 40, 7, 10**6), (3, 2050, 30, 8, 10**6), (4, 4096, 700, 1000, 10**6),
     (5, 2560, 20, 3, 1 << 40), (8, 16384, 150, 100, 10**9), (9, 3000, 16, 5, 4),
-    (13, 2048, 12, 4, 10**6), (16, 2048, 12, 5, 1 << 40)])
+    (13, 2048, 12, 4, 10**6), (16, 2048, 12, 5, 1 << 40),
+    (1, 4098, 40, 7, 10**6), (3, 8192, 30, 8, 10**6), (5, 6000, 20, 3, 1 << 40),
+    (13, 16384, 12, 4, 10**6), (16, 10000, 12, 5, 10**6), (9, 5002, 16, 5, 4),
+    (12, 8192, 10, 5, 1 << 28), (7, 12288, 25, 6, 10**8)])
 def test_gain_rank_tiles(sf, S, R, T, window, hi):
     """From 2048 ranks and up to 16 stages (even R, aligned): several
     512-rank tiles per step with a ragged last one, T below the window, a
-    ragged last window, heavy ties, and values past 2^32."""
+    ragged last window, heavy ties, and values past 2^32; past 4096 ranks
+    the near-frontier pass, full and ragged workgroups, steps with totals
+    past 2^32 next to steps below it in one launch."""
     rng = np.random.Generator(np.random.PCG64(S * 7919 + R))
     d = rng.integers(0, hi, size=(T, S, R), dtype=np.int64)
     bt = rng.integers(0, hi, size=(-(-T // window), S, R), dtype=np.int64)
@@ -705,6 +710,46 @@ def test_gain_large_gain_column(sf):
     d = rng.integers(0, 1000, size=(T, S, R), dtype=np.int64)
     d[:, 2, :] += (1 << 34) + rng.integers(0, 1 << 20, size=(T, R))
     bt = rng.integers(0, 10, size=(-(-T // window), S, R), dtype=np.int64)
+    assert_gain_equal(sf, d, bt, window)
+
+
+def test_gain_stalled_near_frontier(sf):
+    """Forty ranks stalled in one stage hold the frontier; replacing that
+    stage drops all of them below ranks far from F, so the largest
+    replaced-stage total comes from a rank outside the ranks near F (values
+    below 2^32)."""
+    rng = np.random.Generator(np.random.PCG64(515))
+    for R, S in ((4096, 6), (16384, 12), (6000, 4)):
+        T, window = 8, 3
+        d = rng.integers(0, 1000, size=(T, S, R), dtype=np.int64)
+        d[:, 1, :40] += 10**6 + rng.integers(0, 1000, size=(T, 40))
+        bt = rng.integers(0, 10, size=(-(-T // window), S, R), dtype=np.int64)
+        print("case R=%d S=%d" % (R, S), flush=True)
+        assert_gain_equal(sf, d, bt, window)
+
+
+def test_gain_wide_steps_among_narrow(sf):
+    """Past 4096 ranks: the odd steps hold a duration past 2^32 and go to the
+    64-bit kernel, the even ones stay in 32 bits, in one launch."""
+    rng = np.random.Generator(np.random.PCG64(717))
+    T, S, R, window = 9, 12, 8192, 4
+    d = rng.integers(0, 1 << 28, size=(T, S, R), dtype=np.int64)
+    d[1::2, 3, 77] += 1 << 32
+    bt = rng.integers(0, 1 << 28, size=(-(-T // window), S, R), dtype=np.int64)
+    assert_gain_equal(sf, d, bt, window)
+
+
+def test_gain_many_ranks_tied_at_frontier(sf):
+    """600 ranks share the largest total (more than the near-frontier set
+    holds) and the rest trail: the step is resolved from all ranks; then
+    every total equal."""
+    rng = np.random.Generator(np.random.PCG64(616))
+    T, S, R, window = 6, 5, 8192, 4
+    d = rng.integers(0, 1000, size=(T, S, R), dtype=np.int64)
+    d[:, :, :600] = 5000
+    bt = rng.integers(0, 3000, size=(-(-T // window), S, R), dtype=np.int64)
+    assert_gain_equal(sf, d, bt, window)
+    d[:, :, :] = 777
     assert_gain_equal(sf, d, bt, window)
 
 
