@@ -213,7 +213,12 @@ int sf_route(const int64_t* stage_exposed, int64_t W, int32_t S, int64_t tau_num
  *                        per-stage deltas are held in registers and the
  *                        durations read once; past 64 a two-pass kernel
  *                        reads each step's durations twice (slower, same
- *                        results).
+ *                        results).  From 4097 to 16384 ranks (up to 16
+ *                        stages, even R, 16-byte aligned inputs) a step's
+ *                        durations are read once into rank totals and the
+ *                        baseline only for the ranks near the frontier; a
+ *                        step that the bound does not settle is read again
+ *                        over all ranks (same results).
  *   out_gain             [T][S] int64: the gain of each step and stage.
  *   out_makespan         [T] int64: F[t][S-1], the step's exposed makespan.
  *   out_window_gain      [W][S] int64: window sums of out_gain.

@@ -10,6 +10,11 @@
 // a lane keeps its running maxima over the tiles in registers and the group
 // reduces once per step; otherwise the group reduces every tile.  Partial
 // maxima of several groups meet in LDS.
+//
+// Past 4096 ranks (up to 16384, 16 stages) k_exposure_gain_near takes the
+// maximum over the ranks near the frontier first and over all ranks only
+// when a bound requires it; k_exposure_gain<REDO> recomputes the steps it
+// hands over (values of 2^32 or more).
 
 #include "sf_device.h"
 #include "sf_host.h"
@@ -256,7 +261,7 @@ __global__ __launch_bounds__(WG) void k_exposure_gain_wide(
 // step's durations and baseline and takes the maxima over all ranks.  A
 // step with a duration or a total of 2^32 or more is handed over: its gain
 // row starts with kGainRedo and k_exposure_gain<REDO> recomputes it in 64
-// bits.  Measured on MI355X: one 16-wave workgroup per CU (about 72 VGPRs)
+// bits.  Measured on MI355X: one 16-wave workgroup per CU (about 76 VGPRs)
 // ran 5% faster than two at a 64-VGPR cap; loading a stage in one chunk, 3%
 // slower; without the stage barrier, 2% slower; at 4096 ranks the
 // per-step kernel stays ahead (0.62 against 0.65 ms).
