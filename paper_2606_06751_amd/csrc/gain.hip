@@ -385,7 +385,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
     if (anywide == 0 && F != Pmin) {
         int lo = sel_first_lo((u64)(F - Pmin)), hi = 64;
         u64 prefix = 0;
-        uint32_t kk = kNearMin - 1;  // R >= 2048 ranks
+        uint32_t kk = kNearMin - 1;  // R > 4096 ranks
         uint32_t below = 0;          // ranks in Q for certain (below the bracket)
         bool first = true;
         for (;;) {
@@ -472,7 +472,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 if (i0 + (uint32_t)(j * WG) < np) {
-                    const int64_t e = x[j] - y[j];  // x < 2^32 <= ... : e <= x <= total
+                    const int64_t e = x[j] - y[j];  // b >= 0: max(e, 0) <= x <= the total
                     atomicMax(&cand[sj[j]], tq[j] - (uint32_t)(e > 0 ? e : 0));
                 }
             }
