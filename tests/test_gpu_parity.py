@@ -739,6 +739,31 @@ def test_gain_wide_steps_among_narrow(sf):
     assert_gain_equal(sf, d, bt, window)
 
 
+def test_gain_near_frontier_random_shapes(sf):
+    """Random shapes past 4096 ranks with stalls of random size on random
+    ranks (large gains force the second pass over all ranks, small ones
+    stay in the near set) and a baseline from the window median or random."""
+    rng = np.random.Generator(np.random.PCG64(8086))
+    for case in range(24):
+        R = 2 * int(rng.integers(2049, 8193))
+        S = int(rng.integers(1, 17))
+        T = int(rng.integers(1, 9))
+        window = int(rng.integers(1, 6))
+        scale = int(rng.choice([10, 10**4, 10**6, 1 << 26]))
+        d = rng.integers(0, scale, size=(T, S, R), dtype=np.int64)
+        for _ in range(int(rng.integers(0, 4))):
+            r0 = int(rng.integers(0, R))
+            nr = int(rng.integers(1, 64))
+            d[:, int(rng.integers(0, S)), r0:r0 + nr] += int(rng.integers(1, 100)) * scale
+        W = -(-T // window)
+        if case % 2:
+            bt = oracle.window_median(d, window)
+        else:
+            bt = rng.integers(0, scale, size=(W, S, R), dtype=np.int64)
+        print("case %d R=%d S=%d T=%d window=%d scale=%d" % (case, R, S, T, window, scale), flush=True)
+        assert_gain_equal(sf, d, bt, window)
+
+
 def test_gain_many_ranks_tied_at_frontier(sf):
     """600 ranks share the largest total (more than the near-frontier set
     holds) and the rest trail: the step is resolved from all ranks; then
