@@ -49,6 +49,23 @@ __device__ __forceinline__ uint32_t group_max32(uint32_t v)
 // lane 0's value, in every lane
 __device__ __forceinline__ u64 lane0(u64 v) { return lane_value(v, 0); }
 
+// The select's digit and candidate tests on the held values: 64-bit as in
+// sf_select.h, and 32-bit for the narrow pass (its values, and so its
+// range, stay below 2^32: lo <= 24, hi <= 32, a prefix below 2^(32 - hi)),
+// which keeps the shifts and compares in single VALU instructions.
+__device__ __forceinline__ bool held_match(u64 u, int hi, u64 prefix) { return sel_match(u, hi, prefix); }
+__device__ __forceinline__ int held_bin(u64 u, int lo, int hi, u64 prefix) { return sel_bin(u, lo, hi, prefix); }
+__device__ __forceinline__ int held_first_bin(u64 u, int lo) { return sel_first_bin(u, lo); }
+__device__ __forceinline__ bool held_match(uint32_t u, int hi, u64 prefix)
+{
+    return hi >= 32 || (u >> hi) == (uint32_t)prefix;
+}
+__device__ __forceinline__ int held_bin(uint32_t u, int lo, int hi, u64 prefix)
+{
+    return held_match(u, hi, prefix) ? (int)((u >> lo) & ((1u << (hi - lo)) - 1u)) : -1;
+}
+__device__ __forceinline__ int held_first_bin(uint32_t u, int lo) { return (int)(u >> lo); }
+
 // One step per workgroup: at every stage, out[t][s] = max - lower median
 // over ranks of the prefixes (PREFIX: the lag, and out_inc gets its
 // increment) or of the stage's durations themselves (the raw rank spread;
@@ -155,10 +172,12 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
         u64 lmax = 0, lmin = ~0ull;
         if constexpr (NARROW) {
             // the stage's 16-byte loads in CH chunks, each consumed before
-            // the next is issued (two at a time for the lag, whose prefixes
-            // stay live across stages: one at a time measured 9% slower;
-            // four or eight at a time spill and ran 14-20% slower)
-            constexpr int CH = PREFIX ? NLD / 2 : (K <= 32 ? 2 : NLD / 4);
+            // the next is issued.  The lag's prefixes stay live across
+            // stages: at 16 values per lane it takes four loads at a time
+            // (with the select's tests in 32 bits this fits the 64-VGPR
+            // budget; measured at 16384 ranks 3% faster than two at a time,
+            // which the 64-bit tests forced); at 32 values, two at a time
+            constexpr int CH = PREFIX ? (K == 16 ? 2 : NLD / 2) : (K <= 32 ? 2 : NLD / 4);
             // the stage row through a buffer resource: its base in SGPRs, a
             // lane's offset in one VGPR (FULL: the same for every load)
             const auto rs = buffer_rsrc(dt + (int64_t)s * R, (uint32_t)R * 8u);
@@ -258,17 +277,17 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
                     for (int i = tid; i < kLagWords; i += WG) hist[cur][i] = 0;
                 }
                 if (LCAP > 0 && in_list) {
-                    for (uint32_t i = tid; i < n; i += WG) sel_hist_add(h, sel_bin(list[i], lo, hi, prefix));
+                    for (uint32_t i = tid; i < n; i += WG) sel_hist_add(h, held_bin(list[i], lo, hi, prefix));
                 } else if (first) {
                     // one plain atomic per value (3-4% faster than adding
                     // runs of equal bins among a lane's values at once)
 #pragma unroll
                     for (int k = 0; k < K; ++k)
-                        if (ok[k / VEC]) atomicAdd(&h[sel_first_bin(P[k], lo)], 1u);
+                        if (ok[k / VEC]) atomicAdd(&h[held_first_bin(P[k], lo)], 1u);
                 } else {
 #pragma unroll
                     for (int k = 0; k < K; ++k)
-                        sel_hist_add(h, ok[k / VEC] ? sel_bin(P[k], lo, hi, prefix) : -1);
+                        sel_hist_add(h, ok[k / VEC] ? held_bin(P[k], lo, hi, prefix) : -1);
                 }
                 first = false;
                 lds_barrier();
@@ -330,7 +349,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
                     bool holder = false;
                     if (LCAP > 0 && in_list) {
                         for (uint32_t i = tid; i < n; i += WG) {
-                            if (sel_match(list[i], hi, prefix)) {
+                            if (held_match(list[i], hi, prefix)) {
                                 u = list[i];
                                 holder = true;
                             }
@@ -338,7 +357,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
                     } else {
 #pragma unroll
                         for (int k = 0; k < K; ++k) {
-                            if (ok[k / VEC] && sel_match(P[k], hi, prefix)) {
+                            if (ok[k / VEC] && held_match(P[k], hi, prefix)) {
                                 u = P[k];
                                 holder = true;
                             }
@@ -359,7 +378,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
                     uint32_t cand = 0;  // bit k: P[k] is a candidate
 #pragma unroll
                     for (int k = 0; k < K; ++k)
-                        cand |= (ok[k / VEC] && sel_match(P[k], hi, prefix)) ? (1u << k) : 0u;
+                        cand |= (ok[k / VEC] && held_match(P[k], hi, prefix)) ? (1u << k) : 0u;
                     const uint32_t nc = (uint32_t)__popc(cand);
                     const uint32_t incl2 = wave_scan_incl(nc);
                     const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl2, 63);
