@@ -124,7 +124,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(NARROW && K 
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS slots in SGPRs
     const int64_t t = xcd_block();
     if (t >= T) return;  // uniform over the workgroup (the grid is T)
     if (REDO && out[t * S] != kRedo) return;  // a step the narrow pass resolved
