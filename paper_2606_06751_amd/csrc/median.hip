@@ -346,7 +346,11 @@ __device__ bool wave_select_bracket(const uint32_t (&v)[KV], uint32_t g, int e, 
 // their steps, which the HBM channels serve faster than neighbouring pieces
 // of one row (measured on MI355X, plain reads of this walk: 82% of 8 TB/s
 // against 76% with the rank chunk fastest).
-template <int VEC, int K, int RPW>
+// C32: units and windows below 2^31 (every workload here), so the cursor
+// over them is 32-bit: its divisions and the values kept across a tile fit
+// the 128-VGPR budget with 2 spilled VGPRs instead of 7 (1.4% faster at
+// 16384 ranks, 2% at 4096)
+template <int VEC, int K, int RPW, bool C32>
 __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) void k_window_median(
     const int64_t* __restrict__ d, int64_t T, int R, int S, int64_t window, int nchunk, int64_t P,
     int64_t W, int64_t L, int64_t U, int e, int64_t* __restrict__ med)
@@ -372,28 +376,31 @@ __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) voi
     for (int i = lane; i < kSelWords; i += 64) h[i] = 0;  // cleared again by every scan
     if (tid < 2) wide_flag[tid] = 0;
 
+    typedef typename std::conditional<C32, uint32_t, int64_t>::type I;
     struct Cur {
-        int64_t u, w, w0, wend;  // unit, window, the unit's windows [w0, wend)
+        I u, w, w0, wend;  // unit, window, the unit's windows [w0, wend)
         int s, c;
     };
-    auto unit_start = [&](int64_t u) {
-        const int64_t q = u / P;
-        const int64_t p = u - q * P;
+    const I Pi = (I)P, Li = (I)L, Wi = (I)W;
+    auto unit_start = [&](int64_t u64) {
+        const I u = (I)u64;
+        const I q = u / Pi;
+        const I p = u - q * Pi;
         Cur k;
         k.u = u;
-        k.w0 = q * L;
+        k.w0 = q * Li;
         k.w = k.w0;
-        k.wend = k.w0 + L < W ? k.w0 + L : W;
-        k.c = (int)(p / S);
-        k.s = (int)(p - (int64_t)k.c * S);
+        k.wend = k.w0 + Li < Wi ? k.w0 + Li : Wi;
+        k.c = (int)(p / (I)S);
+        k.s = (int)(p - (I)k.c * (I)S);
         return k;
     };
     auto advance = [&](Cur k) {
-        if (++k.w >= k.wend) k = unit_start(k.u + gridDim.x);
+        if (++k.w >= k.wend) k = unit_start((int64_t)k.u + gridDim.x);
         return k;
     };
     auto rows_of = [&](const Cur& k) {  // 1 <= n <= ROWS
-        const int64_t t0 = k.w * window;
+        const int64_t t0 = (int64_t)k.w * window;
         return (int)((t0 + window < T ? t0 + window : T) - t0);
     };
     const int64_t rstride = (int64_t)RPS * S * R;  // elements between sweeps
@@ -403,7 +410,7 @@ __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) voi
     auto load = [&](const Cur& k) {
         const int n = rows_of(k);
         const int r = k.c * RPW + c;
-        const int64_t* q = d + ((k.w * window + i0) * S + k.s) * (int64_t)R + r;
+        const int64_t* q = d + (((int64_t)k.w * window + i0) * S + k.s) * (int64_t)R + r;
 #pragma unroll
         for (int j = 0; j < NSW; ++j) {
             x0[j] = 0;
@@ -429,7 +436,7 @@ __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) voi
     uint32_t guess = 0;
     Cur pos = unit_start(blockIdx.x);  // the grid is at most U
     load(pos);
-    for (int it = 0; pos.u < U; ++it) {
+    for (int it = 0; (int64_t)pos.u < U; ++it) {
         const Cur cur = pos;
         const int n = rows_of(cur);
         pos = advance(pos);
@@ -446,10 +453,10 @@ __global__ __launch_bounds__(kMedWG) __attribute__((amdgpu_waves_per_eu(4))) voi
         if (__ballot(hiw != 0) != 0 && lane == 0) atomicOr(&wide_flag[it & 1], 1u);
         __syncthreads();
         const bool wide = wide_flag[it & 1] != 0;  // uniform over the workgroup
-        const bool more = pos.u < U;
+        const bool more = (int64_t)pos.u < U;
         const bool guessed = cur.w != cur.w0;  // the window before is this unit's
-        const int64_t t0 = cur.w * window;
-        int64_t* mrow = med + (cur.w * S + cur.s) * (int64_t)R + cur.c * RPW;
+        const int64_t t0 = (int64_t)cur.w * window;
+        int64_t* mrow = med + ((int64_t)cur.w * S + cur.s) * (int64_t)R + cur.c * RPW;
         if (!wide) {
             // the next tile's loads fly while this one is resolved
             if (more) load(pos);
@@ -536,21 +543,23 @@ struct MedianVariant {
 };
 
 template <int VEC, int K, int RPW>
-MedianVariant median_variant()
+MedianVariant median_variant(bool c32)
 {
-    return MedianVariant{reinterpret_cast<const void*>(&k_window_median<VEC, K, RPW>), RPW};
+    return MedianVariant{c32 ? reinterpret_cast<const void*>(&k_window_median<VEC, K, RPW, true>)
+                             : reinterpret_cast<const void*>(&k_window_median<VEC, K, RPW, false>),
+                         RPW};
 }
 
 // K values per lane for windows up to 64 K steps; the rank tile widens as
 // the window shortens, so that every tile holds about 128 KB of 32-bit
 // values (256-byte rows at 1024 steps, 2 KB rows at 128)
 template <int VEC>
-MedianVariant pick_median(int64_t n)
+MedianVariant pick_median(int64_t n, bool c32)
 {
-    if (n <= 128) return median_variant<VEC, 2, 256>();
-    if (n <= 256) return median_variant<VEC, 4, 128>();
-    if (n <= 512) return median_variant<VEC, 8, 64>();
-    return median_variant<VEC, 16, 32>();  // n <= kMedTileRows
+    if (n <= 128) return median_variant<VEC, 2, 256>(c32);
+    if (n <= 256) return median_variant<VEC, 4, 128>(c32);
+    if (n <= 512) return median_variant<VEC, 8, 64>(c32);
+    return median_variant<VEC, 16, 32>(c32);  // n <= kMedTileRows
 }
 
 }  // namespace sfk
@@ -585,8 +594,8 @@ SF_API int sf_window_median(const int64_t* durations, int64_t T, int32_t R, int3
                       dim3(kMedLongWG), args, 0, stream);
     }
     const bool vec2 = (R % 2 == 0) && aligned(durations, 16);
-    const MedianVariant v = vec2 ? pick_median<2>(n_max) : pick_median<1>(n_max);
-    const int nchunk = (R + v.RPW - 1) / v.RPW;
+    const int RPW = (vec2 ? pick_median<2>(n_max, false) : pick_median<1>(n_max, false)).RPW;
+    const int nchunk = (R + RPW - 1) / RPW;
     const int64_t P = (int64_t)nchunk * S;  // tile pairs (rank chunk, stage)
     // persistent workgroups, at most one per CU (each holds about 150 KB of
     // LDS), over units of L consecutive windows of one pair: the split Q of
@@ -608,6 +617,10 @@ SF_API int sf_window_median(const int64_t* durations, int64_t T, int32_t R, int3
         }
     }
     const int64_t grid = U < cus ? U : cus;
+    // a 32-bit cursor when the units, and the windows plus a unit's length,
+    // stay below 2^31
+    const bool c32 = U <= INT32_MAX && W + L <= INT32_MAX;
+    const MedianVariant v = vec2 ? pick_median<2>(n_max, c32) : pick_median<1>(n_max, c32);
     // bracket half-width g / 2^e for windows of n_max steps: about 3.7
     // sqrt(n) values inside for a spread of a tenth of the value, so that a
     // guess off by the statistical error of a median still brackets it
