@@ -573,7 +573,7 @@ def main() -> int:
             wg = g_out["window_gain"].sum(dim=0).double()
             wm = float(g_out["window_makespan"].sum())
             next_rows["exposure_gain"] = {
-                "kernel": ("k_exposure_gain_near (+ k_exposure_gain<REDO>, k_window_sum)"
+                "kernel": ("k_exposure_gain_near (+ k_window_sum)"
                            if S <= 16 and 4096 < R <= 16384 and R % 2 == 0
                            else "k_exposure_gain (+ k_window_sum)"),
                 "bound": "hbm",

@@ -13,8 +13,7 @@
 //
 // Past 4096 ranks (up to 16384, 16 stages) k_exposure_gain_near takes the
 // maximum over the ranks near the frontier first and over all ranks only
-// when a bound requires it; k_exposure_gain<REDO> recomputes the steps it
-// hands over (values of 2^32 or more).
+// when a bound requires it.
 
 #include "sf_device.h"
 #include "sf_host.h"
@@ -22,12 +21,7 @@
 
 namespace sfk {
 
-// the gain row of a step that k_exposure_gain_near hands over (gains are >= 0)
-constexpr int64_t kGainRedo = INT64_MIN;
-
-// REDO: only the steps whose gain row starts with kGainRedo (one step per
-// workgroup), the others untouched.
-template <int VEC, int K, int G, int WG, int SMAX, bool RUN, bool REDO = false>
+template <int VEC, int K, int G, int WG, int SMAX, bool RUN>
 __global__ __launch_bounds__(WG) void k_exposure_gain(
     const int64_t* __restrict__ d, const int64_t* __restrict__ btilde, int64_t T, int R, int S,
     int64_t window, int64_t* __restrict__ gain, int64_t* __restrict__ makespan)
@@ -40,7 +34,6 @@ __global__ __launch_bounds__(WG) void k_exposure_gain(
     constexpr int RT = G * K;
     constexpr int NCOL = SMAX + 1;  // SMAX replaced-stage maxima, then F
     static_assert(!RUN || SMAX <= 16, "running maxima of up to 16 stages");
-    static_assert(!REDO || G == WG, "a handed-over step is a whole workgroup");
 
     __shared__ u64 tab[(WG / SUB) * NCOL];
 
@@ -50,7 +43,6 @@ __global__ __launch_bounds__(WG) void k_exposure_gain(
     const bool writer = (tid % SUB) == SUB - 1;
     const int64_t tb = xcd_block() * SPW;
     const int64_t t = tb + tid / G;
-    if (REDO && (t >= T || gain[t * S] != kGainRedo)) return;  // uniform: one step
 
     if (t < T) {
         const int64_t* dt = d + t * (int64_t)S * R;
@@ -248,38 +240,37 @@ __global__ __launch_bounds__(WG) void k_exposure_gain_wide(
 // with v = F - P_S (F = max_r P_S) a rank whose v is at least D contributes
 // at most F - D to max_r (P_S - delta); when the maximum over the set
 // Q = {r : v < D} reaches F - D it is the maximum over all ranks.  One
-// workgroup per step keeps the rank totals in registers (16 per lane, 32
-// bits: one pass over the step's durations, two chunks of loads per stage,
-// the waves kept on one stage row by a barrier), picks D by radix passes
-// over v (256-bin histograms, as in the selects) so that Q holds at least
-// kNearMin ranks (every rank up to the one of rank kNearMin - 1 in
-// ascending v, and the rest of its bin in the last pass) and at most
-// kNearCap, reads the durations and baseline of Q's ranks only, and folds
-// every stage's maximum over Q with LDS atomics.  If some stage's maximum
-// falls below F - D (a gain larger than D), or more than kNearCap ranks sit
-// at the smallest values of v, the workgroup makes a second pass over the
-// step's durations and baseline and takes the maxima over all ranks.  A
-// step with a duration or a total of 2^32 or more is handed over: its gain
-// row starts with kGainRedo and k_exposure_gain<REDO> recomputes it in 64
-// bits.  Measured on MI355X: one 16-wave workgroup per CU (about 76 VGPRs)
-// ran 5% faster than two at a 64-VGPR cap; loading a stage in one chunk, 3%
-// slower; without the stage barrier, 2% slower; at 4096 ranks the
-// per-step kernel stays ahead (0.62 against 0.65 ms).
+// workgroup per step keeps the rank totals in registers (16 per lane: one
+// pass over the step's durations, two chunks of loads per stage, the waves
+// kept on one stage row by a barrier), picks D by radix passes over v
+// (256-bin histograms, as in the selects) so that Q holds at least kNearMin
+// ranks (every rank up to the one of rank kNearMin - 1 in ascending v, and
+// the rest of its bin in the last pass) and at most kNearCap, reads the
+// durations and baseline of Q's ranks only, and folds every stage's maximum
+// over Q with LDS atomics.  If some stage's maximum falls below F - D (a
+// gain larger than D), or more than kNearCap ranks sit at the smallest
+// values of v, the workgroup makes a second pass over the step's durations
+// and baseline and takes the maxima over all ranks.  The totals are 64-bit
+// (32-bit ones ran 0.5% faster but made every step past 2^32 ns, 4.3 s, a
+// second launch).  Measured on MI355X: one 16-wave workgroup per CU beat
+// two at a 64-VGPR cap by 5%; loading a stage in one chunk, 3% slower;
+// without the stage barrier, 2% slower; at 4096 ranks the per-step kernel
+// stays ahead (0.63 against 0.64-0.66 ms).
 constexpr int kNearMin = 32;
 constexpr int kNearCap = 512;
-constexpr int kNearK = 16;  // ranks per lane
 
-// the maximum over the wave of a 32-bit value, in lane 63
-__device__ __forceinline__ uint32_t wave_max32(uint32_t v)
+// digit and candidate tests of the bound's radix passes, on 64-bit values or
+// on 32-bit ones (totals spanning less than 2^32: lo <= 24, hi <= 32, a
+// prefix below 2^(32 - hi)), which keep the shifts and compares in single
+// VALU instructions
+__device__ __forceinline__ int near_first_bin(u64 v, int lo) { return sel_first_bin(v, lo); }
+__device__ __forceinline__ int near_bin(u64 v, int lo, int hi, u64 prefix) { return sel_bin(v, lo, hi, prefix); }
+__device__ __forceinline__ int near_first_bin(uint32_t v, int lo) { return (int)(v >> lo); }
+__device__ __forceinline__ int near_bin(uint32_t v, int lo, int hi, u64 prefix)
 {
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0xB1, 0xF, 0xF, false));
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x4E, 0xF, 0xF, false));
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x141, 0xF, 0xF, false));
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x140, 0xF, 0xF, false));
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x142, 0xA, 0xF, false));
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x143, 0xC, 0xF, false));
-    return v;
+    return (hi >= 32 || (v >> hi) == (uint32_t)prefix) ? (int)((v >> lo) & ((1u << (hi - lo)) - 1u)) : -1;
 }
+constexpr int kNearK = 16;  // ranks per lane
 
 template <int WG, bool FULL>
 __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_exposure_gain_near(
@@ -292,16 +283,16 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
     constexpr int CH = 2;  // chunks of loads per stage
     constexpr int SMAX = 16;
     __shared__ __align__(16) uint32_t hist[kSelWords];
-    __shared__ uint32_t red_max[NW], red_min[NW], red_wide[NW];
+    __shared__ u64 red_max[NW], red_min[NW];
     __shared__ uint32_t sel[3];
     __shared__ int q_rank[kNearCap];
-    __shared__ uint32_t q_tot[kNearCap];
+    __shared__ u64 q_tot[kNearCap];
     __shared__ uint32_t q_n, all_ranks;
-    __shared__ uint32_t cand[SMAX];
+    __shared__ u64 cand[SMAX];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t t = xcd_block();
     if (t >= T) return;  // uniform (the grid is T)
     const int64_t* dt = d + t * (int64_t)S * R;
@@ -315,11 +306,10 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
         ok[l] = FULL || r < R;
         idx[l] = ok[l] ? r : 0;
     }
-    // the rank totals P_S in 32 bits; `wide` notes a high word or a carry
-    uint32_t tot[K];
+    // the rank totals P_S (slots past R stay 0 and are left out below)
+    u64 tot[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) tot[k] = 0;
-    uint32_t wide = 0;
     for (int s = 0; s < S; ++s) {
         const auto rs = buffer_rsrc(dt + (int64_t)s * R, (uint32_t)R * 8u);
 #pragma unroll
@@ -335,36 +325,27 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
 #pragma unroll
             for (int l = 0; l < NLD / CH; ++l) {
                 const int ll = ch * (NLD / CH) + l;
-#pragma unroll
-                for (int e = 0; e < 2; ++e) {
-                    const u64 x = (u64)(e == 0 ? xs[l].x : xs[l].y);
-                    const uint32_t lo = ok[ll] ? (uint32_t)x : 0u;
-                    wide |= ok[ll] ? (uint32_t)(x >> 32) : 0u;
-                    const uint32_t np = tot[2 * ll + e] + lo;
-                    wide |= np < lo ? 1u : 0u;
-                    tot[2 * ll + e] = np;
-                }
+                tot[2 * ll] += ok[ll] ? (u64)xs[l].x : 0ull;
+                tot[2 * ll + 1] += ok[ll] ? (u64)xs[l].y : 0ull;
             }
             __builtin_amdgcn_sched_barrier(0);
         }
         __builtin_amdgcn_s_barrier();  // the waves read a stage's row together
     }
-    // F, the smallest total and the wide flag over the workgroup
-    uint32_t mx = 0, mn = ~0u;
+    // F and the smallest total over the workgroup
+    u64 mx = 0, mn = ~0ull;
 #pragma unroll
     for (int k = 0; k < K; ++k) {
         if (ok[k / 2]) {
-            mx = max(mx, tot[k]);
-            mn = min(mn, tot[k]);
+            mx = umax64(mx, tot[k]);
+            mn = umin64(mn, tot[k]);
         }
     }
-    mx = wave_max32(mx);
-    mn = ~wave_max32(~mn);
-    const uint32_t ww = __ballot(wide != 0) != 0 ? 1u : 0u;
+    mx = group_max<64>(mx);
+    mn = ~group_max<64>(~mn);
     if (lane == 63) {
         red_max[wave] = mx;
         red_min[wave] = mn;
-        red_wide[wave] = ww;
     }
     if (tid < SMAX) cand[tid] = 0;
     if (tid == 0) {
@@ -372,18 +353,23 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
         all_ranks = 0;
     }
     __syncthreads();
-    uint32_t F = 0, Pmin = ~0u, anywide = 0;
+    u64 F = 0, Pmin = ~0ull;
 #pragma unroll
     for (int i = 0; i < NW; ++i) {
-        F = max(F, red_max[i]);
-        Pmin = min(Pmin, red_min[i]);
-        anywide |= red_wide[i];
+        F = umax64(F, red_max[i]);
+        Pmin = umin64(Pmin, red_min[i]);
     }
-    // the bound D: Q = {v < D} with kNearMin <= |Q| <= kNearCap
+    // the bound D: Q = {v < D} with kNearMin <= |Q| <= kNearCap, by radix
+    // passes over v = F - P_S; in 32 bits when the totals span less than
+    // 2^32 (every workload here), else in 64
     u64 D = 0;
     bool have_q = false;
-    if (anywide == 0 && F != Pmin) {
-        int lo = sel_first_lo((u64)(F - Pmin)), hi = 64;
+    auto find_bound = [&](auto vt) {
+        typedef decltype(vt) VT;
+        VT v[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) v[k] = (VT)(F - tot[k]);
+        int lo = sel_first_lo(F - Pmin), hi = 64;
         u64 prefix = 0;
         uint32_t kk = kNearMin - 1;  // R > 4096 ranks
         uint32_t below = 0;          // ranks in Q for certain (below the bracket)
@@ -394,8 +380,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 if (ok[k / 2]) {
-                    const u64 v = (u64)(F - tot[k]);
-                    const int bin = first ? sel_first_bin(v, lo) : sel_bin(v, lo, hi, prefix);
+                    const int bin = first ? near_first_bin(v[k], lo) : near_bin(v[k], lo, hi, prefix);
                     if (bin >= 0) atomicAdd(&hist[bin], 1u);
                 }
             }
@@ -418,21 +403,26 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
             if (below + lower + cn <= (uint32_t)kNearCap) {
                 D = (prefix + 1) << hi;
                 have_q = true;
-                break;
+                return;
             }
-            if (hi == 0) break;  // more than kNearCap ranks up to one value of v
+            if (hi == 0) return;  // more than kNearCap ranks up to one value of v
             below += lower;
             kk = kin;
             lo = lo > 8 ? lo - 8 : 0;
         }
+    };
+    if (F != Pmin) {
+        if (F - Pmin <= 0xFFFFFFFFull)
+            find_bound((uint32_t)0);
+        else
+            find_bound((u64)0);
         // sel and hist are not touched again in this step
     }
     if (have_q) {
         // Q into LDS: a wave scan of the per-lane counts, one atomic per wave
         uint32_t cm = 0;
 #pragma unroll
-        for (int k = 0; k < K; ++k)
-            cm |= (ok[k / 2] && (u64)(F - tot[k]) < D) ? (1u << k) : 0u;
+        for (int k = 0; k < K; ++k) cm |= (ok[k / 2] && F - tot[k] < D) ? (1u << k) : 0u;
         const uint32_t nc = (uint32_t)__popc(cm);
         const uint32_t incl = wave_scan_incl(nc);
         const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
@@ -455,7 +445,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
         // every (rank of Q, stage) pair: four per thread in flight at once
         for (uint32_t i0 = tid; i0 < np; i0 += 4 * WG) {
             int64_t x[4], y[4];
-            uint32_t tq[4];
+            u64 tq[4];
             int sj[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -473,21 +463,16 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
             for (int j = 0; j < 4; ++j) {
                 if (i0 + (uint32_t)(j * WG) < np) {
                     const int64_t e = x[j] - y[j];  // b >= 0: max(e, 0) <= x <= the total
-                    atomicMax(&cand[sj[j]], tq[j] - (uint32_t)(e > 0 ? e : 0));
+                    atomicMax(&cand[sj[j]], tq[j] - (u64)(e > 0 ? e : 0));
                 }
             }
         }
         __syncthreads();
-        if (tid < S && (u64)cand[tid] + D < (u64)F) all_ranks = 1;  // a gain above D
+        if (tid < S && cand[tid] + D < F) all_ranks = 1;  // a gain above D
         __syncthreads();
     }
-    if (anywide != 0) {  // uniform: 64-bit values, left to k_exposure_gain<REDO>
-        if (tid == 0) gain[t * S] = kGainRedo;
-        return;
-    }
     if (!have_q || all_ranks != 0) {
-        // every rank: a second pass over the step's durations and its
-        // baseline (the durations are below 2^32, so delta <= d fits)
+        // every rank: a second pass over the step's durations and baseline
         if (have_q) {
             if (tid < SMAX) cand[tid] = 0;  // the check above has read them
             __syncthreads();
@@ -495,7 +480,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
         for (int s = 0; s < S; ++s) {
             const auto rd = buffer_rsrc(dt + (int64_t)s * R, (uint32_t)R * 8u);
             const auto rb = buffer_rsrc(bw + (int64_t)s * R, (uint32_t)R * 8u);
-            uint32_t m = 0;
+            u64 m = 0;
 #pragma unroll
             for (int ch = 0; ch < CH; ++ch) {
                 v2i64 xs[NLD / CH], ys[NLD / CH];
@@ -513,12 +498,12 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
 #pragma unroll
                     for (int e = 0; e < 2; ++e) {
                         const int64_t e64 = (e == 0 ? xs[l].x : xs[l].y) - (e == 0 ? ys[l].x : ys[l].y);
-                        const uint32_t c = tot[2 * ll + e] - (uint32_t)(e64 > 0 ? e64 : 0);
-                        m = ok[ll] ? max(m, c) : m;
+                        const u64 c = tot[2 * ll + e] - (u64)(e64 > 0 ? e64 : 0);
+                        m = ok[ll] ? umax64(m, c) : m;
                     }
                 }
             }
-            m = wave_max32(m);
+            m = group_max<64>(m);
             if (lane == 63) atomicMax(&cand[s], m);
         }
         __syncthreads();
@@ -606,7 +591,7 @@ SF_API int sf_exposure_gain(const int64_t* durations, const int64_t* baseline, i
     void* a1[] = {(void*)&durations, (void*)&baseline, (void*)&T, (void*)&Ri, (void*)&Si,
                   (void*)&window, (void*)&out_gain, (void*)&out_makespan};
     if (vec2 && S <= 16 && R > kNearK * 256 && R <= kNearK * 1024 && T <= INT32_MAX) {
-        // the ranks near the frontier, then the steps handed over in 64 bits
+        // the ranks near the frontier (all ranks where the bound does not settle it)
         const int WG = R <= kNearK * 512 ? 512 : 1024;
         const bool full = R == kNearK * WG;
         const void* fn =
@@ -614,15 +599,7 @@ SF_API int sf_exposure_gain(const int64_t* durations, const int64_t* baseline, i
                               : reinterpret_cast<const void*>(&k_exposure_gain_near<512, false>))
                       : (full ? reinterpret_cast<const void*>(&k_exposure_gain_near<1024, true>)
                               : reinterpret_cast<const void*>(&k_exposure_gain_near<1024, false>));
-        const void* redo =
-            S <= 4 ? reinterpret_cast<const void*>(&k_exposure_gain<2, 2, 256, 256, 4, true, true>)
-          : S <= 6 ? reinterpret_cast<const void*>(&k_exposure_gain<2, 2, 256, 256, 6, true, true>)
-          : S <= 8 ? reinterpret_cast<const void*>(&k_exposure_gain<2, 2, 256, 256, 8, true, true>)
-          : S <= 12 ? reinterpret_cast<const void*>(&k_exposure_gain<2, 2, 256, 256, 12, true, true>)
-                    : reinterpret_cast<const void*>(&k_exposure_gain<2, 2, 256, 256, 16, true, true>);
         int rc = launch(fn, dim3((unsigned)T), dim3(WG), a1, 0, stream);
-        if (rc != SF_OK) return rc;
-        rc = launch(redo, dim3((unsigned)T), dim3(256), a1, 0, stream);
         if (rc != SF_OK) return rc;
         rc = launch_window_sum(out_gain, T, S, window, W, out_window_gain, stream);
         if (rc != SF_OK) return rc;

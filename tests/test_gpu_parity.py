@@ -729,8 +729,9 @@ def test_gain_stalled_near_frontier(sf):
 
 
 def test_gain_wide_steps_among_narrow(sf):
-    """Past 4096 ranks: the odd steps hold a duration past 2^32 and go to the
-    64-bit kernel, the even ones stay in 32 bits, in one launch."""
+    """Past 4096 ranks: the odd steps hold a duration past 2^32 (their
+    totals span more than 2^32: the bound's radix passes run in 64 bits),
+    the even ones stay below (32-bit passes), in one launch."""
     rng = np.random.Generator(np.random.PCG64(717))
     T, S, R, window = 9, 12, 8192, 4
     d = rng.integers(0, 1 << 28, size=(T, S, R), dtype=np.int64)
