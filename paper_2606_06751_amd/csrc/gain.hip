@@ -92,7 +92,7 @@ __global__ __launch_bounds__(WG) void k_exposure_gain(
             u64 fmax = 0;
 #pragma unroll
             for (int k = 0; k < K; ++k) fmax = umax64(fmax, (u64)tot[k]);
-            if (RUN) {
+            if constexpr (RUN) {
                 run[SMAX] = umax64(run[SMAX], fmax);
             } else {
                 fmax = group_max<SUB>(fmax);
@@ -107,7 +107,7 @@ __global__ __launch_bounds__(WG) void k_exposure_gain(
                     u64 m = 0;
 #pragma unroll
                     for (int k = 0; k < K; ++k) m = umax64(m, (u64)(tot[k] - dl[k][s]));
-                    if (RUN) {
+                    if constexpr (RUN) {
                         run[s] = umax64(run[s], m);
                     } else {
                         m = group_max<SUB>(m);
@@ -119,7 +119,7 @@ __global__ __launch_bounds__(WG) void k_exposure_gain(
                 }
             }
         }
-        if (RUN) {
+        if constexpr (RUN) {
             // one reduction per step over the group
 #pragma unroll
             for (int c = 0; c < (RUN ? NCOL : 1); ++c) {
