@@ -288,6 +288,7 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
     __shared__ int q_rank[kNearCap];
     __shared__ u64 q_tot[kNearCap];
     __shared__ uint32_t q_n, all_ranks;
+    __shared__ int top_rank;  // a rank whose total is F
     __shared__ u64 cand[SMAX];
 
     const int tid = threadIdx.x;
@@ -438,30 +439,46 @@ __global__ __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(4))) void k_
                 }
                 ++pos;
             }
+            if (ok[k / 2] && tot[k] == F) top_rank = idx[k / 2] + (k & 1);  // any one of them
+        }
+        __syncthreads();
+        // first a rank whose total is F, for every stage: its replaced-stage
+        // total F - delta bounds the stage's maximum from below, so only
+        // ranks of Q whose total exceeds it can raise it (fewer scattered
+        // reads: each costs a cache line)
+        if (tid < S) {
+            const int64_t e = dt[(int64_t)tid * R + top_rank] - bw[(int64_t)tid * R + top_rank];
+            cand[tid] = F - (u64)(e > 0 ? e : 0);
         }
         __syncthreads();
         const uint32_t nq = min(q_n, (uint32_t)kNearCap);
         const uint32_t np = nq * (uint32_t)S;
-        // every (rank of Q, stage) pair: four per thread in flight at once
+        // the (rank of Q, stage) pairs left: four per thread in flight at once
         for (uint32_t i0 = tid; i0 < np; i0 += 4 * WG) {
             int64_t x[4], y[4];
             u64 tq[4];
             int sj[4];
+            bool need[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const uint32_t i = i0 + (uint32_t)(j * WG);
                 const uint32_t ii = i < np ? i : 0u;
                 const uint32_t q = ii / (uint32_t)S;
                 const int s = (int)(ii - q * (uint32_t)S);
-                const int r = q_rank[q];
-                x[j] = dt[(int64_t)s * R + r];
-                y[j] = bw[(int64_t)s * R + r];
                 tq[j] = q_tot[q];
                 sj[j] = s;
+                need[j] = i < np && tq[j] > cand[s];  // cand only grows: a stale read is safe
+                x[j] = 0;
+                y[j] = 0;
+                if (need[j]) {
+                    const int r = q_rank[q];
+                    x[j] = dt[(int64_t)s * R + r];
+                    y[j] = bw[(int64_t)s * R + r];
+                }
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                if (i0 + (uint32_t)(j * WG) < np) {
+                if (need[j]) {
                     const int64_t e = x[j] - y[j];  // b >= 0: max(e, 0) <= x <= the total
                     atomicMax(&cand[sj[j]], tq[j] - (u64)(e > 0 ? e : 0));
                 }
